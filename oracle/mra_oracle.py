@@ -1,0 +1,257 @@
+"""Plain float64 CPU oracle of MRA-2 approximate self-attention.
+
+TEST INFRASTRUCTURE ONLY. Nothing on the product path may import, call or
+execute this module; only the tests, the smoke check and the benchmark's
+CPU-baseline leg use it. It shares no code with the HIP kernels.
+
+It computes, slowly and literally, what the paper defines for the
+two-resolution scheme R = {b, 1} ("MRA-2", Sec. 5, b = 32):
+
+* block means of Q, K, V (Sec. 4.1, eq. recursive_pooling; Sec. 4.3,
+  eq. recursive_pooling_V), taken here as the direct mean of each b-row block,
+  which is what b/2-fold pairwise averaging gives in exact arithmetic;
+* coarse logits mu_{b,x,y} = exp(<B^b_{x,y}, P>/b^2) = exp(Q~_x . K~_y)
+  (Sec. 4.1, eq. exp_of_average), with P = Q K^T / sqrt(d);
+* per block-row selection of the `m` coarse blocks with the largest score
+  (Sec. 4.2, Alg. 1, applied row by row; ties go to the lower block index);
+* the approximation A^ of eq. actual_approx_mat_form: inside a selected block
+  every entry is exp(P_ij) (the scale-1 components), every other block is the
+  constant exp(S~_xy) (the scale-b component it was not replaced by);
+* Z = D^ A^ V with D^ the diagonal that makes every row of A^ sum to one
+  (Sec. 3.1, eq. softmax-attention, applied to A^).
+
+Readings of points the paper leaves open (scale 1/sqrt(d) kept in both fine and
+coarse logits, per-row budget, replacement rather than addition, factor b on
+the coarse term in Alg. 2, ties to the lower index, ascending index lists) are
+listed with their reasons in the design notes.
+
+Two forms of the output are provided: the dense definition over the full
+logit slab of each block-row (``mra_dense``) and the factored form of Alg. 2
+(``mra_factored``), where the unselected blocks contribute b*exp(S~)*V~_y.
+The tests check that they agree.
+
+Conventions: single-head functions take 2-D arrays [n, d]; batched wrappers
+take [B, H, n, d]. Every array is converted to float64 on entry.
+"""
+from __future__ import annotations
+
+import math
+import numpy as np
+
+
+# --------------------------------------------------------------------------
+# Sec. 4.1 / 4.3: block means (eq. recursive_pooling, eq. recursive_pooling_V)
+# --------------------------------------------------------------------------
+def block_mean(x, b):
+    """Rows of x averaged over consecutive blocks of b rows: [n, d] -> [n/b, d]."""
+    x = np.asarray(x, dtype=np.float64)
+    n, d = x.shape
+    if n % b:
+        raise ValueError("sequence length must be a multiple of the block size")
+    return x.reshape(n // b, b, d).sum(axis=1) / b
+
+
+# --------------------------------------------------------------------------
+# Sec. 4.1, eq. exp_of_average: coarse logits S~ = Q~ K~^T / sqrt(d)
+# --------------------------------------------------------------------------
+def coarse_logits(qp, kp):
+    """S~[x, y] = Q~_x . K~_y / sqrt(d); mu_{b,x,y} = exp(S~[x, y])."""
+    qp = np.asarray(qp, dtype=np.float64)
+    kp = np.asarray(kp, dtype=np.float64)
+    return (qp @ kp.T) / math.sqrt(qp.shape[1])
+
+
+# --------------------------------------------------------------------------
+# Sec. 4.2, Alg. 1: pop the blocks with the largest mu, per block-row
+# --------------------------------------------------------------------------
+def select_blocks(S, m):
+    """For every block-row x, the m column blocks with the largest S~[x, .]
+    (equivalently the largest mu, exp being increasing); among equal scores
+    the lower index wins. Each row of the result is in ascending order."""
+    S = np.asarray(S, dtype=np.float64)
+    nb = S.shape[1]
+    if not 0 <= m <= nb:
+        raise ValueError("budget out of range")
+    out = np.empty((S.shape[0], m), dtype=np.int64)
+    cols = np.arange(nb)
+    for x in range(S.shape[0]):
+        order = np.lexsort((cols, -S[x]))      # primary: -score, then index
+        out[x] = np.sort(order[:m])
+    return out
+
+
+# --------------------------------------------------------------------------
+# eq. actual_approx_mat_form: the logits of A^ for one block-row
+# --------------------------------------------------------------------------
+def approx_logits_slab(q, k, S, sel, b, x):
+    """log A^ restricted to the b query rows of block-row x: an array [b, n].
+
+    Inside a selected column block the entry is the fine logit P_ij (scale-1
+    component, mu_{1,i,j} = exp(P_ij)); every other column of block y holds the
+    coarse logit S~[x, y] (scale-b component, mu_{b,x,y})."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    n, d = k.shape
+    nb = n // b
+    rows = q[x * b:(x + 1) * b]
+    slab = np.repeat(S[x], b)[None, :].repeat(b, axis=0)      # coarse everywhere
+    for y in sel:
+        cols = slice(y * b, (y + 1) * b)
+        slab[:, cols] = rows @ k[cols].T / math.sqrt(d)         # replace by fine
+    assert slab.shape == (b, nb * b)
+    return slab
+
+
+def approx_matrix(q, k, b, idx):
+    """Dense A^ (n x n) for a single head with the given selection. Tiny n only."""
+    qp, kp = block_mean(q, b), block_mean(k, b)
+    S = coarse_logits(qp, kp)
+    nb = S.shape[0]
+    return np.vstack([np.exp(approx_logits_slab(q, k, S, idx[x], b, x)) for x in range(nb)])
+
+
+def _normalised_rows(logits, v):
+    """Rows of exp(logits) normalised to sum 1, times v; shifted by the row max
+    (the normalised result does not depend on the shift)."""
+    z = logits - logits.max(axis=1, keepdims=True)
+    w = np.exp(z)
+    return (w @ v) / w.sum(axis=1, keepdims=True)
+
+
+def mra_dense(q, k, v, b, m, idx=None):
+    """Z = D^ A^ V for one head from the dense slab of each block-row.
+
+    If idx is given it replaces the selection of Alg. 1 (used to evaluate the
+    output under another, equally valid, tie choice). Returns (Z, idx)."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    qp, kp = block_mean(q, b), block_mean(k, b)
+    S = coarse_logits(qp, kp)
+    if idx is None:
+        idx = select_blocks(S, m)
+    Z = np.empty((q.shape[0], v.shape[1]))
+    for x in range(S.shape[0]):
+        slab = approx_logits_slab(q, k, S, idx[x], b, x)
+        Z[x * b:(x + 1) * b] = _normalised_rows(slab, v)
+    return Z, idx
+
+
+# --------------------------------------------------------------------------
+# Sec. 4.3, Alg. 2 at s = b: the low-resolution term of one block-row
+# --------------------------------------------------------------------------
+def coarse_term(S_row, sel, vp, b):
+    """For the unselected blocks y of one block-row, with M the largest
+    unselected S~: returns (M, c, L) where c = sum_y b*exp(S~_y - M) and
+    L = sum_y b*exp(S~_y - M) * V~_y. With no unselected block, M = -inf and
+    c, L are zero. The factor b counts the b columns each block spans."""
+    S_row = np.asarray(S_row, dtype=np.float64)
+    vp = np.asarray(vp, dtype=np.float64)
+    mask = np.ones(S_row.shape[0], dtype=bool)
+    mask[np.asarray(sel, dtype=np.int64)] = False
+    if not mask.any():
+        return -np.inf, 0.0, np.zeros(vp.shape[1])
+    M = S_row[mask].max()
+    w = b * np.exp(S_row[mask] - M)
+    return M, w.sum(), w @ vp[mask]
+
+
+def mra_factored_rows(q, k, v, b, m, rows=None, idx=None):
+    """Z for the given block-rows of one head, computed as in Alg. 2:
+    fine products exp(P) V over the selected blocks plus the coarse term
+    b*exp(S~_xy) V~_y over the rest, divided by the matching row sums.
+
+    Returns (Z_rows [len(rows)*b, d], idx_rows [len(rows), m], S [nb, nb] rows)."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    n, d = q.shape
+    nb = n // b
+    rows = list(range(nb)) if rows is None else list(rows)
+    qp, kp, vp = block_mean(q, b), block_mean(k, b), block_mean(v, b)
+    S = coarse_logits(qp[rows], kp)
+    sel_all = select_blocks(S, m) if idx is None else np.asarray(idx)
+    out = np.empty((len(rows) * b, v.shape[1]))
+    for r, x in enumerate(rows):
+        sel = np.asarray(sel_all[r], dtype=np.int64)
+        M, c, L = coarse_term(S[r], sel, vp, b)
+        qx = q[x * b:(x + 1) * b]
+        if len(sel):
+            cols = np.concatenate([np.arange(y * b, (y + 1) * b) for y in sel])
+            P = qx @ k[cols].T / math.sqrt(d)
+            mf = P.max(axis=1, keepdims=True)
+        else:
+            cols = np.zeros(0, dtype=np.int64)
+            P = np.zeros((b, 0))
+            mf = np.full((b, 1), -np.inf)
+        top = np.maximum(mf, M)
+        wf = np.exp(P - top)
+        wc = np.exp(M - top) if np.isfinite(M) else np.zeros_like(top)
+        num = wf @ v[cols] + wc * L[None, :]
+        den = wf.sum(axis=1, keepdims=True) + wc * c
+        out[r * b:(r + 1) * b] = num / den
+    return out, sel_all, S
+
+
+def mra_factored(q, k, v, b, m, idx=None):
+    Z, idx, _ = mra_factored_rows(q, k, v, b, m, idx=idx)
+    return Z, idx
+
+
+# --------------------------------------------------------------------------
+# Sec. 3.1, eq. softmax-attention: exact attention (scale 1/sqrt(d))
+# --------------------------------------------------------------------------
+def exact_attention(q, k, v):
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    return _normalised_rows(q @ k.T / math.sqrt(q.shape[1]), v)
+
+
+# --------------------------------------------------------------------------
+# batched wrappers over [B, H, n, d]
+# --------------------------------------------------------------------------
+def pool_batched(x, b):
+    x = np.asarray(x, dtype=np.float64)
+    B, H, n, d = x.shape
+    return x.reshape(B, H, n // b, b, d).sum(axis=3) / b
+
+
+def coarse_batched(qp, kp):
+    qp = np.asarray(qp, dtype=np.float64)
+    kp = np.asarray(kp, dtype=np.float64)
+    return np.einsum("bhxd,bhyd->bhxy", qp, kp) / math.sqrt(qp.shape[-1])
+
+
+def select_batched(S, m):
+    B, H, nb, _ = S.shape
+    out = np.empty((B, H, nb, m), dtype=np.int64)
+    for bb in range(B):
+        for h in range(H):
+            out[bb, h] = select_blocks(S[bb, h], m)
+    return out
+
+
+def coarse_term_batched(S, idx, vp, b):
+    """(M, c, L) arrays [B,H,nb], [B,H,nb], [B,H,nb,d] for all block-rows."""
+    B, H, nb, _ = S.shape
+    d = vp.shape[-1]
+    M = np.empty((B, H, nb)); c = np.empty((B, H, nb)); L = np.empty((B, H, nb, d))
+    for bb in range(B):
+        for h in range(H):
+            for x in range(nb):
+                M[bb, h, x], c[bb, h, x], L[bb, h, x] = coarse_term(S[bb, h, x], idx[bb, h, x], vp[bb, h], b)
+    return M, c, L
+
+
+def mra_batched(q, k, v, b, m, idx=None, form="factored"):
+    """Z and idx for every head of [B, H, n, d] inputs."""
+    fn = mra_factored if form == "factored" else mra_dense
+    B, H, n, d = q.shape
+    Z = np.empty((B, H, n, v.shape[-1]))
+    I = np.empty((B, H, n // b, m), dtype=np.int64)
+    for bb in range(B):
+        for h in range(H):
+            Z[bb, h], I[bb, h] = fn(q[bb, h], k[bb, h], v[bb, h], b, m,
+                                    idx=None if idx is None else idx[bb, h])
+    return Z, I
