@@ -1,0 +1,174 @@
+"""Throughput of the MRA-2 forward pass on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
+
+One step = one mra_attention_forward call (pool, coarse logits, selection with
+the coarse term, tile pass) over the whole workload, inputs resident in HBM.
+Prints one JSON line with tokens/s, the roofline of the dominant kernel (the
+tile pass, timed with HIP events on the stream it runs on) and the float64
+oracle timed on the host as a reported CPU baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 matrix peak
+PEAK_F32_TFLOPS = 157.3        # MI355X fp32 matrix / vector peak
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+
+
+def tile_flops(w) -> float:
+    """Algorithmic flops of the tile pass: per selected 32x32 tile, 2*32*32*d
+    for c Q_x K_y^T and 2*32*32*d for P V_y."""
+    return 4.0 * w.B * w.H * w.nb * w.budget * 32 * 32 * w.d
+
+
+def coarse_flops(w) -> float:
+    """Coarse logits and the low-resolution term: 2*nb*nb*d each per head."""
+    return 4.0 * w.B * w.H * w.nb * w.nb * w.d
+
+
+def pool_bytes(w) -> float:
+    """Pooling pass as run in the forward: Q, K, V read once, the pooled rows
+    written, and K and V written once more in packed order."""
+    e = 2 if w.dtype == "bf16" else 4
+    return 5.0 * w.B * w.H * w.n * w.d * e + 3.0 * w.B * w.H * w.nb * w.d * 4
+
+
+def time_launches(fn, iters: int, warmup: int = 3) -> float:
+    """Average duration (ms) of `fn` (kernel launches on torch's current
+    stream) between HIP events recorded on that stream."""
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(iters):
+        fn()
+    e.record()
+    torch.cuda.synchronize()
+    return s.elapsed_time(e) / iters
+
+
+def cpu_baseline(w, q, k, v):
+    """The float64 oracle (factored form, as it stands) over every head of the
+    workload, timed on the host. Returns the JSON object."""
+    from oracle import mra_oracle as O
+    try:
+        import threadpoolctl
+        threads = max(i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()) or 1
+    except Exception:                                  # pragma: no cover
+        threads = os.cpu_count() or 1
+    budget_s = 25.0
+    t0 = time.perf_counter()
+    heads = 0
+    for b in range(w.B):
+        for h in range(w.H):
+            O.mra_factored(q[b, h], k[b, h], v[b, h], 32, w.budget)
+            heads += 1
+            if time.perf_counter() - t0 > budget_s:
+                break
+        else:
+            continue
+        break
+    dt = time.perf_counter() - t0
+    tokens = heads / w.H * w.n                         # tokens of a full H-head layer
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{heads} of {w.B * w.H} heads ({w.name}), float64 factored form, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-baseline leg")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (the path has no multi-GPU mode); got --gpus {args.gpus}",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2207_10284_amd import inputs, ops
+
+    ops.load()
+    w = inputs.WORKLOADS[args.workload or inputs.BENCH_WORKLOAD]
+    q, k, v = inputs.make_qkv(w)
+    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    dev = torch.device("cuda:0")
+    tq, tk, tv = (torch.from_numpy(a).to(dev).to(tdt) for a in (q, k, v))
+    out = torch.empty_like(tq)
+    idx = torch.empty(w.B, w.H, w.nb, w.budget, dtype=torch.int32, device=dev)
+    ws = torch.empty(ops.forward_workspace_bytes(w.B, w.H, w.n, w.d, w.budget, tdt), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+
+    def step():
+        ops.attention_forward(tq, tk, tv, w.budget, out=out, idx_out=idx, workspace=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    s.record()
+    for _ in range(args.steps):
+        step()
+    e.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = s.elapsed_time(e) / args.steps
+    tokens_per_s = w.B * w.n / (ms * 1e-3)
+
+    # Dominant kernel: the tile pass, the same instantiation as inside the
+    # forward (packed K/V, coarse term given), on the same inputs; timed alone.
+    qp, kp, vp, kvpk = ops.pool(tq, tk, tv, packed=True)
+    S = ops.coarse_scores(qp, kp)
+    sel = ops.select(S, w.budget)
+    cm, cs, cv = ops.coarse_term(S, sel, vp)
+    tile_out = torch.empty_like(tq)
+    it = max(args.steps, 20)
+    tile_ms = time_launches(lambda: ops.block_sddmm_spmm(tq, None, None, sel, cm, cs, cv, out=tile_out, kvpacked=kvpk), it)
+    pool_ms = time_launches(lambda: ops.pool(tq, tk, tv, packed=True), it)
+    coarse_ms = time_launches(lambda: ops.coarse_scores(qp, kp), it)
+    tflops = tile_flops(w) / (tile_ms * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    pool_gbs = pool_bytes(w) / (pool_ms * 1e-3) / 1e9
+
+    res = {
+        "metric": "MRA-2 attention fwd tokens/s at n=4096,d=64 bf16; % MFMA peak on tile path",
+        "value": tokens_per_s, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "n": w.n, "d": w.d, "block": 32,
+                   "budget": w.budget, "inputs": w.kind},
+        "roofline": {"bound": "mfma", "kernel": "tile_kernel (block-sparse SDDMM + SpMM + merge)",
+                     "achieved": tflops, "peak": peak, "unit": "TFLOP/s", "frac": tflops / peak,
+                     "traffic": None, "launch_us": tile_ms * 1e3,
+                     "flops_per_launch": tile_flops(w)},
+        "stages_us": {"pool_and_pack": pool_ms * 1e3, "tile": tile_ms * 1e3,
+                      "select_and_coarse_term_fused": (ms - pool_ms - tile_ms) * 1e3,
+                      "coarse_scores_stepwise": coarse_ms * 1e3},
+        "pool_roofline": {"bound": "hbm", "achieved": pool_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                          "frac": pool_gbs / PEAK_HBM_GBS, "bytes_per_launch": pool_bytes(w)},
+        "tflops_step": (tile_flops(w) + coarse_flops(w)) / (ms * 1e-3) / 1e12,
+        "wall_s_timed": wall,
+    }
+    if not args.no_cpu:
+        res["cpu_baseline"] = cpu_baseline(w, q, k, v)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

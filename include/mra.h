@@ -1,0 +1,205 @@
+/*
+ * mra.h — C ABI of libmra: MRA-2 multiresolution approximate self-attention
+ * (Zeng et al., "Multi Resolution Analysis (MRA) for Approximate
+ * Self-Attention", ICML 2022) on AMD Instinct MI355X (gfx950).
+ *
+ * MRA-2 is the two-resolution scheme R = {b, 1} with b = 32 (Sec. 5). For one
+ * attention head with Q, K, V in R^{n x d} and c = 1/sqrt(d):
+ *
+ *   pooled rows   Q~, K~, V~ : means of consecutive 32-row blocks
+ *                              (Sec. 4.1 eq. recursive_pooling, Sec. 4.3
+ *                              eq. recursive_pooling_V)
+ *   coarse logits S~ = c Q~ K~^T, mu_{b,x,y} = exp(S~[x,y])
+ *                              (Sec. 4.1 eq. exp_of_average)
+ *   selection     T_x = the `budget` column blocks with the largest S~[x,.]
+ *                              (Sec. 4.2 Alg. 1, applied per block-row;
+ *                              ties go to the lower block index)
+ *   approximation A^_ij = exp(c Q_i.K_j) if block(j) in T_block(i),
+ *                         exp(S~[block(i), block(j)]) otherwise
+ *                              (Sec. 4.2 eq. actual_approx_mat_form)
+ *   output        Z = D^ A^ V, D^ normalising each row of A^ to sum 1
+ *                              (Sec. 3.1 eq. softmax-attention applied to A^;
+ *                              computed as in Sec. 4.3 Alg. 2)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Tensors are DEVICE pointers on the current HIP device, dense row-major
+ *   [B][H][rows][cols] (batch, head, row, column), owned by the caller. The
+ *   library never allocates, frees or synchronises; every call only enqueues
+ *   kernels on `stream` (an opaque hipStream_t; NULL = the default stream)
+ *   and returns. Outputs must not alias inputs.
+ * - Every pointer must be 16-byte aligned.
+ * - `block` must be 32 and `d` one of 32, 64, 128 (MRA_ERR_UNSUPPORTED
+ *   otherwise). `n` must be a multiple of `block` and at most 65536.
+ *   nb = n / block is the number of blocks per side of the block grid.
+ * - `budget` is the number of selected blocks per block-row, 0 <= budget <= nb.
+ *   budget = 0 leaves every block at low resolution; budget = nb gives exact
+ *   softmax attention.
+ * - B, H, n may be 0 (an empty problem): the call then validates its other
+ *   arguments and returns MRA_OK without touching any pointer.
+ * - Q/K/V/output element type is `dtype` (float32 or bfloat16). Pooled rows,
+ *   coarse logits and the coarse term are float32. Fine products accumulate in
+ *   float32 (bfloat16 inputs feed bfloat16 matrix-core products); coarse
+ *   logits accumulate in float64 and are rounded once to float32.
+ * - The scale c = 1/sqrt(d) is applied to both the fine and the coarse logits.
+ * - Results for non-finite inputs are unspecified.
+ *
+ * Errors: every argument check runs on the host before any HIP call, so a call
+ * that returns an error other than MRA_ERR_HIP has enqueued nothing. A failed
+ * kernel launch returns MRA_ERR_HIP; mra_last_hip_error() then gives the
+ * hipError_t of the calling thread's last failure. No C++ exception crosses
+ * this interface.
+ */
+#ifndef MRA_H_
+#define MRA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MRA_F32 = 0,
+  MRA_BF16 = 1
+} mra_dtype_t;
+
+typedef enum {
+  MRA_OK = 0,
+  MRA_ERR_INVALID_ARG = 1,   /* NULL pointer, bad size, budget out of range */
+  MRA_ERR_UNSUPPORTED = 2,   /* block != 32, d not in {32,64,128}, n > 65536, unknown dtype */
+  MRA_ERR_MISALIGNED = 3,    /* a pointer not 16-byte aligned */
+  MRA_ERR_WORKSPACE = 4,     /* workspace_bytes smaller than required */
+  MRA_ERR_HIP = 5            /* a HIP launch failed; see mra_last_hip_error() */
+} mra_status_t;
+
+/*
+ * mra_pool — block means of Q, K and V (Sec. 4.1 eq. recursive_pooling,
+ * Sec. 4.3 eq. recursive_pooling_V; for b = 32 the five-fold pairwise
+ * averaging equals the plain 32-row mean).
+ *   q, k, v    : [B,H,n,d] of `dtype`.
+ *   qp, kp, vp : [B,H,nb,d] float32 outputs. A pair (x, xp) may be NULL
+ *                together, in which case that tensor is skipped; at least one
+ *                pair must be given.
+ *   kvpacked   : optional output (NULL to skip; needs k, v, kp, vp):
+ *                2*B*H*n*d elements of `dtype`, K and V rearranged block by
+ *                block into the operand order of the tile pass's matrix-core
+ *                products (an opaque layout, only meant for
+ *                mra_block_sddmm_spmm).
+ * Each mean is summed in float32 in row order and multiplied by 1/32.
+ */
+mra_status_t mra_pool(const void* q, const void* k, const void* v,
+                      float* qp, float* kp, float* vp, void* kvpacked,
+                      int B, int H, int n, int d, int block,
+                      mra_dtype_t dtype, void* stream);
+
+/*
+ * mra_coarse_scores — coarse logits S~ = Q~ K~^T / sqrt(d) (Sec. 4.1,
+ * eq. exp_of_average: mu_{b,x,y} = exp(S~[x,y]) is the exponential of the
+ * block mean of the fine logits).
+ *   qp, kp : [B,H,nb,d] float32 pooled rows (as written by mra_pool).
+ *   scores : [B,H,nb,nb] float32 output; accumulated in float64, rounded once.
+ */
+mra_status_t mra_coarse_scores(const float* qp, const float* kp, float* scores,
+                               int B, int H, int n, int d, int block, void* stream);
+
+/*
+ * mra_select — per block-row choice of the blocks to refine (Sec. 4.2, Alg. 1:
+ * pop the blocks with the largest mu; here `budget` of them in every
+ * block-row). Ranks by S~ (exp is increasing); -0.0 and +0.0 rank equal;
+ * among equal scores the lower column-block index wins.
+ *   scores : [B,H,nb,nb] float32.
+ *   idx    : [B,H,nb,budget] int32 output; each row strictly ascending.
+ */
+mra_status_t mra_select(const float* scores, int32_t* idx,
+                        int B, int H, int n, int block, int budget, void* stream);
+
+/*
+ * mra_coarse_term — the low-resolution part of A^ V and of the row sums of A^
+ * for every block-row: Alg. 2 (Sec. 4.3) at scale b over the blocks NOT in
+ * T_x, each block spanning b columns (eq. actual_approx_mat_form):
+ *   cmax[x]  = M_x = max_{y not in T_x} S~[x,y]            (-inf if none)
+ *   csum[x]  = sum_{y not in T_x} b * exp(S~[x,y] - M_x)     (0 if none)
+ *   cvec[x,:]= sum_{y not in T_x} b * exp(S~[x,y] - M_x) * V~[y,:]
+ *   scores : [B,H,nb,nb] float32; idx : [B,H,nb,budget] int32, rows strictly
+ *            ascending with entries in [0, nb) (entries outside are ignored);
+ *   vp     : [B,H,nb,d] float32 pooled V.
+ *   cmax, csum : [B,H,nb] float32 outputs; cvec : [B,H,nb,d] float32 output.
+ */
+mra_status_t mra_coarse_term(const float* scores, const int32_t* idx, const float* vp,
+                             float* cmax, float* csum, float* cvec,
+                             int B, int H, int n, int d, int block, int budget,
+                             void* stream);
+
+/*
+ * mra_block_sddmm_spmm — the high-resolution part and the output (Sec. 4.2
+ * eq. actual_approx_mat_form with mu_{1,i,j} = exp(P_ij); Sec. 4.3 Alg. 2 at
+ * scale 1; Sec. 3.1 normalisation D^). For every block-row x and every
+ * y in T_x it computes the 32x32 tile exp(c Q_x K_y^T) (block-sparse SDDMM),
+ * multiplies it by V_y (block-sparse SpMM), merges the result with the coarse
+ * term and normalises:
+ *   Z_i = (sum_{j in T} e^{P_ij} V_j + e^{M_x} cvec[x]) /
+ *         (sum_{j in T} e^{P_ij}     + e^{M_x} csum[x])
+ * (evaluated with max shifts; nothing overflows for finite inputs).
+ *   q, k, v : [B,H,n,d] of `dtype`.
+ *   kvpacked: optional: the packed K and V written by mra_pool from these same
+ *             k and v. If not NULL it is read instead of k and v (which may
+ *             then be NULL); the result is identical either way.
+ *   idx     : [B,H,nb,budget] int32, rows strictly ascending in [0, nb);
+ *             entries outside [0, nb) are skipped.
+ *   cmax, csum, cvec : the coarse term from mra_coarse_term. All three may be
+ *             NULL together: then only the selected tiles are normalised
+ *             (the sparse-only variant MRA-2-s of Sec. 5), which needs
+ *             budget >= 1.
+ *   out     : [B,H,n,d] of `dtype`, the output Z (bfloat16 rounded to nearest
+ *             even). With bfloat16 inputs the tile probabilities are rounded
+ *             to bfloat16 before the product with V and the row sums use the
+ *             same rounded values.
+ */
+mra_status_t mra_block_sddmm_spmm(const void* q, const void* k, const void* v,
+                                  const void* kvpacked, const int32_t* idx,
+                                  const float* cmax, const float* csum, const float* cvec,
+                                  void* out,
+                                  int B, int H, int n, int d, int block, int budget,
+                                  mra_dtype_t dtype, void* stream);
+
+/*
+ * mra_forward_workspace_bytes — bytes of device workspace mra_attention_forward
+ * needs for these sizes and dtype: pooled rows, copies of K and V rearranged
+ * into matrix-core operand order, the selection and the coarse term (about
+ * 2*B*H*n*d*elem + B*H*(n/32)*(4d + budget + 2)*4 bytes). Returns 0 for
+ * invalid or unsupported arguments.
+ */
+size_t mra_forward_workspace_bytes(int B, int H, int n, int d, int block, int budget,
+                                   mra_dtype_t dtype);
+
+/*
+ * mra_attention_forward — the whole MRA-2 forward pass: pooling (which also
+ * rearranges K and V for the tile pass), coarse logits with
+ * selection and coarse term fused (the logits never leave on-chip memory),
+ * then the tile pass. Results are bit-identical to the calls above made in
+ * order (mra_pool, mra_coarse_scores, mra_select, mra_coarse_term,
+ * mra_block_sddmm_spmm).
+ *   q, k, v   : [B,H,n,d] of `dtype`; out : [B,H,n,d] of `dtype`.
+ *   idx_out   : optional [B,H,nb,budget] int32 copy of the selection (NULL:
+ *               kept in the workspace only).
+ *   workspace : device buffer of at least mra_forward_workspace_bytes(...)
+ *               bytes (16-byte aligned; contents on entry are ignored).
+ */
+mra_status_t mra_attention_forward(const void* q, const void* k, const void* v, void* out,
+                                   int32_t* idx_out, void* workspace, size_t workspace_bytes,
+                                   int B, int H, int n, int d, int block, int budget,
+                                   mra_dtype_t dtype, void* stream);
+
+/* Static description of a status code. */
+const char* mra_status_str(mra_status_t status);
+
+/* hipError_t (as int) of the calling thread's last MRA_ERR_HIP; 0 if none. */
+int mra_last_hip_error(void);
+
+#ifdef __cplusplus
+}  /* extern "C" */
+#endif
+
+#endif  /* MRA_H_ */

@@ -1,0 +1,247 @@
+// C ABI of libmra (declared in mra.h): argument validation, workspace layout
+// and kernel dispatch. Every check runs before the first HIP call, so a
+// rejected call has enqueued nothing.
+#include "mra.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "kernels.h"
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+constexpr int kBlockSize = 32;
+constexpr int kMaxN = 65536;
+constexpr long long kMaxGrid = 2147483647LL;   // workgroups per launch
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct Shape {
+  long long bh = 0;
+  int nb = 0;
+  bool empty = true;
+};
+
+// B, H, n, block (and d when d_needed) checks shared by every call.
+mra_status_t check_shape(int B, int H, int n, int d, int block, bool d_needed, Shape* s) {
+  if (B < 0 || H < 0 || n < 0 || block <= 0) return MRA_ERR_INVALID_ARG;
+  if (d_needed && d <= 0) return MRA_ERR_INVALID_ARG;
+  if (block != kBlockSize) return MRA_ERR_UNSUPPORTED;
+  if (n % block != 0) return MRA_ERR_INVALID_ARG;
+  if (n > kMaxN) return MRA_ERR_UNSUPPORTED;
+  if (d_needed && d != 32 && d != 64 && d != 128) return MRA_ERR_UNSUPPORTED;
+  s->bh = (long long)B * (long long)H;
+  s->nb = n / block;
+  s->empty = (s->bh == 0 || n == 0);
+  if (!s->empty) {
+    const long long rows = s->bh * s->nb;
+    const long long nt = (s->nb + 63) / 64;
+    // pool: one thread per 16 bytes of a block (at most 32 x 128 / 4 per block-row)
+    if (rows * 32 > kMaxGrid) return MRA_ERR_UNSUPPORTED;
+    if (s->bh * nt * nt > kMaxGrid) return MRA_ERR_UNSUPPORTED;
+  }
+  return MRA_OK;
+}
+
+mra_status_t check_dtype(mra_dtype_t dt) {
+  return (dt == MRA_F32 || dt == MRA_BF16) ? MRA_OK : MRA_ERR_UNSUPPORTED;
+}
+
+mra_status_t check_ptr(const void* p) {
+  if (p == nullptr) return MRA_ERR_INVALID_ARG;
+  return aligned16(p) ? MRA_OK : MRA_ERR_MISALIGNED;
+}
+
+mra_status_t hip_status(hipError_t e) {
+  if (e == hipSuccess) return MRA_OK;
+  g_last_hip_error = (int)e;
+  return MRA_ERR_HIP;
+}
+
+#define MRA_TRY(expr)                 \
+  do {                                \
+    const mra_status_t st_ = (expr);  \
+    if (st_ != MRA_OK) return st_;    \
+  } while (0)
+
+struct WsLayout {
+  size_t qp, kp, vp, kvpacked, idx, cmax, csum, cvec, total;
+};
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+WsLayout ws_layout(long long bh, int nb, int d, int m, mra_dtype_t dtype) {
+  WsLayout L{};
+  size_t off = 0;
+  const size_t pooled = align256((size_t)bh * nb * d * sizeof(float));
+  const size_t elem = dtype == MRA_BF16 ? 2 : 4;
+  L.qp = off; off += pooled;
+  L.kp = off; off += pooled;
+  L.vp = off; off += pooled;
+  L.kvpacked = off; off += align256((size_t)2 * bh * nb * kBlockSize * d * elem);
+  L.idx = off; off += align256((size_t)bh * nb * m * sizeof(int32_t));
+  L.cmax = off; off += align256((size_t)bh * nb * sizeof(float));
+  L.csum = off; off += align256((size_t)bh * nb * sizeof(float));
+  L.cvec = off; off += align256((size_t)bh * nb * d * sizeof(float));
+  L.total = off;
+  return L;
+}
+
+}  // namespace
+
+extern "C" {
+
+mra_status_t mra_pool(const void* q, const void* k, const void* v, float* qp, float* kp,
+                      float* vp, void* kvpacked, int B, int H, int n, int d, int block,
+                      mra_dtype_t dtype, void* stream) {
+  Shape s;
+  MRA_TRY(check_shape(B, H, n, d, block, true, &s));
+  MRA_TRY(check_dtype(dtype));
+  if ((q == nullptr) != (qp == nullptr) || (k == nullptr) != (kp == nullptr) ||
+      (v == nullptr) != (vp == nullptr))
+    return MRA_ERR_INVALID_ARG;
+  if (q == nullptr && k == nullptr && v == nullptr) return MRA_ERR_INVALID_ARG;
+  if (kvpacked != nullptr && (k == nullptr || v == nullptr)) return MRA_ERR_INVALID_ARG;
+  if (s.empty) return MRA_OK;
+  const void* ptrs[7] = {q, k, v, qp, kp, vp, kvpacked};
+  for (const void* p : ptrs)
+    if (p != nullptr && !aligned16(p)) return MRA_ERR_MISALIGNED;
+  return hip_status(mra::launch_pool(q, k, v, qp, kp, vp, kvpacked, s.bh, n, d, (int)dtype,
+                                     static_cast<hipStream_t>(stream)));
+}
+
+mra_status_t mra_coarse_scores(const float* qp, const float* kp, float* scores, int B, int H,
+                               int n, int d, int block, void* stream) {
+  Shape s;
+  MRA_TRY(check_shape(B, H, n, d, block, true, &s));
+  if (s.empty) return MRA_OK;
+  MRA_TRY(check_ptr(qp));
+  MRA_TRY(check_ptr(kp));
+  MRA_TRY(check_ptr(scores));
+  return hip_status(mra::launch_coarse(qp, kp, scores, s.bh, s.nb, d,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+mra_status_t mra_select(const float* scores, int32_t* idx, int B, int H, int n, int block,
+                        int budget, void* stream) {
+  Shape s;
+  MRA_TRY(check_shape(B, H, n, 0, block, false, &s));
+  if (budget < 0 || budget > s.nb) return MRA_ERR_INVALID_ARG;
+  if (s.empty || budget == 0) return MRA_OK;
+  MRA_TRY(check_ptr(scores));
+  MRA_TRY(check_ptr(idx));
+  return hip_status(mra::launch_select(scores, idx, s.bh, s.nb, budget,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+mra_status_t mra_coarse_term(const float* scores, const int32_t* idx, const float* vp,
+                             float* cmax, float* csum, float* cvec, int B, int H, int n, int d,
+                             int block, int budget, void* stream) {
+  Shape s;
+  MRA_TRY(check_shape(B, H, n, d, block, true, &s));
+  if (budget < 0 || budget > s.nb) return MRA_ERR_INVALID_ARG;
+  if (s.empty) return MRA_OK;
+  MRA_TRY(check_ptr(scores));
+  if (budget > 0) MRA_TRY(check_ptr(idx));
+  MRA_TRY(check_ptr(vp));
+  MRA_TRY(check_ptr(cmax));
+  MRA_TRY(check_ptr(csum));
+  MRA_TRY(check_ptr(cvec));
+  return hip_status(mra::launch_coarse_term(scores, idx, vp, cmax, csum, cvec, s.bh, s.nb, d,
+                                            budget, static_cast<hipStream_t>(stream)));
+}
+
+mra_status_t mra_block_sddmm_spmm(const void* q, const void* k, const void* v,
+                                  const void* kvpacked, const int32_t* idx,
+                                  const float* cmax, const float* csum,
+                                  const float* cvec, void* out, int B, int H, int n, int d,
+                                  int block, int budget, mra_dtype_t dtype, void* stream) {
+  Shape s;
+  MRA_TRY(check_shape(B, H, n, d, block, true, &s));
+  MRA_TRY(check_dtype(dtype));
+  if (budget < 0 || budget > s.nb) return MRA_ERR_INVALID_ARG;
+  const int given = (cmax != nullptr) + (csum != nullptr) + (cvec != nullptr);
+  if (given != 0 && given != 3) return MRA_ERR_INVALID_ARG;
+  if (given == 0 && budget == 0) return MRA_ERR_INVALID_ARG;   // nothing to normalise
+  if (s.empty) return MRA_OK;
+  MRA_TRY(check_ptr(q));
+  if (kvpacked) {
+    MRA_TRY(check_ptr(kvpacked));
+  } else {
+    MRA_TRY(check_ptr(k));
+    MRA_TRY(check_ptr(v));
+  }
+  MRA_TRY(check_ptr(out));
+  if (budget > 0) MRA_TRY(check_ptr(idx));
+  if (given) {
+    MRA_TRY(check_ptr(cmax));
+    MRA_TRY(check_ptr(csum));
+    MRA_TRY(check_ptr(cvec));
+  }
+  return hip_status(mra::launch_tile(q, k, v, kvpacked, idx, cmax, csum, cvec, out, s.bh, n, d,
+                                     budget, (int)dtype, static_cast<hipStream_t>(stream)));
+}
+
+size_t mra_forward_workspace_bytes(int B, int H, int n, int d, int block, int budget,
+                                   mra_dtype_t dtype) {
+  Shape s;
+  if (check_shape(B, H, n, d, block, true, &s) != MRA_OK) return 0;
+  if (check_dtype(dtype) != MRA_OK) return 0;
+  if (budget < 0 || budget > s.nb) return 0;
+  return ws_layout(s.bh, s.nb, d, budget, dtype).total;
+}
+
+mra_status_t mra_attention_forward(const void* q, const void* k, const void* v, void* out,
+                                   int32_t* idx_out, void* workspace, size_t workspace_bytes,
+                                   int B, int H, int n, int d, int block, int budget,
+                                   mra_dtype_t dtype, void* stream) {
+  Shape s;
+  MRA_TRY(check_shape(B, H, n, d, block, true, &s));
+  MRA_TRY(check_dtype(dtype));
+  if (budget < 0 || budget > s.nb) return MRA_ERR_INVALID_ARG;
+  if (s.empty) return MRA_OK;
+  MRA_TRY(check_ptr(q));
+  MRA_TRY(check_ptr(k));
+  MRA_TRY(check_ptr(v));
+  MRA_TRY(check_ptr(out));
+  if (idx_out != nullptr && !aligned16(idx_out)) return MRA_ERR_MISALIGNED;
+  MRA_TRY(check_ptr(workspace));
+  const WsLayout L = ws_layout(s.bh, s.nb, d, budget, dtype);
+  if (workspace_bytes < L.total) return MRA_ERR_WORKSPACE;
+
+  char* ws = static_cast<char*>(workspace);
+  float* qp = reinterpret_cast<float*>(ws + L.qp);
+  float* kp = reinterpret_cast<float*>(ws + L.kp);
+  float* vp = reinterpret_cast<float*>(ws + L.vp);
+  void* kvpacked = ws + L.kvpacked;
+  int32_t* idx = idx_out ? idx_out : reinterpret_cast<int32_t*>(ws + L.idx);
+  float* cmax = reinterpret_cast<float*>(ws + L.cmax);
+  float* csum = reinterpret_cast<float*>(ws + L.csum);
+  float* cvec = reinterpret_cast<float*>(ws + L.cvec);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+
+  MRA_TRY(hip_status(mra::launch_pool(q, k, v, qp, kp, vp, kvpacked, s.bh, n, d, (int)dtype, st)));
+  MRA_TRY(hip_status(mra::launch_select_term_fused(qp, kp, idx, vp, cmax, csum, cvec, s.bh, s.nb,
+                                                   d, budget, st)));
+  return hip_status(mra::launch_tile(q, k, v, kvpacked, idx, cmax, csum, cvec, out, s.bh, n, d,
+                                     budget, (int)dtype, st));
+}
+
+const char* mra_status_str(mra_status_t status) {
+  switch (status) {
+    case MRA_OK: return "MRA_OK";
+    case MRA_ERR_INVALID_ARG: return "MRA_ERR_INVALID_ARG: invalid argument";
+    case MRA_ERR_UNSUPPORTED: return "MRA_ERR_UNSUPPORTED: unsupported block, head dim, length or dtype";
+    case MRA_ERR_MISALIGNED: return "MRA_ERR_MISALIGNED: pointer not 16-byte aligned";
+    case MRA_ERR_WORKSPACE: return "MRA_ERR_WORKSPACE: workspace too small";
+    case MRA_ERR_HIP: return "MRA_ERR_HIP: HIP launch failed";
+  }
+  return "unknown mra_status_t";
+}
+
+int mra_last_hip_error(void) { return g_last_hip_error; }
+
+}  // extern "C"

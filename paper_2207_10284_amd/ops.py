@@ -1,0 +1,203 @@
+"""Thin Python binding of libmra (C ABI in include/mra.h).
+
+Argument marshalling only: every function checks tensor placement, dtype and
+shape, allocates outputs with torch (device memory is plumbing here), and
+calls the library on the current torch stream. All arithmetic runs in the HIP
+kernels. There is no fallback: if the library is not built, ``load`` raises.
+
+Shapes: q, k, v are [B, H, n, d] tensors on a ROCm device, float32 or
+bfloat16, contiguous; n is a multiple of 32 and d is 32, 64 or 128.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmra.so")
+BLOCK = 32
+
+MRA_F32, MRA_BF16 = 0, 1
+STATUS = {0: "MRA_OK", 1: "MRA_ERR_INVALID_ARG", 2: "MRA_ERR_UNSUPPORTED",
+          3: "MRA_ERR_MISALIGNED", 4: "MRA_ERR_WORKSPACE", 5: "MRA_ERR_HIP"}
+
+# name -> (restype, argtypes); mirrors include/mra.h
+_P, _I, _Z = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+SIGNATURES = {
+    "mra_pool": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P]),
+    "mra_coarse_scores": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _P]),
+    "mra_select": (_I, [_P, _P, _I, _I, _I, _I, _I, _P]),
+    "mra_coarse_term": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P]),
+    "mra_block_sddmm_spmm": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _P]),
+    "mra_forward_workspace_bytes": (_Z, [_I, _I, _I, _I, _I, _I, _I]),
+    "mra_attention_forward": (_I, [_P, _P, _P, _P, _P, _P, _Z, _I, _I, _I, _I, _I, _I, _I, _P]),
+    "mra_status_str": (ctypes.c_char_p, [_I]),
+    "mra_last_hip_error": (_I, []),
+}
+
+_lib = None
+
+
+class MraError(RuntimeError):
+    def __init__(self, fn: str, status: int, lib):
+        msg = lib.mra_status_str(status).decode()
+        if status == 5:
+            msg += f" (hipError_t {lib.mra_last_hip_error()})"
+        super().__init__(f"{fn}: {msg}")
+        self.status = status
+
+
+def load(path: str = LIB_PATH):
+    """Open libmra.so once and declare its signatures. Raises if it is missing."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is not built; run `python -m paper_2207_10284_amd.build` "
+                               "(hipcc, gfx950) first")
+        lib = ctypes.CDLL(path)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(lib, name)
+            fn.restype, fn.argtypes = res, args
+        _lib = lib
+    return _lib
+
+
+def _call(name: str, *args):
+    lib = load()
+    st = getattr(lib, name)(*args)
+    if st != 0:
+        raise MraError(name, st, lib)
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(device):
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return MRA_F32
+    if t.dtype == torch.bfloat16:
+        return MRA_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}; expected float32 or bfloat16")
+
+
+def _check_qkv(*ts):
+    ref = next(t for t in ts if t is not None)
+    for t in ts:
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise ValueError("tensors must be on a ROCm device")
+        if t.dim() != 4 or t.shape != ref.shape or t.dtype != ref.dtype or t.device != ref.device:
+            raise ValueError("q, k, v must share shape [B, H, n, d], dtype and device")
+        if not t.is_contiguous():
+            raise ValueError("q, k, v must be contiguous")
+    return ref
+
+
+def _check_f32(t, shape, name):
+    if t.dtype != torch.float32 or tuple(t.shape) != tuple(shape) or not t.is_contiguous() or not t.is_cuda:
+        raise ValueError(f"{name} must be a contiguous float32 device tensor of shape {tuple(shape)}")
+
+
+def pool(q, k=None, v=None, packed=False):
+    """Block means (Sec. 4.1/4.3): returns (qp, kp, vp), float32 [B, H, n/32, d]
+    (None for a tensor not given); with ``packed=True`` also the packed copies
+    of k and v for the tile pass, as a fourth element (opaque, [2, B, H, n, d])."""
+    ref = _check_qkv(q, k, v)
+    B, H, n, d = ref.shape
+    outs = [None if t is None else torch.empty(B, H, n // BLOCK, d, device=ref.device, dtype=torch.float32)
+            for t in (q, k, v)]
+    kvpk = torch.empty((2,) + tuple(ref.shape), device=ref.device, dtype=ref.dtype) if packed else None
+    _call("mra_pool", _ptr(q), _ptr(k), _ptr(v), *(_ptr(o) for o in outs), _ptr(kvpk),
+          B, H, n, d, BLOCK, _dtype_code(ref), _stream(ref.device))
+    return tuple(outs) + ((kvpk,) if packed else ())
+
+
+def coarse_scores(qp, kp):
+    """Coarse logits S~ = Q~ K~^T / sqrt(d): float32 [B, H, nb, nb]."""
+    B, H, nb, d = qp.shape
+    _check_f32(qp, (B, H, nb, d), "qp")
+    _check_f32(kp, (B, H, nb, d), "kp")
+    S = torch.empty(B, H, nb, nb, device=qp.device, dtype=torch.float32)
+    _call("mra_coarse_scores", _ptr(qp), _ptr(kp), _ptr(S), B, H, nb * BLOCK, d, BLOCK, _stream(qp.device))
+    return S
+
+
+def select(scores, budget: int):
+    """Per block-row top-`budget` column blocks, ascending: int32 [B, H, nb, budget]."""
+    B, H, nb, _ = scores.shape
+    _check_f32(scores, (B, H, nb, nb), "scores")
+    idx = torch.empty(B, H, nb, budget, device=scores.device, dtype=torch.int32)
+    _call("mra_select", _ptr(scores), _ptr(idx), B, H, nb * BLOCK, BLOCK, budget, _stream(scores.device))
+    return idx
+
+
+def _check_idx(idx, B, H, nb, budget, device):
+    if idx.dtype != torch.int32 or tuple(idx.shape) != (B, H, nb, budget) or not idx.is_contiguous() \
+            or idx.device != device:
+        raise ValueError(f"idx must be a contiguous int32 tensor of shape {(B, H, nb, budget)}")
+
+
+def coarse_term(scores, idx, vp):
+    """Low-resolution term of the unselected blocks: (cmax, csum, cvec)."""
+    B, H, nb, d = vp.shape
+    budget = idx.shape[-1]
+    _check_f32(scores, (B, H, nb, nb), "scores")
+    _check_f32(vp, (B, H, nb, d), "vp")
+    _check_idx(idx, B, H, nb, budget, vp.device)
+    cmax = torch.empty(B, H, nb, device=vp.device, dtype=torch.float32)
+    csum = torch.empty_like(cmax)
+    cvec = torch.empty(B, H, nb, d, device=vp.device, dtype=torch.float32)
+    _call("mra_coarse_term", _ptr(scores), _ptr(idx), _ptr(vp), _ptr(cmax), _ptr(csum), _ptr(cvec),
+          B, H, nb * BLOCK, d, BLOCK, budget, _stream(vp.device))
+    return cmax, csum, cvec
+
+
+def block_sddmm_spmm(q, k, v, idx, cmax=None, csum=None, cvec=None, out=None, kvpacked=None):
+    """Selected tiles exp(c Q_x K_y^T) V_y, merged with the coarse term (if
+    given) and normalised: the output Z, [B, H, n, d] in the input dtype.
+    ``kvpacked`` (from ``pool(..., packed=True)``) replaces k and v when given."""
+    ref = _check_qkv(q, *((k, v) if kvpacked is None else (kvpacked[0], kvpacked[1])))
+    B, H, n, d = ref.shape
+    nb = n // BLOCK
+    budget = idx.shape[-1]
+    _check_idx(idx, B, H, nb, budget, ref.device)
+    if cmax is not None:
+        _check_f32(cmax, (B, H, nb), "cmax")
+        _check_f32(csum, (B, H, nb), "csum")
+        _check_f32(cvec, (B, H, nb, d), "cvec")
+    if out is None:
+        out = torch.empty_like(ref)
+    _call("mra_block_sddmm_spmm", _ptr(q), _ptr(k), _ptr(v), _ptr(kvpacked), _ptr(idx), _ptr(cmax), _ptr(csum),
+          _ptr(cvec), _ptr(out), B, H, n, d, BLOCK, budget, _dtype_code(ref), _stream(ref.device))
+    return out
+
+
+def forward_workspace_bytes(B: int, H: int, n: int, d: int, budget: int, dtype=torch.bfloat16) -> int:
+    code = MRA_BF16 if dtype == torch.bfloat16 else MRA_F32
+    return int(load().mra_forward_workspace_bytes(B, H, n, d, BLOCK, budget, code))
+
+
+def attention_forward(q, k, v, budget: int, out=None, idx_out=None, workspace=None):
+    """The whole MRA-2 forward pass. Returns the output Z ([B, H, n, d], input
+    dtype); the selection is written to ``idx_out`` when given."""
+    ref = _check_qkv(q, k, v)
+    B, H, n, d = ref.shape
+    nb = n // BLOCK
+    if out is None:
+        out = torch.empty_like(ref)
+    if idx_out is not None:
+        _check_idx(idx_out, B, H, nb, budget, ref.device)
+    need = forward_workspace_bytes(B, H, n, d, budget, ref.dtype)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), device=ref.device, dtype=torch.uint8)
+    _call("mra_attention_forward", _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(idx_out),
+          _ptr(workspace), workspace.numel() * workspace.element_size(),
+          B, H, n, d, BLOCK, budget, _dtype_code(ref), _stream(ref.device))
+    return out

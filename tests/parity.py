@@ -1,0 +1,51 @@
+"""Helpers shared by the GPU parity tests: upload, error metrics and the
+tie-aware selection check. Holds no arithmetic of the method."""
+import numpy as np
+import torch
+
+from oracle import mra_oracle as O
+
+TOL = {"f32": 1e-5, "bf16": 2e-2}          # max row-normwise relative error
+TIE_BAND = 1e-6                            # relative band around the m-th score
+
+
+def dev(a, dtype="f32"):
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+    return t.to(torch.bfloat16) if dtype == "bf16" else t
+
+
+def host(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def row_rel_err(Z, Zref):
+    """max over rows of ||Z_i - Zref_i||_inf / ||Zref_i||_inf (rows = last axis)."""
+    num = np.abs(Z - Zref).max(axis=-1)
+    den = np.maximum(np.abs(Zref).max(axis=-1), 1e-30)
+    return float((num / den).max()) if num.size else 0.0
+
+
+def check_selection(gpu_idx, S_ref, m, band=TIE_BAND):
+    """GPU selection for rows of S_ref ([rows, nb], float64). Equal to the
+    oracle's, except that rows may differ in elements whose reference score is
+    within `band` (relative to the row's scale) of the m-th largest score.
+    Also checks every GPU row is strictly ascending, in range, of length m.
+    Returns the number of rows that differ."""
+    gpu_idx = np.asarray(gpu_idx)
+    ref = O.select_blocks(S_ref, m)
+    nb = S_ref.shape[1]
+    differ = 0
+    for x in range(S_ref.shape[0]):
+        g = gpu_idx[x]
+        assert len(g) == m
+        if m:
+            assert (np.diff(g) > 0).all() and g[0] >= 0 and g[-1] < nb, g
+        if np.array_equal(g, ref[x]):
+            continue
+        differ += 1
+        srt = np.sort(S_ref[x])[::-1]
+        tau = srt[m - 1]
+        scale = max(abs(tau), np.abs(S_ref[x]).max())
+        for y in set(g.tolist()) ^ set(ref[x].tolist()):
+            assert abs(S_ref[x, y] - tau) <= band * scale, (x, y, S_ref[x, y], tau)
+    return differ

@@ -1,0 +1,129 @@
+"""The C ABI without a GPU: the library loads, exports every function that
+include/mra.h declares, and rejects invalid arguments on the host before any
+HIP call (each call here either fails validation or is an empty problem, so
+nothing is ever enqueued)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2207_10284_amd import ops
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mra.h")
+
+OK, INVALID, UNSUPPORTED, MISALIGNED, WORKSPACE, HIP = range(6)
+A = 1 << 20            # a fake, 16-byte aligned address: never dereferenced
+MIS = A + 4            # misaligned
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return ops.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mra_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert len(names) == 9, names
+    for name in names:
+        assert hasattr(lib, name), name
+    assert set(names) == set(ops.SIGNATURES)
+
+
+def test_status_strings(lib):
+    for code, name in ops.STATUS.items():
+        assert lib.mra_status_str(code).decode().startswith(name)
+    assert lib.mra_last_hip_error() == 0
+
+
+def fwd(lib, q=A, k=A, v=A, out=A, idx=None, ws=A, wsb=1 << 40, B=1, H=1, n=64, d=64, block=32,
+        budget=1, dtype=1):
+    return lib.mra_attention_forward(q, k, v, out, idx, ws, wsb, B, H, n, d, block, budget, dtype, None)
+
+
+def test_forward_validation(lib):
+    assert fwd(lib, block=16) == UNSUPPORTED
+    assert fwd(lib, block=0) == INVALID
+    assert fwd(lib, d=48) == UNSUPPORTED
+    assert fwd(lib, d=0) == INVALID
+    assert fwd(lib, d=256) == UNSUPPORTED
+    assert fwd(lib, n=48) == INVALID           # not a multiple of the block
+    assert fwd(lib, n=65536 + 32) == UNSUPPORTED
+    assert fwd(lib, B=-1) == INVALID
+    assert fwd(lib, H=-3) == INVALID
+    assert fwd(lib, budget=-1) == INVALID
+    assert fwd(lib, budget=3) == INVALID       # nb = 2
+    assert fwd(lib, dtype=7) == UNSUPPORTED
+    assert fwd(lib, q=None) == INVALID
+    assert fwd(lib, out=None) == INVALID
+    assert fwd(lib, ws=None) == INVALID
+    assert fwd(lib, v=MIS) == MISALIGNED
+    assert fwd(lib, idx=MIS) == MISALIGNED
+    need = lib.mra_forward_workspace_bytes(1, 1, 64, 64, 32, 1, 1)
+    assert fwd(lib, wsb=need - 1) == WORKSPACE
+    # empty problems succeed without touching any pointer
+    assert fwd(lib, B=0, q=None, k=None, v=None, out=None, ws=None) == OK
+    assert fwd(lib, n=0, budget=0, q=None, out=None, ws=None) == OK
+    assert fwd(lib, n=0, budget=1) == INVALID  # nb = 0
+    assert lib.mra_last_hip_error() == 0
+
+
+def test_workspace_bytes(lib):
+    f = lib.mra_forward_workspace_bytes
+    assert f(1, 1, 64, 48, 32, 1, 1) == 0
+    assert f(1, 1, 64, 64, 32, 3, 1) == 0
+    assert f(1, 1, 64, 64, 16, 1, 1) == 0
+    assert f(1, 1, 64, 64, 32, 1, 9) == 0
+    al = lambda x: (x + 255) // 256 * 256
+    B, H, n, d, m = 8, 12, 4096, 64, 16
+    bh, nb = B * H, n // 32
+    for dt, e in ((0, 4), (1, 2)):
+        want = 3 * al(bh * nb * d * 4) + al(2 * bh * n * d * e) + al(bh * nb * m * 4) \
+            + 2 * al(bh * nb * 4) + al(bh * nb * d * 4)
+        assert f(B, H, n, d, 32, m, dt) == want
+
+
+def test_step_validation(lib):
+    # pool: pairs must be given together, at least one pair
+    p = lib.mra_pool
+    assert p(A, None, None, None, None, None, None, 1, 1, 64, 64, 32, 1, None) == INVALID
+    assert p(None, None, None, None, None, None, None, 1, 1, 64, 64, 32, 1, None) == INVALID
+    assert p(A, None, None, MIS, None, None, None, 1, 1, 64, 64, 32, 1, None) == MISALIGNED
+    assert p(A, A, A, A, A, A, None, 1, 1, 64, 64, 32, 5, None) == UNSUPPORTED
+    assert p(A, None, None, A, None, None, A, 1, 1, 64, 64, 32, 1, None) == INVALID   # packing needs k and v
+    assert p(A, A, None, A, A, None, A, 1, 1, 64, 64, 32, 1, None) == INVALID
+    assert p(A, A, A, A, A, A, MIS, 1, 1, 64, 64, 32, 1, None) == MISALIGNED
+    # coarse scores
+    assert lib.mra_coarse_scores(A, A, None, 1, 1, 64, 64, 32, None) == INVALID
+    assert lib.mra_coarse_scores(A, A, A, 1, 1, 64, 100, 32, None) == UNSUPPORTED
+    # select: budget range, pointers only needed for budget > 0
+    assert lib.mra_select(A, A, 1, 1, 64, 32, 3, None) == INVALID
+    assert lib.mra_select(None, None, 1, 1, 64, 32, 0, None) == OK
+    assert lib.mra_select(A, None, 1, 1, 64, 32, 1, None) == INVALID
+    # coarse term
+    assert lib.mra_coarse_term(A, None, A, A, A, A, 1, 1, 64, 64, 32, 1, None) == INVALID
+    assert lib.mra_coarse_term(A, A, A, A, A, MIS, 1, 1, 64, 64, 32, 1, None) == MISALIGNED
+    # tile pass: coarse term all-or-nothing; sparse-only needs budget >= 1
+    t = lib.mra_block_sddmm_spmm
+    assert t(A, A, A, None, A, A, None, A, A, 1, 1, 64, 64, 32, 1, 1, None) == INVALID
+    assert t(A, A, A, None, None, None, None, None, A, 1, 1, 64, 64, 32, 0, 1, None) == INVALID
+    assert t(A, A, A, None, A, A, A, A, A, 1, 1, 64, 64, 32, 3, 1, None) == INVALID
+    assert t(A, A, A, None, A, A, A, A, MIS, 1, 1, 64, 64, 32, 1, 1, None) == MISALIGNED
+    assert t(A, A, A, None, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 2, None) == UNSUPPORTED
+    assert t(A, A, None, None, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 1, None) == INVALID   # no v at all
+    assert t(A, None, A, None, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 1, None) == INVALID   # no k
+    assert t(A, None, None, MIS, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 1, None) == MISALIGNED
+    assert t(None, None, None, None, None, A, A, A, None, 0, 1, 64, 64, 32, 1, 1, None) == OK
+
+
+def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
+    monkeypatch.setattr(ops, "_lib", None)
+    with pytest.raises(RuntimeError, match="not built"):
+        ops.load(str(tmp_path / "missing.so"))

@@ -1,0 +1,291 @@
+"""GPU parity: the HIP kernels (through the C ABI) against the float64 oracle
+on the same seeded inputs. Bars: selection bit-exact except near-ties (within
+1e-6 relative of the m-th score, lower index first); outputs within 1e-5 max
+row-normwise relative error for float32 inputs and 2e-2 for bfloat16 inputs.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import mra_oracle as O
+from paper_2207_10284_amd import inputs
+from tests.parity import TOL, check_selection, dev, host, row_rel_err
+
+pytestmark = pytest.mark.gpu
+
+U = 2.0 ** -24
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+# ------------------------------------------------------------------ per step
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("d", [32, 64, 128])
+def test_pool(gpu, dtype, d):
+    _say("pool", dtype, d)
+    q, k, v = inputs.random_qkv(101 + d, 2, 3, 160, d, dtype, scale=3.0)
+    qp, kp, vp = gpu.pool(dev(q, dtype), dev(k, dtype), dev(v, dtype))
+    torch.cuda.synchronize()
+    for a, g in ((q, qp), (k, kp), (v, vp)):
+        ref = O.pool_batched(a, 32)
+        # float32 sum of 32 terms: |error| <= 31 u sum|x| / 32
+        bound = 31 * U * O.pool_batched(np.abs(a), 32) + 1e-30
+        assert (np.abs(host(g) - ref) <= bound).all()
+    # one tensor alone
+    qp2, kp2, vp2 = gpu.pool(dev(q, dtype))
+    assert kp2 is None and vp2 is None
+    assert torch.equal(qp2, qp)
+
+
+@pytest.mark.parametrize("d", [32, 64, 128])
+@pytest.mark.parametrize("n", [32, 96, 2112])
+def test_coarse_scores(gpu, d, n):
+    _say("coarse", d, n)
+    r = np.random.Generator(np.random.PCG64(7 + n + d))
+    qp = r.standard_normal((2, 3, n // 32, d)).astype(np.float32) * 2
+    kp = r.standard_normal((2, 3, n // 32, d)).astype(np.float32) * 2
+    S = host(gpu.coarse_scores(dev(qp), dev(kp)))
+    ref = O.coarse_batched(qp, kp)
+    # float64 accumulation, one rounding to float32
+    mag = np.einsum("bhxd,bhyd->bhxy", np.abs(qp.astype(np.float64)), np.abs(kp.astype(np.float64))) / math.sqrt(d)
+    assert (np.abs(S - ref) <= U * np.abs(ref) + 1e-12 * mag).all()
+
+
+@pytest.mark.parametrize("nb,m", [(1, 1), (5, 2), (16, 4), (64, 63), (100, 8), (128, 16), (1024, 32), (2048, 5)])
+def test_select_exact(gpu, nb, m):
+    _say("select", nb, m)
+    r = np.random.Generator(np.random.PCG64(nb * 31 + m))
+    S = r.standard_normal((2, 3, nb, nb)).astype(np.float32)
+    S[0, 0] = np.round(S[0, 0] * 2) / 2            # many exact ties
+    S[0, 1] = 0.0
+    S[0, 1, :, ::3] = -0.0                         # -0 ranks equal to +0
+    S[1, 0, :, -1] = np.inf
+    S[1, 0, :, 0] = -np.inf
+    idx = host(gpu.select(dev(S), m)).astype(np.int64)
+    ref = O.select_batched(S.astype(np.float64), m)
+    assert np.array_equal(idx, ref)
+
+
+def test_select_budget_extremes(gpu):
+    S = np.random.Generator(np.random.PCG64(3)).standard_normal((1, 2, 40, 40)).astype(np.float32)
+    assert np.array_equal(host(gpu.select(dev(S), 40)), np.broadcast_to(np.arange(40), (1, 2, 40, 40)))
+    assert gpu.select(dev(S), 0).shape == (1, 2, 40, 0)
+
+
+@pytest.mark.parametrize("d", [32, 64, 128])
+@pytest.mark.parametrize("nb,m", [(1, 0), (1, 1), (7, 3), (128, 16), (1024, 32)])
+def test_coarse_term(gpu, d, nb, m):
+    _say("coarse_term", d, nb, m)
+    r = np.random.Generator(np.random.PCG64(nb + m + d))
+    S = (r.standard_normal((1, 3, nb, nb)) * 8).astype(np.float32)
+    vp = r.standard_normal((1, 3, nb, d)).astype(np.float32)
+    idx = O.select_batched(S.astype(np.float64), m)
+    cmax, csum, cvec = gpu.coarse_term(dev(S), torch.from_numpy(idx.astype(np.int32)).cuda(), dev(vp))
+    M, c, L = O.coarse_term_batched(S.astype(np.float64), idx, vp, 32)
+    gM, gc, gL = host(cmax), host(csum), host(cvec)
+    fin = np.isfinite(M)
+    assert np.array_equal(np.isfinite(gM), fin) and (gM[fin] == M[fin]).all()    # max is exact
+    # float32 exp (a few ulp) and float32 sums of at most nb terms
+    tol = (nb + 8) * U
+    assert (np.abs(gc - c) <= tol * c).all()
+    bound = tol * c[..., None] * np.abs(vp.astype(np.float64)).max(axis=2, keepdims=True)
+    assert (np.abs(gL - L) <= bound + 1e-30).all()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("d", [32, 64, 128])
+def test_tile_pass(gpu, dtype, d):
+    """Tile pass alone, given the oracle's selection and coarse term."""
+    _say("tile", dtype, d)
+    B, H, n, m = 2, 3, 320, 3
+    q, k, v = inputs.random_qkv(500 + d, B, H, n, d, dtype, scale=1.5)
+    Z, idx = O.mra_batched(q, k, v, 32, m)
+    qp, kp, vp = (O.pool_batched(a, 32) for a in (q, k, v))
+    S = O.coarse_batched(qp, kp)
+    M, c, L = O.coarse_term_batched(S, idx, vp, 32)
+    out = gpu.block_sddmm_spmm(dev(q, dtype), dev(k, dtype), dev(v, dtype),
+                               torch.from_numpy(idx.astype(np.int32)).cuda(),
+                               dev(M), dev(c), dev(L))
+    err = row_rel_err(host(out), Z)
+    _say("  err", err)
+    assert err <= TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("d", [32, 64, 128])
+def test_packed_kv_path_identical(gpu, dtype, d):
+    """K and V read from the packed copies (forward path) or row-major
+    (step-wise path) give bit-identical outputs; packing does not change the
+    pooled rows."""
+    _say("packed", dtype, d)
+    q, k, v = inputs.random_qkv(600 + d, 2, 3, 320, d, dtype, scale=1.3)
+    tq, tk, tv = dev(q, dtype), dev(k, dtype), dev(v, dtype)
+    qp, kp, vp, kvpk = gpu.pool(tq, tk, tv, packed=True)
+    qp2, kp2, vp2 = gpu.pool(tq, tk, tv)
+    assert torch.equal(qp, qp2) and torch.equal(kp, kp2) and torch.equal(vp, vp2)
+    S = gpu.coarse_scores(qp, kp)
+    idx = gpu.select(S, 3)
+    cm, cs, cv = gpu.coarse_term(S, idx, vp)
+    o1 = gpu.block_sddmm_spmm(tq, tk, tv, idx, cm, cs, cv)
+    o2 = gpu.block_sddmm_spmm(tq, None, None, idx, cm, cs, cv, kvpacked=kvpk)
+    assert torch.equal(o1, o2)
+    s1 = gpu.block_sddmm_spmm(tq, tk, tv, idx)
+    s2 = gpu.block_sddmm_spmm(tq, None, None, idx, kvpacked=kvpk)
+    assert torch.equal(s1, s2)
+
+
+# ------------------------------------------------------------------ whole pass
+def _forward_and_check(gpu, q, k, v, m, dtype, tol=None):
+    tq, tk, tv = dev(q, dtype), dev(k, dtype), dev(v, dtype)
+    B, H, n, d = q.shape
+    idx = torch.empty(B, H, n // 32, m, dtype=torch.int32, device="cuda")
+    out = gpu.attention_forward(tq, tk, tv, m, idx_out=idx)
+    gi = host(idx).astype(np.int64)
+    differ = 0
+    for b in range(B):
+        for h in range(H):
+            S = O.coarse_logits(O.block_mean(q[b, h], 32), O.block_mean(k[b, h], 32))
+            differ += check_selection(gi[b, h], S, m)
+    Z, _ = O.mra_batched(q, k, v, 32, m, idx=gi)     # oracle under the GPU's (valid) selection
+    err = row_rel_err(host(out), Z)
+    assert err <= (tol or TOL[dtype]), err
+    return out, idx, err, differ
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("d", [32, 64, 128])
+@pytest.mark.parametrize("B,H,n,m", [(1, 1, 32, 0), (1, 1, 32, 1), (2, 3, 160, 2), (1, 2, 512, 0),
+                                     (1, 2, 512, 5), (1, 1, 512, 16), (1, 3, 1056, 7)])
+def test_forward_small(gpu, dtype, d, B, H, n, m):
+    _say("forward", dtype, d, B, H, n, m)
+    q, k, v = inputs.random_qkv(1000 + n + d + m, B, H, n, d, dtype, scale=1.2)
+    _, _, err, differ = _forward_and_check(gpu, q, k, v, m, dtype)
+    _say("  err", err, "rows with tie swaps", differ)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_forward_matches_stepwise_bitwise(gpu, dtype):
+    q, k, v = inputs.random_qkv(77, 2, 2, 640, 64, dtype)
+    m = 4
+    tq, tk, tv = dev(q, dtype), dev(k, dtype), dev(v, dtype)
+    idx_f = torch.empty(2, 2, 20, m, dtype=torch.int32, device="cuda")
+    out_f = gpu.attention_forward(tq, tk, tv, m, idx_out=idx_f)
+    qp, kp, vp = gpu.pool(tq, tk, tv)
+    S = gpu.coarse_scores(qp, kp)
+    idx = gpu.select(S, m)
+    cm, cs, cv = gpu.coarse_term(S, idx, vp)
+    out = gpu.block_sddmm_spmm(tq, tk, tv, idx, cm, cs, cv)
+    assert torch.equal(idx, idx_f)
+    assert torch.equal(out, out_f)
+
+
+# ------------------------------------------------------------------ invariants
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_unit_values_give_unit_output(gpu, dtype):
+    q, k, _ = inputs.random_qkv(11, 1, 2, 512, 64, dtype, scale=3.0)
+    v = np.ones_like(q)
+    for m in (0, 3, 16):
+        out = host(gpu.attention_forward(dev(q, dtype), dev(k, dtype), dev(v, dtype), m))
+        assert np.abs(out - 1).max() <= (2e-6 if dtype == "f32" else 2 ** -8)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_zero_queries(gpu, dtype):
+    _, k, v = inputs.random_qkv(12, 1, 2, 512, 64, dtype)
+    q = np.zeros_like(k)
+    m = 5
+    idx = torch.empty(1, 2, 16, m, dtype=torch.int32, device="cuda")
+    out = host(gpu.attention_forward(dev(q, dtype), dev(k, dtype), dev(v, dtype), m, idx_out=idx))
+    assert np.array_equal(host(idx), np.broadcast_to(np.arange(m), (1, 2, 16, m)))
+    ref = np.broadcast_to(v.astype(np.float64).mean(axis=2, keepdims=True), out.shape)
+    assert row_rel_err(out, ref) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_constant_blocks_exact(gpu, dtype):
+    """Q, K constant within each 32-row block: the approximation is exact for
+    every budget, so the GPU output must match exact attention."""
+    r = np.random.Generator(np.random.PCG64(13))
+    qb = r.standard_normal((1, 2, 8, 64)); kb = r.standard_normal((1, 2, 8, 64))
+    cast = inputs.round_to_bf16 if dtype == "bf16" else (lambda a: a.astype(np.float32))
+    q = cast(np.repeat(qb, 32, axis=2)); k = cast(np.repeat(kb, 32, axis=2))
+    v = cast(r.standard_normal((1, 2, 256, 64)))
+    ref = np.stack([np.stack([O.exact_attention(q[0, h], k[0, h], v[0, h]) for h in range(2)])])
+    for m in (0, 1, 3, 8):
+        out = host(gpu.attention_forward(dev(q, dtype), dev(k, dtype), dev(v, dtype), m))
+        assert row_rel_err(out, ref) <= TOL[dtype], m
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_full_budget_is_exact_attention(gpu, dtype):
+    q, k, v = inputs.random_qkv(14, 1, 2, 384, 64, dtype, scale=2.0)
+    out = host(gpu.attention_forward(dev(q, dtype), dev(k, dtype), dev(v, dtype), 12))
+    ref = np.stack([np.stack([O.exact_attention(q[0, h], k[0, h], v[0, h]) for h in range(2)])])
+    assert row_rel_err(out, ref) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_large_logits_finite(gpu, dtype):
+    """Logits of magnitude ~500: the output stays finite and within the error
+    that a float32 dot product of length d allows. A float32 logit carries an
+    absolute error up to (d+2) u c sum_t |q_t k_t|; the normalised output moves
+    by at most about twice the largest logit error (relative)."""
+    q, k, v = inputs.random_qkv(15, 1, 1, 512, 64, dtype, scale=12.0)
+    d = q.shape[-1]
+    mag = (np.abs(q[0, 0]).astype(np.float64) @ np.abs(k[0, 0]).astype(np.float64).T).max() / math.sqrt(d)
+    tol = max(TOL[dtype], 2 * (d + 2) * U * mag)
+    for m in (0, 2, 16):
+        out, _, err, _ = _forward_and_check(gpu, q, k, v, m, dtype, tol=tol)
+        assert torch.isfinite(out.float()).all()
+        _say("  large logits m", m, "err", err, "tol", tol)
+
+
+def test_empty_problems(gpu):
+    e = torch.empty(0, 2, 64, 64, device="cuda")
+    assert gpu.attention_forward(e, e, e, 1).shape == e.shape
+    e = torch.empty(1, 2, 0, 64, device="cuda")
+    assert gpu.attention_forward(e, e, e, 0).shape == e.shape
+
+
+# ------------------------------------------------------------------ workloads at full size
+@pytest.mark.parametrize("name", list(inputs.WORKLOADS))
+def test_workload_full_size(gpu, name):
+    """Each workload at its real shape, in the launch configuration the
+    benchmark times (one mra_attention_forward call). The oracle checks the
+    selection and the output of sampled block-rows one by one (all rows for
+    the single-head workload)."""
+    w = inputs.WORKLOADS[name]
+    _say("workload", name)
+    q, k, v = inputs.make_qkv(w)
+    tq, tk, tv = dev(q, w.dtype), dev(k, w.dtype), dev(v, w.dtype)
+    idx = torch.empty(w.B, w.H, w.nb, w.budget, dtype=torch.int32, device="cuda")
+    out = gpu.attention_forward(tq, tk, tv, w.budget, idx_out=idx)
+    torch.cuda.synchronize()
+    out_h = out.float().cpu().numpy()
+    gi = idx.cpu().numpy().astype(np.int64)
+    r = np.random.Generator(np.random.PCG64(w.seed))
+    if w.B * w.H * w.nb <= 64:
+        picks = [(b, h, x) for b in range(w.B) for h in range(w.H) for x in range(w.nb)]
+    else:
+        picks = {(0, 0, 0), (w.B - 1, w.H - 1, w.nb - 1)}
+        while len(picks) < 48:
+            picks.add((int(r.integers(w.B)), int(r.integers(w.H)), int(r.integers(w.nb))))
+        picks = sorted(picks)
+    by_head = {}
+    for b, h, x in picks:
+        by_head.setdefault((b, h), []).append(x)
+    worst, differ = 0.0, 0
+    for (b, h), rows in by_head.items():
+        qh, kh = q[b, h].astype(np.float64), k[b, h].astype(np.float64)
+        S = O.coarse_logits(O.block_mean(qh[np.concatenate([np.arange(x * 32, x * 32 + 32) for x in rows])], 32),
+                            O.block_mean(kh, 32))
+        differ += check_selection(gi[b, h, rows], S, w.budget)
+        Z, _, _ = O.mra_factored_rows(qh, kh, v[b, h], 32, w.budget, rows=rows, idx=gi[b, h, rows])
+        got = np.concatenate([out_h[b, h, x * 32:(x + 1) * 32] for x in rows]).astype(np.float64)
+        worst = max(worst, row_rel_err(got, Z))
+    _say(f"  {name}: max row rel err {worst:.3e} over {len(picks)} block-rows, tie swaps {differ}")
+    assert worst <= TOL[w.dtype]
