@@ -2,75 +2,62 @@
 // the exponential of the block mean of the fine logits factors into one dot
 // product of pooled rows).
 //
-// Accumulated in float64 and rounded once to float32, so the ranking that the
-// selection takes from these scores agrees with an exact computation except
-// for scores within a few float32 ulps of each other.
+// Accumulated in float64 on the matrix cores and rounded once to float32, so
+// the ranking that the selection takes from these scores agrees with an exact
+// computation except for scores within a few float32 ulps of each other.
 //
-// One workgroup computes a 64 x 64 tile of S~ for one head; the pooled rows are
-// staged through LDS in 32-column slices (padded rows: the 16 column-rows a
-// wave reads at once fall into distinct banks); every thread accumulates a
-// 4 x 4 register tile.
-#include "common.h"
+// One workgroup (4 waves) computes a 64 x 64 block of S~ for one head; the
+// pooled rows are staged through LDS in 32-column slices (Q~ converted to
+// float64 once), and wave w owns the four 16 x 16 tiles of rows 16w..16w+15.
+#include "coarse_tile.h"
 #include "kernels.h"
 
 namespace mra {
 
-constexpr int kCT = 64;    // output tile edge
+constexpr int kCT = 64;    // output block edge
 constexpr int kCK = 32;    // contraction slice
 
 __global__ __launch_bounds__(256) void coarse_kernel(const float* __restrict__ qp,
                                                       const float* __restrict__ kp,
                                                       float* __restrict__ S, int nb, int d,
                                                       double scale) {
-  __shared__ float qs[kCT][kCK + 1];
+  __shared__ double qs[kCT][kCK + 1];
   __shared__ float ks[kCT][kCK + 1];
-  // flattened grid: (head, tile row, tile column), column fastest
+  // flattened grid: (head, block row, block column), column fastest
   const int nt = (nb + kCT - 1) / kCT;
   const long long bh = blockIdx.x / (nt * nt);
   const int tile = (int)(blockIdx.x - bh * nt * nt);
   const int x0 = (tile / nt) * kCT, y0 = (tile % nt) * kCT;
   const float* qh = qp + bh * nb * d;
   const float* kh = kp + bh * nb * d;
-  const int t = threadIdx.x, ty = t / 16, tx = t % 16;
+  const int t = threadIdx.x, w = wave_uniform(t / kWave), lane = lane_id();
 
-  double acc[4][4];
+  f64x4 acc[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
+  for (int c = 0; c < 4; ++c) acc[c] = f64x4{0.0, 0.0, 0.0, 0.0};
 
   for (int k0 = 0; k0 < d; k0 += kCK) {
-    // 64 rows x 32 columns per operand = 2048 floats: 8 per thread.
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
+    for (int e = 0; e < 8; ++e) {              // 64 x 32 per operand, 8 per thread
       const int li = t + 256 * e, r = li / kCK, c = li % kCK;
-      qs[r][c] = (x0 + r < nb) ? qh[(long long)(x0 + r) * d + k0 + c] : 0.0f;
+      qs[r][c] = (x0 + r < nb) ? (double)qh[(long long)(x0 + r) * d + k0 + c] : 0.0;
       ks[r][c] = (y0 + r < nb) ? kh[(long long)(y0 + r) * d + k0 + c] : 0.0f;
     }
     __syncthreads();
-#pragma unroll 4
-    for (int c = 0; c < kCK; ++c) {
-      double a[4], b[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = (double)qs[ty + 16 * i][c];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) b[j] = (double)ks[tx + 16 * j][c];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fma(a[i], b[j], acc[i][j]);
-    }
+    for (int c = 0; c < 4; ++c)
+      coarse_tile_f64(acc[c], &qs[16 * w][0], kCK + 1, &ks[16 * c][0], kCK + 1, kCK);
     __syncthreads();
   }
   float* Sh = S + bh * nb * nb;
+  const int col = lane & 15;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int x = x0 + ty + 16 * i;
-    if (x >= nb) continue;
+  for (int c = 0; c < 4; ++c) {
+    const int y = y0 + 16 * c + col;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int y = y0 + tx + 16 * j;
-      if (y < nb) Sh[(long long)x * nb + y] = (float)(acc[i][j] * scale);
+    for (int e = 0; e < 4; ++e) {
+      const int x = x0 + 16 * w + coarse_tile_row(lane, e);
+      if (x < nb && y < nb) Sh[(long long)x * nb + y] = coarse_round(acc[c][e], scale);
     }
   }
 }

@@ -9,118 +9,132 @@
 //   M = max S~ over unselected blocks, c = sum b e^{S~ - M},
 //   L = sum b e^{S~ - M} V~_y.
 //
-// One workgroup (4 waves) owns RB consecutive block-rows of one head. Their
-// score rows sit in LDS: loaded from S~, or (fused mode) computed there from
-// the pooled rows in float64 exactly as the coarse-logit kernel does. Each
-// wave then selects for its rows: a radix search for the m-th largest
-// order-preserving 32-bit key (32 rounds of ballot + popcount), then one
-// ascending sweep that resolves ties at the threshold by index and compacts
-// the kept indices with prefix popcounts; the row's keys stay in registers
-// throughout. The score row is overwritten by the weights b e^{S~ - M} (0
-// where selected), and L = W V~ is formed for the RB rows at once on the
-// float32 matrix cores (16x16x4), so V~ is read once per workgroup rather than
-// once per row. Workgroups of one head are kept on one XCD.
-// Every mode runs the same arithmetic in the same order, so the fused forward
-// step is bit-identical to separate score, select and coarse-term calls.
-#include "common.h"
+// One workgroup (16 waves) owns 16 consecutive block-rows of one head, one
+// wave per row. Lane l of a row's wave holds the row's scores for blocks
+// y = 64j + l in registers: loaded from S~, or (fused mode) computed in
+// 64-column chunks on the float64 matrix cores with the same tile routine as
+// the coarse-logit kernel (so the same bits). The selection is a radix search
+// for the m-th largest order-preserving 32-bit key (32 rounds of ballot +
+// popcount over the registers), then one ascending sweep that resolves ties
+// at the threshold by index and compacts the kept indices with prefix
+// popcounts. Max and sum use DPP / lane-swap reductions (no LDS). L = W V~ is
+// formed chunk by chunk on the float32 matrix cores (16x16x4): the weights
+// b e^{S~ - M} (0 where selected) of the 16 rows pass through LDS one 64-block
+// chunk at a time, and the 16 waves split the dims and the blocks of a chunk
+// between them, so V~ is read once per workgroup. Workgroups of one head stay
+// on one XCD. Every mode runs the same arithmetic in the same order, so the
+// fused forward step is bit-identical to separate score, select and
+// coarse-term calls.
+#include "coarse_tile.h"
 #include "kernels.h"
 
 namespace mra {
 
 enum RowsMode { kSelectOnly = 0, kTermOnly = 1, kFused = 2 };
-constexpr int kRowsThreads = 256;
-
-// Block-rows per workgroup: 16, fewer for long rows (LDS holds RB x nb scores).
-static int rows_per_group(int nb) {
-  int rb = 16;
-  while (rb > 4 && rb * nb > 8192) rb >>= 1;
-  return rb;
-}
+constexpr int kRows = 16;                 // block-rows (waves) per workgroup
+constexpr int kChunk = 64;                // score columns per chunk
 
 typedef float f32x4v __attribute__((ext_vector_type(4)));
 
+struct RowsSmem {
+  size_t c_off, q_off, k_off, bytes;      // chunk buffer, Q~ (f64), K~ chunk / partials
+};
+
+static RowsSmem rows_smem(int d, bool fused) {
+  RowsSmem L{};
+  size_t off = 0;
+  L.c_off = off; off += (size_t)kRows * (kChunk + 1) * sizeof(float);
+  off = (off + 15) & ~size_t(15);
+  L.q_off = off; if (fused) off += (size_t)kRows * (d + 1) * sizeof(double);
+  L.k_off = off;
+  const size_t kbuf = fused ? (size_t)kChunk * (d + 1) * sizeof(float) : 0;
+  const size_t part = (size_t)4096 * sizeof(float);   // partial sums of L: (256/d) x 16 x d
+  off += kbuf > part ? kbuf : part;
+  L.bytes = off;
+  return L;
+}
+
 template <int D, int MODE, int JMAX>
-__global__ __launch_bounds__(kRowsThreads) void rows_kernel(
+__global__ __launch_bounds__(1024) void rows_kernel(
     const float* __restrict__ S, const float* __restrict__ qp, const float* __restrict__ kp,
     int32_t* __restrict__ idx_out, const int32_t* __restrict__ idx_in,
     const float* __restrict__ vp, float* __restrict__ cmax, float* __restrict__ csum,
-    float* __restrict__ cvec, int nb, int m, int rb, double scale) {
-  extern __shared__ float smem[];
-  const int nwords = (nb + 31) / 32;
-  const int ldr = nb + 1;                                          // odd row stride: no bank conflicts
-  float* srow = smem;                                              // [rb][ldr]
-  uint32_t* selbits = reinterpret_cast<uint32_t*>(smem + rb * ldr); // [rb][nwords]
+    float* __restrict__ cvec, int nb, int m, int q_off, int k_off, double scale) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  float* Cb = reinterpret_cast<float*>(smem);                      // [16][65] chunk buffer
+  constexpr int ldc = kChunk + 1;
   const int tid = threadIdx.x;
   const int w = wave_uniform(tid / kWave);
   const int lane = lane_id();
-  const int groups = (nb + rb - 1) / rb;
+  const int groups = (nb + kRows - 1) / kRows;
   const long long lwg = xcd_remap(blockIdx.x, gridDim.x);
   const long long bh = lwg / groups;
-  const int x0 = (int)(lwg - bh * groups) * rb;
-  const int rows = min(rb, nb - x0);
+  const int x0 = (int)(lwg - bh * groups) * kRows;
+  const int rows = min(kRows, nb - x0);
   const long long g0 = bh * nb + x0;                               // first global block-row
+  const bool active = w < rows;                                    // this wave owns a row
+  const long long g = g0 + w;
+  const int J = (nb + kChunk - 1) / kChunk;
 
-  // ---- phase 1: the RB score rows into LDS
+  // ---- phase 1: this row's scores into registers, s[j] for y = 64j + lane
+  float s[JMAX];
+#pragma unroll
+  for (int j = 0; j < JMAX; ++j) s[j] = 0.0f;
   if constexpr (MODE == kFused) {
-    // S~ = c Q~ K~^T in float64: 64 columns x rb rows per pass, contraction in
-    // slices of 32; same fma order as the coarse-logit kernel.
-    float* qs = reinterpret_cast<float*>(selbits + rb * nwords);  // [16][33]
-    float* ks = qs + 16 * 33;                                       // [64][33]
+    constexpr int ldq = D + 1, ldk = D + 1;
+    double* Qd = reinterpret_cast<double*>(smem + q_off);          // [16][D+1]
+    float* Kc = reinterpret_cast<float*>(smem + k_off);            // [64][D+1]
     const float* qh = qp + g0 * D;
-    const float* kh = kp + bh * nb * D;
-    const int yl = tid & 63, rg = tid >> 6;
-    for (int y0 = 0; y0 < nb; y0 += 64) {
-      double acc[4] = {0.0, 0.0, 0.0, 0.0};
-      for (int k0 = 0; k0 < D; k0 += 32) {
-        for (int li = tid; li < 16 * 32; li += kRowsThreads) {
-          const int r = li >> 5, cc = li & 31;
-          qs[r * 33 + cc] = r < rows ? qh[(long long)r * D + k0 + cc] : 0.0f;
-        }
-        for (int li = tid; li < 64 * 32; li += kRowsThreads) {
-          const int r = li >> 5, cc = li & 31;
-          ks[r * 33 + cc] = (y0 + r < nb) ? kh[(long long)(y0 + r) * D + k0 + cc] : 0.0f;
-        }
-        __syncthreads();
-#pragma unroll 4
-        for (int cc = 0; cc < 32; ++cc) {
-          const double b = (double)ks[yl * 33 + cc];
+    const float* kh = kp + bh * (long long)nb * D;
+    for (int i = tid; i < kRows * D; i += 1024) {
+      const int r = i / D, c = i % D;
+      Qd[r * ldq + c] = r < rows ? (double)qh[(long long)r * D + c] : 0.0;
+    }
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (rg + 4 * i < rb) acc[i] = fma((double)qs[(rg + 4 * i) * 33 + cc], b, acc[i]);
-        }
-        __syncthreads();
+    for (int j = 0; j < JMAX; ++j) {
+      if (j >= J) break;
+      __syncthreads();                                             // Kc, Cb free; Qd ready
+      const int y0 = kChunk * j;
+      for (int i = tid; i < kChunk * (D / 4); i += 1024) {
+        const int r = i / (D / 4), c4 = i % (D / 4);
+        f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
+        if (y0 + r < nb) v = *reinterpret_cast<const f32x4*>(kh + (long long)(y0 + r) * D + 4 * c4);
+        float* dst = Kc + r * ldk + 4 * c4;
+        dst[0] = v[0]; dst[1] = v[1]; dst[2] = v[2]; dst[3] = v[3];
       }
+      __syncthreads();
+      if (w < kChunk / 16) {                                       // waves 0..3: one 16x16 tile each
+        f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+        coarse_tile_f64(acc, Qd, ldq, Kc + 16 * w * ldk, ldk, D);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = rg + 4 * i;
-        if (r < rows && y0 + yl < nb) srow[r * ldr + y0 + yl] = (float)(acc[i] * scale);
+        for (int e = 0; e < 4; ++e)
+          Cb[coarse_tile_row(lane, e) * ldc + 16 * w + (lane & 15)] = coarse_round(acc[e], scale);
       }
+      __syncthreads();
+      if (active && y0 + lane < nb) s[j] = Cb[w * ldc + lane];
     }
   } else {
-    const float* Sg = S + g0 * nb;
-    for (int i = tid; i < rows * nb; i += kRowsThreads) srow[(i / nb) * ldr + i % nb] = Sg[i];
-  }
-  for (int i = tid; i < rb * nwords; i += kRowsThreads) selbits[i] = 0u;
-  __syncthreads();
-
-  // ---- phase 2: selection (one wave per row)
-  const int J = (nb + kWave - 1) / kWave;
-  for (int r = w; r < rows; r += 4) {
-    float* sr = srow + r * ldr;
-    uint32_t* sb = selbits + r * nwords;
-    const long long g = g0 + r;
-    if constexpr (MODE == kTermOnly) {
-      for (int i = lane; i < m; i += kWave) {
-        const int y = idx_in[g * m + i];
-        if (y >= 0 && y < nb) atomicOr(&sb[y >> 5], 1u << (y & 31));
-      }
-    } else {
-      uint32_t key[JMAX];                    // this lane's keys, y = j*64 + lane
+    if (active) {
 #pragma unroll
       for (int j = 0; j < JMAX; ++j) {
-        const int y = j * kWave + lane;
-        key[j] = (j < J && y < nb) ? ordered_key(sr[y]) : 0u;
+        const int y = kChunk * j + lane;
+        if (j < J && y < nb) s[j] = S[g * nb + y];
       }
+    }
+  }
+
+  // ---- phase 2: selection flags sel (bit j <-> y = 64j + lane)
+  uint32_t sel = 0;
+  if (active) {
+    if constexpr (MODE == kTermOnly) {
+      for (int i = 0; i < m; ++i) {
+        const int y = idx_in[g * m + i];
+        if (y >= 0 && y < nb && (y & 63) == lane) sel |= 1u << (y >> 6);
+      }
+    } else {
+      uint32_t key[JMAX];
+#pragma unroll
+      for (int j = 0; j < JMAX; ++j) key[j] = (j < J && kChunk * j + lane < nb) ? ordered_key(s[j]) : 0u;
       uint32_t T = 0;
       int need = 0;
       const bool all = (m == nb), none = (m == 0);
@@ -143,103 +157,105 @@ __global__ __launch_bounds__(kRowsThreads) void rows_kernel(
 #pragma unroll
       for (int j = 0; j < JMAX; ++j) {
         if (j >= J) break;
-        const int y = j * kWave + lane;
+        const int y = kChunk * j + lane;
         const bool valid = y < nb;
-        bool sel;
+        bool take;
         if (all) {
-          sel = valid;
+          take = valid;
         } else if (none) {
-          sel = false;
+          take = false;
         } else {
           const bool eq = valid && key[j] == T;
           const uint64_t eqm = __ballot(eq);
           const int rank = eq_seen + __popcll(eqm & lanemask_lt());
           eq_seen += __popcll(eqm);
-          sel = valid && (key[j] > T || (eq && rank < need));
+          take = valid && (key[j] > T || (eq && rank < need));
         }
-        const uint64_t smk = __ballot(sel);
-        if (sel && idx_out) idx_out[g * m + written + __popcll(smk & lanemask_lt())] = y;
-        written += __popcll(smk);
-        if (lane == 0) {
-          if (j * 2 < nwords) sb[j * 2] = (uint32_t)smk;
-          if (j * 2 + 1 < nwords) sb[j * 2 + 1] = (uint32_t)(smk >> 32);
-        }
+        const uint64_t tm = __ballot(take);
+        if (take && idx_out) idx_out[g * m + written + __popcll(tm & lanemask_lt())] = y;
+        written += __popcll(tm);
+        if (take) sel |= 1u << j;
       }
     }
-    if constexpr (MODE == kSelectOnly) continue;
-    wave_lds_sync();
-    // ---- phase 3: max and weights of the unselected blocks
+  }
+  if constexpr (MODE == kSelectOnly) return;
+
+  // ---- phase 3: max, weights (kept in s[]) and their sum over unselected blocks
+  if (active) {
     float M = -INFINITY;
-    for (int j = 0; j < J; ++j) {
-      const int y = j * kWave + lane;
-      if (y < nb && !((sb[y >> 5] >> (y & 31)) & 1u)) M = fmaxf(M, sr[y]);
-    }
+#pragma unroll
+    for (int j = 0; j < JMAX; ++j)
+      if (j < J && kChunk * j + lane < nb && !((sel >> j) & 1u)) M = fmaxf(M, s[j]);
     M = wave_max(M);
     const bool any = M != -INFINITY;
     float c = 0.0f;
-    for (int j = 0; j < J; ++j) {
-      const int y = j * kWave + lane;
-      if (y < nb) {
-        const bool unsel = !((sb[y >> 5] >> (y & 31)) & 1u);
-        const float wgt = (any && unsel) ? (float)kBlock * expf(sr[y] - M) : 0.0f;
-        sr[y] = wgt;                           // each lane rewrites only its own entries
-        c += wgt;
-      }
+#pragma unroll
+    for (int j = 0; j < JMAX; ++j) {
+      const int y = kChunk * j + lane;
+      const bool unsel = j < J && y < nb && !((sel >> j) & 1u);
+      s[j] = (any && unsel) ? (float)kBlock * expf(s[j] - M) : 0.0f;
+      c += s[j];
     }
     c = wave_sum(c);
     if (lane == 0) {
       cmax[g] = M;
       csum[g] = c;
     }
-  }
-  if constexpr (MODE == kSelectOnly) return;
-  __syncthreads();
-
-  // ---- phase 4: L = W V~ for the rows of this group on the float32 matrix
-  // cores: v_mfma_f32_16x16x4_f32 with A = W (16 rows x 4 blocks, rows past
-  // `rows` are zero), B = V~ (4 blocks x 16 dims); wave w owns the dim tiles
-  // w, w+4, ...; blocks in ascending order, four per instruction.
-  {
-    constexpr int kNT16 = D / 16;
-    const int ar = lane & 15, ak = lane >> 4;          // A: row, k;  B: dim, k
-    const float* vh = vp + bh * (long long)nb * D;
-    for (int nt = w; nt < kNT16; nt += 4) {
-      f32x4v acc = {0.0f, 0.0f, 0.0f, 0.0f};
-      const int dim = 16 * nt + ar;
-#pragma unroll 4
-      for (int y0 = 0; y0 < nb; y0 += 4) {
-        const int y = y0 + ak;
-        const float a = (ar < rows && y < nb) ? srow[ar * ldr + y] : 0.0f;
-        const float b = y < nb ? vh[(long long)y * D + dim] : 0.0f;
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
-      }
-      // D layout: lane holds rows 4*(lane/16) + e of column lane%16
+  } else {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int r = 4 * ak + e;
-        if (r < rows) cvec[(g0 + r) * D + dim] = acc[e];
-      }
+    for (int j = 0; j < JMAX; ++j) s[j] = 0.0f;
+  }
+
+  // ---- phase 4: L = W V~ on the float32 matrix cores (v_mfma_f32_16x16x4_f32,
+  // A = W: 16 rows x 4 blocks, B = V~: 4 blocks x 16 dims). Wave w takes dim
+  // tile nt = w % (D/16) and, inside every chunk, the block range of quarter
+  // kq = w / (D/16); the per-wave partial sums are added in kq order at the end.
+  constexpr int NTD = D / 16, KQ = kRows / NTD, YPW = kChunk / KQ;
+  const int nt = w % NTD, kq = w / NTD;
+  const int ar = lane & 15, ak = lane >> 4;
+  const float* vh = vp + bh * (long long)nb * D;
+  f32x4v acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int j = 0; j < JMAX; ++j) {
+    if (j >= J) break;
+    __syncthreads();                                               // previous chunk consumed
+    Cb[w * ldc + lane] = s[j];                                     // zero for inactive rows
+    __syncthreads();
+    const int yb = kChunk * j + kq * YPW;
+#pragma unroll
+    for (int t = 0; t < YPW; t += 4) {
+      const int y = yb + t + ak;
+      const float a = Cb[ar * ldc + kq * YPW + t + ak];
+      const float b = y < nb ? vh[(long long)y * D + 16 * nt + ar] : 0.0f;
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
     }
   }
-}
-
-static size_t rows_smem(int nb, int rb, bool fused) {
-  size_t s = (size_t)rb * (nb + 1) * sizeof(float) + (size_t)rb * ((nb + 31) / 32) * sizeof(uint32_t);
-  if (fused) s += (16 * 33 + 64 * 33) * sizeof(float);
-  return s;
+  // partial sums: lane holds rows 4*ak + e of dim 16*nt + ar
+  float* part = reinterpret_cast<float*>(smem + k_off);            // [KQ][16][D]
+  __syncthreads();
+#pragma unroll
+  for (int e = 0; e < 4; ++e) part[(kq * kRows + 4 * ak + e) * D + 16 * nt + ar] = acc[e];
+  __syncthreads();
+  for (int i = tid; i < rows * D; i += 1024) {
+    const int r = i / D, dm = i % D;
+    float sum = part[r * D + dm];
+#pragma unroll
+    for (int q = 1; q < KQ; ++q) sum += part[(q * kRows + r) * D + dm];
+    cvec[(g0 + r) * D + dm] = sum;
+  }
 }
 
 template <int MODE, int JMAX>
 static void launch_rows_j(const float* S, const float* qp, const float* kp, int32_t* idx_out,
                           const int32_t* idx_in, const float* vp, float* cmax, float* csum,
                           float* cvec, long long bh, int nb, int d, int m, hipStream_t stream) {
-  const int rb = rows_per_group(nb);
-  const long long groups = (nb + rb - 1) / rb;
+  const long long groups = (nb + kRows - 1) / kRows;
   const unsigned blocks = (unsigned)(bh * groups);
-  const size_t smem = rows_smem(nb, rb, MODE == kFused);
+  const RowsSmem L = rows_smem(d, MODE == kFused);
   const double scale = 1.0 / sqrt((double)d);
-#define MRA_ROWS_LAUNCH(DD) \
-  rows_kernel<DD, MODE, JMAX><<<blocks, kRowsThreads, smem, stream>>>(S, qp, kp, idx_out, idx_in, vp, cmax, csum, cvec, nb, m, rb, scale)
+#define MRA_ROWS_LAUNCH(DD)                                                                     \
+  rows_kernel<DD, MODE, JMAX><<<blocks, 64 * kRows, L.bytes, stream>>>(                       \
+      S, qp, kp, idx_out, idx_in, vp, cmax, csum, cvec, nb, m, (int)L.q_off, (int)L.k_off, scale)
   switch (d) {
     case 32: MRA_ROWS_LAUNCH(32); break;
     case 64: MRA_ROWS_LAUNCH(64); break;
@@ -248,7 +264,7 @@ static void launch_rows_j(const float* S, const float* qp, const float* kp, int3
 #undef MRA_ROWS_LAUNCH
 }
 
-// Keys per lane: up to 2 (nb <= 128), 8 (nb <= 512) or 32 (nb <= 2048).
+// Score registers per lane: up to 2 (nb <= 128), 8 (nb <= 512) or 32 (nb <= 2048).
 template <int MODE>
 static hipError_t launch_rows(const float* S, const float* qp, const float* kp, int32_t* idx_out,
                               const int32_t* idx_in, const float* vp, float* cmax, float* csum,

@@ -57,7 +57,7 @@ constexpr float kLazy = 8.0f;
 template <int NT>
 __device__ __forceinline__ void rescale_if_grown(float mx, float sl2, float& mrun, float& lrun,
                                                  f32x16 (&o)[NT]) {
-  mx = __builtin_elementwise_maximum(mx, __shfl_xor(mx, 32, kWave));
+  mx = halves_max(mx);
   const float cand = mx * sl2;
   if (__ballot(cand > mrun + kLazy)) {             // wave-uniform, rarely taken
     // keeps the compiler from turning this branch into an unconditional
@@ -308,7 +308,7 @@ __global__ __launch_bounds__((TileCfg<DT, D>::kWaves * kWave)) void tile_kernel(
   }
 
   // ---- merge with the low-resolution term and normalise
-  const float ltot = lrun + __shfl_xor(lrun, 32, kWave);
+  const float ltot = halves_sum(lrun);
   float af = 1.0f, bc = 0.0f, den = ltot;
   if constexpr (COARSE) {
     const float Mx = cmax[g] * kLog2e;
