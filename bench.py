@@ -11,8 +11,10 @@ oracle timed on the host as a reported CPU baseline.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -42,6 +44,34 @@ def pool_bytes(w) -> float:
     written, and K and V written once more in packed order."""
     e = 2 if w.dtype == "bf16" else 4
     return 5.0 * w.B * w.H * w.n * w.d * e + 3.0 * w.B * w.H * w.nb * w.d * 4
+
+
+TILE_SOURCES = ["paper_2207_10284_amd/csrc/tile.hip", "paper_2207_10284_amd/csrc/common.h",
+                "paper_2207_10284_amd/csrc/kernels.h"]
+PROFILE = "profiles/tile_kernel_base-4096.md"
+
+
+def tile_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in TILE_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def recorded_traffic():
+    """HBM bytes per tile-kernel launch from the committed counter summary
+    (FETCH_SIZE + WRITE_SIZE, calibrated), or None when the kernel source has
+    changed since those counters were taken."""
+    try:
+        text = open(os.path.join(ROOT, PROFILE)).read()
+    except OSError:
+        return None
+    h = re.search(r"tile_source_sha256:\s*([0-9a-f]{64})", text)
+    t = re.search(r"tile_traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not h or not t or h.group(1) != tile_source_hash():
+        return None
+    return float(t.group(1))
 
 
 def time_launches(fn, iters: int, warmup: int = 3) -> float:
@@ -155,7 +185,8 @@ def main():
                    "budget": w.budget, "inputs": w.kind},
         "roofline": {"bound": "mfma", "kernel": "tile_kernel (block-sparse SDDMM + SpMM + merge)",
                      "achieved": tflops, "peak": peak, "unit": "TFLOP/s", "frac": tflops / peak,
-                     "traffic": None, "launch_us": tile_ms * 1e3,
+                     "traffic": recorded_traffic(), "traffic_unit": "bytes per launch",
+                     "launch_us": tile_ms * 1e3,
                      "flops_per_launch": tile_flops(w)},
         "stages_us": {"pool_and_pack": pool_ms * 1e3, "tile": tile_ms * 1e3,
                       "select_and_coarse_term_fused": (ms - pool_ms - tile_ms) * 1e3,
