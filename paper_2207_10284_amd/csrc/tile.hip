@@ -3,11 +3,11 @@
 // scale 1; Sec. 3.1 row normalisation D^).
 //
 // One wave owns one block-row x (32 queries). For every selected column block
-// y it computes the 32x32 tile S = c Q_x K_y^T on the matrix cores
-// (block-sparse SDDMM), folds it into a running max / row sum (online
-// softmax), and accumulates P V_y (block-sparse SpMM). At the end the result
-// is merged with the block-row's low-resolution term (M_x, c_x, L_x) and
-// normalised.
+// y, in ascending order, it computes the 32x32 tile S = c Q_x K_y^T on the
+// matrix cores (block-sparse SDDMM), folds it into a running max / row sum
+// (online softmax), and accumulates P V_y (block-sparse SpMM). At the end the
+// result is merged with the block-row's low-resolution term (M_x, c_x, L_x)
+// and normalised.
 //
 // Matrix-core layout (v_mfma_f32_32x32x16_bf16; 32x32x2_f32 for float32):
 //  * S is formed transposed, S^T = K_y Q_x^T, so lane l holds query l%32 and
@@ -16,18 +16,22 @@
 //    permutation of the key index, so P never moves between lanes; only the
 //    row max crosses the two half-waves.
 //  * The contraction index over d is permuted too: lane half h = l/32 takes
-//    the contiguous half [h*d/2, (h+1)*d/2) of each Q and K row, so every lane
-//    streams d bytes (bf16) of one row with 16-byte loads.
-//  * With the packed copies of K and V written by the pooling pass, every
-//    operand load (K_y, and V_y^T, the A operand of the second product) is
-//    one 16-byte chunk per lane, 1 KB contiguous per wave: no LDS, no
-//    shuffles. For raw K/V, K_y rows are read directly and V_y goes through a
-//    wave-private LDS tile stored transposed with the key permutation applied.
-// With packed K/V the next tile's loads are in flight while the current one is
-// computed. O is rescaled only when some query's running max grew a lot.
-// Workgroups of 4 waves take 4 consecutive block-rows; the workgroup order is
-// remapped so each XCD processes a contiguous range of heads and keeps their
-// K/V tiles in its L2.
+//    the contiguous half [h*d/2, (h+1)*d/2) of each Q and K row.
+//  * In the packed copies of K and V written by the pooling pass (layout in
+//    kernels.h) every operand of a tile (K_y, and V_y^T, the A operand of the
+//    second product) is one 16-byte chunk per lane, 1 KB contiguous per wave.
+//
+// Two kernels share that per-row arithmetic (struct TileRow), so their results
+// are bit-identical:
+//  * tile_stream_kernel (packed K/V, tiles up to 8 KB): the next selected tile
+//    is copied HBM/L2 -> a wave-private LDS slot with direct-to-LDS loads
+//    while the current one is computed from registers.
+//  * tile_kernel: raw K/V (K rows read directly, V_y through a wave-private
+//    LDS tile stored transposed with the key permutation applied), and packed
+//    K/V with larger tiles (next tile's loads in flight in registers).
+// The running max moves only when the weights would grow too large. Workgroup order
+// is remapped so each XCD processes a contiguous range of heads and keeps
+// their K/V tiles in its L2.
 #include "common.h"
 #include "kernels.h"
 
@@ -43,36 +47,21 @@ struct TileCfg {
   // 16-byte V operand chunks per lane per tile
   static constexpr int kVChunks = DT == BF16 ? 2 * kNT : 4 * kNT;
   static constexpr int kKChunks = DT == BF16 ? D / 16 : D / 8;  // 16-byte K chunks per lane
+  static constexpr int kChunks = kKChunks + kVChunks;           // 1 KB chunks per K/V tile
   using elem = typename std::conditional<DT == BF16, uint16_t, float>::type;
 };
 
-// Running max of the scores (log2 units) for the online softmax. The max is
-// refreshed, and O and the row sums rescaled, only when some query's tile max
-// exceeds the current one by more than kLazy (log2 units): in between, the
-// weights exp2(s - mrun) stay below 2^kLazy, far inside float32 and bfloat16
-// range, and the final normalisation uses the same mrun, so the result is the
-// same softmax. Lanes l and l^32 share a query.
-constexpr float kLazy = 8.0f;
-
-template <int NT>
-__device__ __forceinline__ void rescale_if_grown(float mx, float sl2, float& mrun, float& lrun,
-                                                 f32x16 (&o)[NT]) {
-  mx = halves_max(mx);
-  const float cand = mx * sl2;
-  if (__ballot(cand > mrun + kLazy)) {             // wave-uniform, rarely taken
-    // keeps the compiler from turning this branch into an unconditional
-    // multiply of every accumulator by a selected factor
-    asm volatile("; mra rescale" ::: "memory");
-    const float mnew = __builtin_elementwise_maximum(mrun, cand);
-    const float alpha = __builtin_amdgcn_exp2f(mrun - mnew);   // 0 at the first tile
-    lrun *= alpha;
-#pragma unroll
-    for (int t = 0; t < NT; ++t)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
-    mrun = mnew;
-  }
-}
+// Reference point of the online softmax (log2 units). The weights of a tile
+// are exp2(s * c * log2(e) - mrun) for the row's reference mrun, which need
+// not be the running max: any reference works as long as weights and
+// accumulators stay finite, because the final normalisation uses the same
+// reference. mrun is set to the exact max of the row's first tile; later tiles
+// only check that their weights sum to at most 2^kWeightCap per lane (far
+// inside float32 and bfloat16 range, 2^128, even summed over 65536 keys). If
+// a tile exceeds it, the row is computed again with the exact max over all its
+// tiles as the reference, where no weight exceeds 1. The loop body thus has no
+// 16-way max, no cross-lane exchange and no branch that rescales O.
+constexpr float kWeightCap = 0x1p64f;
 
 __device__ __forceinline__ float tile_max(const f32x16& s) {
   float a = s[0];
@@ -81,6 +70,194 @@ __device__ __forceinline__ float tile_max(const f32x16& s) {
   return a;
 }
 
+// Accumulator state and arithmetic of one block-row (32 queries) in one wave.
+template <int DT, int D, bool COARSE>
+struct TileRow {
+  using Cfg = TileCfg<DT, D>;
+  using elem = typename Cfg::elem;
+  static constexpr int NT = Cfg::kNT, KC = Cfg::kKChunks;
+  f32x16 o[NT];
+  float mrun, lrun, sl2;
+  bool first;                                      // no reference yet
+  u32x4 qf[KC];
+
+  // Q_x as the B operand: each lane reads d/2 contiguous elements of one row.
+  __device__ __forceinline__ void init(const elem* Q, int x, float scale_log2) {
+    const int lane = lane_id(), jq = lane & 31, h = lane >> 5;
+    const u32x4* qrow = reinterpret_cast<const u32x4*>(Q + (long long)(x * 32 + jq) * D + (D / 2) * h);
+#pragma unroll
+    for (int s = 0; s < KC; ++s) qf[s] = qrow[s];
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[t][r] = 0.0f;
+    mrun = -INFINITY;                              // no fine block: no weight
+    lrun = 0.0f;
+    sl2 = scale_log2;
+    first = true;
+  }
+
+  // S^T = K_y Q_x^T
+  __device__ __forceinline__ f32x16 scores(const u32x4 (&kf)[KC]) const {
+    f32x16 s;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s[r] = 0.0f;
+    if constexpr (DT == BF16) {
+#pragma unroll
+      for (int k = 0; k < KC; ++k)
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[k]),
+                                                    __builtin_bit_cast(bf16x8, qf[k]), s, 0, 0, 0);
+    } else {
+#pragma unroll
+      for (int k = 0; k < KC; ++k)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          s = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(kf[k][e]), __uint_as_float(qf[k][e]), s, 0, 0, 0);
+    }
+    return s;
+  }
+
+  // Max of this tile's scores for this lane's query, in log2 units (lanes l
+  // and l^32 share a query).
+  __device__ __forceinline__ float tile_ref(const f32x16& s) const {
+    return halves_max(tile_max(s)) * sl2;
+  }
+
+  // Start the row again with a fixed reference (no weight above 1).
+  __device__ __forceinline__ void restart(float ref) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[t][r] = 0.0f;
+    lrun = 0.0f;
+    mrun = ref;
+    first = false;
+  }
+
+  // bfloat16 weights of one tile into pk (two per register, the operand
+  // order of the second product); returns their sum in float32.
+  __device__ __forceinline__ float weights_bf16(const f32x16& s, uint32_t (&pk)[8]) const {
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+    float t = 0.0f;
+#pragma unroll
+    for (int rr = 0; rr < 8; ++rr) {
+      const float p0 = __builtin_amdgcn_exp2f(fmaf(s[2 * rr], sl2, -mrun));
+      const float p1 = __builtin_amdgcn_exp2f(fmaf(s[2 * rr + 1], sl2, -mrun));
+      bf16x2 pb;
+      pb[0] = (__bf16)p0;
+      pb[1] = (__bf16)p1;
+      t = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, t, false);   // sum of the rounded weights
+      pk[rr] = __builtin_bit_cast(uint32_t, pb);
+    }
+    return t;
+  }
+
+  __device__ __forceinline__ float weights_f32(const f32x16& s, float (&p)[16]) const {
+    float t = 0.0f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      p[r] = __builtin_amdgcn_exp2f(fmaf(s[r], sl2, -mrun));
+      t += p[r];
+    }
+    return t;
+  }
+
+  // Softmax weights of one tile and O^T += V_y^T P^T. `va(c)` yields the
+  // 16-byte A-operand chunk c of V_y^T for this lane. With use == false (a
+  // block id outside [0, nb)) the weights are zero: the matrix-core
+  // instructions still run, consuming the tile's operands on every path,
+  // which keeps the compiler's load-counter waits tight. Returns false if
+  // some weight of the row may have exceeded the cap (the caller then restarts
+  // the row); with check == false the caller guarantees it cannot.
+  template <class VA>
+  __device__ __forceinline__ bool accumulate(const f32x16& s, bool use, bool check, VA va) {
+    if (first && use) {                              // wave-uniform: the row's first tile
+      mrun = tile_ref(s);
+      first = false;
+    }
+    float t;
+    if constexpr (DT == BF16) {
+      uint32_t pk[8];
+      t = weights_bf16(s, pk);
+      if (!use) {
+#pragma unroll
+        for (int rr = 0; rr < 8; ++rr) pk[rr] = 0u;
+        t = 0.0f;
+      }
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const u32x4 pw = {pk[4 * u], pk[4 * u + 1], pk[4 * u + 2], pk[4 * u + 3]};
+        const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt)
+          o[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, va(u * NT + tt)), pb, o[tt], 0, 0, 0);
+      }
+    } else {
+      float p[16];
+      t = weights_f32(s, p);
+      if (!use) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) p[r] = 0.0f;
+        t = 0.0f;
+      }
+#pragma unroll
+      for (int tt = 0; tt < NT; ++tt)
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          const u32x4 v4 = va(tt * 4 + a);
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            o[tt] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(v4[e]), p[4 * a + e], o[tt], 0, 0, 0);
+        }
+    }
+    lrun += t;
+    return !check || __ballot(!(t <= kWeightCap)) == 0;
+  }
+
+  // Merge with the low-resolution term, normalise and store the 32 x d block.
+  __device__ __forceinline__ void finish(elem* Out, int x, long long g, const float* cmax,
+                                         const float* csum, const float* cvec) {
+    const int lane = lane_id(), jq = lane & 31, h = lane >> 5;
+    const float ltot = halves_sum(lrun);
+    float af = 1.0f, bc = 0.0f, den = ltot;
+    if constexpr (COARSE) {
+      const float Mx = cmax[g] * kLog2e;
+      const float Mt = fmaxf(mrun, Mx);
+      af = exp2f(mrun - Mt);
+      bc = exp2f(Mx - Mt);
+      den = ltot * af + csum[g] * bc;
+    }
+    const float inv = 1.0f / den;
+    const float ao = af * inv, bv = bc * inv;       // z = o * ao + cvec * bv
+    elem* orow = Out + (long long)(x * 32 + jq) * D;
+    const float* cv = COARSE ? cvec + g * D : nullptr;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+#pragma unroll
+      for (int rg = 0; rg < 4; ++rg) {
+        const int d0 = 32 * t + 8 * rg + 4 * h;
+        float z[4];
+        f32x4 c4 = {0.0f, 0.0f, 0.0f, 0.0f};
+        if constexpr (COARSE) c4 = *reinterpret_cast<const f32x4*>(cv + d0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) z[e] = COARSE ? fmaf(o[t][4 * rg + e], ao, c4[e] * bv) : o[t][4 * rg + e] * ao;
+        if constexpr (DT == BF16) {
+          bf16x2 lo, hi;
+          lo[0] = (__bf16)z[0]; lo[1] = (__bf16)z[1];
+          hi[0] = (__bf16)z[2]; hi[1] = (__bf16)z[3];
+          const u32x2 pr = {__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
+          *reinterpret_cast<u32x2*>(orow + d0) = pr;
+        } else {
+          const f32x4 st = {z[0], z[1], z[2], z[3]};
+          *reinterpret_cast<f32x4*>(orow + d0) = st;
+        }
+      }
+    }
+  }
+};
+
+// ---------------------------------------------------------------------------
+// One wave per block-row.
 template <int DT, int D, bool COARSE, bool PACKED>
 __global__ __launch_bounds__((TileCfg<DT, D>::kWaves * kWave)) void tile_kernel(
     const void* __restrict__ qv, const void* __restrict__ kv, const void* __restrict__ vv,
@@ -102,10 +279,7 @@ __global__ __launch_bounds__((TileCfg<DT, D>::kWaves * kWave)) void tile_kernel(
   const long long bh = g / nb;
   const int x = (int)(g - bh * nb);
   const long long hoff = bh * (long long)n * D;
-  const elem* Q = reinterpret_cast<const elem*>(qv) + hoff;
   const elem* K = reinterpret_cast<const elem*>(kv) + hoff;
-  elem* Out = reinterpret_cast<elem*>(outv) + hoff;
-  const float sl2 = scale_log2;
   // The row's selection, staged once in LDS: reading block ids from LDS keeps
   // them off the vector-memory counter, so prefetched K/V loads stay in flight.
   extern __shared__ int32_t sidx_all[];
@@ -113,142 +287,71 @@ __global__ __launch_bounds__((TileCfg<DT, D>::kWaves * kWave)) void tile_kernel(
   for (int i = lane; i < m; i += kWave) myidx[i] = idx[g * m + i];
   wave_lds_sync();
 
-  f32x16 o[NT];
-#pragma unroll
-  for (int t = 0; t < NT; ++t)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) o[t][r] = 0.0f;
-  float mrun = -INFINITY, lrun = 0.0f;
-
-  // Q_x as the B operand, K_y as the A operand: lane reads d/2 contiguous
-  // elements of one row, 16 bytes at a time.
-  u32x4 qf[KC];
-  {
-    const u32x4* qrow = reinterpret_cast<const u32x4*>(Q + (long long)(x * 32 + jq) * D + (D / 2) * h);
-#pragma unroll
-    for (int s = 0; s < KC; ++s) qf[s] = qrow[s];
-  }
-  auto load_k = [&](int y, u32x4 (&kf)[KC]) {
-    const u32x4* krow = reinterpret_cast<const u32x4*>(K + (long long)(y * 32 + jq) * D + (D / 2) * h);
-#pragma unroll
-    for (int s = 0; s < KC; ++s) kf[s] = krow[s];
-  };
-  // packed K/V (see kernels.h): every operand load is 1 KB contiguous per wave
-  auto load_kpacked = [&](int y, u32x4 (&kf)[KC]) {
-    const u32x4* kt = reinterpret_cast<const u32x4*>(kv) + ((bh * nb + y) * KC) * 64 + lane;
-#pragma unroll
-    for (int c = 0; c < KC; ++c) kf[c] = kt[c * 64];
-  };
-  auto load_vpacked = [&](int y, u32x4 (&vf)[VC]) {
-    const u32x4* vt = reinterpret_cast<const u32x4*>(vv) + ((bh * nb + y) * VC) * 64 + lane;
-#pragma unroll
-    for (int c = 0; c < VC; ++c) vf[c] = vt[c * 64];
-  };
-  // S^T = K_y Q_x^T
-  auto scores = [&](const u32x4 (&kf)[KC]) {
-    f32x16 s;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) s[r] = 0.0f;
-    if constexpr (DT == BF16) {
-#pragma unroll
-      for (int k = 0; k < KC; ++k)
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[k]),
-                                                    __builtin_bit_cast(bf16x8, qf[k]), s, 0, 0, 0);
-    } else {
-#pragma unroll
-      for (int k = 0; k < KC; ++k)
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          s = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(kf[k][e]), __uint_as_float(qf[k][e]), s, 0, 0, 0);
-    }
-    return s;
-  };
-  // Softmax weights of one tile and O^T += V_y^T P^T. `va(c)` yields the
-  // 16-byte A-operand chunk c of V_y^T for this lane. The matrix-core
-  // instructions always run (they consume the tile's loads on every path, which
-  // keeps the compiler's load-counter waits tight); a skipped block only
-  // zeroes P, inside a branch that holds no memory operations.
-  auto accumulate = [&](const f32x16& s, bool use, auto va) {
-    if constexpr (DT == BF16) {
-      uint32_t pk[8];
-#pragma unroll
-      for (int rr = 0; rr < 8; ++rr) pk[rr] = 0u;
-      if (use) {
-        rescale_if_grown<NT>(tile_max(s), sl2, mrun, lrun, o);
-        const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-#pragma unroll
-        for (int rr = 0; rr < 8; ++rr) {
-          const float p0 = __builtin_amdgcn_exp2f(fmaf(s[2 * rr], sl2, -mrun));
-          const float p1 = __builtin_amdgcn_exp2f(fmaf(s[2 * rr + 1], sl2, -mrun));
-          bf16x2 pb;
-          pb[0] = (__bf16)p0;
-          pb[1] = (__bf16)p1;
-          lrun = __builtin_amdgcn_fdot2_f32_bf16(pb, ones, lrun, false);   // sum of the rounded P
-          pk[rr] = __builtin_bit_cast(uint32_t, pb);
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const u32x4 pw = {pk[4 * u], pk[4 * u + 1], pk[4 * u + 2], pk[4 * u + 3]};
-        const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
-#pragma unroll
-        for (int t = 0; t < NT; ++t)
-          o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, va(u * NT + t)), pb, o[t], 0, 0, 0);
-      }
-    } else {
-      float p[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) p[r] = 0.0f;
-      if (use) {
-        rescale_if_grown<NT>(tile_max(s), sl2, mrun, lrun, o);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          p[r] = __builtin_amdgcn_exp2f(fmaf(s[r], sl2, -mrun));
-          lrun += p[r];
-        }
-      }
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-#pragma unroll
-        for (int a = 0; a < 4; ++a) {
-          const u32x4 v4 = va(t * 4 + a);
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            o[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(v4[e]), p[4 * a + e], o[t], 0, 0, 0);
-        }
-    }
-  };
+  TileRow<DT, D, COARSE> row;
+  row.init(reinterpret_cast<const elem*>(qv) + hoff, x, scale_log2);
   auto clampy = [&](int y) { return (y < 0 || y >= nb) ? 0 : y; };
+  auto valid = [&](int y) { return y >= 0 && y < nb; };
 
   if constexpr (PACKED) {
+    auto load_kpacked = [&](int y, u32x4 (&kf)[KC]) {
+      const u32x4* kt = reinterpret_cast<const u32x4*>(kv) + ((bh * nb + y) * KC) * 64 + lane;
+#pragma unroll
+      for (int c = 0; c < KC; ++c) kf[c] = kt[c * 64];
+    };
+    auto load_vpacked = [&](int y, u32x4 (&vf)[VC]) {
+      const u32x4* vt = reinterpret_cast<const u32x4*>(vv) + ((bh * nb + y) * VC) * 64 + lane;
+#pragma unroll
+      for (int c = 0; c < VC; ++c) vf[c] = vt[c * 64];
+    };
     // Two register buffers: tile i+1 loads while tile i is computed. Loads
     // are issued unconditionally (past the last tile they re-read the last
     // tile, a cache hit) so every path leaves the same loads in flight.
-    u32x4 kA[KC], vA[VC], kB[KC], vB[VC];
-    auto valid = [&](int y) { return y >= 0 && y < nb; };
-    if (m > 0) {
-      const int y0 = clampy(wave_uniform(myidx[0]));
-      load_kpacked(y0, kA);
-      load_vpacked(y0, vA);
-    }
-    for (int i = 0; i < m; i += 2) {
-      const int ya = wave_uniform(myidx[i]);
-      const int yb = wave_uniform(myidx[min(i + 1, m - 1)]);
-      load_kpacked(clampy(yb), kB);
-      load_vpacked(clampy(yb), vB);
-      accumulate(scores(kA), valid(ya), [&](int c) { return vA[c]; });
-      if (i + 1 >= m) break;
-      const int yc = clampy(wave_uniform(myidx[min(i + 2, m - 1)]));
-      load_kpacked(yc, kA);
-      load_vpacked(yc, vA);
-      accumulate(scores(kB), valid(yb), [&](int c) { return vB[c]; });
+    auto pass = [&](bool check) -> bool {
+      u32x4 kA[KC], vA[VC], kB[KC], vB[VC];
+      if (m > 0) {
+        const int y0 = clampy(wave_uniform(myidx[0]));
+        load_kpacked(y0, kA);
+        load_vpacked(y0, vA);
+      }
+      for (int i = 0; i < m; i += 2) {
+        const int ya = wave_uniform(myidx[i]);
+        const int yb = wave_uniform(myidx[min(i + 1, m - 1)]);
+        load_kpacked(clampy(yb), kB);
+        load_vpacked(clampy(yb), vB);
+        if (!row.accumulate(row.scores(kA), valid(ya), check, [&](int c) { return vA[c]; })) return false;
+        if (i + 1 >= m) break;
+        const int yc = clampy(wave_uniform(myidx[min(i + 2, m - 1)]));
+        load_kpacked(yc, kA);
+        load_vpacked(yc, vA);
+        if (!row.accumulate(row.scores(kB), valid(yb), check, [&](int c) { return vB[c]; })) return false;
+      }
+      return true;
+    };
+    if (!pass(true)) {
+      // some weight grew too large: again, relative to the row's exact max
+      float mx = -INFINITY;
+      for (int i = 0; i < m; ++i) {
+        const int yy = wave_uniform(myidx[i]);
+        if (!valid(yy)) continue;
+        u32x4 kf[KC];
+        load_kpacked(yy, kf);
+        mx = __builtin_elementwise_maximum(mx, row.tile_ref(row.scores(kf)));
+      }
+      row.restart(mx);
+      pass(false);
     }
   } else {
     elem* vt = vt_all[w];
     const elem* V = reinterpret_cast<const elem*>(vv) + hoff;
+    auto load_k = [&](int y, u32x4 (&kc)[KC]) {
+      const u32x4* krow = reinterpret_cast<const u32x4*>(K + (long long)(y * 32 + jq) * D + (D / 2) * h);
+#pragma unroll
+      for (int s = 0; s < KC; ++s) kc[s] = krow[s];
+    };
+    auto pass = [&](bool check) -> bool {
     for (int i = 0; i < m; ++i) {
       const int y = wave_uniform(myidx[i]);
-      if (y < 0 || y >= nb) continue;
+      if (!valid(y)) continue;
       u32x4 kc[KC];
       load_k(y, kc);
       // V_y -> LDS transposed, keys in the operand order of the packed layout
@@ -290,60 +393,154 @@ __global__ __launch_bounds__((TileCfg<DT, D>::kWaves * kWave)) void tile_kernel(
           }
         }
       }
-      const f32x16 s = scores(kc);
+      const f32x16 s = row.scores(kc);
       wave_lds_sync();
+      bool ok;
       if constexpr (DT == BF16) {
-        accumulate(s, true, [&](int c) {
+        ok = row.accumulate(s, true, check, [&](int c) {
           const int u = c / NT, t = c % NT;
           return *reinterpret_cast<const u32x4*>(vt + (32 * t + jq) * PITCH + 16 * u + 8 * h);
         });
       } else {
-        accumulate(s, true, [&](int c) {
+        ok = row.accumulate(s, true, check, [&](int c) {
           const int t = c / 4, a = c % 4;
           return *reinterpret_cast<const u32x4*>(vt + (32 * t + jq) * PITCH + 16 * h + 4 * a);
         });
       }
       wave_lds_sync();                               // reads done before the next overwrite
+      if (!ok) return false;
     }
-  }
-
-  // ---- merge with the low-resolution term and normalise
-  const float ltot = halves_sum(lrun);
-  float af = 1.0f, bc = 0.0f, den = ltot;
-  if constexpr (COARSE) {
-    const float Mx = cmax[g] * kLog2e;
-    const float Mt = fmaxf(mrun, Mx);
-    af = exp2f(mrun - Mt);
-    bc = exp2f(Mx - Mt);
-    den = ltot * af + csum[g] * bc;
-  }
-  const float inv = 1.0f / den;
-  elem* orow = Out + (long long)(x * 32 + jq) * D;
-  const float* cv = COARSE ? cvec + g * D : nullptr;
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-#pragma unroll
-    for (int rg = 0; rg < 4; ++rg) {
-      const int d0 = 32 * t + 8 * rg + 4 * h;
-      float z[4];
-      f32x4 c4 = {0.0f, 0.0f, 0.0f, 0.0f};
-      if constexpr (COARSE) c4 = *reinterpret_cast<const f32x4*>(cv + d0);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) z[e] = (o[t][4 * rg + e] * af + c4[e] * bc) * inv;
-      if constexpr (DT == BF16) {
-        bf16x2 lo, hi;
-        lo[0] = (__bf16)z[0]; lo[1] = (__bf16)z[1];
-        hi[0] = (__bf16)z[2]; hi[1] = (__bf16)z[3];
-        const u32x2 pr = {__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
-        *reinterpret_cast<u32x2*>(orow + d0) = pr;
-      } else {
-        const f32x4 st = {z[0], z[1], z[2], z[3]};
-        *reinterpret_cast<f32x4*>(orow + d0) = st;
+    return true;
+    };
+    if (!pass(true)) {
+      float mx = -INFINITY;
+      for (int i = 0; i < m; ++i) {
+        const int yy = wave_uniform(myidx[i]);
+        if (!valid(yy)) continue;
+        u32x4 kf[KC];
+        load_k(yy, kf);
+        mx = __builtin_elementwise_maximum(mx, row.tile_ref(row.scores(kf)));
       }
+      row.restart(mx);
+      pass(false);
     }
+  }
+  row.finish(reinterpret_cast<elem*>(outv) + hoff, x, g, cmax, csum, cvec);
+}
+
+// C consecutive 1 KB chunks HBM/L2 -> LDS, 16 bytes per lane each; chunk c is
+// addressed through the load's immediate offset, which moves the global and
+// the LDS address alike.
+template <int C>
+__device__ __forceinline__ void load_chunks_lds(const __attribute__((address_space(1))) char* src,
+                                                __attribute__((address_space(3))) char* dst) {
+  if constexpr (C > 0) {
+    load_chunks_lds<C - 1>(src, dst);
+    __builtin_amdgcn_global_load_lds(src, dst, 16, (C - 1) * 1024, 0);
   }
 }
 
+// ---------------------------------------------------------------------------
+// One wave per block-row, packed K/V staged through a wave-private LDS slot:
+// the next selected tile is copied HBM/L2 -> LDS with direct-to-LDS loads
+// while the current one is computed from registers. Prefetching into LDS
+// instead of registers leaves room for four waves per SIMD.
+constexpr int kStreamWaves = 4;
+
+template <int DT, int D, bool COARSE>
+__global__ __launch_bounds__(kStreamWaves * kWave) void tile_stream_kernel(
+    const void* __restrict__ qv, const void* __restrict__ kpk, const void* __restrict__ vpk,
+    const int32_t* __restrict__ idx, const float* __restrict__ cmax,
+    const float* __restrict__ csum, const float* __restrict__ cvec, void* __restrict__ outv,
+    int n, int nb, int m, long long rows, float scale_log2) {
+  using Cfg = TileCfg<DT, D>;
+  using elem = typename Cfg::elem;
+  constexpr int KC = Cfg::kKChunks, VC = Cfg::kVChunks, CH = Cfg::kChunks;
+  static_assert(CH <= 8, "operands of a tile are held in registers");
+  // the slots are their own LDS object, apart from the selection lists, so
+  // reading a list does not wait for loads in flight into a slot
+  __shared__ __attribute__((aligned(16))) u32x4 slot_all[kStreamWaves][CH * 64];
+  extern __shared__ int32_t sidx_all[];
+
+  const int w = wave_uniform(threadIdx.x / kWave);
+  const int lane = lane_id();
+  const long long wg = xcd_remap(blockIdx.x, gridDim.x);
+  const long long g = wg * kStreamWaves + w;         // global block-row
+  if (g >= rows) return;                             // no workgroup barriers below
+  const long long bh = g / nb;
+  const int x = (int)(g - bh * nb);
+  const long long hoff = bh * (long long)n * D;
+  int32_t* myidx = sidx_all + w * m;
+  for (int i = lane; i < m; i += kWave) myidx[i] = idx[g * m + i];
+  wave_lds_sync();
+
+  TileRow<DT, D, COARSE> row;
+  row.init(reinterpret_cast<const elem*>(qv) + hoff, x, scale_log2);
+  const char* kslab = static_cast<const char*>(kpk) + (size_t)bh * nb * KC * 1024;
+  const char* vslab = static_cast<const char*>(vpk) + (size_t)bh * nb * VC * 1024;
+  const unsigned loff = lane * 16u;
+  unsigned char* slot = reinterpret_cast<unsigned char*>(slot_all[w]);
+  // One lane address per operand; its chunks are 1 KB apart in memory and in
+  // the slot, and the load's immediate offset moves both addresses.
+  static_assert(KC <= 4 && VC <= 4, "chunk offsets fit the immediate field");
+  auto issue = [&](int y) {
+    const auto* kp = (const __attribute__((address_space(1))) char*)(kslab + (size_t)y * KC * 1024 + loff);
+    const auto* vp = (const __attribute__((address_space(1))) char*)(vslab + (size_t)y * VC * 1024 + loff);
+    auto* ks = (__attribute__((address_space(3))) char*)slot;
+    auto* vs = (__attribute__((address_space(3))) char*)(slot + KC * 1024);
+    load_chunks_lds<KC>(kp, ks);
+    load_chunks_lds<VC>(vp, vs);
+  };
+  // entries outside [0, nb) are skipped
+  auto next_valid = [&](int j, int& y) {
+    for (; j < m; ++j) {
+      y = wave_uniform(myidx[j]);
+      if (y >= 0 && y < nb) break;
+    }
+    return j;
+  };
+  const u32x4* sl = slot_all[w] + lane;
+  auto pass = [&](bool check) -> bool {
+    int y = 0;
+    int i = next_valid(0, y);
+    if (i < m) issue(y);
+    while (i < m) {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");    // tile i is in the slot
+      u32x4 kf[KC], vf[VC];
+#pragma unroll
+      for (int c = 0; c < KC; ++c) kf[c] = sl[c * 64];
+#pragma unroll
+      for (int c = 0; c < VC; ++c) vf[c] = sl[(KC + c) * 64];
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // operands in registers
+      const int inext = next_valid(i + 1, y);
+      if (inext < m) issue(y);
+      if (!row.accumulate(row.scores(kf), true, check, [&](int c) { return vf[c]; })) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the slot is idle again
+        return false;
+      }
+      i = inext;
+    }
+    return true;
+  };
+  if (!pass(true)) {
+    // some weight grew too large: again, relative to the row's exact max
+    float mx = -INFINITY;
+    for (int i = 0; i < m; ++i) {
+      const int yy = wave_uniform(myidx[i]);
+      if (yy < 0 || yy >= nb) continue;
+      const u32x4* kt = reinterpret_cast<const u32x4*>(kslab + (size_t)yy * KC * 1024) + lane;
+      u32x4 kf[KC];
+#pragma unroll
+      for (int c = 0; c < KC; ++c) kf[c] = kt[c * 64];
+      mx = __builtin_elementwise_maximum(mx, row.tile_ref(row.scores(kf)));
+    }
+    row.restart(mx);
+    pass(false);
+  }
+  row.finish(reinterpret_cast<elem*>(outv) + hoff, x, g, cmax, csum, cvec);
+}
+
+// ---------------------------------------------------------------------------
 template <int DT, int D, bool PACKED>
 static void launch_tile_t(const void* q, const void* k, const void* v, const int32_t* idx,
                           const float* cmax, const float* csum, const float* cvec, void* out,
@@ -351,8 +548,20 @@ static void launch_tile_t(const void* q, const void* k, const void* v, const int
   constexpr int W = TileCfg<DT, D>::kWaves;
   const int nb = n / kBlock;
   const long long rows = bh * nb;
-  const unsigned blocks = (unsigned)((rows + W - 1) / W);
   const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
+  // tiles of up to 8 KB (bfloat16 d <= 64, float32 d = 32) stream through LDS
+  if constexpr (PACKED && TileCfg<DT, D>::kChunks <= 8) {
+    const unsigned blocks = (unsigned)((rows + kStreamWaves - 1) / kStreamWaves);
+    const size_t smem = (size_t)kStreamWaves * m * sizeof(int32_t);
+    if (cmax)
+      tile_stream_kernel<DT, D, true><<<blocks, kStreamWaves * kWave, smem, stream>>>(
+          q, k, v, idx, cmax, csum, cvec, out, n, nb, m, rows, scale_log2);
+    else
+      tile_stream_kernel<DT, D, false><<<blocks, kStreamWaves * kWave, smem, stream>>>(
+          q, k, v, idx, cmax, csum, cvec, out, n, nb, m, rows, scale_log2);
+    return;
+  }
+  const unsigned blocks = (unsigned)((rows + W - 1) / W);
   const size_t smem = (size_t)W * m * sizeof(int32_t);     // per-wave selection lists
   if (cmax)
     tile_kernel<DT, D, true, PACKED><<<blocks, W * kWave, smem, stream>>>(q, k, v, idx, cmax, csum, cvec, out, n, nb, m, rows, scale_log2);

@@ -244,6 +244,40 @@ def test_large_logits_finite(gpu, dtype):
         _say("  large logits m", m, "err", err, "tol", tol)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("d", [32, 64, 128])
+def test_reference_restart(gpu, dtype, d):
+    """The first selected block of every row has logits near -2 while a later
+    selected block has logits of 120: relative to the first block's max the
+    later weights would overflow, so the tile pass computes the row again
+    relative to its exact max. The result matches the oracle, is finite, and
+    the packed-operand and row-major paths agree bitwise."""
+    _say("restart", dtype, d)
+    n, m = 256, 4
+    r = np.random.Generator(np.random.PCG64(4242 + d))
+    logit = np.full(n // 32, -2.0)
+    logit[1], logit[6] = 2.0, 120.0                 # selected: blocks 0, 1, 2 (ties), 6
+    q = np.zeros((1, 1, n, d)); q[..., 0] = 16.0
+    k = np.zeros((1, 1, n, d)); k[0, 0, :, 0] = np.repeat(logit, 32) * math.sqrt(d) / 16.0
+    v = r.standard_normal((1, 1, n, d))
+    if dtype == "bf16":
+        k, v = inputs.round_to_bf16(k), inputs.round_to_bf16(v)
+    else:
+        k, v = k.astype(np.float32).astype(np.float64), v.astype(np.float32).astype(np.float64)
+    out, idx, err, _ = _forward_and_check(gpu, q, k, v, m, dtype)
+    assert (host(idx)[0, 0] == np.array([0, 1, 2, 6])).all()
+    assert torch.isfinite(out.float()).all()
+    tq, tk, tv = dev(q, dtype), dev(k, dtype), dev(v, dtype)
+    qp, kp, vp, kvpk = gpu.pool(tq, tk, tv, packed=True)
+    S = gpu.coarse_scores(qp, kp)
+    sel = gpu.select(S, m)
+    cm, cs, cv = gpu.coarse_term(S, sel, vp)
+    o1 = gpu.block_sddmm_spmm(tq, tk, tv, sel, cm, cs, cv)
+    o2 = gpu.block_sddmm_spmm(tq, None, None, sel, cm, cs, cv, kvpacked=kvpk)
+    assert torch.equal(o1, o2) and torch.equal(o2, out)
+    _say("  restart err", err)
+
+
 def test_empty_problems(gpu):
     e = torch.empty(0, 2, 64, 64, device="cuda")
     assert gpu.attention_forward(e, e, e, 1).shape == e.shape
