@@ -4,7 +4,7 @@
 //
 // One wave owns one block-row x (32 queries). For every selected column block
 // y, in ascending order, it computes the 32x32 tile S = c Q_x K_y^T on the
-// matrix cores (block-sparse SDDMM), folds it into a running max / row sum
+// matrix cores (block-sparse SDDMM), turns it into softmax weights and row sums
 // (online softmax), and accumulates P V_y (block-sparse SpMM). At the end the
 // result is merged with the block-row's low-resolution term (M_x, c_x, L_x)
 // and normalised.
@@ -29,7 +29,7 @@
 //  * tile_kernel: raw K/V (K rows read directly, V_y through a wave-private
 //    LDS tile stored transposed with the key permutation applied), and packed
 //    K/V with larger tiles (next tile's loads in flight in registers).
-// The running max moves only when the weights would grow too large. Workgroup order
+// The softmax reference is set once per row (restart on overflow). Workgroup order
 // is remapped so each XCD processes a contiguous range of heads and keeps
 // their K/V tiles in its L2.
 #include "common.h"
