@@ -9,8 +9,9 @@
 //
 // Optionally K and V are also written in the tile kernel's matrix-core operand
 // order ("packed K/V", layout in kernels.h), so every operand load of the tile
-// pass is one contiguous 1 KB wave access; that pass stages blocks through
-// LDS so its writes stay contiguous.
+// pass is one contiguous 1 KB wave access; that configuration pools Q, K and V
+// in one launch that stages blocks through LDS so the packed writes stay
+// contiguous.
 #include "common.h"
 #include "kernels.h"
 
@@ -65,13 +66,15 @@ __global__ __launch_bounds__(256) void pool_kernel(const void* __restrict__ x0,
   }
 }
 
-// K and V: block means (same row order as above, so the same bits) and the
-// packed copies (blockIdx.y = 0: K, 1: V). Whole 32-row blocks are staged
-// through LDS so that both the reads and the packed writes are contiguous
-// 16-byte chunks across lanes.
+// Q, K and V in one launch (blockIdx.y = 0: K, 1: V, 2: Q): block means
+// (same row order as above, so the same bits) and, for K and V, the packed
+// copies. Whole 32-row blocks are staged through LDS so that both the reads
+// and the packed writes are contiguous 16-byte chunks across lanes.
 template <int DT, int D>
-__global__ __launch_bounds__(256) void pool_pack_kernel(const void* __restrict__ kin,
+__global__ __launch_bounds__(256) void pool_pack_kernel(const void* __restrict__ qin,
+                                                         const void* __restrict__ kin,
                                                          const void* __restrict__ vin,
+                                                         float* __restrict__ qp,
                                                          float* __restrict__ kp,
                                                          float* __restrict__ vp,
                                                          void* __restrict__ kvpacked,
@@ -80,14 +83,16 @@ __global__ __launch_bounds__(256) void pool_pack_kernel(const void* __restrict__
   constexpr int kPer = DT == BF16 ? 8 : 4;         // elements per chunk
   constexpr int CPR = D / kPer;                    // chunks per row
   constexpr int CPB = kBlock * CPR;                // chunks per block
-  constexpr int NBLK = CPB >= 512 ? 1 : 512 / CPB; // blocks per workgroup pass
+  constexpr int NBLK = CPB >= 1024 ? 1 : 1024 / CPB; // blocks per workgroup pass (16 KB)
   constexpr int NT = D / 32;
   __shared__ __attribute__((aligned(16))) u32x4 tile[NBLK * CPB];
   const elem* te = reinterpret_cast<const elem*>(tile);
-  const bool is_k = blockIdx.y == 0;
-  const u32x4* src = reinterpret_cast<const u32x4*>(is_k ? kin : vin);
-  float* pooled = is_k ? kp : vp;
+  const int which = blockIdx.y;
+  const bool is_k = which == 0, pack = which < 2;
+  const u32x4* src = reinterpret_cast<const u32x4*>(which == 0 ? kin : (which == 1 ? vin : qin));
+  float* pooled = which == 0 ? kp : (which == 1 ? vp : qp);
   u32x4* dst = reinterpret_cast<u32x4*>(kvpacked) + (is_k ? 0 : nblocks * CPB);
+  if (src == nullptr) return;                      // Q not requested (whole workgroup)
   const int tid = threadIdx.x;
 
   for (long long b0 = (long long)blockIdx.x * NBLK; b0 < nblocks; b0 += (long long)gridDim.x * NBLK) {
@@ -129,7 +134,7 @@ __global__ __launch_bounds__(256) void pool_pack_kernel(const void* __restrict__
     // packed copy, one 16-byte output chunk per thread and pass
 #pragma unroll
     for (int oc = tid; oc < NBLK * CPB; oc += 256) {
-      if (oc >= nblk * CPB) continue;
+      if (!pack || oc >= nblk * CPB) continue;
       const int bl = oc / CPB, k = oc % CPB;
       const elem* tb = te + bl * kBlock * D;
       u32x4 o;
@@ -162,34 +167,31 @@ __global__ __launch_bounds__(256) void pool_pack_kernel(const void* __restrict__
 hipError_t launch_pool(const void* q, const void* k, const void* v, float* qp, float* kp,
                        float* vp, void* kvpacked, long long bh, int n, int d, int dtype,
                        hipStream_t stream) {
-  const int per = dtype == BF16 ? 8 : 4;
-  const long long chunks = bh * (n / kBlock) * (d / per);
   const int threads = 256;
-  const long long blocks = (chunks + threads - 1) / threads;
-  // K and V go through the packing kernel when their packed copies are wanted
-  const bool pack = kvpacked != nullptr;
-  const void* kd = pack ? nullptr : k;
-  const void* vd = pack ? nullptr : v;
-  float* kpd = pack ? nullptr : kp;
-  float* vpd = pack ? nullptr : vp;
-  if (qp || kpd || vpd) {
-    dim3 grid((unsigned)blocks, 3);
-    if (dtype == BF16)
-      pool_kernel<BF16><<<grid, threads, 0, stream>>>(q, kd, vd, qp, kpd, vpd, chunks, d);
-    else
-      pool_kernel<F32><<<grid, threads, 0, stream>>>(q, kd, vd, qp, kpd, vpd, chunks, d);
-  }
-  if (pack) {
+  if (kvpacked != nullptr) {
+    // the forward's configuration: Q, K, V pooled and K, V packed in one launch
     const long long nblocks = bh * (n / kBlock);
-    const dim3 g((unsigned)(nblocks < 65536 ? nblocks : 65536), 2);
-#define MRA_PACK(DT_, D_) pool_pack_kernel<DT_, D_><<<g, threads, 0, stream>>>(k, v, kp, vp, kvpacked, nblocks)
+    const int cpb = kBlock * d / (dtype == BF16 ? 8 : 4);
+    const long long nblk = cpb >= 1024 ? 1 : 1024 / cpb;
+    const long long wgs = (nblocks + nblk - 1) / nblk;
+    const dim3 g((unsigned)(wgs < 65536 ? wgs : 65536), 3);
+#define MRA_PACK(DT_, D_) pool_pack_kernel<DT_, D_><<<g, threads, 0, stream>>>(q, k, v, qp, kp, vp, kvpacked, nblocks)
     if (dtype == BF16) {
       if (d == 32) MRA_PACK(BF16, 32); else if (d == 64) MRA_PACK(BF16, 64); else MRA_PACK(BF16, 128);
     } else {
       if (d == 32) MRA_PACK(F32, 32); else if (d == 64) MRA_PACK(F32, 64); else MRA_PACK(F32, 128);
     }
 #undef MRA_PACK
+    return hipGetLastError();
   }
+  const int per = dtype == BF16 ? 8 : 4;
+  const long long chunks = bh * (n / kBlock) * (d / per);
+  const long long blocks = (chunks + threads - 1) / threads;
+  dim3 grid((unsigned)blocks, 3);
+  if (dtype == BF16)
+    pool_kernel<BF16><<<grid, threads, 0, stream>>>(q, k, v, qp, kp, vp, chunks, d);
+  else
+    pool_kernel<F32><<<grid, threads, 0, stream>>>(q, k, v, qp, kp, vp, chunks, d);
   return hipGetLastError();
 }
 

@@ -446,9 +446,19 @@ __device__ __forceinline__ void load_chunks_lds(const __attribute__((address_spa
 // while the current one is computed from registers. Prefetching into LDS
 // instead of registers leaves room for four waves per SIMD.
 constexpr int kStreamWaves = 4;
+constexpr int kStreamSlots = 1;
 
-template <int DT, int D, bool COARSE>
-__global__ __launch_bounds__(kStreamWaves * kWave) void tile_stream_kernel(
+// Wait until at most `keep` tiles of CH loads each are still in flight (the
+// load counter counts down in issue order, so the older tiles have landed).
+template <int CH>
+__device__ __forceinline__ void wait_tiles_in_flight(int keep) {
+  if (keep <= 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  else if (keep == 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(CH) : "memory");
+  else asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * CH) : "memory");
+}
+
+template <int DT, int D, bool COARSE, int WAVES, int SLOTS>
+__global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
     const void* __restrict__ qv, const void* __restrict__ kpk, const void* __restrict__ vpk,
     const int32_t* __restrict__ idx, const float* __restrict__ cmax,
     const float* __restrict__ csum, const float* __restrict__ cvec, void* __restrict__ outv,
@@ -457,15 +467,16 @@ __global__ __launch_bounds__(kStreamWaves * kWave) void tile_stream_kernel(
   using elem = typename Cfg::elem;
   constexpr int KC = Cfg::kKChunks, VC = Cfg::kVChunks, CH = Cfg::kChunks;
   static_assert(CH <= 8, "operands of a tile are held in registers");
+  static_assert(SLOTS >= 1 && SLOTS <= 3, "tiles in flight per wave");
   // the slots are their own LDS object, apart from the selection lists, so
   // reading a list does not wait for loads in flight into a slot
-  __shared__ __attribute__((aligned(16))) u32x4 slot_all[kStreamWaves][CH * 64];
+  __shared__ __attribute__((aligned(16))) u32x4 slot_all[WAVES][SLOTS][CH * 64];
   extern __shared__ int32_t sidx_all[];
 
   const int w = wave_uniform(threadIdx.x / kWave);
   const int lane = lane_id();
   const long long wg = xcd_remap(blockIdx.x, gridDim.x);
-  const long long g = wg * kStreamWaves + w;         // global block-row
+  const long long g = wg * WAVES + w;                // global block-row
   if (g >= rows) return;                             // no workgroup barriers below
   const long long bh = g / nb;
   const int x = (int)(g - bh * nb);
@@ -479,11 +490,11 @@ __global__ __launch_bounds__(kStreamWaves * kWave) void tile_stream_kernel(
   const char* kslab = static_cast<const char*>(kpk) + (size_t)bh * nb * KC * 1024;
   const char* vslab = static_cast<const char*>(vpk) + (size_t)bh * nb * VC * 1024;
   const unsigned loff = lane * 16u;
-  unsigned char* slot = reinterpret_cast<unsigned char*>(slot_all[w]);
   // One lane address per operand; its chunks are 1 KB apart in memory and in
   // the slot, and the load's immediate offset moves both addresses.
   static_assert(KC <= 4 && VC <= 4, "chunk offsets fit the immediate field");
-  auto issue = [&](int y) {
+  auto issue = [&](int y, int sidx) {
+    unsigned char* slot = reinterpret_cast<unsigned char*>(slot_all[w][sidx]);
     const auto* kp = (const __attribute__((address_space(1))) char*)(kslab + (size_t)y * KC * 1024 + loff);
     const auto* vp = (const __attribute__((address_space(1))) char*)(vslab + (size_t)y * VC * 1024 + loff);
     auto* ks = (__attribute__((address_space(3))) char*)slot;
@@ -499,26 +510,38 @@ __global__ __launch_bounds__(kStreamWaves * kWave) void tile_stream_kernel(
     }
     return j;
   };
-  const u32x4* sl = slot_all[w] + lane;
+  // Tiles are numbered in the order they are used; tile t goes to slot
+  // t % SLOTS, and up to SLOTS of them are in flight.
   auto pass = [&](bool check) -> bool {
-    int y = 0;
-    int i = next_valid(0, y);
-    if (i < m) issue(y);
-    while (i < m) {
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");    // tile i is in the slot
+    int yn = 0;
+    int ni = next_valid(0, yn);                      // next list entry to load
+    int issued = 0, used = 0;
+#pragma unroll
+    for (int t = 0; t < SLOTS; ++t)
+      if (ni < m) {
+        issue(yn, t);
+        ++issued;
+        ni = next_valid(ni + 1, yn);
+      }
+    while (used < issued) {
+      wait_tiles_in_flight<CH>(issued - used - 1);   // tile `used` is in its slot
+      const u32x4* sl = slot_all[w][used % SLOTS] + lane;
       u32x4 kf[KC], vf[VC];
 #pragma unroll
       for (int c = 0; c < KC; ++c) kf[c] = sl[c * 64];
 #pragma unroll
       for (int c = 0; c < VC; ++c) vf[c] = sl[(KC + c) * 64];
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // operands in registers
-      const int inext = next_valid(i + 1, y);
-      if (inext < m) issue(y);
+      ++used;
+      if (ni < m) {                                  // refill the slot just read
+        issue(yn, issued % SLOTS);
+        ++issued;
+        ni = next_valid(ni + 1, yn);
+      }
       if (!row.accumulate(row.scores(kf), true, check, [&](int c) { return vf[c]; })) {
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the slot is idle again
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the slots are idle again
         return false;
       }
-      i = inext;
     }
     return true;
   };
@@ -554,10 +577,10 @@ static void launch_tile_t(const void* q, const void* k, const void* v, const int
     const unsigned blocks = (unsigned)((rows + kStreamWaves - 1) / kStreamWaves);
     const size_t smem = (size_t)kStreamWaves * m * sizeof(int32_t);
     if (cmax)
-      tile_stream_kernel<DT, D, true><<<blocks, kStreamWaves * kWave, smem, stream>>>(
+      tile_stream_kernel<DT, D, true, kStreamWaves, kStreamSlots><<<blocks, kStreamWaves * kWave, smem, stream>>>(
           q, k, v, idx, cmax, csum, cvec, out, n, nb, m, rows, scale_log2);
     else
-      tile_stream_kernel<DT, D, false><<<blocks, kStreamWaves * kWave, smem, stream>>>(
+      tile_stream_kernel<DT, D, false, kStreamWaves, kStreamSlots><<<blocks, kStreamWaves * kWave, smem, stream>>>(
           q, k, v, idx, cmax, csum, cvec, out, n, nb, m, rows, scale_log2);
     return;
   }
