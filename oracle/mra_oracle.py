@@ -25,6 +25,9 @@ coarse logits, per-row budget, replacement rather than addition, factor b on
 the coarse term in Alg. 2, ties to the lower index, ascending index lists) are
 listed with their reasons in the design notes.
 
+The sparse-only variant MRA-2-s (Sec. 5: only the scale-1 components over the
+selected blocks, normalised by their own row sums) is ``mra2s_rows``.
+
 Two forms of the output are provided: the dense definition over the full
 logit slab of each block-row (``mra_dense``) and the factored form of Alg. 2
 (``mra_factored``), where the unselected blocks contribute b*exp(S~)*V~_y.
@@ -196,6 +199,44 @@ def mra_factored_rows(q, k, v, b, m, rows=None, idx=None):
 def mra_factored(q, k, v, b, m, idx=None):
     Z, idx, _ = mra_factored_rows(q, k, v, b, m, idx=idx)
     return Z, idx
+
+
+# --------------------------------------------------------------------------
+# Sec. 5, MRA-2-s: only the scale-1 part A^_1 over the selected blocks J,
+# normalised by its own row sums (D^ applied to A^_1)
+# --------------------------------------------------------------------------
+def mra2s_rows(q, k, v, b, m, idx=None):
+    """Z = D^ A^_1 V for one head: for query i in block-row x, the softmax of
+    the fine logits P_ij = q_i . k_j / sqrt(d) over the columns j of the
+    selected blocks T_x only, times V. Needs m >= 1. Returns (Z, idx)."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    n, d = q.shape
+    qp, kp = block_mean(q, b), block_mean(k, b)
+    S = coarse_logits(qp, kp)
+    if idx is None:
+        if m < 1:
+            raise ValueError("MRA-2-s needs at least one selected block per row")
+        idx = select_blocks(S, m)
+    Z = np.empty((n, v.shape[1]))
+    for x in range(S.shape[0]):
+        cols = np.concatenate([np.arange(y * b, (y + 1) * b) for y in np.asarray(idx[x], dtype=np.int64)])
+        P = q[x * b:(x + 1) * b] @ k[cols].T / math.sqrt(d)
+        Z[x * b:(x + 1) * b] = _normalised_rows(P, v[cols])
+    return Z, idx
+
+
+def mra2s_batched(q, k, v, b, m, idx=None):
+    """MRA-2-s Z and idx for every head of [B, H, n, d] inputs."""
+    B, H, n, d = q.shape
+    Z = np.empty((B, H, n, v.shape[-1]))
+    I = np.empty((B, H, n // b, m), dtype=np.int64)
+    for bb in range(B):
+        for h in range(H):
+            Z[bb, h], I[bb, h] = mra2s_rows(q[bb, h], k[bb, h], v[bb, h], b, m,
+                                            idx=None if idx is None else idx[bb, h])
+    return Z, I
 
 
 # --------------------------------------------------------------------------

@@ -318,3 +318,77 @@ def test_batched_wrappers_match_single_head():
     assert np.array_equal(I, Ib)
     M, c, L = O.coarse_term_batched(S, I, vp, 32)
     assert M.shape == (1, 1, 16) and L.shape == (1, 1, 16, 64)
+
+
+# ---------------------------------------------------------------- MRA-2-s (Sec. 5)
+def _brute_mra2s(q, k, v, b, m):
+    """MRA-2-s written out with Python loops: block means, coarse logits, the m
+    best blocks per block-row (ties to the lower index), then the softmax of
+    the fine logits over the columns of those blocks only."""
+    n, d = q.shape
+    nb = n // b
+    mean = lambda x, blk: [sum(x[blk * b + r][t] for r in range(b)) / b for t in range(d)]
+    qm = [mean(q, x) for x in range(nb)]
+    km = [mean(k, y) for y in range(nb)]
+    out = np.zeros((n, v.shape[1]))
+    for x in range(nb):
+        score = [sum(qm[x][t] * km[y][t] for t in range(d)) / math.sqrt(d) for y in range(nb)]
+        keep = [y for _, y in sorted((-score[y], y) for y in range(nb))[:m]]
+        cols = [j for y in keep for j in range(y * b, (y + 1) * b)]
+        for i in range(x * b, (x + 1) * b):
+            logits = [sum(q[i, t] * k[j, t] for t in range(d)) / math.sqrt(d) for j in cols]
+            top = max(logits)
+            w = [math.exp(a - top) for a in logits]
+            s = sum(w)
+            for j, wj in zip(cols, w):
+                out[i] += wj / s * v[j]
+    return out
+
+
+@pytest.mark.parametrize("n,b,d,m", [(16, 4, 3, 1), (24, 8, 5, 2), (32, 4, 2, 3)])
+def test_mra2s_bruteforce(n, b, d, m):
+    r = _rng(31 + m)
+    q, k, v = r.standard_normal((n, d)), r.standard_normal((n, d)), r.standard_normal((n, d))
+    Z, idx = O.mra2s_rows(q, k, v, b, m)
+    np.testing.assert_allclose(Z, _brute_mra2s(q, k, v, b, m), rtol=1e-12, atol=1e-13)
+    assert idx.shape == (n // b, m)
+
+
+@pytest.mark.parametrize("n,b,d,m,scale", [(256, 32, 16, 3, 1.0), (512, 32, 64, 5, 2.0), (128, 16, 8, 8, 0.5)])
+def test_mra2s_is_masked_torch_softmax(n, b, d, m, scale):
+    """Against torch's attention with a boolean mask that keeps exactly the
+    columns of each row's selected blocks; at full budget, against plain
+    attention."""
+    r = _rng(40 + m)
+    q, k, v = (r.standard_normal((n, d)) * scale for _ in range(3))
+    Z, idx = O.mra2s_rows(q, k, v, b, m)
+    keep = np.zeros((n, n), dtype=bool)
+    for x in range(n // b):
+        for y in idx[x]:
+            keep[x * b:(x + 1) * b, y * b:(y + 1) * b] = True
+    t = lambda a: torch.from_numpy(a)[None]
+    ref = torch.nn.functional.scaled_dot_product_attention(t(q), t(k), t(v), attn_mask=t(keep))[0].numpy()
+    np.testing.assert_allclose(Z, ref, rtol=1e-11, atol=1e-12)
+    Zf, _ = O.mra2s_rows(q, k, v, b, n // b)
+    full = torch.nn.functional.scaled_dot_product_attention(t(q), t(k), t(v))[0].numpy()
+    np.testing.assert_allclose(Zf, full, rtol=1e-11, atol=1e-12)
+
+
+def test_mra2s_invariants():
+    """V = 1 gives 1 (the weights of a row sum to one); with one selected block
+    whose keys are all equal, every query averages that block's values; the
+    empty selection is rejected."""
+    r = _rng(50)
+    n, b, d = 128, 32, 8
+    q, k = r.standard_normal((n, d)), r.standard_normal((n, d))
+    Z, _ = O.mra2s_rows(q, k, np.ones((n, 3)), b, 2)
+    np.testing.assert_allclose(Z, 1.0, rtol=0, atol=1e-14)
+    kc = np.repeat(r.standard_normal((n // b, d)), b, axis=0)
+    v = r.standard_normal((n, d))
+    Z, idx = O.mra2s_rows(q, kc, v, b, 1)
+    for x in range(n // b):
+        y = idx[x, 0]
+        np.testing.assert_allclose(Z[x * b:(x + 1) * b], np.broadcast_to(v[y * b:(y + 1) * b].mean(0), (b, d)),
+                                   rtol=1e-12, atol=1e-13)
+    with pytest.raises(ValueError):
+        O.mra2s_rows(q, k, v, b, 0)
