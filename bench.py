@@ -166,6 +166,11 @@ def main():
     ms = s.elapsed_time(e) / args.steps
     tokens_per_s = w.B * w.n / (ms * 1e-3)
 
+    # The sparse-only variant MRA-2-s (Sec. 5) on the same inputs: reported
+    # beside the headline, which is MRA-2.
+    sparse_ms = time_launches(lambda: ops.sparse_attention_forward(tq, tk, tv, w.budget, out=out, idx_out=idx,
+                                                                   workspace=ws), max(args.steps, 20))
+
     # Dominant kernel: the tile pass, the same instantiation as inside the
     # forward (packed K/V, coarse term given), on the same inputs; timed alone.
     qp, kp, vp, kvpk = ops.pool(tq, tk, tv, packed=True)
@@ -198,6 +203,7 @@ def main():
                       "coarse_scores_stepwise": coarse_ms * 1e3},
         "pool_roofline": {"bound": "hbm", "achieved": pool_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                           "frac": pool_gbs / PEAK_HBM_GBS, "bytes_per_launch": pool_bytes(w)},
+        "mra2s": {"ms_per_step": sparse_ms, "tokens_per_s": w.B * w.n / (sparse_ms * 1e-3)},
         "tflops_step": (tile_flops(w) + coarse_flops(w)) / (ms * 1e-3) / 1e12,
         "wall_s_timed": wall,
     }

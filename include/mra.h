@@ -192,6 +192,25 @@ mra_status_t mra_attention_forward(const void* q, const void* k, const void* v, 
                                    int B, int H, int n, int d, int block, int budget,
                                    mra_dtype_t dtype, void* stream);
 
+/*
+ * mra_sparse_attention_forward — the sparse-only variant MRA-2-s (Sec. 5):
+ * after the selection T_x, only the scale-1 part over the selected blocks is
+ * kept, normalised by its own row sums:
+ *   Z_i = sum_{j in T_x} e^{P_ij} V_j / sum_{j in T_x} e^{P_ij},  P = Q K^T / sqrt(d)
+ * (no low-resolution term). Enqueues pooling, the fused coarse logits and
+ * selection, and the tile pass without the coarse merge; bit-identical to
+ * mra_pool, mra_coarse_scores, mra_select and mra_block_sddmm_spmm (cmax,
+ * csum, cvec NULL) called in that order.
+ *   Arguments, layouts, workspace (mra_forward_workspace_bytes) and errors as
+ *   for mra_attention_forward, except that budget must be at least 1 (at most
+ *   nb) whenever n > 0: MRA_ERR_INVALID_ARG otherwise.
+ */
+mra_status_t mra_sparse_attention_forward(const void* q, const void* k, const void* v,
+                                          void* out, int32_t* idx_out, void* workspace,
+                                          size_t workspace_bytes, int B, int H, int n, int d,
+                                          int block, int budget, mra_dtype_t dtype,
+                                          void* stream);
+
 /* Static description of a status code. */
 const char* mra_status_str(mra_status_t status);
 

@@ -205,25 +205,28 @@ def mra_factored(q, k, v, b, m, idx=None):
 # Sec. 5, MRA-2-s: only the scale-1 part A^_1 over the selected blocks J,
 # normalised by its own row sums (D^ applied to A^_1)
 # --------------------------------------------------------------------------
-def mra2s_rows(q, k, v, b, m, idx=None):
+def mra2s_rows(q, k, v, b, m, idx=None, rows=None):
     """Z = D^ A^_1 V for one head: for query i in block-row x, the softmax of
     the fine logits P_ij = q_i . k_j / sqrt(d) over the columns j of the
-    selected blocks T_x only, times V. Needs m >= 1. Returns (Z, idx)."""
+    selected blocks T_x only, times V. Needs m >= 1. With `rows`, only those
+    block-rows (idx then lists their selections in the same order). Returns
+    (Z [len(rows)*b, d], idx)."""
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
     v = np.asarray(v, dtype=np.float64)
     n, d = q.shape
-    qp, kp = block_mean(q, b), block_mean(k, b)
-    S = coarse_logits(qp, kp)
+    nb = n // b
+    rows = list(range(nb)) if rows is None else list(rows)
     if idx is None:
         if m < 1:
             raise ValueError("MRA-2-s needs at least one selected block per row")
+        S = coarse_logits(block_mean(q, b)[rows], block_mean(k, b))
         idx = select_blocks(S, m)
-    Z = np.empty((n, v.shape[1]))
-    for x in range(S.shape[0]):
-        cols = np.concatenate([np.arange(y * b, (y + 1) * b) for y in np.asarray(idx[x], dtype=np.int64)])
+    Z = np.empty((len(rows) * b, v.shape[1]))
+    for r, x in enumerate(rows):
+        cols = np.concatenate([np.arange(y * b, (y + 1) * b) for y in np.asarray(idx[r], dtype=np.int64)])
         P = q[x * b:(x + 1) * b] @ k[cols].T / math.sqrt(d)
-        Z[x * b:(x + 1) * b] = _normalised_rows(P, v[cols])
+        Z[r * b:(r + 1) * b] = _normalised_rows(P, v[cols])
     return Z, idx
 
 

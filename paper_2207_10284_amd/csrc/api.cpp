@@ -230,6 +230,40 @@ mra_status_t mra_attention_forward(const void* q, const void* k, const void* v, 
                                      budget, (int)dtype, st));
 }
 
+mra_status_t mra_sparse_attention_forward(const void* q, const void* k, const void* v,
+                                          void* out, int32_t* idx_out, void* workspace,
+                                          size_t workspace_bytes, int B, int H, int n, int d,
+                                          int block, int budget, mra_dtype_t dtype,
+                                          void* stream) {
+  Shape s;
+  MRA_TRY(check_shape(B, H, n, d, block, true, &s));
+  MRA_TRY(check_dtype(dtype));
+  // at least one selected block per row (n = 0 leaves no block to select)
+  if (budget < 0 || budget > s.nb || (s.nb > 0 && budget < 1)) return MRA_ERR_INVALID_ARG;
+  if (s.empty) return MRA_OK;
+  MRA_TRY(check_ptr(q));
+  MRA_TRY(check_ptr(k));
+  MRA_TRY(check_ptr(v));
+  MRA_TRY(check_ptr(out));
+  if (idx_out != nullptr && !aligned16(idx_out)) return MRA_ERR_MISALIGNED;
+  MRA_TRY(check_ptr(workspace));
+  const WsLayout L = ws_layout(s.bh, s.nb, d, budget, dtype);
+  if (workspace_bytes < L.total) return MRA_ERR_WORKSPACE;
+
+  char* ws = static_cast<char*>(workspace);
+  float* qp = reinterpret_cast<float*>(ws + L.qp);
+  float* kp = reinterpret_cast<float*>(ws + L.kp);
+  float* vp = reinterpret_cast<float*>(ws + L.vp);
+  void* kvpacked = ws + L.kvpacked;
+  int32_t* idx = idx_out ? idx_out : reinterpret_cast<int32_t*>(ws + L.idx);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+
+  MRA_TRY(hip_status(mra::launch_pool(q, k, v, qp, kp, vp, kvpacked, s.bh, n, d, (int)dtype, st)));
+  MRA_TRY(hip_status(mra::launch_select_fused(qp, kp, idx, s.bh, s.nb, d, budget, st)));
+  return hip_status(mra::launch_tile(q, k, v, kvpacked, idx, nullptr, nullptr, nullptr, out, s.bh,
+                                     n, d, budget, (int)dtype, st));
+}
+
 const char* mra_status_str(mra_status_t status) {
   switch (status) {
     case MRA_OK: return "MRA_OK";

@@ -24,13 +24,13 @@
 // between them, so V~ is read once per workgroup. Workgroups of one head stay
 // on one XCD. Every mode runs the same arithmetic in the same order, so the
 // fused forward step is bit-identical to separate score, select and
-// coarse-term calls.
+// coarse-term calls. A fused select-only mode serves MRA-2-s.
 #include "coarse_tile.h"
 #include "kernels.h"
 
 namespace mra {
 
-enum RowsMode { kSelectOnly = 0, kTermOnly = 1, kFused = 2 };
+enum RowsMode { kSelectOnly = 0, kTermOnly = 1, kFused = 2, kFusedSelect = 3 };
 constexpr int kRows = 16;                 // block-rows (waves) per workgroup
 constexpr int kChunk = 64;                // score columns per chunk
 
@@ -80,7 +80,7 @@ __global__ __launch_bounds__(1024) void rows_kernel(
   float s[JMAX];
 #pragma unroll
   for (int j = 0; j < JMAX; ++j) s[j] = 0.0f;
-  if constexpr (MODE == kFused) {
+  if constexpr (MODE == kFused || MODE == kFusedSelect) {
     constexpr int ldq = D + 1, ldk = D + 1;
     double* Qd = reinterpret_cast<double*>(smem + q_off);          // [16][D+1]
     float* Kc = reinterpret_cast<float*>(smem + k_off);            // [64][D+1]
@@ -178,7 +178,7 @@ __global__ __launch_bounds__(1024) void rows_kernel(
       }
     }
   }
-  if constexpr (MODE == kSelectOnly) return;
+  if constexpr (MODE == kSelectOnly || MODE == kFusedSelect) return;
 
   // ---- phase 3: max, weights (kept in s[]) and their sum over unselected blocks
   if (active) {
@@ -251,7 +251,7 @@ static void launch_rows_j(const float* S, const float* qp, const float* kp, int3
                           float* cvec, long long bh, int nb, int d, int m, hipStream_t stream) {
   const long long groups = (nb + kRows - 1) / kRows;
   const unsigned blocks = (unsigned)(bh * groups);
-  const RowsSmem L = rows_smem(d, MODE == kFused);
+  const RowsSmem L = rows_smem(d, MODE == kFused || MODE == kFusedSelect);
   const double scale = 1.0 / sqrt((double)d);
 #define MRA_ROWS_LAUNCH(DD)                                                                     \
   rows_kernel<DD, MODE, JMAX><<<blocks, 64 * kRows, L.bytes, stream>>>(                       \
@@ -289,6 +289,12 @@ hipError_t launch_coarse_term(const float* S, const int32_t* idx, const float* v
                               hipStream_t stream) {
   return launch_rows<kTermOnly>(S, nullptr, nullptr, nullptr, idx, vp, cmax, csum, cvec, bh, nb,
                                 d, m, stream);
+}
+
+hipError_t launch_select_fused(const float* qp, const float* kp, int32_t* idx, long long bh,
+                               int nb, int d, int m, hipStream_t stream) {
+  return launch_rows<kFusedSelect>(nullptr, qp, kp, idx, nullptr, nullptr, nullptr, nullptr,
+                                   nullptr, bh, nb, d, m, stream);
 }
 
 hipError_t launch_select_term_fused(const float* qp, const float* kp, int32_t* idx,

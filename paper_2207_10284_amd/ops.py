@@ -32,6 +32,7 @@ SIGNATURES = {
     "mra_block_sddmm_spmm": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _P]),
     "mra_forward_workspace_bytes": (_Z, [_I, _I, _I, _I, _I, _I, _I]),
     "mra_attention_forward": (_I, [_P, _P, _P, _P, _P, _P, _Z, _I, _I, _I, _I, _I, _I, _I, _P]),
+    "mra_sparse_attention_forward": (_I, [_P, _P, _P, _P, _P, _P, _Z, _I, _I, _I, _I, _I, _I, _I, _P]),
     "mra_status_str": (ctypes.c_char_p, [_I]),
     "mra_last_hip_error": (_I, []),
 }
@@ -187,6 +188,17 @@ def forward_workspace_bytes(B: int, H: int, n: int, d: int, budget: int, dtype=t
 def attention_forward(q, k, v, budget: int, out=None, idx_out=None, workspace=None):
     """The whole MRA-2 forward pass. Returns the output Z ([B, H, n, d], input
     dtype); the selection is written to ``idx_out`` when given."""
+    return _forward("mra_attention_forward", q, k, v, budget, out, idx_out, workspace)
+
+
+def sparse_attention_forward(q, k, v, budget: int, out=None, idx_out=None, workspace=None):
+    """The sparse-only variant MRA-2-s (Sec. 5): softmax over the selected
+    blocks only, no low-resolution term; budget >= 1. Same arguments and
+    result as ``attention_forward``."""
+    return _forward("mra_sparse_attention_forward", q, k, v, budget, out, idx_out, workspace)
+
+
+def _forward(entry, q, k, v, budget, out, idx_out, workspace):
     ref = _check_qkv(q, k, v)
     B, H, n, d = ref.shape
     nb = n // BLOCK
@@ -197,7 +209,7 @@ def attention_forward(q, k, v, budget: int, out=None, idx_out=None, workspace=No
     need = forward_workspace_bytes(B, H, n, d, budget, ref.dtype)
     if workspace is None:
         workspace = torch.empty(max(need, 1), device=ref.device, dtype=torch.uint8)
-    _call("mra_attention_forward", _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(idx_out),
+    _call(entry, _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(idx_out),
           _ptr(workspace), workspace.numel() * workspace.element_size(),
           B, H, n, d, BLOCK, budget, _dtype_code(ref), _stream(ref.device))
     return out

@@ -31,7 +31,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 9, names
+    assert len(names) == 10, names
     for name in names:
         assert hasattr(lib, name), name
     assert set(names) == set(ops.SIGNATURES)
@@ -72,6 +72,29 @@ def test_forward_validation(lib):
     assert fwd(lib, B=0, q=None, k=None, v=None, out=None, ws=None) == OK
     assert fwd(lib, n=0, budget=0, q=None, out=None, ws=None) == OK
     assert fwd(lib, n=0, budget=1) == INVALID  # nb = 0
+    assert lib.mra_last_hip_error() == 0
+
+
+def sfwd(lib, q=A, k=A, v=A, out=A, idx=None, ws=A, wsb=1 << 40, B=1, H=1, n=64, d=64, block=32,
+         budget=1, dtype=1):
+    return lib.mra_sparse_attention_forward(q, k, v, out, idx, ws, wsb, B, H, n, d, block, budget,
+                                            dtype, None)
+
+
+def test_sparse_forward_validation(lib):
+    """MRA-2-s: the forward's checks, and at least one selected block per row."""
+    assert sfwd(lib, budget=0) == INVALID
+    assert sfwd(lib, budget=-1) == INVALID
+    assert sfwd(lib, budget=3) == INVALID      # nb = 2
+    assert sfwd(lib, block=16) == UNSUPPORTED
+    assert sfwd(lib, d=48) == UNSUPPORTED
+    assert sfwd(lib, q=None) == INVALID
+    assert sfwd(lib, k=MIS) == MISALIGNED
+    need = lib.mra_forward_workspace_bytes(1, 1, 64, 64, 32, 1, 1)
+    assert sfwd(lib, wsb=need - 1) == WORKSPACE
+    assert sfwd(lib, B=0, q=None, k=None, v=None, out=None, ws=None) == OK
+    assert sfwd(lib, B=0, budget=0) == INVALID  # nb = 2: a block must be selected
+    assert sfwd(lib, n=0, budget=0, q=None, out=None, ws=None) == OK
     assert lib.mra_last_hip_error() == 0
 
 
