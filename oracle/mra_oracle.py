@@ -84,6 +84,58 @@ def select_blocks(S, m):
 
 
 # --------------------------------------------------------------------------
+# Sec. 4.2, Alg. 1 with one budget for the whole head (R = {b, 1}): pop the
+# m_1 blocks with the largest mu over all (x, y); J may start with priors
+# --------------------------------------------------------------------------
+def select_global(S, budget, prior_diagonal=False):
+    """The blocks refined for one head when Alg. 1 pops `budget` blocks over
+    all nb x nb coarse blocks at once: the `budget` largest S~[x, y] (equal
+    scores: the lower flat index x*nb + y first) among the blocks that are not
+    priors, plus the priors (with prior_diagonal, every diagonal block (x, x)
+    is refined from the start and does not count against the budget).
+
+    Returns an int64 array [nb, nb]: row x lists its refined column blocks in
+    ascending order, followed by -1 up to nb entries."""
+    S = np.asarray(S, dtype=np.float64)
+    nb = S.shape[0]
+    assert S.shape == (nb, nb)
+    prior = np.eye(nb, dtype=bool) if prior_diagonal else np.zeros((nb, nb), dtype=bool)
+    free = np.flatnonzero(~prior.ravel())
+    if not 0 <= budget <= free.size:
+        raise ValueError("budget out of range")
+    order = free[np.lexsort((free, -S.ravel()[free]))]   # primary: -score, then flat index
+    keep = prior.ravel().copy()
+    keep[order[:budget]] = True
+    keep = keep.reshape(nb, nb)
+    out = np.full((nb, nb), -1, dtype=np.int64)
+    for x in range(nb):
+        ys = np.flatnonzero(keep[x])
+        out[x, :ys.size] = ys
+    return out
+
+
+def rows_of(idx):
+    """The valid entries (0 <= y < nb) of every row of a padded selection."""
+    idx = np.asarray(idx, dtype=np.int64)
+    nb = idx.shape[0]
+    return [r[(r >= 0) & (r < nb)] for r in idx]
+
+
+def mra_global(q, k, v, b, budget, prior_diagonal=False, idx=None):
+    """MRA-2 for one head with the head-wide budget of select_global: Z and the
+    padded selection. The approximation and its normalisation are those of
+    mra_factored_rows (scale-1 entries on refined blocks, b*exp(S~) V~ on the
+    others)."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    if idx is None:
+        S = coarse_logits(block_mean(q, b), block_mean(k, b))
+        idx = select_global(S, budget, prior_diagonal)
+    Z, _, _ = mra_factored_rows(q, k, v, b, 0, idx=rows_of(idx))
+    return Z, idx
+
+
+# --------------------------------------------------------------------------
 # eq. actual_approx_mat_form: the logits of A^ for one block-row
 # --------------------------------------------------------------------------
 def approx_logits_slab(q, k, S, sel, b, x):
@@ -173,7 +225,7 @@ def mra_factored_rows(q, k, v, b, m, rows=None, idx=None):
     rows = list(range(nb)) if rows is None else list(rows)
     qp, kp, vp = block_mean(q, b), block_mean(k, b), block_mean(v, b)
     S = coarse_logits(qp[rows], kp)
-    sel_all = select_blocks(S, m) if idx is None else np.asarray(idx)
+    sel_all = select_blocks(S, m) if idx is None else idx   # rows may differ in length
     out = np.empty((len(rows) * b, v.shape[1]))
     for r, x in enumerate(rows):
         sel = np.asarray(sel_all[r], dtype=np.int64)

@@ -392,3 +392,77 @@ def test_mra2s_invariants():
                                    rtol=1e-12, atol=1e-13)
     with pytest.raises(ValueError):
         O.mra2s_rows(q, k, v, b, 0)
+
+
+# ---------------------------------------------------------------- head-wide budget (Alg. 1, R = {b, 1})
+def _brute_select_global(S, budget, prior_diagonal):
+    """Sort every non-prior block by (-score, flat index) with Python's sort,
+    keep the first `budget`, add the priors, list each row ascending."""
+    nb = len(S)
+    cand = sorted((-S[x][y], x * nb + y) for x in range(nb) for y in range(nb)
+                  if not (prior_diagonal and x == y))
+    keep = {f for _, f in cand[:budget]}
+    if prior_diagonal:
+        keep |= {x * nb + x for x in range(nb)}
+    return [[y for y in range(nb) if x * nb + y in keep] for x in range(nb)]
+
+
+@pytest.mark.parametrize("nb,budget,prior", [(4, 3, False), (6, 7, True), (8, 0, True), (8, 64, False),
+                                             (7, 20, False), (5, 20, True)])
+def test_select_global_bruteforce_with_ties(nb, budget, prior):
+    r = _rng(60 + nb + budget)
+    S = np.round(r.standard_normal((nb, nb)) * 2) / 2        # many exact ties
+    got = O.select_global(S, budget, prior)
+    want = _brute_select_global(S.tolist(), budget, prior)
+    for x in range(nb):
+        row = [int(y) for y in got[x] if y >= 0]
+        assert row == want[x]
+        assert (got[x][len(row):] == -1).all()
+    assert sum(len(w) for w in want) == budget + (nb if prior else 0)
+
+
+def test_select_global_reduces_to_per_row():
+    """If every row's m best scores exceed every score not among them, the
+    head-wide pop of m*nb blocks is the per-row selection."""
+    r = _rng(70)
+    nb, m = 12, 3
+    S = -r.random((nb, nb))
+    for x in range(nb):
+        S[x, r.choice(nb, m, replace=False)] = 10.0 + r.random(m)
+    got = O.select_global(S, m * nb)
+    assert (got[:, :m] == O.select_blocks(S, m)).all() and (got[:, m:] == -1).all()
+
+
+@pytest.mark.parametrize("budget,prior", [(5, False), (0, True), (9, True)])
+def test_global_budget_constant_blocks_exact(budget, prior):
+    """Block-constant Q and K make every coarse block exact, so any head-wide
+    selection reproduces softmax attention (checked against torch)."""
+    r = _rng(80 + budget)
+    n, b, d = 128, 32, 8
+    q, k = _constant_block_qk(r, n, b, d, 1.5)
+    v = r.standard_normal((n, d))
+    Z, idx = O.mra_global(q, k, v, b, budget, prior)
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q)[None], torch.from_numpy(k)[None], torch.from_numpy(v)[None])[0].numpy()
+    np.testing.assert_allclose(Z, ref, rtol=1e-11, atol=1e-12)
+
+
+def test_global_full_budget_is_exact_and_dense_agrees():
+    r = _rng(90)
+    n, b, d = 128, 16, 8
+    q, k, v = r.standard_normal((n, d)), r.standard_normal((n, d)), r.standard_normal((n, d))
+    nb = n // b
+    Z, idx = O.mra_global(q, k, v, b, nb * nb)
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q)[None], torch.from_numpy(k)[None], torch.from_numpy(v)[None])[0].numpy()
+    np.testing.assert_allclose(Z, ref, rtol=1e-11, atol=1e-12)
+    # partial budget with the diagonal prior: the factored form equals the
+    # dense slab definition row by row
+    Z, idx = O.mra_global(q, k, v, b, 13, True)
+    S = O.coarse_logits(O.block_mean(q, b), O.block_mean(k, b))
+    for x, sel in enumerate(O.rows_of(idx)):
+        assert x in sel
+        slab = O.approx_logits_slab(q, k, S, sel, b, x)
+        w = np.exp(slab - slab.max(axis=1, keepdims=True))
+        np.testing.assert_allclose(Z[x * b:(x + 1) * b], (w @ v) / w.sum(axis=1, keepdims=True),
+                                   rtol=1e-12, atol=1e-13)
