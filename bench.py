@@ -171,6 +171,13 @@ def main():
     sparse_ms = time_launches(lambda: ops.sparse_attention_forward(tq, tk, tv, w.budget, out=out, idx_out=idx,
                                                                    workspace=ws), max(args.steps, 20))
 
+    # MRA-2 with the head-wide budget of Alg. 1 (same total: m * nb blocks per
+    # head, the nb diagonal blocks as priors), reported beside the headline.
+    gidx = torch.empty(w.B, w.H, w.nb, w.nb, dtype=torch.int32, device=dev)
+    gws = torch.empty(ops.forward_global_workspace_bytes(w.B, w.H, w.n, w.d, tdt), dtype=torch.uint8, device=dev)
+    global_ms = time_launches(lambda: ops.attention_forward_global(tq, tk, tv, w.budget * w.nb - w.nb, True, out=out,
+                                                                   idx_out=gidx, workspace=gws), max(args.steps, 20))
+
     # Dominant kernel: the tile pass, the same instantiation as inside the
     # forward (packed K/V, coarse term given), on the same inputs; timed alone.
     qp, kp, vp, kvpk = ops.pool(tq, tk, tv, packed=True)
@@ -204,6 +211,8 @@ def main():
         "pool_roofline": {"bound": "hbm", "achieved": pool_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                           "frac": pool_gbs / PEAK_HBM_GBS, "bytes_per_launch": pool_bytes(w)},
         "mra2s": {"ms_per_step": sparse_ms, "tokens_per_s": w.B * w.n / (sparse_ms * 1e-3)},
+        "mra2_global_budget": {"ms_per_step": global_ms, "tokens_per_s": w.B * w.n / (global_ms * 1e-3),
+                               "budget_per_head": w.budget * w.nb - w.nb, "prior": "diagonal"},
         "tflops_step": (tile_flops(w) + coarse_flops(w)) / (ms * 1e-3) / 1e12,
         "wall_s_timed": wall,
     }

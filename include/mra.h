@@ -116,6 +116,23 @@ mra_status_t mra_select(const float* scores, int32_t* idx,
                         int B, int H, int n, int block, int budget, void* stream);
 
 /*
+ * mra_select_global — the selection of Alg. 1 (Sec. 4.2) with one budget for
+ * the whole head (R = {b, 1}): pop the `budget` blocks with the largest
+ * S~[x,y] over all nb x nb blocks of a head, among the blocks that are not
+ * priors; with prior_diagonal = 1 every diagonal block (x, x) is refined as
+ * well (the initial J of Alg. 1, not counted against the budget). Equal
+ * scores: the lower flat index x*nb + y wins.
+ *   scores : [B,H,nb,nb] float32.
+ *   idx    : [B,H,nb,nb] int32 output; row x lists its refined column blocks in
+ *            strictly ascending order, then -1 up to nb entries.
+ *   budget : 0 <= budget <= nb*nb - (prior_diagonal ? nb : 0), per head.
+ *   prior_diagonal : 0 or 1; anything else is MRA_ERR_INVALID_ARG.
+ */
+mra_status_t mra_select_global(const float* scores, int32_t* idx,
+                               int B, int H, int n, int block, int budget,
+                               int prior_diagonal, void* stream);
+
+/*
  * mra_coarse_term — the low-resolution part of A^ V and of the row sums of A^
  * for every block-row: Alg. 2 (Sec. 4.3) at scale b over the blocks NOT in
  * T_x, each block spanning b columns (eq. actual_approx_mat_form):
@@ -123,7 +140,8 @@ mra_status_t mra_select(const float* scores, int32_t* idx,
  *   csum[x]  = sum_{y not in T_x} b * exp(S~[x,y] - M_x)     (0 if none)
  *   cvec[x,:]= sum_{y not in T_x} b * exp(S~[x,y] - M_x) * V~[y,:]
  *   scores : [B,H,nb,nb] float32; idx : [B,H,nb,budget] int32, rows strictly
- *            ascending with entries in [0, nb) (entries outside are ignored);
+ *            ascending in [0, nb); entries outside [0, nb) are ignored (e.g.
+ *            the -1 padding of mra_select_global with budget = nb);
  *   vp     : [B,H,nb,d] float32 pooled V.
  *   cmax, csum : [B,H,nb] float32 outputs; cvec : [B,H,nb,d] float32 output.
  */
@@ -191,6 +209,34 @@ mra_status_t mra_attention_forward(const void* q, const void* k, const void* v, 
                                    int32_t* idx_out, void* workspace, size_t workspace_bytes,
                                    int B, int H, int n, int d, int block, int budget,
                                    mra_dtype_t dtype, void* stream);
+
+/*
+ * mra_forward_global_workspace_bytes — workspace of
+ * mra_attention_forward_global: that of mra_attention_forward with budget nb
+ * plus the coarse logits of every head (B*H*nb*nb*4 bytes). 0 for invalid or
+ * unsupported arguments.
+ */
+size_t mra_forward_global_workspace_bytes(int B, int H, int n, int d, int block,
+                                          mra_dtype_t dtype);
+
+/*
+ * mra_attention_forward_global — MRA-2 with the head-wide budget of
+ * mra_select_global: pooling, coarse logits, head-wide selection, the
+ * low-resolution term over every block a row did not refine, the tile pass
+ * (rows refine different numbers of blocks). Bit-identical to mra_pool,
+ * mra_coarse_scores, mra_select_global, mra_coarse_term and
+ * mra_block_sddmm_spmm called in that order with budget (row width) nb.
+ *   idx_out : optional [B,H,nb,nb] int32 copy of the selection (NULL: kept in
+ *             the workspace only).
+ *   budget, prior_diagonal : as for mra_select_global.
+ *   Other arguments and errors as for mra_attention_forward; workspace of at
+ *   least mra_forward_global_workspace_bytes(...) bytes.
+ */
+mra_status_t mra_attention_forward_global(const void* q, const void* k, const void* v,
+                                          void* out, int32_t* idx_out, void* workspace,
+                                          size_t workspace_bytes, int B, int H, int n, int d,
+                                          int block, int budget, int prior_diagonal,
+                                          mra_dtype_t dtype, void* stream);
 
 /*
  * mra_sparse_attention_forward — the sparse-only variant MRA-2-s (Sec. 5):

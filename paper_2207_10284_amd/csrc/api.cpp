@@ -90,6 +90,28 @@ WsLayout ws_layout(long long bh, int nb, int d, int m, mra_dtype_t dtype) {
   return L;
 }
 
+// The head-wide-budget forward: the forward's layout with nb-wide selection
+// rows, plus the coarse logits of every head (the selection needs all of them).
+struct WsGlobal {
+  WsLayout base;
+  size_t scores, total;
+};
+
+WsGlobal ws_global(long long bh, int nb, int d, mra_dtype_t dtype) {
+  WsGlobal G{};
+  G.base = ws_layout(bh, nb, d, nb, dtype);
+  G.scores = G.base.total;
+  G.total = G.scores + align256((size_t)bh * nb * nb * sizeof(float));
+  return G;
+}
+
+mra_status_t check_global_budget(const Shape& s, int budget, int prior_diagonal) {
+  if (prior_diagonal != 0 && prior_diagonal != 1) return MRA_ERR_INVALID_ARG;
+  const long long nfree = (long long)s.nb * s.nb - (prior_diagonal ? s.nb : 0);
+  if (budget < 0 || budget > nfree) return MRA_ERR_INVALID_ARG;
+  return MRA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -262,6 +284,67 @@ mra_status_t mra_sparse_attention_forward(const void* q, const void* k, const vo
   MRA_TRY(hip_status(mra::launch_select_fused(qp, kp, idx, s.bh, s.nb, d, budget, st)));
   return hip_status(mra::launch_tile(q, k, v, kvpacked, idx, nullptr, nullptr, nullptr, out, s.bh,
                                      n, d, budget, (int)dtype, st));
+}
+
+mra_status_t mra_select_global(const float* scores, int32_t* idx, int B, int H, int n,
+                               int block, int budget, int prior_diagonal, void* stream) {
+  Shape s;
+  MRA_TRY(check_shape(B, H, n, 0, block, false, &s));
+  MRA_TRY(check_global_budget(s, budget, prior_diagonal));
+  if (s.empty) return MRA_OK;
+  MRA_TRY(check_ptr(scores));
+  MRA_TRY(check_ptr(idx));
+  return hip_status(mra::launch_select_global(scores, idx, s.bh, s.nb, budget, prior_diagonal,
+                                              static_cast<hipStream_t>(stream)));
+}
+
+size_t mra_forward_global_workspace_bytes(int B, int H, int n, int d, int block,
+                                          mra_dtype_t dtype) {
+  Shape s;
+  if (check_shape(B, H, n, d, block, true, &s) != MRA_OK) return 0;
+  if (check_dtype(dtype) != MRA_OK) return 0;
+  return ws_global(s.bh, s.nb, d, dtype).total;
+}
+
+mra_status_t mra_attention_forward_global(const void* q, const void* k, const void* v,
+                                          void* out, int32_t* idx_out, void* workspace,
+                                          size_t workspace_bytes, int B, int H, int n, int d,
+                                          int block, int budget, int prior_diagonal,
+                                          mra_dtype_t dtype, void* stream) {
+  Shape s;
+  MRA_TRY(check_shape(B, H, n, d, block, true, &s));
+  MRA_TRY(check_dtype(dtype));
+  MRA_TRY(check_global_budget(s, budget, prior_diagonal));
+  if (s.empty) return MRA_OK;
+  MRA_TRY(check_ptr(q));
+  MRA_TRY(check_ptr(k));
+  MRA_TRY(check_ptr(v));
+  MRA_TRY(check_ptr(out));
+  if (idx_out != nullptr && !aligned16(idx_out)) return MRA_ERR_MISALIGNED;
+  MRA_TRY(check_ptr(workspace));
+  const WsGlobal G = ws_global(s.bh, s.nb, d, dtype);
+  if (workspace_bytes < G.total) return MRA_ERR_WORKSPACE;
+
+  char* ws = static_cast<char*>(workspace);
+  const WsLayout& L = G.base;
+  float* qp = reinterpret_cast<float*>(ws + L.qp);
+  float* kp = reinterpret_cast<float*>(ws + L.kp);
+  float* vp = reinterpret_cast<float*>(ws + L.vp);
+  void* kvpacked = ws + L.kvpacked;
+  int32_t* idx = idx_out ? idx_out : reinterpret_cast<int32_t*>(ws + L.idx);
+  float* cmax = reinterpret_cast<float*>(ws + L.cmax);
+  float* csum = reinterpret_cast<float*>(ws + L.csum);
+  float* cvec = reinterpret_cast<float*>(ws + L.cvec);
+  float* S = reinterpret_cast<float*>(ws + G.scores);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int nb = s.nb;
+
+  MRA_TRY(hip_status(mra::launch_pool(q, k, v, qp, kp, vp, kvpacked, s.bh, n, d, (int)dtype, st)));
+  MRA_TRY(hip_status(mra::launch_coarse(qp, kp, S, s.bh, nb, d, st)));
+  MRA_TRY(hip_status(mra::launch_select_global(S, idx, s.bh, nb, budget, prior_diagonal, st)));
+  MRA_TRY(hip_status(mra::launch_coarse_term(S, idx, vp, cmax, csum, cvec, s.bh, nb, d, nb, st)));
+  return hip_status(mra::launch_tile(q, k, v, kvpacked, idx, cmax, csum, cvec, out, s.bh, n, d, nb,
+                                     (int)dtype, st));
 }
 
 const char* mra_status_str(mra_status_t status) {

@@ -36,6 +36,11 @@ hipError_t launch_coarse_term(const float* S, const int32_t* idx, const float* v
                               float* csum, float* cvec, long long bh, int nb, int d, int m,
                               hipStream_t stream);
 
+// Head-wide selection (one budget per head over all nb x nb blocks, optional
+// diagonal priors) into idx [bh, nb, nb]: ascending rows padded with -1.
+hipError_t launch_select_global(const float* S, int32_t* idx, long long bh, int nb, int budget,
+                                int prior_diagonal, hipStream_t stream);
+
 // Coarse logits and selection in one pass (the logits kept in LDS), for the
 // sparse-only variant; same arithmetic and order as the two calls above.
 hipError_t launch_select_fused(const float* qp, const float* kp, int32_t* idx, long long bh,

@@ -127,9 +127,20 @@ __global__ __launch_bounds__(1024) void rows_kernel(
   uint32_t sel = 0;
   if (active) {
     if constexpr (MODE == kTermOnly) {
-      for (int i = 0; i < m; ++i) {
-        const int y = idx_in[g * m + i];
-        if (y >= 0 && y < nb && (y & 63) == lane) sel |= 1u << (y >> 6);
+      // the row's list (any width, entries outside [0, nb) ignored) as a
+      // bitmap in this wave's part of the chunk buffer, 64 entries per step
+      uint32_t* bm = reinterpret_cast<uint32_t*>(Cb) + w * 64;     // nb <= 2048 bits
+      bm[lane] = 0u;
+      wave_lds_sync();
+      for (int i0 = 0; i0 < m; i0 += kWave) {
+        const int y = i0 + lane < m ? idx_in[g * m + i0 + lane] : -1;
+        if (y >= 0 && y < nb) atomicOr(&bm[y >> 5], 1u << (y & 31));
+      }
+      wave_lds_sync();
+#pragma unroll
+      for (int j = 0; j < JMAX; ++j) {
+        const int y = kChunk * j + lane;
+        if (j < J && y < nb && ((bm[y >> 5] >> (y & 31)) & 1u)) sel |= 1u << j;
       }
     } else {
       uint32_t key[JMAX];

@@ -63,6 +63,26 @@ struct TileCfg {
 // 16-way max, no cross-lane exchange and no branch that rescales O.
 constexpr float kWeightCap = 0x1p64f;
 
+// Copies a row's selection list into LDS keeping only the entries in [0, nb),
+// in their order, and returns how many there are (wave-uniform). Reading the
+// block ids from LDS keeps them off the vector-memory counter, so prefetched
+// tile loads stay in flight; dropping entries outside [0, nb) here (the
+// padding of a head-wide selection, for instance) keeps them out of the loop.
+__device__ __forceinline__ int stage_selection(const int32_t* __restrict__ row, int m, int nb,
+                                               int32_t* dst) {
+  const int lane = lane_id();
+  int cnt = 0;
+  for (int i0 = 0; i0 < m; i0 += kWave) {
+    const int y = i0 + lane < m ? row[i0 + lane] : -1;
+    const bool ok = y >= 0 && y < nb;
+    const uint64_t mk = __ballot(ok);
+    if (ok) dst[cnt + __popcll(mk & lanemask_lt())] = y;
+    cnt += __popcll(mk);
+  }
+  wave_lds_sync();
+  return wave_uniform(cnt);
+}
+
 __device__ __forceinline__ float tile_max(const f32x16& s) {
   float a = s[0];
 #pragma unroll
@@ -280,12 +300,9 @@ __global__ __launch_bounds__((TileCfg<DT, D>::kWaves * kWave)) void tile_kernel(
   const int x = (int)(g - bh * nb);
   const long long hoff = bh * (long long)n * D;
   const elem* K = reinterpret_cast<const elem*>(kv) + hoff;
-  // The row's selection, staged once in LDS: reading block ids from LDS keeps
-  // them off the vector-memory counter, so prefetched K/V loads stay in flight.
   extern __shared__ int32_t sidx_all[];
   int32_t* myidx = sidx_all + w * m;
-  for (int i = lane; i < m; i += kWave) myidx[i] = idx[g * m + i];
-  wave_lds_sync();
+  m = stage_selection(idx + g * m, m, nb, myidx);  // valid entries only, in order
 
   TileRow<DT, D, COARSE> row;
   row.init(reinterpret_cast<const elem*>(qv) + hoff, x, scale_log2);
@@ -482,8 +499,7 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
   const int x = (int)(g - bh * nb);
   const long long hoff = bh * (long long)n * D;
   int32_t* myidx = sidx_all + w * m;
-  for (int i = lane; i < m; i += kWave) myidx[i] = idx[g * m + i];
-  wave_lds_sync();
+  m = stage_selection(idx + g * m, m, nb, myidx);  // valid entries only, in order
 
   TileRow<DT, D, COARSE> row;
   row.init(reinterpret_cast<const elem*>(qv) + hoff, x, scale_log2);

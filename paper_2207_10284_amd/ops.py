@@ -33,6 +33,9 @@ SIGNATURES = {
     "mra_forward_workspace_bytes": (_Z, [_I, _I, _I, _I, _I, _I, _I]),
     "mra_attention_forward": (_I, [_P, _P, _P, _P, _P, _P, _Z, _I, _I, _I, _I, _I, _I, _I, _P]),
     "mra_sparse_attention_forward": (_I, [_P, _P, _P, _P, _P, _P, _Z, _I, _I, _I, _I, _I, _I, _I, _P]),
+    "mra_select_global": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, _P]),
+    "mra_forward_global_workspace_bytes": (_Z, [_I, _I, _I, _I, _I, _I]),
+    "mra_attention_forward_global": (_I, [_P, _P, _P, _P, _P, _P, _Z, _I, _I, _I, _I, _I, _I, _I, _I, _P]),
     "mra_status_str": (ctypes.c_char_p, [_I]),
     "mra_last_hip_error": (_I, []),
 }
@@ -139,6 +142,18 @@ def select(scores, budget: int):
     return idx
 
 
+def select_global(scores, budget: int, prior_diagonal: bool = False):
+    """Head-wide selection of Alg. 1: the `budget` best blocks of each head
+    (plus the diagonal blocks with ``prior_diagonal``); int32 [B, H, nb, nb],
+    each row ascending, padded with -1."""
+    B, H, nb, _ = scores.shape
+    _check_f32(scores, (B, H, nb, nb), "scores")
+    idx = torch.empty(B, H, nb, nb, device=scores.device, dtype=torch.int32)
+    _call("mra_select_global", _ptr(scores), _ptr(idx), B, H, nb * BLOCK, BLOCK, budget,
+          int(bool(prior_diagonal)), _stream(scores.device))
+    return idx
+
+
 def _check_idx(idx, B, H, nb, budget, device):
     if idx.dtype != torch.int32 or tuple(idx.shape) != (B, H, nb, budget) or not idx.is_contiguous() \
             or idx.device != device:
@@ -212,4 +227,30 @@ def _forward(entry, q, k, v, budget, out, idx_out, workspace):
     _call(entry, _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(idx_out),
           _ptr(workspace), workspace.numel() * workspace.element_size(),
           B, H, n, d, BLOCK, budget, _dtype_code(ref), _stream(ref.device))
+    return out
+
+
+def forward_global_workspace_bytes(B: int, H: int, n: int, d: int, dtype=torch.bfloat16) -> int:
+    code = MRA_BF16 if dtype == torch.bfloat16 else MRA_F32
+    return int(load().mra_forward_global_workspace_bytes(B, H, n, d, BLOCK, code))
+
+
+def attention_forward_global(q, k, v, budget: int, prior_diagonal: bool = False, out=None, idx_out=None,
+                             workspace=None):
+    """MRA-2 with the head-wide budget of Alg. 1 (``budget`` blocks per head,
+    plus the diagonal with ``prior_diagonal``). Returns Z; the selection
+    (int32 [B, H, nb, nb], rows padded with -1) goes to ``idx_out`` when given."""
+    ref = _check_qkv(q, k, v)
+    B, H, n, d = ref.shape
+    nb = n // BLOCK
+    if out is None:
+        out = torch.empty_like(ref)
+    if idx_out is not None:
+        _check_idx(idx_out, B, H, nb, nb, ref.device)
+    need = forward_global_workspace_bytes(B, H, n, d, ref.dtype)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), device=ref.device, dtype=torch.uint8)
+    _call("mra_attention_forward_global", _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(idx_out),
+          _ptr(workspace), workspace.numel() * workspace.element_size(),
+          B, H, n, d, BLOCK, budget, int(bool(prior_diagonal)), _dtype_code(ref), _stream(ref.device))
     return out

@@ -49,3 +49,33 @@ def check_selection(gpu_idx, S_ref, m, band=TIE_BAND):
         for y in set(g.tolist()) ^ set(ref[x].tolist()):
             assert abs(S_ref[x, y] - tau) <= band * scale, (x, y, S_ref[x, y], tau)
     return differ
+
+
+def check_selection_global(gpu_idx, S_ref, budget, prior_diagonal, band=TIE_BAND):
+    """GPU head-wide selection ([nb, nb] rows padded with -1) for one head with
+    float64 scores S_ref: rows strictly ascending and padded; priors present;
+    equal to the oracle's set except blocks whose score lies within `band`
+    (relative to the head's scale) of the budget-th largest non-prior score.
+    Returns the number of blocks that differ."""
+    gpu_idx = np.asarray(gpu_idx)
+    nb = S_ref.shape[0]
+    got = set()
+    for x in range(nb):
+        row = gpu_idx[x]
+        k = int((row >= 0).sum())
+        assert (row[k:] == -1).all() and (row[:k] >= 0).all() and (row[:k] < nb).all(), row
+        assert (np.diff(row[:k]) > 0).all(), row
+        got |= {x * nb + int(y) for y in row[:k]}
+    ref_idx = O.select_global(S_ref, budget, prior_diagonal)
+    want = {x * nb + int(y) for x in range(nb) for y in ref_idx[x] if y >= 0}
+    if prior_diagonal:
+        assert {x * nb + x for x in range(nb)} <= got
+    assert len(got) == len(want)
+    diff = got ^ want
+    if diff:
+        free = np.array([S_ref.ravel()[f] for f in range(nb * nb) if not (prior_diagonal and f // nb == f % nb)])
+        tau = np.sort(free)[::-1][budget - 1]
+        scale = max(abs(tau), np.abs(S_ref).max())
+        for f in diff:
+            assert abs(S_ref.ravel()[f] - tau) <= band * scale, (f, S_ref.ravel()[f], tau)
+    return len(diff)

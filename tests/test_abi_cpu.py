@@ -31,7 +31,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 10, names
+    assert len(names) == 13, names
     for name in names:
         assert hasattr(lib, name), name
     assert set(names) == set(ops.SIGNATURES)
@@ -111,6 +111,45 @@ def test_workspace_bytes(lib):
         want = 3 * al(bh * nb * d * 4) + al(2 * bh * n * d * e) + al(bh * nb * m * 4) \
             + 2 * al(bh * nb * 4) + al(bh * nb * d * 4)
         assert f(B, H, n, d, 32, m, dt) == want
+
+
+def test_global_workspace_bytes(lib):
+    f = lib.mra_forward_global_workspace_bytes
+    assert f(1, 1, 64, 48, 32, 1) == 0
+    assert f(1, 1, 64, 64, 16, 1) == 0
+    assert f(1, 1, 64, 64, 32, 9) == 0
+    al = lambda x: (x + 255) // 256 * 256
+    B, H, n, d = 8, 12, 4096, 64
+    bh, nb = B * H, n // 32
+    for dt in (0, 1):
+        want = lib.mra_forward_workspace_bytes(B, H, n, d, 32, nb, dt) + al(bh * nb * nb * 4)
+        assert f(B, H, n, d, 32, dt) == want
+
+
+def test_global_selection_validation(lib):
+    """Head-wide budget: 0 <= budget <= nb*nb (minus the nb diagonal priors),
+    prior flag 0 or 1; the forward checks like mra_attention_forward."""
+    sg = lambda scores=A, idx=A, B=1, H=1, n=128, budget=1, prior=0: \
+        lib.mra_select_global(scores, idx, B, H, n, 32, budget, prior, None)
+    assert sg(budget=-1) == INVALID
+    assert sg(budget=17) == INVALID            # nb = 4
+    assert sg(budget=13, prior=1) == INVALID   # 16 - 4 diagonal priors
+    assert sg(prior=2) == INVALID
+    assert sg(scores=None) == INVALID
+    assert sg(idx=MIS) == MISALIGNED
+    assert sg(n=48) == INVALID
+    assert sg(B=0, scores=None, idx=None) == OK
+    fg = lambda q=A, out=A, ws=A, wsb=1 << 40, n=128, d=64, budget=1, prior=0, dtype=1: \
+        lib.mra_attention_forward_global(q, A, A, out, None, ws, wsb, 1, 1, n, d, 32, budget, prior, dtype, None)
+    assert fg(budget=17) == INVALID
+    assert fg(prior=-1) == INVALID
+    assert fg(d=48) == UNSUPPORTED
+    assert fg(q=None) == INVALID
+    assert fg(ws=MIS) == MISALIGNED
+    need = lib.mra_forward_global_workspace_bytes(1, 1, 128, 64, 32, 1)
+    assert fg(wsb=need - 1) == WORKSPACE
+    assert fg(n=0, budget=0, q=None, out=None, ws=None) == OK
+    assert lib.mra_last_hip_error() == 0
 
 
 def test_step_validation(lib):
