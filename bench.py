@@ -129,6 +129,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default=None)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-baseline leg")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip timing MRA-2-s and the head-wide budget (profiling runs)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (the path has no multi-GPU mode); got --gpus {args.gpus}",
@@ -168,15 +170,22 @@ def main():
 
     # The sparse-only variant MRA-2-s (Sec. 5) on the same inputs: reported
     # beside the headline, which is MRA-2.
-    sparse_ms = time_launches(lambda: ops.sparse_attention_forward(tq, tk, tv, w.budget, out=out, idx_out=idx,
-                                                                   workspace=ws), max(args.steps, 20))
+    variants = {}
+    if not args.no_variants:
+        sparse_ms = time_launches(lambda: ops.sparse_attention_forward(tq, tk, tv, w.budget, out=out, idx_out=idx,
+                                                                       workspace=ws), max(args.steps, 20))
+        variants["mra2s"] = {"ms_per_step": sparse_ms, "tokens_per_s": w.B * w.n / (sparse_ms * 1e-3)}
 
     # MRA-2 with the head-wide budget of Alg. 1 (same total: m * nb blocks per
     # head, the nb diagonal blocks as priors), reported beside the headline.
-    gidx = torch.empty(w.B, w.H, w.nb, w.nb, dtype=torch.int32, device=dev)
-    gws = torch.empty(ops.forward_global_workspace_bytes(w.B, w.H, w.n, w.d, tdt), dtype=torch.uint8, device=dev)
-    global_ms = time_launches(lambda: ops.attention_forward_global(tq, tk, tv, w.budget * w.nb - w.nb, True, out=out,
-                                                                   idx_out=gidx, workspace=gws), max(args.steps, 20))
+    if not args.no_variants:
+        gidx = torch.empty(w.B, w.H, w.nb, w.nb, dtype=torch.int32, device=dev)
+        gws = torch.empty(ops.forward_global_workspace_bytes(w.B, w.H, w.n, w.d, tdt), dtype=torch.uint8, device=dev)
+        gb = w.budget * w.nb - w.nb
+        global_ms = time_launches(lambda: ops.attention_forward_global(tq, tk, tv, gb, True, out=out, idx_out=gidx,
+                                                                       workspace=gws), max(args.steps, 20))
+        variants["mra2_global_budget"] = {"ms_per_step": global_ms, "tokens_per_s": w.B * w.n / (global_ms * 1e-3),
+                                          "budget_per_head": gb, "prior": "diagonal"}
 
     # Dominant kernel: the tile pass, the same instantiation as inside the
     # forward (packed K/V, coarse term given), on the same inputs; timed alone.
@@ -210,9 +219,7 @@ def main():
                       "coarse_scores_stepwise": coarse_ms * 1e3},
         "pool_roofline": {"bound": "hbm", "achieved": pool_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                           "frac": pool_gbs / PEAK_HBM_GBS, "bytes_per_launch": pool_bytes(w)},
-        "mra2s": {"ms_per_step": sparse_ms, "tokens_per_s": w.B * w.n / (sparse_ms * 1e-3)},
-        "mra2_global_budget": {"ms_per_step": global_ms, "tokens_per_s": w.B * w.n / (global_ms * 1e-3),
-                               "budget_per_head": w.budget * w.nb - w.nb, "prior": "diagonal"},
+        **variants,
         "tflops_step": (tile_flops(w) + coarse_flops(w)) / (ms * 1e-3) / 1e12,
         "wall_s_timed": wall,
     }
