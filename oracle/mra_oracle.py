@@ -295,6 +295,52 @@ def mra2s_batched(q, k, v, b, m, idx=None):
 
 
 # --------------------------------------------------------------------------
+# Gradients of the MRA-2 output (the selection held fixed): the factored form
+# written with torch float64 CPU operations and differentiated by autograd
+# --------------------------------------------------------------------------
+def mra_torch(q, k, v, b, idx):
+    """Z for one head as a differentiable function of q, k, v (torch float64
+    tensors [n, d]) for a fixed selection `idx` (rows of block ids; entries
+    outside [0, nb) ignored). Block-row x's queries take the softmax over the
+    fine logits of its refined blocks' columns and the coarse logits
+    S~[x, y] + log b of the others (b e^{S~} is e^{S~ + log b}), applied to
+    the rows of V and the pooled rows V~ respectively (Alg. 2, eq.
+    actual_approx_mat_form)."""
+    import torch
+    n, d = q.shape
+    nb = n // b
+    qp = q.reshape(nb, b, d).mean(dim=1)
+    kp = k.reshape(nb, b, d).mean(dim=1)
+    vp = v.reshape(nb, b, v.shape[1]).mean(dim=1)
+    S = qp @ kp.T / math.sqrt(d)
+    rows = []
+    for x in range(nb):
+        sel = [int(y) for y in idx[x] if 0 <= int(y) < nb]
+        rest = [y for y in range(nb) if y not in set(sel)]
+        cols = [j for y in sel for j in range(y * b, (y + 1) * b)]
+        parts_l, parts_v = [], []
+        if cols:
+            parts_l.append(q[x * b:(x + 1) * b] @ k[cols].T / math.sqrt(d))
+            parts_v.append(v[cols])
+        if rest:
+            parts_l.append((S[x, rest] + math.log(b)).expand(b, len(rest)))
+            parts_v.append(vp[rest])
+        w = torch.softmax(torch.cat(parts_l, dim=1), dim=1)
+        rows.append(w @ torch.cat(parts_v, dim=0))
+    return torch.cat(rows, dim=0)
+
+
+def mra_grads(q, k, v, g, b, idx):
+    """(dq, dk, dv) = the gradient of sum(g * Z) for one head, Z = mra_torch
+    under the fixed selection idx. Arrays in, float64 numpy arrays out."""
+    import torch
+    tq, tk, tv = (torch.tensor(np.asarray(a, dtype=np.float64), requires_grad=True) for a in (q, k, v))
+    Z = mra_torch(tq, tk, tv, b, idx)
+    Z.backward(torch.tensor(np.asarray(g, dtype=np.float64)))
+    return tq.grad.numpy(), tk.grad.numpy(), tv.grad.numpy()
+
+
+# --------------------------------------------------------------------------
 # Sec. 3.1, eq. softmax-attention: exact attention (scale 1/sqrt(d))
 # --------------------------------------------------------------------------
 def exact_attention(q, k, v):

@@ -466,3 +466,52 @@ def test_global_full_budget_is_exact_and_dense_agrees():
         w = np.exp(slab - slab.max(axis=1, keepdims=True))
         np.testing.assert_allclose(Z[x * b:(x + 1) * b], (w @ v) / w.sum(axis=1, keepdims=True),
                                    rtol=1e-12, atol=1e-13)
+
+
+# ---------------------------------------------------------------- gradients (selection fixed)
+def test_mra_torch_forward_matches_factored():
+    r = _rng(100)
+    n, b, d, m = 128, 16, 8, 3
+    q, k, v = (r.standard_normal((n, d)) for _ in range(3))
+    Z, idx = O.mra_factored(q, k, v, b, m)
+    Zt = O.mra_torch(*(torch.from_numpy(a) for a in (q, k, v)), b, idx).numpy()
+    np.testing.assert_allclose(Zt, Z, rtol=1e-13, atol=1e-14)
+    # ragged rows (head-wide selection) and an empty row
+    idx_g = O.select_global(O.coarse_logits(O.block_mean(q, b), O.block_mean(k, b)), 9)
+    Zg, _ = O.mra_global(q, k, v, b, 9, idx=idx_g)
+    Zt = O.mra_torch(*(torch.from_numpy(a) for a in (q, k, v)), b, idx_g).numpy()
+    np.testing.assert_allclose(Zt, Zg, rtol=1e-13, atol=1e-14)
+
+
+@pytest.mark.parametrize("n,b,d,m", [(12, 4, 3, 1), (16, 4, 2, 2), (16, 8, 3, 0)])
+def test_mra_grads_finite_differences(n, b, d, m):
+    """The autograd gradient against central finite differences of
+    sum(g * Z) (float64, selection fixed)."""
+    r = _rng(110 + n + m)
+    q, k, v, g = (r.standard_normal((n, d)) for _ in range(4))
+    idx = O.select_blocks(O.coarse_logits(O.block_mean(q, b), O.block_mean(k, b)), m)
+    dq, dk, dv = O.mra_grads(q, k, v, g, b, idx)
+    f = lambda qq, kk, vv: float((O.mra_factored(qq, kk, vv, b, m, idx=idx)[0] * g).sum())
+    h = 1e-6
+    for arr, grad, which in ((q, dq, 0), (k, dk, 1), (v, dv, 2)):
+        num = np.zeros_like(arr)
+        for i in range(n):
+            for j in range(d):
+                a1 = [q.copy(), k.copy(), v.copy()]; a2 = [q.copy(), k.copy(), v.copy()]
+                a1[which][i, j] += h; a2[which][i, j] -= h
+                num[i, j] = (f(*a1) - f(*a2)) / (2 * h)
+        np.testing.assert_allclose(grad, num, rtol=1e-6, atol=1e-7)
+
+
+def test_mra_grads_full_budget_are_attention_grads():
+    """With every block refined the gradients are those of softmax attention
+    (torch scaled_dot_product_attention in float64)."""
+    r = _rng(120)
+    n, b, d = 64, 16, 8
+    q, k, v, g = (r.standard_normal((n, d)) for _ in range(4))
+    idx = np.tile(np.arange(n // b), (n // b, 1))
+    dq, dk, dv = O.mra_grads(q, k, v, g, b, idx)
+    tq, tk, tv = (torch.tensor(a, requires_grad=True) for a in (q, k, v))
+    torch.nn.functional.scaled_dot_product_attention(tq[None], tk[None], tv[None])[0].backward(torch.from_numpy(g))
+    for a, t in ((dq, tq), (dk, tk), (dv, tv)):
+        np.testing.assert_allclose(a, t.grad.numpy(), rtol=1e-11, atol=1e-12)
