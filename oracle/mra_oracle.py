@@ -28,6 +28,11 @@ listed with their reasons in the design notes.
 The sparse-only variant MRA-2-s (Sec. 5: only the scale-1 components over the
 selected blocks, normalised by their own row sums) is ``mra2s_rows``.
 
+Gradients with the selection held fixed (``mra_grads``) differentiate the
+factored form written with torch float64 CPU operations (``mra_torch``, which
+can also leave out the coarse part: MRA-2-s); ``mra_lse`` gives each query's
+log normaliser, the natural log of its row sum of A^.
+
 Two forms of the output are provided: the dense definition over the full
 logit slab of each block-row (``mra_dense``) and the factored form of Alg. 2
 (``mra_factored``), where the unselected blocks contribute b*exp(S~)*V~_y.
@@ -298,14 +303,15 @@ def mra2s_batched(q, k, v, b, m, idx=None):
 # Gradients of the MRA-2 output (the selection held fixed): the factored form
 # written with torch float64 CPU operations and differentiated by autograd
 # --------------------------------------------------------------------------
-def mra_torch(q, k, v, b, idx):
+def mra_torch(q, k, v, b, idx, coarse=True):
     """Z for one head as a differentiable function of q, k, v (torch float64
     tensors [n, d]) for a fixed selection `idx` (rows of block ids; entries
     outside [0, nb) ignored). Block-row x's queries take the softmax over the
     fine logits of its refined blocks' columns and the coarse logits
     S~[x, y] + log b of the others (b e^{S~} is e^{S~ + log b}), applied to
     the rows of V and the pooled rows V~ respectively (Alg. 2, eq.
-    actual_approx_mat_form)."""
+    actual_approx_mat_form). With coarse=False the coarse part is left out:
+    the sparse-only variant MRA-2-s (Sec. 5)."""
     import torch
     n, d = q.shape
     nb = n // b
@@ -316,7 +322,7 @@ def mra_torch(q, k, v, b, idx):
     rows = []
     for x in range(nb):
         sel = [int(y) for y in idx[x] if 0 <= int(y) < nb]
-        rest = [y for y in range(nb) if y not in set(sel)]
+        rest = [y for y in range(nb) if y not in set(sel)] if coarse else []
         cols = [j for y in sel for j in range(y * b, (y + 1) * b)]
         parts_l, parts_v = [], []
         if cols:
@@ -330,14 +336,40 @@ def mra_torch(q, k, v, b, idx):
     return torch.cat(rows, dim=0)
 
 
-def mra_grads(q, k, v, g, b, idx):
+def mra_grads(q, k, v, g, b, idx, coarse=True):
     """(dq, dk, dv) = the gradient of sum(g * Z) for one head, Z = mra_torch
     under the fixed selection idx. Arrays in, float64 numpy arrays out."""
     import torch
     tq, tk, tv = (torch.tensor(np.asarray(a, dtype=np.float64), requires_grad=True) for a in (q, k, v))
-    Z = mra_torch(tq, tk, tv, b, idx)
+    Z = mra_torch(tq, tk, tv, b, idx, coarse)
     Z.backward(torch.tensor(np.asarray(g, dtype=np.float64)))
     return tq.grad.numpy(), tk.grad.numpy(), tv.grad.numpy()
+
+
+def mra_lse(q, k, b, idx, coarse=True):
+    """Each query's log normaliser L_i = ln(sum of row i of A^): the fine
+    terms exp(P_ij) of its refined blocks plus, with coarse=True, b exp(S~)
+    for every other block (eq. actual_approx_mat_form; the row sums that
+    D^ of Sec. 3.1 divides by). Taken with a max shift; float64 [n]."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    n, d = q.shape
+    nb = n // b
+    S = coarse_logits(block_mean(q, b), block_mean(k, b))
+    L = np.empty(n)
+    for x in range(nb):
+        sel = [int(y) for y in idx[x] if 0 <= int(y) < nb]
+        rest = [y for y in range(nb) if y not in set(sel)] if coarse else []
+        cols = [j for y in sel for j in range(y * b, (y + 1) * b)]
+        parts = []
+        if cols:
+            parts.append(q[x * b:(x + 1) * b] @ k[cols].T / math.sqrt(d))
+        if rest:
+            parts.append(np.broadcast_to(S[x, rest] + math.log(b), (b, len(rest))))
+        logits = np.concatenate(parts, axis=1)
+        mx = logits.max(axis=1)
+        L[x * b:(x + 1) * b] = mx + np.log(np.exp(logits - mx[:, None]).sum(axis=1))
+    return L
 
 
 # --------------------------------------------------------------------------

@@ -515,3 +515,82 @@ def test_mra_grads_full_budget_are_attention_grads():
     torch.nn.functional.scaled_dot_product_attention(tq[None], tk[None], tv[None])[0].backward(torch.from_numpy(g))
     for a, t in ((dq, tq), (dk, tk), (dv, tv)):
         np.testing.assert_allclose(a, t.grad.numpy(), rtol=1e-11, atol=1e-12)
+
+
+def test_mra_torch_sparse_matches_mra2s():
+    """coarse=False drops the low-resolution part: the MRA-2-s forward."""
+    r = _rng(130)
+    n, b, d, m = 96, 16, 8, 2
+    q, k, v = (r.standard_normal((n, d)) for _ in range(3))
+    Z, idx = O.mra2s_rows(q, k, v, b, m)
+    Zt = O.mra_torch(*(torch.from_numpy(a) for a in (q, k, v)), b, idx, coarse=False).numpy()
+    np.testing.assert_allclose(Zt, Z, rtol=1e-13, atol=1e-14)
+
+
+@pytest.mark.parametrize("n,b,d,m", [(12, 4, 3, 1), (16, 4, 2, 2)])
+def test_mra2s_grads_finite_differences(n, b, d, m):
+    """MRA-2-s gradients against central finite differences of the MRA-2-s
+    forward (selection fixed)."""
+    r = _rng(140 + n + m)
+    q, k, v, g = (r.standard_normal((n, d)) for _ in range(4))
+    idx = O.select_blocks(O.coarse_logits(O.block_mean(q, b), O.block_mean(k, b)), m)
+    dq, dk, dv = O.mra_grads(q, k, v, g, b, idx, coarse=False)
+    f = lambda qq, kk, vv: float((O.mra2s_rows(qq, kk, vv, b, m, idx=idx)[0] * g).sum())
+    h = 1e-6
+    for arr, grad, which in ((q, dq, 0), (k, dk, 1), (v, dv, 2)):
+        num = np.zeros_like(arr)
+        for i in range(n):
+            for j in range(d):
+                a1 = [q.copy(), k.copy(), v.copy()]; a2 = [q.copy(), k.copy(), v.copy()]
+                a1[which][i, j] += h; a2[which][i, j] -= h
+                num[i, j] = (f(*a1) - f(*a2)) / (2 * h)
+        np.testing.assert_allclose(grad, num, rtol=1e-6, atol=1e-7)
+
+
+def test_mra2s_grads_full_budget_are_attention_grads():
+    r = _rng(150)
+    n, b, d = 64, 16, 8
+    q, k, v, g = (r.standard_normal((n, d)) for _ in range(4))
+    idx = np.tile(np.arange(n // b), (n // b, 1))
+    dq, dk, dv = O.mra_grads(q, k, v, g, b, idx, coarse=False)
+    tq, tk, tv = (torch.tensor(a, requires_grad=True) for a in (q, k, v))
+    torch.nn.functional.scaled_dot_product_attention(tq[None], tk[None], tv[None])[0].backward(torch.from_numpy(g))
+    for a, t in ((dq, tq), (dk, tk), (dv, tv)):
+        np.testing.assert_allclose(a, t.grad.numpy(), rtol=1e-11, atol=1e-12)
+
+
+def test_mra_lse_is_log_row_sum_of_dense_approximation():
+    """L_i against the log of the row sums of the dense A^ (the dense
+    definition, built entry by entry), for per-row and head-wide selections."""
+    r = _rng(160)
+    n, b, d = 64, 8, 4
+    q, k = r.standard_normal((n, d)), r.standard_normal((n, d))
+    S = O.coarse_logits(O.block_mean(q, b), O.block_mean(k, b))
+    for idx in (O.select_blocks(S, 3), O.select_blocks(S, 0)):
+        np.testing.assert_allclose(O.mra_lse(q, k, b, idx), np.log(O.approx_matrix(q, k, b, idx).sum(axis=1)),
+                                   rtol=1e-13, atol=1e-13)
+    idx_g = O.select_global(S, 11, True)
+    dense = O.approx_matrix(q, k, b, O.rows_of(idx_g))
+    np.testing.assert_allclose(O.mra_lse(q, k, b, idx_g), np.log(dense.sum(axis=1)), rtol=1e-13, atol=1e-13)
+
+
+def test_mra_lse_special_cases():
+    """Full budget: scipy's logsumexp of the exact logits. Sparse only: the
+    logsumexp of the logits masked to the refined blocks (scipy's weighted
+    form). Large logits stay finite."""
+    from scipy.special import logsumexp
+    r = _rng(170)
+    n, b, d = 96, 16, 8
+    q, k = r.standard_normal((n, d)), r.standard_normal((n, d))
+    P = q @ k.T / math.sqrt(d)
+    full = np.tile(np.arange(n // b), (n // b, 1))
+    np.testing.assert_allclose(O.mra_lse(q, k, b, full), logsumexp(P, axis=1), rtol=1e-13)
+    S = O.coarse_logits(O.block_mean(q, b), O.block_mean(k, b))
+    idx = O.select_blocks(S, 2)
+    mask = np.zeros((n, n))
+    for x in range(n // b):
+        for y in idx[x]:
+            mask[x * b:(x + 1) * b, y * b:(y + 1) * b] = 1.0
+    np.testing.assert_allclose(O.mra_lse(q, k, b, idx, coarse=False), logsumexp(P, axis=1, b=mask), rtol=1e-13)
+    big = O.mra_lse(q * 60, k * 60, b, idx)
+    assert np.isfinite(big).all() and big.max() > 500
