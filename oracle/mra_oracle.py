@@ -303,7 +303,7 @@ def mra2s_batched(q, k, v, b, m, idx=None):
 # Gradients of the MRA-2 output (the selection held fixed): the factored form
 # written with torch float64 CPU operations and differentiated by autograd
 # --------------------------------------------------------------------------
-def mra_torch(q, k, v, b, idx, coarse=True):
+def mra_torch(q, k, v, b, idx, coarse=True, rows=None):
     """Z for one head as a differentiable function of q, k, v (torch float64
     tensors [n, d]) for a fixed selection `idx` (rows of block ids; entries
     outside [0, nb) ignored). Block-row x's queries take the softmax over the
@@ -311,7 +311,8 @@ def mra_torch(q, k, v, b, idx, coarse=True):
     S~[x, y] + log b of the others (b e^{S~} is e^{S~ + log b}), applied to
     the rows of V and the pooled rows V~ respectively (Alg. 2, eq.
     actual_approx_mat_form). With coarse=False the coarse part is left out:
-    the sparse-only variant MRA-2-s (Sec. 5)."""
+    the sparse-only variant MRA-2-s (Sec. 5). With `rows`, only those
+    block-rows' outputs, stacked in that order."""
     import torch
     n, d = q.shape
     nb = n // b
@@ -319,10 +320,11 @@ def mra_torch(q, k, v, b, idx, coarse=True):
     kp = k.reshape(nb, b, d).mean(dim=1)
     vp = v.reshape(nb, b, v.shape[1]).mean(dim=1)
     S = qp @ kp.T / math.sqrt(d)
-    rows = []
-    for x in range(nb):
+    out = []
+    for x in (range(nb) if rows is None else rows):
         sel = [int(y) for y in idx[x] if 0 <= int(y) < nb]
-        rest = [y for y in range(nb) if y not in set(sel)] if coarse else []
+        chosen = set(sel)
+        rest = [y for y in range(nb) if y not in chosen] if coarse else []
         cols = [j for y in sel for j in range(y * b, (y + 1) * b)]
         parts_l, parts_v = [], []
         if cols:
@@ -332,17 +334,23 @@ def mra_torch(q, k, v, b, idx, coarse=True):
             parts_l.append((S[x, rest] + math.log(b)).expand(b, len(rest)))
             parts_v.append(vp[rest])
         w = torch.softmax(torch.cat(parts_l, dim=1), dim=1)
-        rows.append(w @ torch.cat(parts_v, dim=0))
-    return torch.cat(rows, dim=0)
+        out.append(w @ torch.cat(parts_v, dim=0))
+    return torch.cat(out, dim=0)
 
 
-def mra_grads(q, k, v, g, b, idx, coarse=True):
+def mra_grads(q, k, v, g, b, idx, coarse=True, rows=None):
     """(dq, dk, dv) = the gradient of sum(g * Z) for one head, Z = mra_torch
-    under the fixed selection idx. Arrays in, float64 numpy arrays out."""
+    under the fixed selection idx. Arrays in, float64 numpy arrays out. With
+    `rows`, the loss covers only those block-rows (g still [n, d]; its other
+    rows unused); block-row x's output depends on Q only through Q's rows in
+    block x, so dq on those rows is then the full gradient's."""
     import torch
     tq, tk, tv = (torch.tensor(np.asarray(a, dtype=np.float64), requires_grad=True) for a in (q, k, v))
-    Z = mra_torch(tq, tk, tv, b, idx, coarse)
-    Z.backward(torch.tensor(np.asarray(g, dtype=np.float64)))
+    Z = mra_torch(tq, tk, tv, b, idx, coarse, rows)
+    gt = torch.tensor(np.asarray(g, dtype=np.float64))
+    if rows is not None:
+        gt = torch.cat([gt[x * b:(x + 1) * b] for x in rows], dim=0)
+    Z.backward(gt)
     return tq.grad.numpy(), tk.grad.numpy(), tv.grad.numpy()
 
 
@@ -359,7 +367,8 @@ def mra_lse(q, k, b, idx, coarse=True):
     L = np.empty(n)
     for x in range(nb):
         sel = [int(y) for y in idx[x] if 0 <= int(y) < nb]
-        rest = [y for y in range(nb) if y not in set(sel)] if coarse else []
+        chosen = set(sel)
+        rest = [y for y in range(nb) if y not in chosen] if coarse else []
         cols = [j for y in sel for j in range(y * b, (y + 1) * b)]
         parts = []
         if cols:

@@ -594,3 +594,26 @@ def test_mra_lse_special_cases():
     np.testing.assert_allclose(O.mra_lse(q, k, b, idx, coarse=False), logsumexp(P, axis=1, b=mask), rtol=1e-13)
     big = O.mra_lse(q * 60, k * 60, b, idx)
     assert np.isfinite(big).all() and big.max() > 500
+
+
+def test_mra_grads_rows_subset():
+    """Restricting the loss to some block-rows leaves dq on those rows equal to
+    the full gradient's (block-row x's output reads Q only through block x),
+    and the restricted forward stacks exactly those rows of the full one."""
+    r = _rng(180)
+    n, b, d, m = 128, 16, 8, 2
+    q, k, v, g = (r.standard_normal((n, d)) for _ in range(4))
+    idx = O.select_blocks(O.coarse_logits(O.block_mean(q, b), O.block_mean(k, b)), m)
+    rows = [6, 1, 3]
+    tq, tk, tv = (torch.from_numpy(a) for a in (q, k, v))
+    full = O.mra_torch(tq, tk, tv, b, idx).numpy()
+    part = O.mra_torch(tq, tk, tv, b, idx, rows=rows).numpy()
+    np.testing.assert_array_equal(part, np.concatenate([full[x * b:(x + 1) * b] for x in rows]))
+    dq, _, _ = O.mra_grads(q, k, v, g, b, idx)
+    dq_r, _, _ = O.mra_grads(q, k, v, g, b, idx, rows=rows)
+    for x in range(n // b):
+        blk = slice(x * b, (x + 1) * b)
+        if x in rows:
+            np.testing.assert_allclose(dq_r[blk], dq[blk], rtol=1e-12, atol=1e-13)
+        else:
+            assert not dq_r[blk].any()
