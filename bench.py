@@ -6,7 +6,9 @@ One step = one mra_attention_forward call (pool, coarse logits, selection with
 the coarse term, tile pass) over the whole workload, inputs resident in HBM.
 Prints one JSON line with tokens/s, the roofline of the dominant kernel (the
 tile pass, timed with HIP events on the stream it runs on) and the float64
-oracle timed on the host as a reported CPU baseline.
+oracle timed on the host as a reported CPU baseline. Beside the headline it
+reports MRA-2-s, the head-wide budget and the gradient pass (forward with log
+normalisers, then mra_attention_backward) on the same inputs.
 """
 from __future__ import annotations
 
@@ -39,6 +41,14 @@ def coarse_flops(w) -> float:
     return 4.0 * w.B * w.H * w.nb * w.nb * w.d
 
 
+def backward_flops(w) -> float:
+    """Algorithmic flops of the gradient pass's tile products: per selected
+    tile the five 32x32xd products S = c Q_x K_y^T, dP = G_x V_y^T,
+    dV += A^T G, dQ += dP K, dK += dP^T Q (2*32*32*d each). The kernels run
+    seven: S and dP are formed in both the dQ and the dK/dV pass."""
+    return 10.0 * w.B * w.H * w.nb * w.budget * 32 * 32 * w.d
+
+
 def pool_bytes(w) -> float:
     """Pooling pass as run in the forward: Q, K, V read once, the pooled rows
     written, and K and V written once more in packed order."""
@@ -46,8 +56,8 @@ def pool_bytes(w) -> float:
     return 5.0 * w.B * w.H * w.n * w.d * e + 3.0 * w.B * w.H * w.nb * w.d * 4
 
 
-TILE_SOURCES = ["paper_2207_10284_amd/csrc/tile.hip", "paper_2207_10284_amd/csrc/common.h",
-                "paper_2207_10284_amd/csrc/kernels.h"]
+TILE_SOURCES = ["paper_2207_10284_amd/csrc/tile.hip", "paper_2207_10284_amd/csrc/tile_ops.h",
+                "paper_2207_10284_amd/csrc/common.h", "paper_2207_10284_amd/csrc/kernels.h"]
 PROFILE = "profiles/tile_stream_kernel_base-4096.md"
 
 
@@ -95,6 +105,35 @@ def time_launches(fn, iters: int, warmup: int = 3) -> float:
     return s.elapsed_time(e) / iters
 
 
+def backward_leg(w, ops, tq, tk, tv, out, idx, ws, iters):
+    """The gradient pass on the workload: mra_attention_backward alone, and a
+    forward that also writes the log normalisers followed by the backward
+    (one training step of the attention layer). Output gradient G ~ N(0, 1)."""
+    import torch
+    from paper_2207_10284_amd import inputs
+    dev = tq.device
+    lse = torch.empty(w.B, w.H, w.n, dtype=torch.float32, device=dev)
+    g = np.random.Generator(np.random.PCG64(w.seed + 7)).standard_normal(tq.shape)
+    g = inputs.round_to_bf16(g) if w.dtype == "bf16" else g.astype(np.float32)
+    tg = torch.from_numpy(g).to(dev).to(tq.dtype)
+    bws = torch.empty(ops.backward_workspace_bytes(w.B, w.H, w.n, w.d, tq.dtype), dtype=torch.uint8, device=dev)
+    dq, dk, dv = (torch.empty_like(tq) for _ in range(3))
+
+    def fwd():
+        ops.attention_forward(tq, tk, tv, w.budget, out=out, idx_out=idx, workspace=ws, lse_out=lse)
+
+    def bwd():
+        ops.attention_backward(tq, tk, tv, out, tg, lse, idx, dq=dq, dk=dk, dv=dv, workspace=bws)
+
+    fwd()
+    bwd_ms = time_launches(bwd, iters)
+    fb_ms = time_launches(lambda: (fwd(), bwd()), iters)
+    tf = backward_flops(w) / (bwd_ms * 1e-3) / 1e12
+    return {"ms_per_step": bwd_ms, "fwd_bwd_ms": fb_ms, "fwd_bwd_tokens_per_s": w.B * w.n / (fb_ms * 1e-3),
+            "tile_tflops": tf, "tile_flops_per_step": backward_flops(w),
+            "workspace_bytes": bws.numel()}
+
+
 def cpu_baseline(w, q, k, v):
     """The float64 oracle (factored form, as it stands) over every head of the
     workload, timed on the host. Returns the JSON object."""
@@ -130,7 +169,9 @@ def main():
     ap.add_argument("--workload", default=None)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-baseline leg")
     ap.add_argument("--no-variants", action="store_true",
-                    help="skip timing MRA-2-s and the head-wide budget (profiling runs)")
+                    help="skip timing MRA-2-s, the head-wide budget and the backward (profiling runs)")
+    ap.add_argument("--backward-only", action="store_true",
+                    help="time only the forward with log normalisers and the backward (profiling runs)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (the path has no multi-GPU mode); got --gpus {args.gpus}",
@@ -153,6 +194,10 @@ def main():
 
     def step():
         ops.attention_forward(tq, tk, tv, w.budget, out=out, idx_out=idx, workspace=ws)
+
+    if args.backward_only:
+        print(json.dumps({"backward": backward_leg(w, ops, tq, tk, tv, out, idx, ws, args.steps)}), flush=True)
+        return
 
     for _ in range(args.warmup):
         step()
@@ -186,6 +231,9 @@ def main():
                                                                        workspace=gws), max(args.steps, 20))
         variants["mra2_global_budget"] = {"ms_per_step": global_ms, "tokens_per_s": w.B * w.n / (global_ms * 1e-3),
                                           "budget_per_head": gb, "prior": "diagonal"}
+
+    if not args.no_variants:
+        variants["backward"] = backward_leg(w, ops, tq, tk, tv, out, idx, ws, max(args.steps, 20))
 
     # Dominant kernel: the tile pass, the same instantiation as inside the
     # forward (packed K/V, coarse term given), on the same inputs; timed alone.

@@ -174,11 +174,15 @@ mra_status_t mra_coarse_term(const float* scores, const int32_t* idx, const floa
  *             even). With bfloat16 inputs the tile probabilities are rounded
  *             to bfloat16 before the product with V and the row sums use the
  *             same rounded values.
+ *   lse_out : optional [B,H,n] float32 output (NULL to skip): each query's
+ *             log normaliser L_i = ln(sum_{j in T} e^{P_ij} + e^{M_x} csum[x]),
+ *             the natural log of the denominator above (the row sum of A^).
+ *             mra_attention_backward takes it.
  */
 mra_status_t mra_block_sddmm_spmm(const void* q, const void* k, const void* v,
                                   const void* kvpacked, const int32_t* idx,
                                   const float* cmax, const float* csum, const float* cvec,
-                                  void* out,
+                                  void* out, float* lse_out,
                                   int B, int H, int n, int d, int block, int budget,
                                   mra_dtype_t dtype, void* stream);
 
@@ -202,11 +206,15 @@ size_t mra_forward_workspace_bytes(int B, int H, int n, int d, int block, int bu
  *   q, k, v   : [B,H,n,d] of `dtype`; out : [B,H,n,d] of `dtype`.
  *   idx_out   : optional [B,H,nb,budget] int32 copy of the selection (NULL:
  *               kept in the workspace only).
+ *   lse_out   : optional [B,H,n] float32 log normalisers (as for
+ *               mra_block_sddmm_spmm; NULL to skip). With idx_out they are
+ *               what mra_attention_backward needs.
  *   workspace : device buffer of at least mra_forward_workspace_bytes(...)
  *               bytes (16-byte aligned; contents on entry are ignored).
  */
 mra_status_t mra_attention_forward(const void* q, const void* k, const void* v, void* out,
-                                   int32_t* idx_out, void* workspace, size_t workspace_bytes,
+                                   int32_t* idx_out, float* lse_out, void* workspace,
+                                   size_t workspace_bytes,
                                    int B, int H, int n, int d, int block, int budget,
                                    mra_dtype_t dtype, void* stream);
 
@@ -228,12 +236,14 @@ size_t mra_forward_global_workspace_bytes(int B, int H, int n, int d, int block,
  * mra_block_sddmm_spmm called in that order with budget (row width) nb.
  *   idx_out : optional [B,H,nb,nb] int32 copy of the selection (NULL: kept in
  *             the workspace only).
+ *   lse_out : optional [B,H,n] float32 log normalisers (NULL to skip).
  *   budget, prior_diagonal : as for mra_select_global.
  *   Other arguments and errors as for mra_attention_forward; workspace of at
  *   least mra_forward_global_workspace_bytes(...) bytes.
  */
 mra_status_t mra_attention_forward_global(const void* q, const void* k, const void* v,
-                                          void* out, int32_t* idx_out, void* workspace,
+                                          void* out, int32_t* idx_out, float* lse_out,
+                                          void* workspace,
                                           size_t workspace_bytes, int B, int H, int n, int d,
                                           int block, int budget, int prior_diagonal,
                                           mra_dtype_t dtype, void* stream);
@@ -249,13 +259,69 @@ mra_status_t mra_attention_forward_global(const void* q, const void* k, const vo
  * csum, cvec NULL) called in that order.
  *   Arguments, layouts, workspace (mra_forward_workspace_bytes) and errors as
  *   for mra_attention_forward, except that budget must be at least 1 (at most
- *   nb) whenever n > 0: MRA_ERR_INVALID_ARG otherwise.
+ *   nb) whenever n > 0: MRA_ERR_INVALID_ARG otherwise. lse_out receives
+ *   ln sum_{j in T_x} e^{P_ij}.
  */
 mra_status_t mra_sparse_attention_forward(const void* q, const void* k, const void* v,
-                                          void* out, int32_t* idx_out, void* workspace,
+                                          void* out, int32_t* idx_out, float* lse_out,
+                                          void* workspace,
                                           size_t workspace_bytes, int B, int H, int n, int d,
                                           int block, int budget, mra_dtype_t dtype,
                                           void* stream);
+
+/*
+ * mra_backward_workspace_bytes — device workspace of mra_attention_backward:
+ * seven rearranged copies of Q, K, V and dZ (7*B*H*n*d*elem bytes), pooled
+ * rows and their gradients, two float32 values per query, the selection as a
+ * bitmap and two float32 nb x nb grids per head (W and dS~ below). 0 for
+ * invalid or unsupported arguments.
+ */
+size_t mra_backward_workspace_bytes(int B, int H, int n, int d, int block, mra_dtype_t dtype);
+
+/*
+ * mra_attention_backward — gradients dQ, dK, dV of a scalar loss through one
+ * MRA-2 (or MRA-2-s) forward, given dZ, with the selection held fixed (the
+ * selection is a discrete choice with no gradient). The forward is the
+ * softmax of Sec. 3.1 over the approximation A^ of Sec. 4.2
+ * (eq. actual_approx_mat_form): each query's logits are the fine c Q_i.K_j
+ * of its refined blocks and, with the low-resolution term, the coarse
+ * S~[x,y] + ln b of the others, applied to V_j and V~_y. The coarse logits
+ * and V~ depend on Q, K, V through the block means (Sec. 4.1
+ * eq. recursive_pooling, Sec. 4.3 eq. recursive_pooling_V), so their
+ * gradients reach every row of a block divided by 32. With
+ * delta_i = dZ_i . Z_i and probabilities p = e^{logit - L_i}:
+ *   d logit = p (dZ_i . value - delta_i)
+ * then the chain rule through c Q K^T, c Q~ K~^T and the means.
+ *   q, k, v   : [B,H,n,d] of `dtype`, the forward's inputs.
+ *   out       : [B,H,n,d] of `dtype`, the forward's output Z.
+ *   dout      : [B,H,n,d] of `dtype`, dZ.
+ *   lse       : [B,H,n] float32, the forward's lse_out.
+ *   idx       : [B,H,nb,width] int32, the forward's selection: entries
+ *               outside [0, nb) are ignored, the others must be distinct
+ *               (every selection of this library is); may be NULL when
+ *               width = 0.
+ *   width     : entries per row of idx, 0 <= width <= nb (the budget of
+ *               mra_attention_forward / mra_sparse_attention_forward, nb for
+ *               mra_attention_forward_global).
+ *   coarse    : 1 for MRA-2 (the forward merged the low-resolution term),
+ *               0 for MRA-2-s (mra_sparse_attention_forward); otherwise
+ *               MRA_ERR_INVALID_ARG.
+ *   dq, dk, dv: [B,H,n,d] of `dtype` outputs (bfloat16 rounded to nearest
+ *               even); every element is written.
+ *   workspace : at least mra_backward_workspace_bytes(...) bytes, 16-byte
+ *               aligned; contents on entry are ignored.
+ * Fine products run on the matrix cores in float32 accumulation; with
+ * bfloat16 inputs the probabilities and logit gradients are rounded to
+ * bfloat16 before their products. The coarse terms are float32. Rows whose
+ * forward normaliser is zero (MRA-2-s with no valid entry in the row) give
+ * unspecified gradients.
+ */
+mra_status_t mra_attention_backward(const void* q, const void* k, const void* v,
+                                    const void* out, const void* dout, const float* lse,
+                                    const int32_t* idx, void* dq, void* dk, void* dv,
+                                    void* workspace, size_t workspace_bytes,
+                                    int B, int H, int n, int d, int block, int width,
+                                    int coarse, mra_dtype_t dtype, void* stream);
 
 /* Static description of a status code. */
 const char* mra_status_str(mra_status_t status);

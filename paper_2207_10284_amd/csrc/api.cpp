@@ -112,6 +112,42 @@ mra_status_t check_global_budget(const Shape& s, int budget, int prior_diagonal)
   return MRA_OK;
 }
 
+// Workspace of the gradient pass (pointer roles in kernels.h, BwdArgs).
+struct WsBwd {
+  size_t qp, kp, vp, q_row, q_t, k_row, k_t, v_row, g_row, g_t, l2, delta, bits, gh, W, dS, dqp,
+      dkp, dvp, total;
+};
+
+WsBwd ws_bwd(long long bh, int nb, int d, mra_dtype_t dtype) {
+  WsBwd L{};
+  size_t off = 0;
+  const size_t pooled = align256((size_t)bh * nb * d * sizeof(float));
+  const size_t packed = align256((size_t)bh * nb * kBlockSize * d * (dtype == MRA_BF16 ? 2 : 4));
+  const size_t per_query = align256((size_t)bh * nb * kBlockSize * sizeof(float));
+  const size_t grid = align256((size_t)bh * nb * nb * sizeof(float));
+  L.qp = off; off += pooled;
+  L.kp = off; off += pooled;
+  L.vp = off; off += pooled;
+  L.q_row = off; off += packed;
+  L.q_t = off; off += packed;
+  L.k_row = off; off += packed;
+  L.k_t = off; off += packed;
+  L.v_row = off; off += packed;
+  L.g_row = off; off += packed;
+  L.g_t = off; off += packed;
+  L.l2 = off; off += per_query;
+  L.delta = off; off += per_query;
+  L.bits = off; off += align256((size_t)bh * nb * ((nb + 31) / 32) * sizeof(uint32_t));
+  L.gh = off; off += pooled;
+  L.W = off; off += grid;
+  L.dS = off; off += grid;
+  L.dqp = off; off += pooled;
+  L.dkp = off; off += pooled;
+  L.dvp = off; off += pooled;
+  L.total = off;
+  return L;
+}
+
 }  // namespace
 
 extern "C" {
@@ -179,8 +215,9 @@ mra_status_t mra_coarse_term(const float* scores, const int32_t* idx, const floa
 mra_status_t mra_block_sddmm_spmm(const void* q, const void* k, const void* v,
                                   const void* kvpacked, const int32_t* idx,
                                   const float* cmax, const float* csum,
-                                  const float* cvec, void* out, int B, int H, int n, int d,
-                                  int block, int budget, mra_dtype_t dtype, void* stream) {
+                                  const float* cvec, void* out, float* lse_out, int B, int H,
+                                  int n, int d, int block, int budget, mra_dtype_t dtype,
+                                  void* stream) {
   Shape s;
   MRA_TRY(check_shape(B, H, n, d, block, true, &s));
   MRA_TRY(check_dtype(dtype));
@@ -197,14 +234,15 @@ mra_status_t mra_block_sddmm_spmm(const void* q, const void* k, const void* v,
     MRA_TRY(check_ptr(v));
   }
   MRA_TRY(check_ptr(out));
+  if (lse_out != nullptr && !aligned16(lse_out)) return MRA_ERR_MISALIGNED;
   if (budget > 0) MRA_TRY(check_ptr(idx));
   if (given) {
     MRA_TRY(check_ptr(cmax));
     MRA_TRY(check_ptr(csum));
     MRA_TRY(check_ptr(cvec));
   }
-  return hip_status(mra::launch_tile(q, k, v, kvpacked, idx, cmax, csum, cvec, out, s.bh, n, d,
-                                     budget, (int)dtype, static_cast<hipStream_t>(stream)));
+  return hip_status(mra::launch_tile(q, k, v, kvpacked, idx, cmax, csum, cvec, out, lse_out, s.bh,
+                                     n, d, budget, (int)dtype, static_cast<hipStream_t>(stream)));
 }
 
 size_t mra_forward_workspace_bytes(int B, int H, int n, int d, int block, int budget,
@@ -217,7 +255,8 @@ size_t mra_forward_workspace_bytes(int B, int H, int n, int d, int block, int bu
 }
 
 mra_status_t mra_attention_forward(const void* q, const void* k, const void* v, void* out,
-                                   int32_t* idx_out, void* workspace, size_t workspace_bytes,
+                                   int32_t* idx_out, float* lse_out, void* workspace,
+                                   size_t workspace_bytes,
                                    int B, int H, int n, int d, int block, int budget,
                                    mra_dtype_t dtype, void* stream) {
   Shape s;
@@ -230,6 +269,7 @@ mra_status_t mra_attention_forward(const void* q, const void* k, const void* v, 
   MRA_TRY(check_ptr(v));
   MRA_TRY(check_ptr(out));
   if (idx_out != nullptr && !aligned16(idx_out)) return MRA_ERR_MISALIGNED;
+  if (lse_out != nullptr && !aligned16(lse_out)) return MRA_ERR_MISALIGNED;
   MRA_TRY(check_ptr(workspace));
   const WsLayout L = ws_layout(s.bh, s.nb, d, budget, dtype);
   if (workspace_bytes < L.total) return MRA_ERR_WORKSPACE;
@@ -248,12 +288,13 @@ mra_status_t mra_attention_forward(const void* q, const void* k, const void* v, 
   MRA_TRY(hip_status(mra::launch_pool(q, k, v, qp, kp, vp, kvpacked, s.bh, n, d, (int)dtype, st)));
   MRA_TRY(hip_status(mra::launch_select_term_fused(qp, kp, idx, vp, cmax, csum, cvec, s.bh, s.nb,
                                                    d, budget, st)));
-  return hip_status(mra::launch_tile(q, k, v, kvpacked, idx, cmax, csum, cvec, out, s.bh, n, d,
-                                     budget, (int)dtype, st));
+  return hip_status(mra::launch_tile(q, k, v, kvpacked, idx, cmax, csum, cvec, out, lse_out, s.bh,
+                                     n, d, budget, (int)dtype, st));
 }
 
 mra_status_t mra_sparse_attention_forward(const void* q, const void* k, const void* v,
-                                          void* out, int32_t* idx_out, void* workspace,
+                                          void* out, int32_t* idx_out, float* lse_out,
+                                          void* workspace,
                                           size_t workspace_bytes, int B, int H, int n, int d,
                                           int block, int budget, mra_dtype_t dtype,
                                           void* stream) {
@@ -268,6 +309,7 @@ mra_status_t mra_sparse_attention_forward(const void* q, const void* k, const vo
   MRA_TRY(check_ptr(v));
   MRA_TRY(check_ptr(out));
   if (idx_out != nullptr && !aligned16(idx_out)) return MRA_ERR_MISALIGNED;
+  if (lse_out != nullptr && !aligned16(lse_out)) return MRA_ERR_MISALIGNED;
   MRA_TRY(check_ptr(workspace));
   const WsLayout L = ws_layout(s.bh, s.nb, d, budget, dtype);
   if (workspace_bytes < L.total) return MRA_ERR_WORKSPACE;
@@ -282,8 +324,8 @@ mra_status_t mra_sparse_attention_forward(const void* q, const void* k, const vo
 
   MRA_TRY(hip_status(mra::launch_pool(q, k, v, qp, kp, vp, kvpacked, s.bh, n, d, (int)dtype, st)));
   MRA_TRY(hip_status(mra::launch_select_fused(qp, kp, idx, s.bh, s.nb, d, budget, st)));
-  return hip_status(mra::launch_tile(q, k, v, kvpacked, idx, nullptr, nullptr, nullptr, out, s.bh,
-                                     n, d, budget, (int)dtype, st));
+  return hip_status(mra::launch_tile(q, k, v, kvpacked, idx, nullptr, nullptr, nullptr, out,
+                                     lse_out, s.bh, n, d, budget, (int)dtype, st));
 }
 
 mra_status_t mra_select_global(const float* scores, int32_t* idx, int B, int H, int n,
@@ -307,7 +349,8 @@ size_t mra_forward_global_workspace_bytes(int B, int H, int n, int d, int block,
 }
 
 mra_status_t mra_attention_forward_global(const void* q, const void* k, const void* v,
-                                          void* out, int32_t* idx_out, void* workspace,
+                                          void* out, int32_t* idx_out, float* lse_out,
+                                          void* workspace,
                                           size_t workspace_bytes, int B, int H, int n, int d,
                                           int block, int budget, int prior_diagonal,
                                           mra_dtype_t dtype, void* stream) {
@@ -321,6 +364,7 @@ mra_status_t mra_attention_forward_global(const void* q, const void* k, const vo
   MRA_TRY(check_ptr(v));
   MRA_TRY(check_ptr(out));
   if (idx_out != nullptr && !aligned16(idx_out)) return MRA_ERR_MISALIGNED;
+  if (lse_out != nullptr && !aligned16(lse_out)) return MRA_ERR_MISALIGNED;
   MRA_TRY(check_ptr(workspace));
   const WsGlobal G = ws_global(s.bh, s.nb, d, dtype);
   if (workspace_bytes < G.total) return MRA_ERR_WORKSPACE;
@@ -343,8 +387,52 @@ mra_status_t mra_attention_forward_global(const void* q, const void* k, const vo
   MRA_TRY(hip_status(mra::launch_coarse(qp, kp, S, s.bh, nb, d, st)));
   MRA_TRY(hip_status(mra::launch_select_global(S, idx, s.bh, nb, budget, prior_diagonal, st)));
   MRA_TRY(hip_status(mra::launch_coarse_term(S, idx, vp, cmax, csum, cvec, s.bh, nb, d, nb, st)));
-  return hip_status(mra::launch_tile(q, k, v, kvpacked, idx, cmax, csum, cvec, out, s.bh, n, d, nb,
-                                     (int)dtype, st));
+  return hip_status(mra::launch_tile(q, k, v, kvpacked, idx, cmax, csum, cvec, out, lse_out, s.bh,
+                                     n, d, nb, (int)dtype, st));
+}
+
+size_t mra_backward_workspace_bytes(int B, int H, int n, int d, int block, mra_dtype_t dtype) {
+  Shape s;
+  if (check_shape(B, H, n, d, block, true, &s) != MRA_OK) return 0;
+  if (check_dtype(dtype) != MRA_OK) return 0;
+  return ws_bwd(s.bh, s.nb, d, dtype).total;
+}
+
+mra_status_t mra_attention_backward(const void* q, const void* k, const void* v, const void* out,
+                                    const void* dout, const float* lse, const int32_t* idx,
+                                    void* dq, void* dk, void* dv, void* workspace,
+                                    size_t workspace_bytes, int B, int H, int n, int d, int block,
+                                    int width, int coarse, mra_dtype_t dtype, void* stream) {
+  Shape s;
+  MRA_TRY(check_shape(B, H, n, d, block, true, &s));
+  MRA_TRY(check_dtype(dtype));
+  if (width < 0 || width > s.nb) return MRA_ERR_INVALID_ARG;
+  if (coarse != 0 && coarse != 1) return MRA_ERR_INVALID_ARG;
+  if (s.empty) return MRA_OK;
+  const void* in[7] = {q, k, v, out, dout, lse, workspace};
+  for (const void* p : in) MRA_TRY(check_ptr(p));
+  if (width > 0) MRA_TRY(check_ptr(idx));
+  MRA_TRY(check_ptr(dq));
+  MRA_TRY(check_ptr(dk));
+  MRA_TRY(check_ptr(dv));
+  const WsBwd L = ws_bwd(s.bh, s.nb, d, dtype);
+  if (workspace_bytes < L.total) return MRA_ERR_WORKSPACE;
+
+  char* ws = static_cast<char*>(workspace);
+  auto f32 = [&](size_t off) { return reinterpret_cast<float*>(ws + off); };
+  mra::BwdArgs A{};
+  A.q = q; A.k = k; A.v = v; A.out = out; A.dout = dout;
+  A.lse = lse; A.idx = idx;
+  A.dq = dq; A.dk = dk; A.dv = dv;
+  A.bh = s.bh; A.n = n; A.d = d; A.m = width; A.dtype = (int)dtype; A.coarse = coarse != 0;
+  A.qp = f32(L.qp); A.kp = f32(L.kp); A.vp = f32(L.vp);
+  A.q_row = ws + L.q_row; A.q_t = ws + L.q_t; A.k_row = ws + L.k_row; A.k_t = ws + L.k_t;
+  A.v_row = ws + L.v_row; A.g_row = ws + L.g_row; A.g_t = ws + L.g_t;
+  A.l2 = f32(L.l2); A.delta = f32(L.delta);
+  A.bits = reinterpret_cast<uint32_t*>(ws + L.bits);
+  A.gh = f32(L.gh); A.W = f32(L.W); A.dS = f32(L.dS);
+  A.dqp = f32(L.dqp); A.dkp = f32(L.dkp); A.dvp = f32(L.dvp);
+  return hip_status(mra::launch_bwd(A, static_cast<hipStream_t>(stream)));
 }
 
 const char* mra_status_str(mra_status_t status) {

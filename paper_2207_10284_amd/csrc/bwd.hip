@@ -1,0 +1,543 @@
+// Gradients of the MRA-2 output with the selection held fixed (Sec. 4.2 eq.
+// actual_approx_mat_form, Sec. 4.3 Alg. 2; R = {b, 1}, b = 32).
+//
+// Query i of block-row x takes a softmax over the fine logits P_ij = c Q_i.K_j
+// of the columns j of its refined blocks T_x and, with the low-resolution
+// term, over the coarse logits S~[x,y] + ln b of the other blocks y, applied
+// to the rows V_j and V~_y. With L_i its log normaliser (saved by the
+// forward), G = dZ and delta_i = G_i . Z_i, each logit's gradient is its
+// probability times (G_i . value - delta_i):
+//   fine:   dP_ij = e^{P_ij - L_i} (G_i . V_j - delta_i)
+//           dQ_i += c sum_j dP_ij K_j,   dK_j += c sum_i dP_ij Q_i,
+//           dV_j += sum_i e^{P_ij - L_i} G_i
+//   coarse: the 32 queries of block-row x share S~[x,y]. For a reference m_x,
+//           W[x,y] = b e^{S~[x,y] - m_x} (0 for y in T_x),
+//           G^_x = sum_{i in x} e^{m_x - L_i} G_i,  d^_x = sum e^{m_x - L_i} delta_i:
+//           dS~[x,y] = W[x,y] (V~_y . G^_x - d^_x),   dV~_y = sum_x W[x,y] G^_x,
+//           dQ~_x = c sum_y dS~[x,y] K~_y,           dK~_y = c sum_x dS~[x,y] Q~_x.
+//           A pooled row is a block mean, so its gradient reaches each of the
+//           block's 32 rows divided by 32.
+// m_x = min_{i in x} L_i keeps both exponentials at most 1: every L_i is at
+// least each coarse logit S~[x,y] + ln b of its own row.
+//
+// Kernels, in launch order (after the packing pass of pool.hip):
+//  * bwd_rows_kernel: per block-row (a wave; 16 per workgroup): delta, the
+//    log normaliser in log2 units, the selection as a bitmap; with the coarse
+//    term also G^, d^ and the row's W, dS~ and dQ~ (K~ and V~ staged through
+//    LDS 64 blocks at a time).
+//  * bwd_cols_kernel: per column block (a wave; 16 per workgroup): dK~, dV~.
+//  * bwd_dq_kernel: per block-row (a wave), over its refined tiles: the
+//    products K_y Q_x^T and V_y G_x^T on the matrix cores, then
+//    dQ^T += K_y^T dP^T.
+//  * bwd_dkdv_kernel: per column block (a wave), over the block-rows that
+//    refined it (ascending): dV^T += G_x^T A, dK^T += c Q_x^T dP.
+// Tile operands come from packed copies in the layouts of tile_ops.h.
+#include "common.h"
+#include "kernels.h"
+#include "tile_ops.h"
+
+namespace mra {
+
+constexpr int kBwdRows = 16;              // waves (block-rows or columns) per workgroup
+constexpr int kBwdChunk = 64;             // blocks staged per step
+constexpr int kBwdTileWaves = 4;          // waves per workgroup of the tile passes
+
+template <int DT>
+__device__ __forceinline__ float elem_lo(uint32_t w) {
+  return DT == BF16 ? bf16_to_f32(w & 0xFFFFu) : __uint_as_float(w);
+}
+
+// ---------------------------------------------------------------------------
+template <int DT, int D, bool COARSE>
+__global__ __launch_bounds__(kBwdRows * kWave) void bwd_rows_kernel(
+    const void* __restrict__ gin, const void* __restrict__ zin, const float* __restrict__ lse,
+    const int32_t* __restrict__ idx, const float* __restrict__ qp, const float* __restrict__ kp,
+    const float* __restrict__ vp, float* __restrict__ l2, float* __restrict__ delta,
+    uint32_t* __restrict__ bits, float* __restrict__ gh, float* __restrict__ Wout,
+    float* __restrict__ dSout, float* __restrict__ dqp, int nb, int m, float scale) {
+  using Cfg = TileCfg<DT, D>;
+  using elem = typename Cfg::elem;
+  constexpr int KC = Cfg::kKChunks;                        // 16-byte chunks per half row
+  constexpr int PK = D + 1;                                 // LDS pitch of staged rows
+  __shared__ float Kc[COARSE ? kBwdChunk * PK : 1];
+  __shared__ float Vc[COARSE ? kBwdChunk * PK : 1];
+  __shared__ float Qx[kBwdRows][D];
+  __shared__ float Gx[kBwdRows][D];
+  __shared__ float wq[kBwdRows][32];
+  __shared__ float dsl[kBwdRows][kBwdChunk];
+  __shared__ uint32_t bm_all[kBwdRows][64];                 // nb <= 2048 bits
+
+  const int tid = threadIdx.x;
+  const int w = wave_uniform(tid / kWave);
+  const int lane = lane_id(), j = lane & 31, h = lane >> 5;
+  const int groups = (nb + kBwdRows - 1) / kBwdRows;
+  const long long lwg = xcd_remap(blockIdx.x, gridDim.x);
+  const long long bh = lwg / groups;
+  const int x0 = (int)(lwg - bh * groups) * kBwdRows;
+  const bool active = x0 + w < nb;                          // wave-uniform
+  const long long g = bh * nb + x0 + w;                     // this wave's block-row
+  const int nbw = (nb + 31) / 32;
+  uint32_t* bm = bm_all[w];
+
+  float mref = 0.0f, dhat = 0.0f;
+  if (active) {
+    // delta_i = G_i . Z_i: lane (h, j) takes half h of row j
+    const long long roff = (g * 32 + j) * D + (D / 2) * h;
+    const u32x4* gp = reinterpret_cast<const u32x4*>(reinterpret_cast<const elem*>(gin) + roff);
+    const u32x4* zp = reinterpret_cast<const u32x4*>(reinterpret_cast<const elem*>(zin) + roff);
+    float part = 0.0f;
+#pragma unroll 4
+    for (int s = 0; s < KC; ++s) {
+      const u32x4 gw = gp[s], zw = zp[s];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        part = fmaf(elem_lo<DT>(gw[e]), elem_lo<DT>(zw[e]), part);
+        if constexpr (DT == BF16) part = fmaf(bf16_to_f32(gw[e] >> 16), bf16_to_f32(zw[e] >> 16), part);
+      }
+    }
+    const float dl = halves_sum(part);
+    const float L = lse[g * 32 + j];
+    if (h == 0) {
+      l2[g * 32 + j] = L * kLog2e;
+      delta[g * 32 + j] = dl;
+    }
+    // the selection as a bitmap (entries outside [0, nb) ignored)
+    for (int i = lane; i < nbw; i += kWave) bm[i] = 0u;
+    wave_lds_sync();
+    for (int i0 = 0; i0 < m; i0 += kWave) {
+      const int y = i0 + lane < m ? idx[g * m + i0 + lane] : -1;
+      if (y >= 0 && y < nb) atomicOr(&bm[y >> 5], 1u << (y & 31));
+    }
+    wave_lds_sync();
+    for (int i = lane; i < nbw; i += kWave) bits[g * nbw + i] = bm[i];
+    if constexpr (COARSE) {
+      mref = -wave_max(-L);                                 // min over the 32 queries
+      const float wi = exp2f((mref - L) * kLog2e);
+      dhat = wave_sum(h == 0 ? wi * dl : 0.0f);
+      if (h == 0) wq[w][j] = wi;
+      wave_lds_sync();
+      // G^_x: lanes over the dims, rows in order
+      const elem* G = reinterpret_cast<const elem*>(gin) + g * 32 * D;
+      for (int dd = lane; dd < D; dd += kWave) {
+        float acc = 0.0f;
+        for (int i = 0; i < 32; ++i) {
+          float gv;
+          if constexpr (DT == BF16) gv = bf16_to_f32(G[i * D + dd]);
+          else gv = G[i * D + dd];
+          acc = fmaf(wq[w][i], gv, acc);
+        }
+        Gx[w][dd] = acc;
+        gh[g * D + dd] = acc;
+        Qx[w][dd] = qp[g * D + dd];
+      }
+      wave_lds_sync();
+    }
+  }
+  if constexpr (!COARSE) return;
+
+  // ---- coarse row terms, 64 column blocks per step
+  const float* kh = kp + bh * (long long)nb * D;
+  const float* vh = vp + bh * (long long)nb * D;
+  constexpr int DQ = (D + kWave - 1) / kWave;
+  float accq[DQ];
+#pragma unroll
+  for (int q = 0; q < DQ; ++q) accq[q] = 0.0f;
+  for (int y0 = 0; y0 < nb; y0 += kBwdChunk) {
+    __syncthreads();                                        // previous chunk consumed
+    for (int i = tid; i < kBwdChunk * D; i += kBwdRows * kWave) {
+      const int r = i / D, c = i % D;
+      const bool in = y0 + r < nb;
+      Kc[r * PK + c] = in ? kh[(long long)(y0 + r) * D + c] : 0.0f;
+      Vc[r * PK + c] = in ? vh[(long long)(y0 + r) * D + c] : 0.0f;
+    }
+    __syncthreads();
+    if (active) {
+      const int y = y0 + lane;
+      float dsv = 0.0f;
+      if (y < nb) {
+        const bool sel = (bm[y >> 5] >> (y & 31)) & 1u;
+        float wv = 0.0f;
+        if (!sel) {
+          float s = 0.0f, vg = 0.0f;
+#pragma unroll 8
+          for (int c = 0; c < D; ++c) {
+            s = fmaf(Qx[w][c], Kc[lane * PK + c], s);
+            vg = fmaf(Gx[w][c], Vc[lane * PK + c], vg);
+          }
+          wv = (float)kBlock * exp2f(fmaf(s, scale, -mref) * kLog2e);
+          dsv = wv * (vg - dhat);
+        }
+        Wout[g * nb + y] = wv;
+        dSout[g * nb + y] = dsv;
+      }
+      dsl[w][lane] = dsv;
+      wave_lds_sync();
+#pragma unroll
+      for (int q = 0; q < DQ; ++q) {
+        const int dd = lane + kWave * q;
+        if (dd < D) {
+          float a = accq[q];
+          for (int t = 0; t < kBwdChunk; ++t) a = fmaf(dsl[w][t], Kc[t * PK + dd], a);
+          accq[q] = a;
+        }
+      }
+    }
+  }
+  if (active) {
+#pragma unroll
+    for (int q = 0; q < DQ; ++q) {
+      const int dd = lane + kWave * q;
+      if (dd < D) dqp[g * D + dd] = accq[q] * scale;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dK~_y = c sum_x dS~[x,y] Q~_x, dV~_y = sum_x W[x,y] G^_x: one wave per
+// column block, 16 per workgroup; Q~, G^ and the columns of W and dS~ staged
+// through LDS 64 block-rows at a time; rows summed in ascending order.
+template <int D>
+__global__ __launch_bounds__(kBwdRows * kWave) void bwd_cols_kernel(
+    const float* __restrict__ qp, const float* __restrict__ gh, const float* __restrict__ W,
+    const float* __restrict__ dS, float* __restrict__ dkp, float* __restrict__ dvp, int nb,
+    float scale) {
+  constexpr int PC = kBwdRows + 1;
+  __shared__ float Qc[kBwdChunk][D];
+  __shared__ float Gc[kBwdChunk][D];
+  __shared__ float Wc[kBwdChunk * PC];
+  __shared__ float Sc[kBwdChunk * PC];
+  const int tid = threadIdx.x;
+  const int w = wave_uniform(tid / kWave);
+  const int lane = lane_id();
+  const int groups = (nb + kBwdRows - 1) / kBwdRows;
+  const long long lwg = xcd_remap(blockIdx.x, gridDim.x);
+  const long long bh = lwg / groups;
+  const int y0 = (int)(lwg - bh * groups) * kBwdRows;
+  const bool active = y0 + w < nb;
+  const long long hb = bh * nb;                             // first block of the head
+  constexpr int DQ = (D + kWave - 1) / kWave;
+  float ak[DQ], av[DQ];
+#pragma unroll
+  for (int q = 0; q < DQ; ++q) ak[q] = av[q] = 0.0f;
+  for (int r0 = 0; r0 < nb; r0 += kBwdChunk) {
+    __syncthreads();
+    for (int i = tid; i < kBwdChunk * D; i += kBwdRows * kWave) {
+      const int r = i / D, c = i % D;
+      const bool in = r0 + r < nb;
+      Qc[r][c] = in ? qp[(hb + r0 + r) * D + c] : 0.0f;
+      Gc[r][c] = in ? gh[(hb + r0 + r) * D + c] : 0.0f;
+    }
+    for (int i = tid; i < kBwdChunk * kBwdRows; i += kBwdRows * kWave) {
+      const int r = i / kBwdRows, c = i % kBwdRows;
+      const bool in = r0 + r < nb && y0 + c < nb;
+      Wc[r * PC + c] = in ? W[(hb + r0 + r) * nb + y0 + c] : 0.0f;
+      Sc[r * PC + c] = in ? dS[(hb + r0 + r) * nb + y0 + c] : 0.0f;
+    }
+    __syncthreads();
+    if (active) {
+#pragma unroll
+      for (int q = 0; q < DQ; ++q) {
+        const int dd = lane + kWave * q;
+        if (dd < D) {
+          float a = ak[q], b = av[q];
+          for (int r = 0; r < kBwdChunk; ++r) {
+            a = fmaf(Sc[r * PC + w], Qc[r][dd], a);
+            b = fmaf(Wc[r * PC + w], Gc[r][dd], b);
+          }
+          ak[q] = a;
+          av[q] = b;
+        }
+      }
+    }
+  }
+  if (active) {
+#pragma unroll
+    for (int q = 0; q < DQ; ++q) {
+      const int dd = lane + kWave * q;
+      if (dd < D) {
+        dkp[(hb + y0 + w) * D + dd] = ak[q] * scale;
+        dvp[(hb + y0 + w) * D + dd] = av[q];
+      }
+    }
+  }
+}
+
+// Stores a 32 x D block from d-major tiles acc (lane: row j; register r of
+// tile t: dim 32t + 8(r/4) + 4h + r%4) as acc * a + (add ? add[dim] / 32 : 0).
+template <int DT, int D>
+__device__ __forceinline__ void store_block(typename TileCfg<DT, D>::elem* dst,
+                                            const f32x16 (&acc)[D / 32], float a,
+                                            const float* add) {
+  constexpr int NT = D / 32;
+  const int lane = lane_id(), j = lane & 31, h = lane >> 5;
+  auto* row = dst + (long long)j * D;
+  constexpr float inv = 1.0f / kBlock;
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int rg = 0; rg < 4; ++rg) {
+      const int d0 = 32 * t + 8 * rg + 4 * h;
+      f32x4 c4 = {0.0f, 0.0f, 0.0f, 0.0f};
+      if (add != nullptr) c4 = *reinterpret_cast<const f32x4*>(add + d0);
+      float z[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) z[e] = fmaf(acc[t][4 * rg + e], a, c4[e] * inv);
+      if constexpr (DT == BF16) {
+        const u32x2 pr = {pack_bf16x2(z[0], z[1]), pack_bf16x2(z[2], z[3])};
+        *reinterpret_cast<u32x2*>(row + d0) = pr;
+      } else {
+        const f32x4 st = {z[0], z[1], z[2], z[3]};
+        *reinterpret_cast<f32x4*>(row + d0) = st;
+      }
+    }
+}
+
+// bfloat16 pairs of 16 float32 values in register order (the B operand of
+// mfma_acc_bf16).
+__device__ __forceinline__ void pack16(const float (&v)[16], uint32_t (&pk)[8]) {
+#pragma unroll
+  for (int rr = 0; rr < 8; ++rr) {
+    bf16x2 pb;
+    pb[0] = (__bf16)v[2 * rr];
+    pb[1] = (__bf16)v[2 * rr + 1];
+    pk[rr] = __builtin_bit_cast(uint32_t, pb);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dQ: one wave per block-row x. For each refined block y (ascending):
+// S^T = K_y Q_x^T and (V_y G_x^T) on the matrix cores (lane: query, 16 keys),
+// dP^T = e^{S^T c - L} o (V G^T - delta), dQ^T += K_y^T dP^T. The epilogue
+// scales by c and adds dQ~_x / 32. Operand loads for the next tile are issued
+// before the current tile is computed (past the last one they re-read it).
+template <int DT, int D, bool COARSE>
+__global__ __launch_bounds__(kBwdTileWaves * kWave) void bwd_dq_kernel(
+    const void* __restrict__ qin, const void* __restrict__ gin, const void* __restrict__ krow,
+    const void* __restrict__ vrow, const void* __restrict__ kt, const int32_t* __restrict__ idx,
+    const float* __restrict__ l2, const float* __restrict__ delta, const float* __restrict__ dqp,
+    void* __restrict__ dq, int nb, int m, long long rows, float scale, float scale_log2) {
+  using Cfg = TileCfg<DT, D>;
+  using elem = typename Cfg::elem;
+  constexpr int KC = Cfg::kKChunks, VC = Cfg::kVChunks, NT = Cfg::kNT;
+  extern __shared__ int32_t sidx_all[];
+  const int w = wave_uniform(threadIdx.x / kWave);
+  const int lane = lane_id(), jq = lane & 31;
+  const long long g = xcd_remap(blockIdx.x, gridDim.x) * (long long)kBwdTileWaves + w;
+  if (g >= rows) return;                                    // no workgroup barriers below
+  const long long bh = g / nb;
+  int32_t* myidx = sidx_all + w * m;
+  const int cnt = stage_selection(idx + g * m, m, nb, myidx);
+
+  u32x4 qf[KC], gf[KC];
+  load_rows<DT, D>(reinterpret_cast<const elem*>(qin) + g * 32 * D, qf);
+  load_rows<DT, D>(reinterpret_cast<const elem*>(gin) + g * 32 * D, gf);
+  const float lq = l2[g * 32 + jq], dl = delta[g * 32 + jq];
+  f32x16 acc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[t][r] = 0.0f;
+
+  const u32x4* kr = reinterpret_cast<const u32x4*>(krow) + bh * nb * KC * 64 + lane;
+  const u32x4* vr = reinterpret_cast<const u32x4*>(vrow) + bh * nb * KC * 64 + lane;
+  const u32x4* ktp = reinterpret_cast<const u32x4*>(kt) + bh * nb * VC * 64 + lane;
+  struct Ops {
+    u32x4 k[KC], v[KC], t[VC];
+  };
+  auto load = [&](int y, Ops& o) {
+#pragma unroll
+    for (int c = 0; c < KC; ++c) o.k[c] = kr[((long long)y * KC + c) * 64];
+#pragma unroll
+    for (int c = 0; c < KC; ++c) o.v[c] = vr[((long long)y * KC + c) * 64];
+#pragma unroll
+    for (int c = 0; c < VC; ++c) o.t[c] = ktp[((long long)y * VC + c) * 64];
+  };
+  Ops cur, nxt;
+  if (cnt > 0) load(wave_uniform(myidx[0]), cur);
+  for (int i = 0; i < cnt; ++i) {
+    load(wave_uniform(myidx[min(i + 1, cnt - 1)]), nxt);
+    const f32x16 s = mfma_abt<DT, KC>(cur.k, qf);
+    const f32x16 pv = mfma_abt<DT, KC>(cur.v, gf);
+    float ds[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      ds[r] = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -lq)) * (pv[r] - dl);
+    if constexpr (DT == BF16) {
+      uint32_t pk[8];
+      pack16(ds, pk);
+      mfma_acc_bf16<NT>(acc, pk, [&](int c) { return cur.t[c]; });
+    } else {
+      mfma_acc_f32<NT>(acc, ds, [&](int c) { return cur.t[c]; });
+    }
+    cur = nxt;
+  }
+  store_block<DT, D>(reinterpret_cast<elem*>(dq) + g * 32 * D, acc, scale,
+                     COARSE ? dqp + g * D : nullptr);
+}
+
+// ---------------------------------------------------------------------------
+// dK, dV: one wave per column block y. For each block-row x whose selection
+// holds y (ascending): S = Q_x K_y^T and G_x V_y^T (lane: key, 16 queries),
+// A = e^{S c - L}, dP = A o (G V^T - delta), dV^T += G_x^T A,
+// dK^T += Q_x^T dP. The epilogue scales dK by c and adds dK~_y / 32 and
+// dV~_y / 32.
+template <int DT, int D, bool COARSE>
+__global__ __launch_bounds__(kBwdTileWaves * kWave) void bwd_dkdv_kernel(
+    const void* __restrict__ kin, const void* __restrict__ vin, const void* __restrict__ qrow,
+    const void* __restrict__ grow, const void* __restrict__ qt, const void* __restrict__ gt,
+    const uint32_t* __restrict__ bits, const float* __restrict__ l2,
+    const float* __restrict__ delta, const float* __restrict__ dkp,
+    const float* __restrict__ dvp, void* __restrict__ dk, void* __restrict__ dv, int nb,
+    long long rows, float scale, float scale_log2) {
+  using Cfg = TileCfg<DT, D>;
+  using elem = typename Cfg::elem;
+  constexpr int KC = Cfg::kKChunks, VC = Cfg::kVChunks, NT = Cfg::kNT;
+  extern __shared__ int32_t sidx_all[];
+  const int w = wave_uniform(threadIdx.x / kWave);
+  const int lane = lane_id(), h = lane >> 5;
+  const long long gy = xcd_remap(blockIdx.x, gridDim.x) * (long long)kBwdTileWaves + w;
+  if (gy >= rows) return;                                   // no workgroup barriers below
+  const long long bh = gy / nb;
+  const int y = (int)(gy - bh * nb);
+  const long long hb = bh * nb;
+  const int nbw = (nb + 31) / 32;
+
+  // block-rows whose selection holds y, ascending
+  int32_t* myx = sidx_all + w * nb;
+  int cnt = 0;
+  for (int x0 = 0; x0 < nb; x0 += kWave) {
+    const int x = x0 + lane;
+    const bool ok = x < nb && ((bits[(hb + x) * nbw + (y >> 5)] >> (y & 31)) & 1u);
+    const uint64_t mk = __ballot(ok);
+    if (ok) myx[cnt + __popcll(mk & lanemask_lt())] = x;
+    cnt += __popcll(mk);
+  }
+  wave_lds_sync();
+  cnt = wave_uniform(cnt);
+
+  u32x4 kf[KC], vf[KC];
+  load_rows<DT, D>(reinterpret_cast<const elem*>(kin) + gy * 32 * D, kf);
+  load_rows<DT, D>(reinterpret_cast<const elem*>(vin) + gy * 32 * D, vf);
+  f32x16 ak[NT], av[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) ak[t][r] = av[t][r] = 0.0f;
+
+  const u32x4* qr = reinterpret_cast<const u32x4*>(qrow) + hb * KC * 64 + lane;
+  const u32x4* gr = reinterpret_cast<const u32x4*>(grow) + hb * KC * 64 + lane;
+  const u32x4* qtp = reinterpret_cast<const u32x4*>(qt) + hb * VC * 64 + lane;
+  const u32x4* gtp = reinterpret_cast<const u32x4*>(gt) + hb * VC * 64 + lane;
+  struct Ops {
+    u32x4 q[KC], g[KC], qt[VC], gt[VC];
+    f32x4 l[4], d[4];
+  };
+  auto load = [&](int x, Ops& o) {
+#pragma unroll
+    for (int c = 0; c < KC; ++c) o.q[c] = qr[((long long)x * KC + c) * 64];
+#pragma unroll
+    for (int c = 0; c < KC; ++c) o.g[c] = gr[((long long)x * KC + c) * 64];
+#pragma unroll
+    for (int c = 0; c < VC; ++c) o.qt[c] = qtp[((long long)x * VC + c) * 64];
+#pragma unroll
+    for (int c = 0; c < VC; ++c) o.gt[c] = gtp[((long long)x * VC + c) * 64];
+    // queries 8rg + 4h + e of block-row x (the rows of this lane's registers)
+    const float* lx = l2 + (hb + x) * 32 + 4 * h;
+    const float* dx = delta + (hb + x) * 32 + 4 * h;
+#pragma unroll
+    for (int rg = 0; rg < 4; ++rg) {
+      o.l[rg] = *reinterpret_cast<const f32x4*>(lx + 8 * rg);
+      o.d[rg] = *reinterpret_cast<const f32x4*>(dx + 8 * rg);
+    }
+  };
+  Ops cur, nxt;
+  if (cnt > 0) load(wave_uniform(myx[0]), cur);
+  for (int i = 0; i < cnt; ++i) {
+    load(wave_uniform(myx[min(i + 1, cnt - 1)]), nxt);
+    const f32x16 s = mfma_abt<DT, KC>(cur.q, kf);
+    const f32x16 pv = mfma_abt<DT, KC>(cur.g, vf);
+    float a[16], ds[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      a[r] = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -cur.l[r / 4][r % 4]));
+      ds[r] = a[r] * (pv[r] - cur.d[r / 4][r % 4]);
+    }
+    if constexpr (DT == BF16) {
+      uint32_t pa[8], pd[8];
+      pack16(a, pa);
+      pack16(ds, pd);
+      mfma_acc_bf16<NT>(av, pa, [&](int c) { return cur.gt[c]; });
+      mfma_acc_bf16<NT>(ak, pd, [&](int c) { return cur.qt[c]; });
+    } else {
+      mfma_acc_f32<NT>(av, a, [&](int c) { return cur.gt[c]; });
+      mfma_acc_f32<NT>(ak, ds, [&](int c) { return cur.qt[c]; });
+    }
+    cur = nxt;
+  }
+  store_block<DT, D>(reinterpret_cast<elem*>(dk) + gy * 32 * D, ak, scale,
+                     COARSE ? dkp + gy * D : nullptr);
+  store_block<DT, D>(reinterpret_cast<elem*>(dv) + gy * 32 * D, av, 1.0f,
+                     COARSE ? dvp + gy * D : nullptr);
+}
+
+// ---------------------------------------------------------------------------
+template <int DT, int D>
+static void launch_bwd_t(const BwdArgs& A, hipStream_t stream) {
+  const int nb = A.n / kBlock;
+  const long long rows = A.bh * nb;
+  const float scale = (float)(1.0 / sqrt((double)D));
+  const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
+  const long long groups = (nb + kBwdRows - 1) / kBwdRows;
+  const unsigned wg_rows = (unsigned)(A.bh * groups);
+  if (A.coarse) {
+    bwd_rows_kernel<DT, D, true><<<wg_rows, kBwdRows * kWave, 0, stream>>>(
+        A.dout, A.out, A.lse, A.idx, A.qp, A.kp, A.vp, A.l2, A.delta, A.bits, A.gh, A.W, A.dS,
+        A.dqp, nb, A.m, scale);
+    bwd_cols_kernel<D><<<wg_rows, kBwdRows * kWave, 0, stream>>>(A.qp, A.gh, A.W, A.dS, A.dkp,
+                                                                 A.dvp, nb, scale);
+  } else {
+    bwd_rows_kernel<DT, D, false><<<wg_rows, kBwdRows * kWave, 0, stream>>>(
+        A.dout, A.out, A.lse, A.idx, A.qp, A.kp, A.vp, A.l2, A.delta, A.bits, A.gh, A.W, A.dS,
+        A.dqp, nb, A.m, scale);
+  }
+  const unsigned wg_tiles = (unsigned)((rows + kBwdTileWaves - 1) / kBwdTileWaves);
+  const size_t smem_dq = (size_t)kBwdTileWaves * A.m * sizeof(int32_t);
+  const size_t smem_dkdv = (size_t)kBwdTileWaves * nb * sizeof(int32_t);
+  if (A.coarse) {
+    bwd_dq_kernel<DT, D, true><<<wg_tiles, kBwdTileWaves * kWave, smem_dq, stream>>>(
+        A.q, A.dout, A.k_row, A.v_row, A.k_t, A.idx, A.l2, A.delta, A.dqp, A.dq, nb, A.m,
+        rows, scale, scale_log2);
+    bwd_dkdv_kernel<DT, D, true><<<wg_tiles, kBwdTileWaves * kWave, smem_dkdv, stream>>>(
+        A.k, A.v, A.q_row, A.g_row, A.q_t, A.g_t, A.bits, A.l2, A.delta, A.dkp, A.dvp,
+        A.dk, A.dv, nb, rows, scale, scale_log2);
+  } else {
+    bwd_dq_kernel<DT, D, false><<<wg_tiles, kBwdTileWaves * kWave, smem_dq, stream>>>(
+        A.q, A.dout, A.k_row, A.v_row, A.k_t, A.idx, A.l2, A.delta, A.dqp, A.dq, nb, A.m,
+        rows, scale, scale_log2);
+    bwd_dkdv_kernel<DT, D, false><<<wg_tiles, kBwdTileWaves * kWave, smem_dkdv, stream>>>(
+        A.k, A.v, A.q_row, A.g_row, A.q_t, A.g_t, A.bits, A.l2, A.delta, A.dkp, A.dvp,
+        A.dk, A.dv, nb, rows, scale, scale_log2);
+  }
+}
+
+hipError_t launch_bwd(const BwdArgs& A, hipStream_t stream) {
+  // pooled rows and packed operands of Q, K, V and G = dZ
+  const PackJob jobs[4] = {{A.q, A.coarse ? A.qp : nullptr, A.q_row, A.q_t},
+                           {A.k, A.coarse ? A.kp : nullptr, A.k_row, A.k_t},
+                           {A.v, A.coarse ? A.vp : nullptr, A.v_row, nullptr},
+                           {A.dout, nullptr, A.g_row, A.g_t}};
+  const hipError_t e = launch_pack(jobs, 4, A.bh, A.n, A.d, A.dtype, stream);
+  if (e != hipSuccess) return e;
+  if (A.dtype == BF16) {
+    if (A.d == 32) launch_bwd_t<BF16, 32>(A, stream);
+    else if (A.d == 64) launch_bwd_t<BF16, 64>(A, stream);
+    else launch_bwd_t<BF16, 128>(A, stream);
+  } else {
+    if (A.d == 32) launch_bwd_t<F32, 32>(A, stream);
+    else if (A.d == 64) launch_bwd_t<F32, 64>(A, stream);
+    else launch_bwd_t<F32, 128>(A, stream);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace mra

@@ -11,6 +11,7 @@ namespace mra {
 constexpr int kBlock = 32;          // MRA-2 coarse block size b (R = {32, 1})
 constexpr int kWave = 64;
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
 
 enum DType { F32 = 0, BF16 = 1 };
 

@@ -16,6 +16,25 @@ namespace mra {
 //  V bf16, chunk (u*NT + t)*64 + 32h + j, NT = d/32: the 8 values
 //        V[16u + 8(s/4) + 4h + s%4][32t + j], s = 0..7 (u = 0, 1)
 //  V f32, chunk (t*4 + a)*64 + 32h + j: V[8a + 4h + kk][32t + j], kk = 0..3
+
+// One tensor of a packing launch: src [bh, n, d] of dtype; each output may be
+// NULL: pooled (block means, [bh, n/32, d] f32), row_layout (the K part's
+// layout above) and t_layout (the V part's layout above), each bh*n*d
+// elements of dtype.
+struct PackJob {
+  const void* src;
+  float* pooled;
+  void* row_layout;
+  void* t_layout;
+};
+struct PackJobs {
+  PackJob job[4];
+};
+
+// Up to four packing jobs in one launch (jobs with src NULL do nothing).
+hipError_t launch_pack(const PackJob* jobs, int njobs, long long bh, int n, int d, int dtype,
+                       hipStream_t stream);
+
 // Block-means of q/k/v ([bh, n, d], dtype) into qp/kp/vp ([bh, n/32, d] f32);
 // a NULL output skips that tensor. If kvpacked is not NULL (k, v, kp, vp
 // given), the packed copies of k and v are written too.
@@ -53,11 +72,37 @@ hipError_t launch_select_term_fused(const float* qp, const float* kp, int32_t* i
                                     long long bh, int nb, int d, int m, hipStream_t stream);
 
 // Selected 32x32 tiles, merge with the low-resolution term (or none if cmax is
-// NULL) and normalise into out [bh, n, d] of dtype. K and V are read from
+// NULL) and normalise into out [bh, n, d] of dtype; if lse is not NULL, each
+// query's natural log normaliser into lse [bh, n] f32. K and V are read from
 // kvpacked when it is not NULL, else from the row-major k and v.
 hipError_t launch_tile(const void* q, const void* k, const void* v, const void* kvpacked,
                        const int32_t* idx, const float* cmax, const float* csum,
-                       const float* cvec, void* out, long long bh, int n, int d, int m, int dtype,
-                       hipStream_t stream);
+                       const float* cvec, void* out, float* lse, long long bh, int n, int d,
+                       int m, int dtype, hipStream_t stream);
+
+// Gradient pass (bwd.hip) of one MRA-2 forward with the selection held fixed.
+// Inputs q, k, v, out (Z), dout (G) [bh, n, d] of dtype; lse [bh, n] f32 (the
+// forward's natural log normalisers); idx [bh, n/32, m] (entries outside
+// [0, n/32) ignored, the others distinct); coarse = false for the
+// sparse-only variant. Outputs dq, dk, dv [bh, n, d] of dtype. The remaining
+// pointers are workspace: pooled rows (coarse only) [bh, nb, d] f32; packed
+// operand copies (row / transposed layout above) of bh*n*d elements of
+// dtype; l2, delta [bh, n] f32; bits [bh*nb, ceil(nb/32)] u32; gh, dqp, dkp,
+// dvp [bh, nb, d] f32 and W, dS [bh, nb, nb] f32 (coarse only).
+struct BwdArgs {
+  const void *q, *k, *v, *out, *dout;
+  const float* lse;
+  const int32_t* idx;
+  void *dq, *dk, *dv;
+  long long bh;
+  int n, d, m, dtype;
+  bool coarse;
+  float *qp, *kp, *vp;
+  void *q_row, *q_t, *k_row, *k_t, *v_row, *g_row, *g_t;
+  float *l2, *delta;
+  uint32_t* bits;
+  float *gh, *W, *dS, *dqp, *dkp, *dvp;
+};
+hipError_t launch_bwd(const BwdArgs& args, hipStream_t stream);
 
 }  // namespace mra

@@ -34,22 +34,9 @@
 // their K/V tiles in its L2.
 #include "common.h"
 #include "kernels.h"
+#include "tile_ops.h"
 
 namespace mra {
-
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-
-template <int DT, int D>
-struct TileCfg {
-  static constexpr int kWaves = (DT == F32 && D == 128) ? 2 : 4;
-  static constexpr int kPitch = DT == BF16 ? 40 : 36;           // LDS row pitch, elements
-  static constexpr int kNT = D / 32;                            // output tiles over d
-  // 16-byte V operand chunks per lane per tile
-  static constexpr int kVChunks = DT == BF16 ? 2 * kNT : 4 * kNT;
-  static constexpr int kKChunks = DT == BF16 ? D / 16 : D / 8;  // 16-byte K chunks per lane
-  static constexpr int kChunks = kKChunks + kVChunks;           // 1 KB chunks per K/V tile
-  using elem = typename std::conditional<DT == BF16, uint16_t, float>::type;
-};
 
 // Reference point of the online softmax (log2 units). The weights of a tile
 // are exp2(s * c * log2(e) - mrun) for the row's reference mrun, which need
@@ -62,26 +49,6 @@ struct TileCfg {
 // tiles as the reference, where no weight exceeds 1. The loop body thus has no
 // 16-way max, no cross-lane exchange and no branch that rescales O.
 constexpr float kWeightCap = 0x1p64f;
-
-// Copies a row's selection list into LDS keeping only the entries in [0, nb),
-// in their order, and returns how many there are (wave-uniform). Reading the
-// block ids from LDS keeps them off the vector-memory counter, so prefetched
-// tile loads stay in flight; dropping entries outside [0, nb) here (the
-// padding of a head-wide selection, for instance) keeps them out of the loop.
-__device__ __forceinline__ int stage_selection(const int32_t* __restrict__ row, int m, int nb,
-                                               int32_t* dst) {
-  const int lane = lane_id();
-  int cnt = 0;
-  for (int i0 = 0; i0 < m; i0 += kWave) {
-    const int y = i0 + lane < m ? row[i0 + lane] : -1;
-    const bool ok = y >= 0 && y < nb;
-    const uint64_t mk = __ballot(ok);
-    if (ok) dst[cnt + __popcll(mk & lanemask_lt())] = y;
-    cnt += __popcll(mk);
-  }
-  wave_lds_sync();
-  return wave_uniform(cnt);
-}
 
 __device__ __forceinline__ float tile_max(const f32x16& s) {
   float a = s[0];
@@ -119,22 +86,7 @@ struct TileRow {
 
   // S^T = K_y Q_x^T
   __device__ __forceinline__ f32x16 scores(const u32x4 (&kf)[KC]) const {
-    f32x16 s;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) s[r] = 0.0f;
-    if constexpr (DT == BF16) {
-#pragma unroll
-      for (int k = 0; k < KC; ++k)
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kf[k]),
-                                                    __builtin_bit_cast(bf16x8, qf[k]), s, 0, 0, 0);
-    } else {
-#pragma unroll
-      for (int k = 0; k < KC; ++k)
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          s = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(kf[k][e]), __uint_as_float(qf[k][e]), s, 0, 0, 0);
-    }
-    return s;
+    return mfma_abt<DT, KC>(kf, qf);
   }
 
   // Max of this tile's scores for this lane's query, in log2 units (lanes l
@@ -204,14 +156,7 @@ struct TileRow {
         for (int rr = 0; rr < 8; ++rr) pk[rr] = 0u;
         t = 0.0f;
       }
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const u32x4 pw = {pk[4 * u], pk[4 * u + 1], pk[4 * u + 2], pk[4 * u + 3]};
-        const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
-#pragma unroll
-        for (int tt = 0; tt < NT; ++tt)
-          o[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, va(u * NT + tt)), pb, o[tt], 0, 0, 0);
-      }
+      mfma_acc_bf16<NT>(o, pk, va);
     } else {
       float p[16];
       t = weights_f32(s, p);
@@ -220,33 +165,29 @@ struct TileRow {
         for (int r = 0; r < 16; ++r) p[r] = 0.0f;
         t = 0.0f;
       }
-#pragma unroll
-      for (int tt = 0; tt < NT; ++tt)
-#pragma unroll
-        for (int a = 0; a < 4; ++a) {
-          const u32x4 v4 = va(tt * 4 + a);
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            o[tt] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(v4[e]), p[4 * a + e], o[tt], 0, 0, 0);
-        }
+      mfma_acc_f32<NT>(o, p, va);
     }
     lrun += t;
     return !check || __ballot(!(t <= kWeightCap)) == 0;
   }
 
-  // Merge with the low-resolution term, normalise and store the 32 x d block.
-  __device__ __forceinline__ void finish(elem* Out, int x, long long g, const float* cmax,
-                                         const float* csum, const float* cvec) {
+  // Merge with the low-resolution term, normalise and store the 32 x d block;
+  // if lse is not NULL also each query's log normaliser, ln of the row sum of
+  // A^ (natural units).
+  __device__ __forceinline__ void finish(elem* Out, float* lse, int x, long long g,
+                                         const float* cmax, const float* csum,
+                                         const float* cvec) {
     const int lane = lane_id(), jq = lane & 31, h = lane >> 5;
     const float ltot = halves_sum(lrun);
-    float af = 1.0f, bc = 0.0f, den = ltot;
+    float af = 1.0f, bc = 0.0f, den = ltot, Mt = mrun;
     if constexpr (COARSE) {
       const float Mx = cmax[g] * kLog2e;
-      const float Mt = fmaxf(mrun, Mx);
+      Mt = fmaxf(mrun, Mx);
       af = exp2f(mrun - Mt);
       bc = exp2f(Mx - Mt);
       den = ltot * af + csum[g] * bc;
     }
+    if (lse != nullptr && h == 0) lse[g * 32 + jq] = (log2f(den) + Mt) * kLn2;
     const float inv = 1.0f / den;
     const float ao = af * inv, bv = bc * inv;       // z = o * ao + cvec * bv
     elem* orow = Out + (long long)(x * 32 + jq) * D;
@@ -283,7 +224,7 @@ __global__ __launch_bounds__((TileCfg<DT, D>::kWaves * kWave)) void tile_kernel(
     const void* __restrict__ qv, const void* __restrict__ kv, const void* __restrict__ vv,
     const int32_t* __restrict__ idx, const float* __restrict__ cmax,
     const float* __restrict__ csum, const float* __restrict__ cvec, void* __restrict__ outv,
-    int n, int nb, int m, long long rows, float scale_log2) {
+    float* __restrict__ lse, int n, int nb, int m, long long rows, float scale_log2) {
   using Cfg = TileCfg<DT, D>;
   using elem = typename Cfg::elem;
   constexpr int W = Cfg::kWaves, PITCH = Cfg::kPitch, NT = Cfg::kNT;
@@ -442,7 +383,7 @@ __global__ __launch_bounds__((TileCfg<DT, D>::kWaves * kWave)) void tile_kernel(
       pass(false);
     }
   }
-  row.finish(reinterpret_cast<elem*>(outv) + hoff, x, g, cmax, csum, cvec);
+  row.finish(reinterpret_cast<elem*>(outv) + hoff, lse, x, g, cmax, csum, cvec);
 }
 
 // C consecutive 1 KB chunks HBM/L2 -> LDS, 16 bytes per lane each; chunk c is
@@ -479,7 +420,7 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
     const void* __restrict__ qv, const void* __restrict__ kpk, const void* __restrict__ vpk,
     const int32_t* __restrict__ idx, const float* __restrict__ cmax,
     const float* __restrict__ csum, const float* __restrict__ cvec, void* __restrict__ outv,
-    int n, int nb, int m, long long rows, float scale_log2) {
+    float* __restrict__ lse, int n, int nb, int m, long long rows, float scale_log2) {
   using Cfg = TileCfg<DT, D>;
   using elem = typename Cfg::elem;
   constexpr int KC = Cfg::kKChunks, VC = Cfg::kVChunks, CH = Cfg::kChunks;
@@ -576,14 +517,14 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
     row.restart(mx);
     pass(false);
   }
-  row.finish(reinterpret_cast<elem*>(outv) + hoff, x, g, cmax, csum, cvec);
+  row.finish(reinterpret_cast<elem*>(outv) + hoff, lse, x, g, cmax, csum, cvec);
 }
 
 // ---------------------------------------------------------------------------
 template <int DT, int D, bool PACKED>
 static void launch_tile_t(const void* q, const void* k, const void* v, const int32_t* idx,
                           const float* cmax, const float* csum, const float* cvec, void* out,
-                          long long bh, int n, int m, hipStream_t stream) {
+                          float* lse, long long bh, int n, int m, hipStream_t stream) {
   constexpr int W = TileCfg<DT, D>::kWaves;
   const int nb = n / kBlock;
   const long long rows = bh * nb;
@@ -594,46 +535,46 @@ static void launch_tile_t(const void* q, const void* k, const void* v, const int
     const size_t smem = (size_t)kStreamWaves * m * sizeof(int32_t);
     if (cmax)
       tile_stream_kernel<DT, D, true, kStreamWaves, kStreamSlots><<<blocks, kStreamWaves * kWave, smem, stream>>>(
-          q, k, v, idx, cmax, csum, cvec, out, n, nb, m, rows, scale_log2);
+          q, k, v, idx, cmax, csum, cvec, out, lse, n, nb, m, rows, scale_log2);
     else
       tile_stream_kernel<DT, D, false, kStreamWaves, kStreamSlots><<<blocks, kStreamWaves * kWave, smem, stream>>>(
-          q, k, v, idx, cmax, csum, cvec, out, n, nb, m, rows, scale_log2);
+          q, k, v, idx, cmax, csum, cvec, out, lse, n, nb, m, rows, scale_log2);
     return;
   }
   const unsigned blocks = (unsigned)((rows + W - 1) / W);
   const size_t smem = (size_t)W * m * sizeof(int32_t);     // per-wave selection lists
   if (cmax)
-    tile_kernel<DT, D, true, PACKED><<<blocks, W * kWave, smem, stream>>>(q, k, v, idx, cmax, csum, cvec, out, n, nb, m, rows, scale_log2);
+    tile_kernel<DT, D, true, PACKED><<<blocks, W * kWave, smem, stream>>>(q, k, v, idx, cmax, csum, cvec, out, lse, n, nb, m, rows, scale_log2);
   else
-    tile_kernel<DT, D, false, PACKED><<<blocks, W * kWave, smem, stream>>>(q, k, v, idx, cmax, csum, cvec, out, n, nb, m, rows, scale_log2);
+    tile_kernel<DT, D, false, PACKED><<<blocks, W * kWave, smem, stream>>>(q, k, v, idx, cmax, csum, cvec, out, lse, n, nb, m, rows, scale_log2);
 }
 
 template <bool PACKED>
 static void launch_tile_p(const void* q, const void* k, const void* v, const int32_t* idx,
                           const float* cmax, const float* csum, const float* cvec, void* out,
-                          long long bh, int n, int d, int m, int dtype, hipStream_t stream) {
+                          float* lse, long long bh, int n, int d, int m, int dtype, hipStream_t stream) {
   if (dtype == BF16) {
-    if (d == 32) launch_tile_t<BF16, 32, PACKED>(q, k, v, idx, cmax, csum, cvec, out, bh, n, m, stream);
-    else if (d == 64) launch_tile_t<BF16, 64, PACKED>(q, k, v, idx, cmax, csum, cvec, out, bh, n, m, stream);
-    else launch_tile_t<BF16, 128, PACKED>(q, k, v, idx, cmax, csum, cvec, out, bh, n, m, stream);
+    if (d == 32) launch_tile_t<BF16, 32, PACKED>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, m, stream);
+    else if (d == 64) launch_tile_t<BF16, 64, PACKED>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, m, stream);
+    else launch_tile_t<BF16, 128, PACKED>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, m, stream);
   } else {
-    if (d == 32) launch_tile_t<F32, 32, PACKED>(q, k, v, idx, cmax, csum, cvec, out, bh, n, m, stream);
-    else if (d == 64) launch_tile_t<F32, 64, PACKED>(q, k, v, idx, cmax, csum, cvec, out, bh, n, m, stream);
-    else launch_tile_t<F32, 128, PACKED>(q, k, v, idx, cmax, csum, cvec, out, bh, n, m, stream);
+    if (d == 32) launch_tile_t<F32, 32, PACKED>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, m, stream);
+    else if (d == 64) launch_tile_t<F32, 64, PACKED>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, m, stream);
+    else launch_tile_t<F32, 128, PACKED>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, m, stream);
   }
 }
 
 hipError_t launch_tile(const void* q, const void* k, const void* v, const void* kvpacked,
                        const int32_t* idx, const float* cmax, const float* csum,
-                       const float* cvec, void* out, long long bh, int n, int d, int m, int dtype,
-                       hipStream_t stream) {
+                       const float* cvec, void* out, float* lse, long long bh, int n, int d,
+                       int m, int dtype, hipStream_t stream) {
   if (kvpacked) {
     const size_t half = (size_t)bh * n * d * (dtype == BF16 ? 2 : 4);
     const void* kpk = kvpacked;
     const void* vpk = static_cast<const char*>(kvpacked) + half;
-    launch_tile_p<true>(q, kpk, vpk, idx, cmax, csum, cvec, out, bh, n, d, m, dtype, stream);
+    launch_tile_p<true>(q, kpk, vpk, idx, cmax, csum, cvec, out, lse, bh, n, d, m, dtype, stream);
   } else {
-    launch_tile_p<false>(q, k, v, idx, cmax, csum, cvec, out, bh, n, d, m, dtype, stream);
+    launch_tile_p<false>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, d, m, dtype, stream);
   }
   return hipGetLastError();
 }

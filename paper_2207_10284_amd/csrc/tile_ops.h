@@ -1,0 +1,120 @@
+// Matrix-core operands and products of one 32x32 tile (v_mfma_f32_32x32x16_bf16;
+// 32x32x2_f32 for float32), shared by the forward tile pass and the two
+// gradient passes.
+//
+// Operand layouts (bf16: 8 elements per 16-byte chunk, f32: 4):
+//  * Row layout, 32 rows x d: lane (h, j) = (l/32, l%32) holds row j,
+//    columns (d/2)h + e*s .. +e-1 in chunk s (KC chunks). Read straight from
+//    row-major memory, or from the packed "K layout" (chunk s*64 + lane, 1 KB
+//    per chunk and wave).
+//  * Transposed layout, d rows x 32 (the A operand of C^T += X^T P^T): the
+//    packed "V layout" (kernels.h), VC chunks per lane, which orders the 32
+//    contraction indices exactly as the B-operand registers of a tile product
+//    hold them.
+//  * A product C = A B^T of two row-layout operands leaves, in lane l,
+//    column l%32 of C (B's row) and its rows 8(r/4) + 4(l/32) + r%4 in
+//    register r. Those 16 values are directly the B operand of the next
+//    product over the same index (mfma_acc_*), so weights never move between
+//    lanes.
+#pragma once
+
+#include "common.h"
+
+namespace mra {
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+template <int DT, int D>
+struct TileCfg {
+  static constexpr int kWaves = (DT == F32 && D == 128) ? 2 : 4;
+  static constexpr int kPitch = DT == BF16 ? 40 : 36;           // LDS row pitch, elements
+  static constexpr int kNT = D / 32;                            // output tiles over d
+  // 16-byte transposed-layout chunks per lane per tile
+  static constexpr int kVChunks = DT == BF16 ? 2 * kNT : 4 * kNT;
+  static constexpr int kKChunks = DT == BF16 ? D / 16 : D / 8;  // 16-byte row-layout chunks per lane
+  static constexpr int kChunks = kKChunks + kVChunks;           // 1 KB chunks per K/V tile
+  using elem = typename std::conditional<DT == BF16, uint16_t, float>::type;
+};
+
+// Row j = l%32 of a 32-row block at `rows` (row-major, D columns) in the row
+// layout: lane half h reads columns [h*D/2, (h+1)*D/2).
+template <int DT, int D>
+__device__ __forceinline__ void load_rows(const typename TileCfg<DT, D>::elem* rows,
+                                          u32x4 (&f)[TileCfg<DT, D>::kKChunks]) {
+  const int lane = lane_id(), j = lane & 31, h = lane >> 5;
+  const u32x4* p = reinterpret_cast<const u32x4*>(rows + (long long)j * D + (D / 2) * h);
+#pragma unroll
+  for (int s = 0; s < TileCfg<DT, D>::kKChunks; ++s) f[s] = p[s];
+}
+
+// C = A B^T over the d columns, both in the row layout.
+template <int DT, int KC>
+__device__ __forceinline__ f32x16 mfma_abt(const u32x4 (&a)[KC], const u32x4 (&b)[KC]) {
+  f32x16 s;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) s[r] = 0.0f;
+  if constexpr (DT == BF16) {
+#pragma unroll
+    for (int k = 0; k < KC; ++k)
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[k]),
+                                                  __builtin_bit_cast(bf16x8, b[k]), s, 0, 0, 0);
+  } else {
+#pragma unroll
+    for (int k = 0; k < KC; ++k)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        s = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[k][e]), __uint_as_float(b[k][e]), s, 0, 0, 0);
+  }
+  return s;
+}
+
+// o[t] (d rows 32t.., 32 columns) += X^T W for bfloat16 weights pk (two per
+// register, in the order of a product's result registers); `xa(c)` yields
+// the 16-byte transposed-layout chunk c of X.
+template <int NT, class XA>
+__device__ __forceinline__ void mfma_acc_bf16(f32x16 (&o)[NT], const uint32_t (&pk)[8], XA xa) {
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const u32x4 pw = {pk[4 * u], pk[4 * u + 1], pk[4 * u + 2], pk[4 * u + 3]};
+    const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
+#pragma unroll
+    for (int tt = 0; tt < NT; ++tt)
+      o[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, xa(u * NT + tt)), pb, o[tt], 0, 0, 0);
+  }
+}
+
+// The same for float32 weights p (one per register).
+template <int NT, class XA>
+__device__ __forceinline__ void mfma_acc_f32(f32x16 (&o)[NT], const float (&p)[16], XA xa) {
+#pragma unroll
+  for (int tt = 0; tt < NT; ++tt)
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      const u32x4 v4 = xa(tt * 4 + a);
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        o[tt] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(v4[e]), p[4 * a + e], o[tt], 0, 0, 0);
+    }
+}
+
+// Copies a list of m block ids into LDS keeping only the entries in [0, nb),
+// in their order, and returns how many there are (wave-uniform). Reading the
+// ids from LDS keeps them off the vector-memory counter, so prefetched loads
+// stay in flight; dropping entries outside [0, nb) here (the padding of a
+// head-wide selection, for instance) keeps them out of the loop.
+__device__ __forceinline__ int stage_selection(const int32_t* __restrict__ row, int m, int nb,
+                                               int32_t* dst) {
+  const int lane = lane_id();
+  int cnt = 0;
+  for (int i0 = 0; i0 < m; i0 += kWave) {
+    const int y = i0 + lane < m ? row[i0 + lane] : -1;
+    const bool ok = y >= 0 && y < nb;
+    const uint64_t mk = __ballot(ok);
+    if (ok) dst[cnt + __popcll(mk & lanemask_lt())] = y;
+    cnt += __popcll(mk);
+  }
+  wave_lds_sync();
+  return wave_uniform(cnt);
+}
+
+}  // namespace mra

@@ -29,13 +29,16 @@ SIGNATURES = {
     "mra_coarse_scores": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _P]),
     "mra_select": (_I, [_P, _P, _I, _I, _I, _I, _I, _P]),
     "mra_coarse_term": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P]),
-    "mra_block_sddmm_spmm": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _P]),
+    "mra_block_sddmm_spmm": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _P]),
     "mra_forward_workspace_bytes": (_Z, [_I, _I, _I, _I, _I, _I, _I]),
-    "mra_attention_forward": (_I, [_P, _P, _P, _P, _P, _P, _Z, _I, _I, _I, _I, _I, _I, _I, _P]),
-    "mra_sparse_attention_forward": (_I, [_P, _P, _P, _P, _P, _P, _Z, _I, _I, _I, _I, _I, _I, _I, _P]),
+    "mra_attention_forward": (_I, [_P, _P, _P, _P, _P, _P, _P, _Z, _I, _I, _I, _I, _I, _I, _I, _P]),
+    "mra_sparse_attention_forward": (_I, [_P, _P, _P, _P, _P, _P, _P, _Z, _I, _I, _I, _I, _I, _I, _I, _P]),
     "mra_select_global": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, _P]),
     "mra_forward_global_workspace_bytes": (_Z, [_I, _I, _I, _I, _I, _I]),
-    "mra_attention_forward_global": (_I, [_P, _P, _P, _P, _P, _P, _Z, _I, _I, _I, _I, _I, _I, _I, _I, _P]),
+    "mra_attention_forward_global": (_I, [_P, _P, _P, _P, _P, _P, _P, _Z, _I, _I, _I, _I, _I, _I, _I, _I, _P]),
+    "mra_backward_workspace_bytes": (_Z, [_I, _I, _I, _I, _I, _I]),
+    "mra_attention_backward": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _Z,
+                                    _I, _I, _I, _I, _I, _I, _I, _I, _P]),
     "mra_status_str": (ctypes.c_char_p, [_I]),
     "mra_last_hip_error": (_I, []),
 }
@@ -175,10 +178,11 @@ def coarse_term(scores, idx, vp):
     return cmax, csum, cvec
 
 
-def block_sddmm_spmm(q, k, v, idx, cmax=None, csum=None, cvec=None, out=None, kvpacked=None):
+def block_sddmm_spmm(q, k, v, idx, cmax=None, csum=None, cvec=None, out=None, kvpacked=None, lse_out=None):
     """Selected tiles exp(c Q_x K_y^T) V_y, merged with the coarse term (if
     given) and normalised: the output Z, [B, H, n, d] in the input dtype.
-    ``kvpacked`` (from ``pool(..., packed=True)``) replaces k and v when given."""
+    ``kvpacked`` (from ``pool(..., packed=True)``) replaces k and v when given;
+    ``lse_out`` (float32 [B, H, n]) receives each query's log normaliser."""
     ref = _check_qkv(q, *((k, v) if kvpacked is None else (kvpacked[0], kvpacked[1])))
     B, H, n, d = ref.shape
     nb = n // BLOCK
@@ -190,8 +194,10 @@ def block_sddmm_spmm(q, k, v, idx, cmax=None, csum=None, cvec=None, out=None, kv
         _check_f32(cvec, (B, H, nb, d), "cvec")
     if out is None:
         out = torch.empty_like(ref)
+    if lse_out is not None:
+        _check_f32(lse_out, (B, H, n), "lse_out")
     _call("mra_block_sddmm_spmm", _ptr(q), _ptr(k), _ptr(v), _ptr(kvpacked), _ptr(idx), _ptr(cmax), _ptr(csum),
-          _ptr(cvec), _ptr(out), B, H, n, d, BLOCK, budget, _dtype_code(ref), _stream(ref.device))
+          _ptr(cvec), _ptr(out), _ptr(lse_out), B, H, n, d, BLOCK, budget, _dtype_code(ref), _stream(ref.device))
     return out
 
 
@@ -200,20 +206,21 @@ def forward_workspace_bytes(B: int, H: int, n: int, d: int, budget: int, dtype=t
     return int(load().mra_forward_workspace_bytes(B, H, n, d, BLOCK, budget, code))
 
 
-def attention_forward(q, k, v, budget: int, out=None, idx_out=None, workspace=None):
+def attention_forward(q, k, v, budget: int, out=None, idx_out=None, workspace=None, lse_out=None):
     """The whole MRA-2 forward pass. Returns the output Z ([B, H, n, d], input
-    dtype); the selection is written to ``idx_out`` when given."""
-    return _forward("mra_attention_forward", q, k, v, budget, out, idx_out, workspace)
+    dtype); the selection is written to ``idx_out`` and each query's log
+    normaliser (float32 [B, H, n]) to ``lse_out`` when given."""
+    return _forward("mra_attention_forward", q, k, v, budget, out, idx_out, workspace, lse_out)
 
 
-def sparse_attention_forward(q, k, v, budget: int, out=None, idx_out=None, workspace=None):
+def sparse_attention_forward(q, k, v, budget: int, out=None, idx_out=None, workspace=None, lse_out=None):
     """The sparse-only variant MRA-2-s (Sec. 5): softmax over the selected
     blocks only, no low-resolution term; budget >= 1. Same arguments and
     result as ``attention_forward``."""
-    return _forward("mra_sparse_attention_forward", q, k, v, budget, out, idx_out, workspace)
+    return _forward("mra_sparse_attention_forward", q, k, v, budget, out, idx_out, workspace, lse_out)
 
 
-def _forward(entry, q, k, v, budget, out, idx_out, workspace):
+def _forward(entry, q, k, v, budget, out, idx_out, workspace, lse_out):
     ref = _check_qkv(q, k, v)
     B, H, n, d = ref.shape
     nb = n // BLOCK
@@ -221,10 +228,12 @@ def _forward(entry, q, k, v, budget, out, idx_out, workspace):
         out = torch.empty_like(ref)
     if idx_out is not None:
         _check_idx(idx_out, B, H, nb, budget, ref.device)
+    if lse_out is not None:
+        _check_f32(lse_out, (B, H, n), "lse_out")
     need = forward_workspace_bytes(B, H, n, d, budget, ref.dtype)
     if workspace is None:
         workspace = torch.empty(max(need, 1), device=ref.device, dtype=torch.uint8)
-    _call(entry, _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(idx_out),
+    _call(entry, _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(idx_out), _ptr(lse_out),
           _ptr(workspace), workspace.numel() * workspace.element_size(),
           B, H, n, d, BLOCK, budget, _dtype_code(ref), _stream(ref.device))
     return out
@@ -236,10 +245,11 @@ def forward_global_workspace_bytes(B: int, H: int, n: int, d: int, dtype=torch.b
 
 
 def attention_forward_global(q, k, v, budget: int, prior_diagonal: bool = False, out=None, idx_out=None,
-                             workspace=None):
+                             workspace=None, lse_out=None):
     """MRA-2 with the head-wide budget of Alg. 1 (``budget`` blocks per head,
     plus the diagonal with ``prior_diagonal``). Returns Z; the selection
-    (int32 [B, H, nb, nb], rows padded with -1) goes to ``idx_out`` when given."""
+    (int32 [B, H, nb, nb], rows padded with -1) goes to ``idx_out`` and the
+    log normalisers to ``lse_out`` when given."""
     ref = _check_qkv(q, k, v)
     B, H, n, d = ref.shape
     nb = n // BLOCK
@@ -247,10 +257,80 @@ def attention_forward_global(q, k, v, budget: int, prior_diagonal: bool = False,
         out = torch.empty_like(ref)
     if idx_out is not None:
         _check_idx(idx_out, B, H, nb, nb, ref.device)
+    if lse_out is not None:
+        _check_f32(lse_out, (B, H, n), "lse_out")
     need = forward_global_workspace_bytes(B, H, n, d, ref.dtype)
     if workspace is None:
         workspace = torch.empty(max(need, 1), device=ref.device, dtype=torch.uint8)
-    _call("mra_attention_forward_global", _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(idx_out),
+    _call("mra_attention_forward_global", _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(idx_out), _ptr(lse_out),
           _ptr(workspace), workspace.numel() * workspace.element_size(),
           B, H, n, d, BLOCK, budget, int(bool(prior_diagonal)), _dtype_code(ref), _stream(ref.device))
     return out
+
+
+def backward_workspace_bytes(B: int, H: int, n: int, d: int, dtype=torch.bfloat16) -> int:
+    code = MRA_BF16 if dtype == torch.bfloat16 else MRA_F32
+    return int(load().mra_backward_workspace_bytes(B, H, n, d, BLOCK, code))
+
+
+def attention_backward(q, k, v, out, dout, lse, idx, coarse: bool = True, dq=None, dk=None, dv=None,
+                       workspace=None):
+    """Gradients (dq, dk, dv) through one forward (``coarse=True``: MRA-2,
+    per-row or head-wide budget; ``False``: MRA-2-s) with its selection
+    ``idx`` (int32 [B, H, nb, width]) held fixed; ``out`` and ``lse`` are the
+    forward's output and log normalisers, ``dout`` the gradient of the output."""
+    ref = _check_qkv(q, k, v, out, dout)
+    B, H, n, d = ref.shape
+    nb = n // BLOCK
+    width = idx.shape[-1]
+    _check_idx(idx, B, H, nb, width, ref.device)
+    _check_f32(lse, (B, H, n), "lse")
+    dq = torch.empty_like(ref) if dq is None else dq
+    dk = torch.empty_like(ref) if dk is None else dk
+    dv = torch.empty_like(ref) if dv is None else dv
+    _check_qkv(ref, dq, dk, dv)
+    need = backward_workspace_bytes(B, H, n, d, ref.dtype)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), device=ref.device, dtype=torch.uint8)
+    _call("mra_attention_backward", _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(lse), _ptr(idx),
+          _ptr(dq), _ptr(dk), _ptr(dv), _ptr(workspace), workspace.numel() * workspace.element_size(),
+          B, H, n, d, BLOCK, width, int(bool(coarse)), _dtype_code(ref), _stream(ref.device))
+    return dq, dk, dv
+
+
+class MraAttention(torch.autograd.Function):
+    """Z = MRA-2 attention of (q, k, v) as a differentiable op: the forward
+    keeps its selection and log normalisers, the backward hands them to
+    ``attention_backward`` (selection held fixed). ``variant`` is "mra2"
+    (per-row budget), "mra2s" (sparse only) or "global" (head-wide budget,
+    with ``prior_diagonal``)."""
+
+    @staticmethod
+    def forward(ctx, q, k, v, budget: int, variant: str = "mra2", prior_diagonal: bool = False):
+        ref = _check_qkv(q, k, v)
+        B, H, n, d = ref.shape
+        nb = n // BLOCK
+        lse = torch.empty(B, H, n, device=ref.device, dtype=torch.float32)
+        if variant == "global":
+            idx = torch.empty(B, H, nb, nb, device=ref.device, dtype=torch.int32)
+            out = attention_forward_global(q, k, v, budget, prior_diagonal, idx_out=idx, lse_out=lse)
+        elif variant in ("mra2", "mra2s"):
+            idx = torch.empty(B, H, nb, budget, device=ref.device, dtype=torch.int32)
+            fwd = attention_forward if variant == "mra2" else sparse_attention_forward
+            out = fwd(q, k, v, budget, idx_out=idx, lse_out=lse)
+        else:
+            raise ValueError(f"unknown variant {variant!r}")
+        ctx.save_for_backward(q, k, v, out, lse, idx)
+        ctx.coarse = variant != "mra2s"
+        return out
+
+    @staticmethod
+    def backward(ctx, dout):
+        q, k, v, out, lse, idx = ctx.saved_tensors
+        dq, dk, dv = attention_backward(q, k, v, out, dout.contiguous(), lse, idx, coarse=ctx.coarse)
+        return dq, dk, dv, None, None, None
+
+
+def mra_attention(q, k, v, budget: int, variant: str = "mra2", prior_diagonal: bool = False):
+    """Differentiable MRA-2 attention (see ``MraAttention``)."""
+    return MraAttention.apply(q, k, v, budget, variant, prior_diagonal)

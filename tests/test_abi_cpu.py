@@ -31,7 +31,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 13, names
+    assert len(names) == 15, names
     for name in names:
         assert hasattr(lib, name), name
     assert set(names) == set(ops.SIGNATURES)
@@ -44,8 +44,8 @@ def test_status_strings(lib):
 
 
 def fwd(lib, q=A, k=A, v=A, out=A, idx=None, ws=A, wsb=1 << 40, B=1, H=1, n=64, d=64, block=32,
-        budget=1, dtype=1):
-    return lib.mra_attention_forward(q, k, v, out, idx, ws, wsb, B, H, n, d, block, budget, dtype, None)
+        budget=1, dtype=1, lse=None):
+    return lib.mra_attention_forward(q, k, v, out, idx, lse, ws, wsb, B, H, n, d, block, budget, dtype, None)
 
 
 def test_forward_validation(lib):
@@ -66,6 +66,7 @@ def test_forward_validation(lib):
     assert fwd(lib, ws=None) == INVALID
     assert fwd(lib, v=MIS) == MISALIGNED
     assert fwd(lib, idx=MIS) == MISALIGNED
+    assert fwd(lib, lse=MIS) == MISALIGNED
     need = lib.mra_forward_workspace_bytes(1, 1, 64, 64, 32, 1, 1)
     assert fwd(lib, wsb=need - 1) == WORKSPACE
     # empty problems succeed without touching any pointer
@@ -76,8 +77,8 @@ def test_forward_validation(lib):
 
 
 def sfwd(lib, q=A, k=A, v=A, out=A, idx=None, ws=A, wsb=1 << 40, B=1, H=1, n=64, d=64, block=32,
-         budget=1, dtype=1):
-    return lib.mra_sparse_attention_forward(q, k, v, out, idx, ws, wsb, B, H, n, d, block, budget,
+         budget=1, dtype=1, lse=None):
+    return lib.mra_sparse_attention_forward(q, k, v, out, idx, lse, ws, wsb, B, H, n, d, block, budget,
                                             dtype, None)
 
 
@@ -90,6 +91,7 @@ def test_sparse_forward_validation(lib):
     assert sfwd(lib, d=48) == UNSUPPORTED
     assert sfwd(lib, q=None) == INVALID
     assert sfwd(lib, k=MIS) == MISALIGNED
+    assert sfwd(lib, lse=MIS) == MISALIGNED
     need = lib.mra_forward_workspace_bytes(1, 1, 64, 64, 32, 1, 1)
     assert sfwd(lib, wsb=need - 1) == WORKSPACE
     assert sfwd(lib, B=0, q=None, k=None, v=None, out=None, ws=None) == OK
@@ -139,13 +141,15 @@ def test_global_selection_validation(lib):
     assert sg(idx=MIS) == MISALIGNED
     assert sg(n=48) == INVALID
     assert sg(B=0, scores=None, idx=None) == OK
-    fg = lambda q=A, out=A, ws=A, wsb=1 << 40, n=128, d=64, budget=1, prior=0, dtype=1: \
-        lib.mra_attention_forward_global(q, A, A, out, None, ws, wsb, 1, 1, n, d, 32, budget, prior, dtype, None)
+    fg = lambda q=A, out=A, ws=A, wsb=1 << 40, n=128, d=64, budget=1, prior=0, dtype=1, lse=None: \
+        lib.mra_attention_forward_global(q, A, A, out, None, lse, ws, wsb, 1, 1, n, d, 32, budget, prior, dtype,
+                                         None)
     assert fg(budget=17) == INVALID
     assert fg(prior=-1) == INVALID
     assert fg(d=48) == UNSUPPORTED
     assert fg(q=None) == INVALID
     assert fg(ws=MIS) == MISALIGNED
+    assert fg(lse=MIS) == MISALIGNED
     need = lib.mra_forward_global_workspace_bytes(1, 1, 128, 64, 32, 1)
     assert fg(wsb=need - 1) == WORKSPACE
     assert fg(n=0, budget=0, q=None, out=None, ws=None) == OK
@@ -173,16 +177,58 @@ def test_step_validation(lib):
     assert lib.mra_coarse_term(A, None, A, A, A, A, 1, 1, 64, 64, 32, 1, None) == INVALID
     assert lib.mra_coarse_term(A, A, A, A, A, MIS, 1, 1, 64, 64, 32, 1, None) == MISALIGNED
     # tile pass: coarse term all-or-nothing; sparse-only needs budget >= 1
-    t = lib.mra_block_sddmm_spmm
-    assert t(A, A, A, None, A, A, None, A, A, 1, 1, 64, 64, 32, 1, 1, None) == INVALID
-    assert t(A, A, A, None, None, None, None, None, A, 1, 1, 64, 64, 32, 0, 1, None) == INVALID
-    assert t(A, A, A, None, A, A, A, A, A, 1, 1, 64, 64, 32, 3, 1, None) == INVALID
-    assert t(A, A, A, None, A, A, A, A, MIS, 1, 1, 64, 64, 32, 1, 1, None) == MISALIGNED
-    assert t(A, A, A, None, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 2, None) == UNSUPPORTED
-    assert t(A, A, None, None, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 1, None) == INVALID   # no v at all
-    assert t(A, None, A, None, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 1, None) == INVALID   # no k
-    assert t(A, None, None, MIS, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 1, None) == MISALIGNED
-    assert t(None, None, None, None, None, A, A, A, None, 0, 1, 64, 64, 32, 1, 1, None) == OK
+    t = lambda q, k, v, kv, idx, cm, cs, cv, out, B, H, n, d, blk, m, dt, lse=None: \
+        lib.mra_block_sddmm_spmm(q, k, v, kv, idx, cm, cs, cv, out, lse, B, H, n, d, blk, m, dt, None)
+    assert t(A, A, A, None, A, A, None, A, A, 1, 1, 64, 64, 32, 1, 1) == INVALID
+    assert t(A, A, A, None, None, None, None, None, A, 1, 1, 64, 64, 32, 0, 1) == INVALID
+    assert t(A, A, A, None, A, A, A, A, A, 1, 1, 64, 64, 32, 3, 1) == INVALID
+    assert t(A, A, A, None, A, A, A, A, MIS, 1, 1, 64, 64, 32, 1, 1) == MISALIGNED
+    assert t(A, A, A, None, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 1, lse=MIS) == MISALIGNED
+    assert t(A, A, A, None, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 2) == UNSUPPORTED
+    assert t(A, A, None, None, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 1) == INVALID   # no v at all
+    assert t(A, None, A, None, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 1) == INVALID   # no k
+    assert t(A, None, None, MIS, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 1) == MISALIGNED
+    assert t(None, None, None, None, None, A, A, A, None, 0, 1, 64, 64, 32, 1, 1) == OK
+
+
+def bwd(lib, q=A, k=A, v=A, out=A, dout=A, lse=A, idx=A, dq=A, dk=A, dv=A, ws=A, wsb=1 << 40,
+        B=1, H=1, n=64, d=64, block=32, width=1, coarse=1, dtype=1):
+    return lib.mra_attention_backward(q, k, v, out, dout, lse, idx, dq, dk, dv, ws, wsb,
+                                      B, H, n, d, block, width, coarse, dtype, None)
+
+
+def test_backward_validation(lib):
+    assert bwd(lib, block=16) == UNSUPPORTED
+    assert bwd(lib, d=48) == UNSUPPORTED
+    assert bwd(lib, n=48) == INVALID
+    assert bwd(lib, dtype=3) == UNSUPPORTED
+    assert bwd(lib, width=-1) == INVALID
+    assert bwd(lib, width=3) == INVALID       # nb = 2
+    assert bwd(lib, coarse=2) == INVALID
+    for name in ("q", "k", "v", "out", "dout", "lse", "dq", "dk", "dv", "ws"):
+        assert bwd(lib, **{name: None}) == INVALID, name
+        assert bwd(lib, **{name: MIS}) == MISALIGNED, name
+    assert bwd(lib, idx=None) == INVALID      # width > 0 needs the selection
+    assert bwd(lib, idx=MIS) == MISALIGNED
+    need = lib.mra_backward_workspace_bytes(1, 1, 64, 64, 32, 1)
+    assert bwd(lib, wsb=need - 1) == WORKSPACE
+    assert bwd(lib, B=0, q=None, k=None, v=None, out=None, dout=None, lse=None, idx=None, dq=None,
+               dk=None, dv=None, ws=None) == OK
+    assert lib.mra_last_hip_error() == 0
+
+
+def test_backward_workspace_bytes(lib):
+    f = lib.mra_backward_workspace_bytes
+    assert f(1, 1, 64, 48, 32, 1) == 0
+    assert f(1, 1, 64, 64, 16, 1) == 0
+    assert f(1, 1, 64, 64, 32, 9) == 0
+    al = lambda x: (x + 255) // 256 * 256
+    B, H, n, d = 8, 12, 4096, 64
+    bh, nb = B * H, n // 32
+    for dt, e in ((0, 4), (1, 2)):
+        want = 7 * al(bh * nb * d * 4) + 7 * al(bh * n * d * e) + 2 * al(bh * n * 4) \
+            + al(bh * nb * (nb // 32) * 4) + 2 * al(bh * nb * nb * 4)
+        assert f(B, H, n, d, 32, dt) == want
 
 
 def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
