@@ -114,8 +114,8 @@ mra_status_t check_global_budget(const Shape& s, int budget, int prior_diagonal)
 
 // Workspace of the gradient pass (pointer roles in kernels.h, BwdArgs).
 struct WsBwd {
-  size_t qp, kp, vp, q_row, q_t, k_row, k_t, v_row, g_row, g_t, l2, delta, bits, gh, W, dS, dqp,
-      dkp, dvp, total;
+  size_t qp, kp, vp, q_row, q_t, k_row, k_t, v_row, g_row, g_t, ld, bits, gh, W, dS, dqp, dkp,
+      dvp, total;
 };
 
 WsBwd ws_bwd(long long bh, int nb, int d, mra_dtype_t dtype) {
@@ -123,7 +123,6 @@ WsBwd ws_bwd(long long bh, int nb, int d, mra_dtype_t dtype) {
   size_t off = 0;
   const size_t pooled = align256((size_t)bh * nb * d * sizeof(float));
   const size_t packed = align256((size_t)bh * nb * kBlockSize * d * (dtype == MRA_BF16 ? 2 : 4));
-  const size_t per_query = align256((size_t)bh * nb * kBlockSize * sizeof(float));
   const size_t grid = align256((size_t)bh * nb * nb * sizeof(float));
   L.qp = off; off += pooled;
   L.kp = off; off += pooled;
@@ -135,8 +134,7 @@ WsBwd ws_bwd(long long bh, int nb, int d, mra_dtype_t dtype) {
   L.v_row = off; off += packed;
   L.g_row = off; off += packed;
   L.g_t = off; off += packed;
-  L.l2 = off; off += per_query;
-  L.delta = off; off += per_query;
+  L.ld = off; off += align256((size_t)bh * nb * 64 * sizeof(float));
   L.bits = off; off += align256((size_t)bh * nb * ((nb + 31) / 32) * sizeof(uint32_t));
   L.gh = off; off += pooled;
   L.W = off; off += grid;
@@ -428,7 +426,7 @@ mra_status_t mra_attention_backward(const void* q, const void* k, const void* v,
   A.qp = f32(L.qp); A.kp = f32(L.kp); A.vp = f32(L.vp);
   A.q_row = ws + L.q_row; A.q_t = ws + L.q_t; A.k_row = ws + L.k_row; A.k_t = ws + L.k_t;
   A.v_row = ws + L.v_row; A.g_row = ws + L.g_row; A.g_t = ws + L.g_t;
-  A.l2 = f32(L.l2); A.delta = f32(L.delta);
+  A.ld = f32(L.ld);
   A.bits = reinterpret_cast<uint32_t*>(ws + L.bits);
   A.gh = f32(L.gh); A.W = f32(L.W); A.dS = f32(L.dS);
   A.dqp = f32(L.dqp); A.dkp = f32(L.dkp); A.dvp = f32(L.dvp);

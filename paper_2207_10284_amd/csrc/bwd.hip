@@ -21,15 +21,16 @@
 // least each coarse logit S~[x,y] + ln b of its own row.
 //
 // Kernels, in launch order (after the packing pass of pool.hip):
-//  * bwd_rows_kernel: per block-row (a wave; 16 per workgroup): delta, the
-//    log normaliser in log2 units, the selection as a bitmap; with the coarse
+//  * bwd_rows_kernel: per block-row (a wave; 16 per workgroup): a 256-byte
+//    record of the 32 log normalisers (log2 units) and the 32 deltas, the
+//    selection as a bitmap; with the coarse
 //    term also G^, d^ and the row's W, dS~ and dQ~ (K~ and V~ staged through
 //    LDS 64 blocks at a time).
 //  * bwd_cols_kernel: per column block (a wave; 16 per workgroup): dK~, dV~.
-//  * bwd_dq_kernel: per block-row (a wave), over its refined tiles: the
+//  * bwd_dq_(stream_)kernel: per block-row (a wave), over its refined tiles: the
 //    products K_y Q_x^T and V_y G_x^T on the matrix cores, then
 //    dQ^T += K_y^T dP^T.
-//  * bwd_dkdv_kernel: per column block (a wave), over the block-rows that
+//  * bwd_dkdv_(stream_)kernel: per column block (a wave), over the block-rows that
 //    refined it (ascending): dV^T += G_x^T A, dK^T += c Q_x^T dP.
 // Tile operands come from packed copies in the layouts of tile_ops.h.
 #include "common.h"
@@ -52,8 +53,7 @@ template <int DT, int D, bool COARSE>
 __global__ __launch_bounds__(kBwdRows * kWave) void bwd_rows_kernel(
     const void* __restrict__ gin, const void* __restrict__ zin, const float* __restrict__ lse,
     const int32_t* __restrict__ idx, const float* __restrict__ qp, const float* __restrict__ kp,
-    const float* __restrict__ vp, float* __restrict__ l2, float* __restrict__ delta,
-    uint32_t* __restrict__ bits, float* __restrict__ gh, float* __restrict__ Wout,
+    const float* __restrict__ vp, float* __restrict__ ld, uint32_t* __restrict__ bits, float* __restrict__ gh, float* __restrict__ Wout,
     float* __restrict__ dSout, float* __restrict__ dqp, int nb, int m, float scale) {
   using Cfg = TileCfg<DT, D>;
   using elem = typename Cfg::elem;
@@ -97,9 +97,9 @@ __global__ __launch_bounds__(kBwdRows * kWave) void bwd_rows_kernel(
     }
     const float dl = halves_sum(part);
     const float L = lse[g * 32 + j];
-    if (h == 0) {
-      l2[g * 32 + j] = L * kLog2e;
-      delta[g * 32 + j] = dl;
+    if (h == 0) {                                           // the block-row's record
+      ld[g * 64 + j] = L * kLog2e;
+      ld[g * 64 + 32 + j] = dl;
     }
     // the selection as a bitmap (entries outside [0, nb) ignored)
     for (int i = lane; i < nbw; i += kWave) bm[i] = 0u;
@@ -314,8 +314,8 @@ template <int DT, int D, bool COARSE>
 __global__ __launch_bounds__(kBwdTileWaves * kWave) void bwd_dq_kernel(
     const void* __restrict__ qin, const void* __restrict__ gin, const void* __restrict__ krow,
     const void* __restrict__ vrow, const void* __restrict__ kt, const int32_t* __restrict__ idx,
-    const float* __restrict__ l2, const float* __restrict__ delta, const float* __restrict__ dqp,
-    void* __restrict__ dq, int nb, int m, long long rows, float scale, float scale_log2) {
+    const float* __restrict__ ld, const float* __restrict__ dqp, void* __restrict__ dq, int nb,
+    int m, long long rows, float scale, float scale_log2) {
   using Cfg = TileCfg<DT, D>;
   using elem = typename Cfg::elem;
   constexpr int KC = Cfg::kKChunks, VC = Cfg::kVChunks, NT = Cfg::kNT;
@@ -331,7 +331,7 @@ __global__ __launch_bounds__(kBwdTileWaves * kWave) void bwd_dq_kernel(
   u32x4 qf[KC], gf[KC];
   load_rows<DT, D>(reinterpret_cast<const elem*>(qin) + g * 32 * D, qf);
   load_rows<DT, D>(reinterpret_cast<const elem*>(gin) + g * 32 * D, gf);
-  const float lq = l2[g * 32 + jq], dl = delta[g * 32 + jq];
+  const float lq = ld[g * 64 + jq], dl = ld[g * 64 + 32 + jq];
   f32x16 acc[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t)
@@ -385,10 +385,9 @@ template <int DT, int D, bool COARSE>
 __global__ __launch_bounds__(kBwdTileWaves * kWave) void bwd_dkdv_kernel(
     const void* __restrict__ kin, const void* __restrict__ vin, const void* __restrict__ qrow,
     const void* __restrict__ grow, const void* __restrict__ qt, const void* __restrict__ gt,
-    const uint32_t* __restrict__ bits, const float* __restrict__ l2,
-    const float* __restrict__ delta, const float* __restrict__ dkp,
-    const float* __restrict__ dvp, void* __restrict__ dk, void* __restrict__ dv, int nb,
-    long long rows, float scale, float scale_log2) {
+    const uint32_t* __restrict__ bits, const float* __restrict__ ld,
+    const float* __restrict__ dkp, const float* __restrict__ dvp, void* __restrict__ dk,
+    void* __restrict__ dv, int nb, long long rows, float scale, float scale_log2) {
   using Cfg = TileCfg<DT, D>;
   using elem = typename Cfg::elem;
   constexpr int KC = Cfg::kKChunks, VC = Cfg::kVChunks, NT = Cfg::kNT;
@@ -442,8 +441,8 @@ __global__ __launch_bounds__(kBwdTileWaves * kWave) void bwd_dkdv_kernel(
 #pragma unroll
     for (int c = 0; c < VC; ++c) o.gt[c] = gtp[((long long)x * VC + c) * 64];
     // queries 8rg + 4h + e of block-row x (the rows of this lane's registers)
-    const float* lx = l2 + (hb + x) * 32 + 4 * h;
-    const float* dx = delta + (hb + x) * 32 + 4 * h;
+    const float* lx = ld + (hb + x) * 64 + 4 * h;
+    const float* dx = lx + 32;
 #pragma unroll
     for (int rg = 0; rg < 4; ++rg) {
       o.l[rg] = *reinterpret_cast<const f32x4*>(lx + 8 * rg);
@@ -481,42 +480,335 @@ __global__ __launch_bounds__(kBwdTileWaves * kWave) void bwd_dkdv_kernel(
 }
 
 // ---------------------------------------------------------------------------
-template <int DT, int D>
-static void launch_bwd_t(const BwdArgs& A, hipStream_t stream) {
+// Streaming forms of the two tile passes (tiles whose chunks fit the load's
+// immediate offset: bf16 d <= 64, f32 d = 32). A wave's next tile is copied
+// HBM/L2 -> LDS with direct-to-LDS loads while the current one is computed.
+// Each wave owns a slot split into parts that are consumed at different
+// times (separate LDS objects, so reading one part does not wait for loads in
+// flight into another); a part is refilled with the next tile's operands as
+// soon as it has been read into registers. Loads complete in issue order, so
+// "part P of tile i has landed" is a wait until at most the number of loads
+// issued after it are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_loads() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+__device__ __forceinline__ void wait_lds_reads() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+}
+
+// Slot reads are issued as inline assembly: the compiler cannot tell the
+// slot's parts apart and, seeing loads in flight into LDS, would wait for all
+// of them before any slot read. Here the caller's wait_loads<> covers the part
+// being read; lds_done() waits for the reads and ties each value to that wait
+// so that no use is scheduled before it.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+}
+
+template <int OFF>
+__device__ __forceinline__ u32x4 lds_read16(uint32_t addr) {
+  u32x4 v;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF) : "memory");
+  return v;
+}
+
+// v[i] = chunk C0 + i of a part (chunks 1 KB apart) for this lane, i < C
+template <int I, int C, int C0>
+struct LdsChunks {
+  static __device__ __forceinline__ void run(uint32_t addr, u32x4* v) {
+    v[I] = lds_read16<(C0 + I) * 1024>(addr);
+    LdsChunks<I + 1, C, C0>::run(addr, v);
+  }
+};
+template <int C, int C0>
+struct LdsChunks<C, C, C0> {
+  static __device__ __forceinline__ void run(uint32_t, u32x4*) {}
+};
+
+template <int C, int C0 = 0>
+__device__ __forceinline__ void lds_read_chunks(uint32_t addr, u32x4 (&v)[C]) {
+  LdsChunks<0, C, C0>::run(addr, v);
+}
+
+template <int C>
+__device__ __forceinline__ void lds_done(u32x4 (&v)[C]) {
+  wait_lds_reads();
+#pragma unroll
+  for (int c = 0; c < C; ++c) asm volatile("" : "+v"(v[c]));
+}
+
+// dQ, one wave per block-row. Part A: K_y and V_y in the row layout (the
+// products with Q_x and G_x); part B: K_y in the transposed layout.
+template <int DT, int D, bool COARSE, int WAVES>
+__global__ __launch_bounds__(WAVES * kWave) void bwd_dq_stream_kernel(
+    const void* __restrict__ qin, const void* __restrict__ gin, const void* __restrict__ krow,
+    const void* __restrict__ vrow, const void* __restrict__ kt, const int32_t* __restrict__ idx,
+    const float* __restrict__ ld, const float* __restrict__ dqp, void* __restrict__ dq, int nb,
+    int m, long long rows, float scale, float scale_log2) {
+  using Cfg = TileCfg<DT, D>;
+  using elem = typename Cfg::elem;
+  constexpr int KC = Cfg::kKChunks, VC = Cfg::kVChunks, NT = Cfg::kNT;
+  constexpr int NA = 2 * KC, NB = VC;                      // loads per part
+  static_assert(KC <= 4 && VC <= 4, "chunk offsets fit the immediate field");
+  __shared__ __attribute__((aligned(16))) u32x4 partA[WAVES][NA * 64];
+  __shared__ __attribute__((aligned(16))) u32x4 partB[WAVES][NB * 64];
+  extern __shared__ int32_t sidx_all[];
+  const int w = wave_uniform(threadIdx.x / kWave);
+  const int lane = lane_id(), jq = lane & 31;
+  const long long g = xcd_remap(blockIdx.x, gridDim.x) * (long long)WAVES + w;
+  if (g >= rows) return;                                    // no workgroup barriers below
+  const long long bh = g / nb;
+  int32_t* myidx = sidx_all + w * m;
+  const int cnt = stage_selection(idx + g * m, m, nb, myidx);
+
+  u32x4 qf[KC], gf[KC];
+  load_rows<DT, D>(reinterpret_cast<const elem*>(qin) + g * 32 * D, qf);
+  load_rows<DT, D>(reinterpret_cast<const elem*>(gin) + g * 32 * D, gf);
+  const float lq = ld[g * 64 + jq], dl = ld[g * 64 + 32 + jq];
+  f32x16 acc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[t][r] = 0.0f;
+
+  const unsigned loff = lane * 16u;
+  const char* ks = static_cast<const char*>(krow) + (size_t)bh * nb * KC * 1024 + loff;
+  const char* vs = static_cast<const char*>(vrow) + (size_t)bh * nb * KC * 1024 + loff;
+  const char* ts = static_cast<const char*>(kt) + (size_t)bh * nb * VC * 1024 + loff;
+  const lptr_t la = (lptr_t)partA[w];
+  const lptr_t lb = (lptr_t)partB[w];
+  const uint32_t aA = lds_addr(partA[w]) + loff, aB = lds_addr(partB[w]) + loff;
+  auto issueA = [&](int y) {
+    load_chunks_lds<KC>((gptr_t)(ks + (size_t)y * KC * 1024), la);
+    load_chunks_lds<KC>((gptr_t)(vs + (size_t)y * KC * 1024), la + KC * 1024);
+  };
+  auto issueB = [&](int y) { load_chunks_lds<VC>((gptr_t)(ts + (size_t)y * VC * 1024), lb); };
+  if (cnt > 0) {
+    const int y0 = wave_uniform(myidx[0]);
+    issueA(y0);
+    issueB(y0);
+  }
+  for (int i = 0; i < cnt; ++i) {
+    const bool more = i + 1 < cnt;                          // wave-uniform
+    const int yn = more ? wave_uniform(myidx[i + 1]) : 0;
+    wait_loads<NB>();                                       // A(i) landed; B(i) may not have
+    u32x4 kf[KC], vf[KC];
+    lds_read_chunks<KC>(aA, kf);
+    lds_read_chunks<KC, KC>(aA, vf);
+    lds_done(kf);
+    lds_done(vf);
+    if (more) issueA(yn);
+    const f32x16 s = mfma_abt<DT, KC>(kf, qf);
+    const f32x16 pv = mfma_abt<DT, KC>(vf, gf);
+    float ds[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      ds[r] = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -lq)) * (pv[r] - dl);
+    if (more) wait_loads<NA>();                             // B(i) landed; A(i+1) may not have
+    else wait_loads<0>();
+    u32x4 tf[VC];
+    lds_read_chunks<VC>(aB, tf);
+    lds_done(tf);
+    if (more) issueB(yn);
+    if constexpr (DT == BF16) {
+      uint32_t pk[8];
+      pack16(ds, pk);
+      mfma_acc_bf16<NT>(acc, pk, [&](int c) { return tf[c]; });
+    } else {
+      mfma_acc_f32<NT>(acc, ds, [&](int c) { return tf[c]; });
+    }
+  }
+  store_block<DT, D>(reinterpret_cast<elem*>(dq) + g * 32 * D, acc, scale,
+                     COARSE ? dqp + g * D : nullptr);
+}
+
+// dK, dV, one wave per column block. Part A: Q_x and G_x in the row layout;
+// part X: block-row x's record (log normalisers and deltas, 256 bytes, one
+// dword per lane); part B: Q_x and G_x in the transposed layout.
+template <int DT, int D, bool COARSE, int WAVES>
+__global__ __launch_bounds__(WAVES * kWave) void bwd_dkdv_stream_kernel(
+    const void* __restrict__ kin, const void* __restrict__ vin, const void* __restrict__ qrow,
+    const void* __restrict__ grow, const void* __restrict__ qt, const void* __restrict__ gt,
+    const uint32_t* __restrict__ bits, const float* __restrict__ ld,
+    const float* __restrict__ dkp, const float* __restrict__ dvp, void* __restrict__ dk,
+    void* __restrict__ dv, int nb, long long rows, float scale, float scale_log2) {
+  using Cfg = TileCfg<DT, D>;
+  using elem = typename Cfg::elem;
+  constexpr int KC = Cfg::kKChunks, VC = Cfg::kVChunks, NT = Cfg::kNT;
+  constexpr int NA = 2 * KC, NX = 1, NB = 2 * VC;          // loads per part
+  static_assert(KC <= 4 && VC <= 4, "chunk offsets fit the immediate field");
+  __shared__ __attribute__((aligned(16))) u32x4 partA[WAVES][NA * 64];
+  __shared__ __attribute__((aligned(16))) u32x4 partB[WAVES][NB * 64];
+  __shared__ __attribute__((aligned(16))) float partX[WAVES][64];
+  extern __shared__ int32_t sidx_all[];
+  const int w = wave_uniform(threadIdx.x / kWave);
+  const int lane = lane_id(), h = lane >> 5;
+  const long long gy = xcd_remap(blockIdx.x, gridDim.x) * (long long)WAVES + w;
+  if (gy >= rows) return;                                   // no workgroup barriers below
+  const long long bh = gy / nb;
+  const int y = (int)(gy - bh * nb);
+  const long long hb = bh * nb;
+  const int nbw = (nb + 31) / 32;
+
+  // block-rows whose selection holds y, ascending
+  int32_t* myx = sidx_all + w * nb;
+  int cnt = 0;
+  for (int x0 = 0; x0 < nb; x0 += kWave) {
+    const int x = x0 + lane;
+    const bool ok = x < nb && ((bits[(hb + x) * nbw + (y >> 5)] >> (y & 31)) & 1u);
+    const uint64_t mk = __ballot(ok);
+    if (ok) myx[cnt + __popcll(mk & lanemask_lt())] = x;
+    cnt += __popcll(mk);
+  }
+  wave_lds_sync();
+  cnt = wave_uniform(cnt);
+
+  u32x4 kf[KC], vf[KC];
+  load_rows<DT, D>(reinterpret_cast<const elem*>(kin) + gy * 32 * D, kf);
+  load_rows<DT, D>(reinterpret_cast<const elem*>(vin) + gy * 32 * D, vf);
+  f32x16 ak[NT], av[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) ak[t][r] = av[t][r] = 0.0f;
+
+  const unsigned loff = lane * 16u;
+  const char* qs = static_cast<const char*>(qrow) + (size_t)hb * KC * 1024 + loff;
+  const char* gs = static_cast<const char*>(grow) + (size_t)hb * KC * 1024 + loff;
+  const char* qts = static_cast<const char*>(qt) + (size_t)hb * VC * 1024 + loff;
+  const char* gts = static_cast<const char*>(gt) + (size_t)hb * VC * 1024 + loff;
+  const char* xs = reinterpret_cast<const char*>(ld + hb * 64) + lane * 4u;
+  const lptr_t la = (lptr_t)partA[w];
+  const lptr_t lb = (lptr_t)partB[w];
+  const lptr_t lx = (lptr_t)partX[w];
+  const uint32_t aA = lds_addr(partA[w]) + loff, aB = lds_addr(partB[w]) + loff;
+  const uint32_t aX = lds_addr(partX[w]) + 16u * h;          // this half's queries
+  auto issueA = [&](int x) {
+    load_chunks_lds<KC>((gptr_t)(qs + (size_t)x * KC * 1024), la);
+    load_chunks_lds<KC>((gptr_t)(gs + (size_t)x * KC * 1024), la + KC * 1024);
+  };
+  auto issueX = [&](int x) { __builtin_amdgcn_global_load_lds((gptr_t)(xs + (size_t)x * 256), lx, 4, 0, 0); };
+  auto issueB = [&](int x) {
+    load_chunks_lds<VC>((gptr_t)(qts + (size_t)x * VC * 1024), lb);
+    load_chunks_lds<VC>((gptr_t)(gts + (size_t)x * VC * 1024), lb + VC * 1024);
+  };
+  if (cnt > 0) {
+    const int x0 = wave_uniform(myx[0]);
+    issueA(x0);
+    issueX(x0);
+    issueB(x0);
+  }
+  for (int i = 0; i < cnt; ++i) {
+    const bool more = i + 1 < cnt;                          // wave-uniform
+    const int xn = more ? wave_uniform(myx[i + 1]) : 0;
+    wait_loads<NX + NB>();                                  // A(i) landed
+    u32x4 qa[KC], ga[KC];
+    lds_read_chunks<KC>(aA, qa);
+    lds_read_chunks<KC, KC>(aA, ga);
+    lds_done(qa);
+    lds_done(ga);
+    if (more) issueA(xn);
+    const f32x16 s = mfma_abt<DT, KC>(qa, kf);             // lane: key, 16 queries
+    const f32x16 pv = mfma_abt<DT, KC>(ga, vf);
+    if (more) wait_loads<NB + NA>();                        // X(i) landed
+    else wait_loads<NB>();
+    u32x4 xr[8];                                            // queries 8rg + 4h + e
+    xr[0] = lds_read16<0>(aX);
+    xr[1] = lds_read16<32>(aX);
+    xr[2] = lds_read16<64>(aX);
+    xr[3] = lds_read16<96>(aX);
+    xr[4] = lds_read16<128>(aX);
+    xr[5] = lds_read16<160>(aX);
+    xr[6] = lds_read16<192>(aX);
+    xr[7] = lds_read16<224>(aX);
+    lds_done(xr);
+    if (more) issueX(xn);
+    f32x4 lq[4], dl[4];
+#pragma unroll
+    for (int rg = 0; rg < 4; ++rg) {
+      lq[rg] = __builtin_bit_cast(f32x4, xr[rg]);
+      dl[rg] = __builtin_bit_cast(f32x4, xr[4 + rg]);
+    }
+    float a[16], ds[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      a[r] = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -lq[r / 4][r % 4]));
+      ds[r] = a[r] * (pv[r] - dl[r / 4][r % 4]);
+    }
+    if (more) wait_loads<NA + NX>();                        // B(i) landed
+    else wait_loads<0>();
+    u32x4 qb[VC], gb[VC];
+    lds_read_chunks<VC>(aB, qb);
+    lds_read_chunks<VC, VC>(aB, gb);
+    lds_done(qb);
+    lds_done(gb);
+    if (more) issueB(xn);
+    if constexpr (DT == BF16) {
+      uint32_t pa8[8], pd8[8];
+      pack16(a, pa8);
+      pack16(ds, pd8);
+      mfma_acc_bf16<NT>(av, pa8, [&](int c) { return gb[c]; });
+      mfma_acc_bf16<NT>(ak, pd8, [&](int c) { return qb[c]; });
+    } else {
+      mfma_acc_f32<NT>(av, a, [&](int c) { return gb[c]; });
+      mfma_acc_f32<NT>(ak, ds, [&](int c) { return qb[c]; });
+    }
+  }
+  store_block<DT, D>(reinterpret_cast<elem*>(dk) + gy * 32 * D, ak, scale,
+                     COARSE ? dkp + gy * D : nullptr);
+  store_block<DT, D>(reinterpret_cast<elem*>(dv) + gy * 32 * D, av, 1.0f,
+                     COARSE ? dvp + gy * D : nullptr);
+}
+
+// ---------------------------------------------------------------------------
+template <int DT, int D, bool COARSE>
+static void launch_tiles_t(const BwdArgs& A, hipStream_t stream) {
+  using Cfg = TileCfg<DT, D>;
   const int nb = A.n / kBlock;
   const long long rows = A.bh * nb;
   const float scale = (float)(1.0 / sqrt((double)D));
   const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
+  const unsigned wgs = (unsigned)((rows + kBwdTileWaves - 1) / kBwdTileWaves);
+  const size_t smem_dq = (size_t)kBwdTileWaves * A.m * sizeof(int32_t);
+  const size_t smem_dkdv = (size_t)kBwdTileWaves * nb * sizeof(int32_t);
+  constexpr int W = kBwdTileWaves;
+  if constexpr (Cfg::kKChunks <= 4 && Cfg::kVChunks <= 4) {
+    bwd_dq_stream_kernel<DT, D, COARSE, W><<<wgs, W * kWave, smem_dq, stream>>>(
+        A.q, A.dout, A.k_row, A.v_row, A.k_t, A.idx, A.ld, A.dqp, A.dq, nb, A.m, rows, scale,
+        scale_log2);
+    bwd_dkdv_stream_kernel<DT, D, COARSE, W><<<wgs, W * kWave, smem_dkdv, stream>>>(
+        A.k, A.v, A.q_row, A.g_row, A.q_t, A.g_t, A.bits, A.ld, A.dkp, A.dvp, A.dk, A.dv, nb, rows,
+        scale, scale_log2);
+  } else {
+    bwd_dq_kernel<DT, D, COARSE><<<wgs, W * kWave, smem_dq, stream>>>(
+        A.q, A.dout, A.k_row, A.v_row, A.k_t, A.idx, A.ld, A.dqp, A.dq, nb, A.m, rows, scale,
+        scale_log2);
+    bwd_dkdv_kernel<DT, D, COARSE><<<wgs, W * kWave, smem_dkdv, stream>>>(
+        A.k, A.v, A.q_row, A.g_row, A.q_t, A.g_t, A.bits, A.ld, A.dkp, A.dvp, A.dk, A.dv, nb, rows,
+        scale, scale_log2);
+  }
+}
+
+template <int DT, int D>
+static void launch_bwd_t(const BwdArgs& A, hipStream_t stream) {
+  const int nb = A.n / kBlock;
+  const float scale = (float)(1.0 / sqrt((double)D));
   const long long groups = (nb + kBwdRows - 1) / kBwdRows;
   const unsigned wg_rows = (unsigned)(A.bh * groups);
   if (A.coarse) {
     bwd_rows_kernel<DT, D, true><<<wg_rows, kBwdRows * kWave, 0, stream>>>(
-        A.dout, A.out, A.lse, A.idx, A.qp, A.kp, A.vp, A.l2, A.delta, A.bits, A.gh, A.W, A.dS,
-        A.dqp, nb, A.m, scale);
+        A.dout, A.out, A.lse, A.idx, A.qp, A.kp, A.vp, A.ld, A.bits, A.gh, A.W, A.dS, A.dqp, nb,
+        A.m, scale);
     bwd_cols_kernel<D><<<wg_rows, kBwdRows * kWave, 0, stream>>>(A.qp, A.gh, A.W, A.dS, A.dkp,
                                                                  A.dvp, nb, scale);
+    launch_tiles_t<DT, D, true>(A, stream);
   } else {
     bwd_rows_kernel<DT, D, false><<<wg_rows, kBwdRows * kWave, 0, stream>>>(
-        A.dout, A.out, A.lse, A.idx, A.qp, A.kp, A.vp, A.l2, A.delta, A.bits, A.gh, A.W, A.dS,
-        A.dqp, nb, A.m, scale);
-  }
-  const unsigned wg_tiles = (unsigned)((rows + kBwdTileWaves - 1) / kBwdTileWaves);
-  const size_t smem_dq = (size_t)kBwdTileWaves * A.m * sizeof(int32_t);
-  const size_t smem_dkdv = (size_t)kBwdTileWaves * nb * sizeof(int32_t);
-  if (A.coarse) {
-    bwd_dq_kernel<DT, D, true><<<wg_tiles, kBwdTileWaves * kWave, smem_dq, stream>>>(
-        A.q, A.dout, A.k_row, A.v_row, A.k_t, A.idx, A.l2, A.delta, A.dqp, A.dq, nb, A.m,
-        rows, scale, scale_log2);
-    bwd_dkdv_kernel<DT, D, true><<<wg_tiles, kBwdTileWaves * kWave, smem_dkdv, stream>>>(
-        A.k, A.v, A.q_row, A.g_row, A.q_t, A.g_t, A.bits, A.l2, A.delta, A.dkp, A.dvp,
-        A.dk, A.dv, nb, rows, scale, scale_log2);
-  } else {
-    bwd_dq_kernel<DT, D, false><<<wg_tiles, kBwdTileWaves * kWave, smem_dq, stream>>>(
-        A.q, A.dout, A.k_row, A.v_row, A.k_t, A.idx, A.l2, A.delta, A.dqp, A.dq, nb, A.m,
-        rows, scale, scale_log2);
-    bwd_dkdv_kernel<DT, D, false><<<wg_tiles, kBwdTileWaves * kWave, smem_dkdv, stream>>>(
-        A.k, A.v, A.q_row, A.g_row, A.q_t, A.g_t, A.bits, A.l2, A.delta, A.dkp, A.dvp,
-        A.dk, A.dv, nb, rows, scale, scale_log2);
+        A.dout, A.out, A.lse, A.idx, A.qp, A.kp, A.vp, A.ld, A.bits, A.gh, A.W, A.dS, A.dqp, nb,
+        A.m, scale);
+    launch_tiles_t<DT, D, false>(A, stream);
   }
 }
 

@@ -87,8 +87,9 @@ hipError_t launch_tile(const void* q, const void* k, const void* v, const void* 
 // sparse-only variant. Outputs dq, dk, dv [bh, n, d] of dtype. The remaining
 // pointers are workspace: pooled rows (coarse only) [bh, nb, d] f32; packed
 // operand copies (row / transposed layout above) of bh*n*d elements of
-// dtype; l2, delta [bh, n] f32; bits [bh*nb, ceil(nb/32)] u32; gh, dqp, dkp,
-// dvp [bh, nb, d] f32 and W, dS [bh, nb, nb] f32 (coarse only).
+// dtype; ld [bh*nb, 64] f32 (per block-row: 32 log normalisers in log2 units,
+// then 32 deltas); bits [bh*nb, ceil(nb/32)] u32; gh, dqp, dkp, dvp
+// [bh, nb, d] f32 and W, dS [bh, nb, nb] f32 (coarse only).
 struct BwdArgs {
   const void *q, *k, *v, *out, *dout;
   const float* lse;
@@ -99,7 +100,7 @@ struct BwdArgs {
   bool coarse;
   float *qp, *kp, *vp;
   void *q_row, *q_t, *k_row, *k_t, *v_row, *g_row, *g_t;
-  float *l2, *delta;
+  float* ld;
   uint32_t* bits;
   float *gh, *W, *dS, *dqp, *dkp, *dvp;
 };

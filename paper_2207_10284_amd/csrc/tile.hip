@@ -386,18 +386,6 @@ __global__ __launch_bounds__((TileCfg<DT, D>::kWaves * kWave)) void tile_kernel(
   row.finish(reinterpret_cast<elem*>(outv) + hoff, lse, x, g, cmax, csum, cvec);
 }
 
-// C consecutive 1 KB chunks HBM/L2 -> LDS, 16 bytes per lane each; chunk c is
-// addressed through the load's immediate offset, which moves the global and
-// the LDS address alike.
-template <int C>
-__device__ __forceinline__ void load_chunks_lds(const __attribute__((address_space(1))) char* src,
-                                                __attribute__((address_space(3))) char* dst) {
-  if constexpr (C > 0) {
-    load_chunks_lds<C - 1>(src, dst);
-    __builtin_amdgcn_global_load_lds(src, dst, 16, (C - 1) * 1024, 0);
-  }
-}
-
 // ---------------------------------------------------------------------------
 // One wave per block-row, packed K/V staged through a wave-private LDS slot:
 // the next selected tile is copied HBM/L2 -> LDS with direct-to-LDS loads

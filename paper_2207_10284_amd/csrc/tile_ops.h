@@ -97,6 +97,21 @@ __device__ __forceinline__ void mfma_acc_f32(f32x16 (&o)[NT], const float (&p)[1
     }
 }
 
+// C consecutive 1 KB chunks HBM/L2 -> LDS, 16 bytes per lane each; chunk c is
+// addressed through the load's immediate offset, which moves the global and
+// the LDS address alike.
+template <int C>
+__device__ __forceinline__ void load_chunks_lds(const __attribute__((address_space(1))) char* src,
+                                                __attribute__((address_space(3))) char* dst) {
+  if constexpr (C > 0) {
+    load_chunks_lds<C - 1>(src, dst);
+    __builtin_amdgcn_global_load_lds(src, dst, 16, (C - 1) * 1024, 0);
+  }
+}
+
+typedef const __attribute__((address_space(1))) char* gptr_t;
+typedef __attribute__((address_space(3))) char* lptr_t;
+
 // Copies a list of m block ids into LDS keeping only the entries in [0, nb),
 // in their order, and returns how many there are (wave-uniform). Reading the
 // ids from LDS keeps them off the vector-memory counter, so prefetched loads

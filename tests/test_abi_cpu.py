@@ -226,7 +226,7 @@ def test_backward_workspace_bytes(lib):
     B, H, n, d = 8, 12, 4096, 64
     bh, nb = B * H, n // 32
     for dt, e in ((0, 4), (1, 2)):
-        want = 7 * al(bh * nb * d * 4) + 7 * al(bh * n * d * e) + 2 * al(bh * n * 4) \
+        want = 7 * al(bh * nb * d * 4) + 7 * al(bh * n * d * e) + al(bh * nb * 64 * 4) \
             + al(bh * nb * (nb // 32) * 4) + 2 * al(bh * nb * nb * 4)
         assert f(B, H, n, d, 32, dt) == want
 
