@@ -763,6 +763,267 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dkdv_stream_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// bfloat16 forms that read the transposed operands straight from the
+// row-layout copy in LDS with gfx950's transposing read ds_read_b64_tr_b16:
+// within each group of 16 lanes, lane i receives as value k (k = 0..3) the
+// 16-bit element i%4 of the 8 bytes at the address that lane 4k + i/4 of the
+// group supplies (lane layout checked on the device). Chunk (u, t) of the
+// transposed operand X^T for lane l = 32h + j holds X[16u + 8(s/4) + 4h + s%4]
+// [32t + j], s = 0..7; so each lane supplies, for each half e = 0, 1, the
+// address of X[16u + 8e + 4(l/32) + (l%16)/4][32t + 16((l/16)&1) + 4(l&3)]
+// (four consecutive columns of one row, 8 bytes) and two reads fill a chunk.
+// Only the row-layout copies are then loaded per tile (dQ: K_y, V_y, 8 KB;
+// dK/dV: Q_x, G_x and the record, 8.25 KB), and each wave keeps two whole
+// tiles in flight in two LDS slots while it computes a third from registers.
+
+// In LDS each 1 KB chunk of a row-layout block is followed by 64 bytes of
+// padding, so the four chunks a transposing read touches start 16 banks apart:
+// its 32 lanes per pass then hit 64 distinct banks (without the padding, lanes
+// whose addresses differ by whole chunks share banks).
+constexpr int kChunkPad = 64;
+constexpr int kChunkStride = 1024 + kChunkPad;
+
+// Byte offset of X[r][c] in a padded row-layout block (bf16, D columns) in LDS.
+template <int D>
+__host__ __device__ constexpr int row_layout_offset(int r, int c) {
+  return ((c % (D / 2)) / 8) * kChunkStride + (32 * (c / (D / 2)) + r) * 16 + (c % 8) * 2;
+}
+
+// C consecutive 1 KB chunks HBM/L2 -> LDS at kChunkStride apart: the load's
+// immediate offset steps both addresses by 1 KB, the LDS base adds the pad.
+template <int C>
+__device__ __forceinline__ void load_chunks_lds_padded(gptr_t src, lptr_t dst) {
+  if constexpr (C > 0) {
+    load_chunks_lds_padded<C - 1>(src, dst);
+    __builtin_amdgcn_global_load_lds(src, dst + (C - 1) * kChunkPad, 16, (C - 1) * 1024, 0);
+  }
+}
+
+// v[i] = padded chunk C0 + i for this lane, i < C
+template <int I, int C, int C0>
+struct LdsChunksPadded {
+  static __device__ __forceinline__ void run(uint32_t addr, u32x4* v) {
+    v[I] = lds_read16<(C0 + I) * kChunkStride>(addr);
+    LdsChunksPadded<I + 1, C, C0>::run(addr, v);
+  }
+};
+template <int C, int C0>
+struct LdsChunksPadded<C, C, C0> {
+  static __device__ __forceinline__ void run(uint32_t, u32x4*) {}
+};
+
+template <int OFF>
+__device__ __forceinline__ u32x2 lds_read_tr16(uint32_t addr) {
+  u32x2 v;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF) : "memory");
+  return v;
+}
+
+// this lane's address term for the transposed reads of a row-layout block
+template <int D>
+__device__ __forceinline__ uint32_t tr_lane_offset() {
+  const int l = lane_id();
+  return (uint32_t)row_layout_offset<D>(4 * (l >> 5) + ((l & 15) >> 2), 16 * ((l >> 4) & 1) + 4 * (l & 3));
+}
+
+// Transposed chunks c = u*NT + t (c < VC) of the row-layout block at `base`
+// (+ this lane's tr_lane_offset); the caller completes them with lds_done().
+template <int D, int C, int VC>
+struct TrChunks {
+  static constexpr int NT = D / 32;
+  static __device__ __forceinline__ void run(uint32_t addr, u32x4* v) {
+    if constexpr (C < VC) {
+      constexpr int u = C / NT, t = C % NT;
+      constexpr int o0 = row_layout_offset<D>(16 * u, 32 * t) - row_layout_offset<D>(0, 0);
+      constexpr int o1 = row_layout_offset<D>(16 * u + 8, 32 * t) - row_layout_offset<D>(0, 0);
+      const u32x2 a = lds_read_tr16<o0>(addr);
+      const u32x2 b = lds_read_tr16<o1>(addr);
+      v[C] = u32x4{a[0], a[1], b[0], b[1]};
+      TrChunks<D, C + 1, VC>::run(addr, v);
+    }
+  }
+};
+
+// dQ (bf16): one wave per block-row; a slot holds K_y and V_y in the row
+// layout (K^T is read transposed from the K part).
+template <int D, bool COARSE, int WAVES>
+__global__ __launch_bounds__(WAVES * kWave) void bwd_dq_tr_kernel(
+    const void* __restrict__ qin, const void* __restrict__ gin, const void* __restrict__ krow,
+    const void* __restrict__ vrow, const int32_t* __restrict__ idx,
+    const float* __restrict__ ld, const float* __restrict__ dqp, void* __restrict__ dq, int nb,
+    int m, long long rows, float scale, float scale_log2) {
+  using Cfg = TileCfg<BF16, D>;
+  using elem = typename Cfg::elem;
+  constexpr int KC = Cfg::kKChunks, VC = Cfg::kVChunks, NT = Cfg::kNT;
+  constexpr int N = 2 * KC;                                 // loads per tile
+  constexpr int SLOT = N * kChunkStride;
+  static_assert(KC <= 4 && VC <= 4, "chunk offsets fit the immediate field");
+  __shared__ __attribute__((aligned(16))) unsigned char slots[WAVES][2][SLOT];
+  extern __shared__ int32_t sidx_all[];
+  const int w = wave_uniform(threadIdx.x / kWave);
+  const int lane = lane_id(), jq = lane & 31;
+  const long long g = xcd_remap(blockIdx.x, gridDim.x) * (long long)WAVES + w;
+  if (g >= rows) return;                                    // no workgroup barriers below
+  const long long bh = g / nb;
+  int32_t* myidx = sidx_all + w * m;
+  const int cnt = stage_selection(idx + g * m, m, nb, myidx);
+
+  u32x4 qf[KC], gf[KC];
+  load_rows<BF16, D>(reinterpret_cast<const elem*>(qin) + g * 32 * D, qf);
+  load_rows<BF16, D>(reinterpret_cast<const elem*>(gin) + g * 32 * D, gf);
+  const float lq = ld[g * 64 + jq], dl = ld[g * 64 + 32 + jq];
+  f32x16 acc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[t][r] = 0.0f;
+
+  const unsigned loff = lane * 16u;
+  const char* ks = static_cast<const char*>(krow) + (size_t)bh * nb * KC * 1024 + loff;
+  const char* vs = static_cast<const char*>(vrow) + (size_t)bh * nb * KC * 1024 + loff;
+  const uint32_t a0 = lds_addr(slots[w][0]);
+  const uint32_t trl = tr_lane_offset<D>();
+  auto issue = [&](int y, int sl) {
+    const lptr_t dst = (lptr_t)slots[w][sl];
+    load_chunks_lds_padded<KC>((gptr_t)(ks + (size_t)y * KC * 1024), dst);
+    load_chunks_lds_padded<KC>((gptr_t)(vs + (size_t)y * KC * 1024), dst + KC * kChunkStride);
+  };
+  if (cnt > 0) issue(wave_uniform(myidx[0]), 0);
+  if (cnt > 1) issue(wave_uniform(myidx[1]), 1);
+  for (int i = 0; i < cnt; ++i) {
+    if (i + 1 < cnt) wait_loads<N>();                       // tile i landed, i+1 may not have
+    else wait_loads<0>();
+    const uint32_t base = a0 + (uint32_t)((i & 1) * SLOT);
+    u32x4 kf[KC], vf[KC], tf[VC];
+    LdsChunksPadded<0, KC, 0>::run(base + loff, kf);
+    LdsChunksPadded<0, KC, KC>::run(base + loff, vf);
+    TrChunks<D, 0, VC>::run(base + trl, tf);
+    lds_done(kf);
+    lds_done(vf);
+    lds_done(tf);
+    if (i + 2 < cnt) issue(wave_uniform(myidx[i + 2]), i & 1);
+    const f32x16 s = mfma_abt<BF16, KC>(kf, qf);
+    const f32x16 pv = mfma_abt<BF16, KC>(vf, gf);
+    float ds[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      ds[r] = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -lq)) * (pv[r] - dl);
+    uint32_t pk[8];
+    pack16(ds, pk);
+    mfma_acc_bf16<NT>(acc, pk, [&](int c) { return tf[c]; });
+  }
+  store_block<BF16, D>(reinterpret_cast<elem*>(dq) + g * 32 * D, acc, scale,
+                       COARSE ? dqp + g * D : nullptr);
+}
+
+// dK, dV (bf16): one wave per column block; a slot holds Q_x and G_x in the
+// row layout and block-row x's record (Q^T and G^T are read transposed).
+template <int D, bool COARSE, int WAVES>
+__global__ __launch_bounds__(WAVES * kWave) void bwd_dkdv_tr_kernel(
+    const void* __restrict__ kin, const void* __restrict__ vin, const void* __restrict__ qrow,
+    const void* __restrict__ grow, const uint32_t* __restrict__ bits,
+    const float* __restrict__ ld, const float* __restrict__ dkp, const float* __restrict__ dvp,
+    void* __restrict__ dk, void* __restrict__ dv, int nb, long long rows, float scale,
+    float scale_log2) {
+  using Cfg = TileCfg<BF16, D>;
+  using elem = typename Cfg::elem;
+  constexpr int KC = Cfg::kKChunks, VC = Cfg::kVChunks, NT = Cfg::kNT;
+  constexpr int N = 2 * KC + 1;                             // loads per tile
+  constexpr int SLOT = 2 * KC * kChunkStride + 256;
+  static_assert(KC <= 4 && VC <= 4, "chunk offsets fit the immediate field");
+  __shared__ __attribute__((aligned(16))) unsigned char slots[WAVES][2][SLOT];
+  extern __shared__ int32_t sidx_all[];
+  const int w = wave_uniform(threadIdx.x / kWave);
+  const int lane = lane_id(), h = lane >> 5;
+  const long long gy = xcd_remap(blockIdx.x, gridDim.x) * (long long)WAVES + w;
+  if (gy >= rows) return;                                   // no workgroup barriers below
+  const long long bh = gy / nb;
+  const int y = (int)(gy - bh * nb);
+  const long long hb = bh * nb;
+  const int nbw = (nb + 31) / 32;
+
+  // block-rows whose selection holds y, ascending
+  int32_t* myx = sidx_all + w * nb;
+  int cnt = 0;
+  for (int x0 = 0; x0 < nb; x0 += kWave) {
+    const int x = x0 + lane;
+    const bool ok = x < nb && ((bits[(hb + x) * nbw + (y >> 5)] >> (y & 31)) & 1u);
+    const uint64_t mk = __ballot(ok);
+    if (ok) myx[cnt + __popcll(mk & lanemask_lt())] = x;
+    cnt += __popcll(mk);
+  }
+  wave_lds_sync();
+  cnt = wave_uniform(cnt);
+
+  u32x4 kf[KC], vf[KC];
+  load_rows<BF16, D>(reinterpret_cast<const elem*>(kin) + gy * 32 * D, kf);
+  load_rows<BF16, D>(reinterpret_cast<const elem*>(vin) + gy * 32 * D, vf);
+  f32x16 ak[NT], av[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) ak[t][r] = av[t][r] = 0.0f;
+
+  const unsigned loff = lane * 16u;
+  const char* qs = static_cast<const char*>(qrow) + (size_t)hb * KC * 1024 + loff;
+  const char* gs = static_cast<const char*>(grow) + (size_t)hb * KC * 1024 + loff;
+  const char* xs = reinterpret_cast<const char*>(ld + hb * 64) + lane * 4u;
+  const uint32_t a0 = lds_addr(slots[w][0]);
+  const uint32_t trl = tr_lane_offset<D>();
+  const uint32_t xl = (uint32_t)(2 * KC * kChunkStride) + 16u * h;   // this half's queries in the record
+  auto issue = [&](int x, int sl) {
+    const lptr_t dst = (lptr_t)slots[w][sl];
+    load_chunks_lds_padded<KC>((gptr_t)(qs + (size_t)x * KC * 1024), dst);
+    load_chunks_lds_padded<KC>((gptr_t)(gs + (size_t)x * KC * 1024), dst + KC * kChunkStride);
+    __builtin_amdgcn_global_load_lds((gptr_t)(xs + (size_t)x * 256), dst + 2 * KC * kChunkStride, 4, 0, 0);
+  };
+  if (cnt > 0) issue(wave_uniform(myx[0]), 0);
+  if (cnt > 1) issue(wave_uniform(myx[1]), 1);
+  for (int i = 0; i < cnt; ++i) {
+    if (i + 1 < cnt) wait_loads<N>();                       // tile i landed, i+1 may not have
+    else wait_loads<0>();
+    const uint32_t base = a0 + (uint32_t)((i & 1) * SLOT);
+    u32x4 qa[KC], ga[KC], qt[VC], gtc[VC], xr[8];
+    LdsChunksPadded<0, KC, 0>::run(base + loff, qa);
+    LdsChunksPadded<0, KC, KC>::run(base + loff, ga);
+    TrChunks<D, 0, VC>::run(base + trl, qt);
+    TrChunks<D, 0, VC>::run(base + KC * kChunkStride + trl, gtc);
+    xr[0] = lds_read16<0>(base + xl);
+    xr[1] = lds_read16<32>(base + xl);
+    xr[2] = lds_read16<64>(base + xl);
+    xr[3] = lds_read16<96>(base + xl);
+    xr[4] = lds_read16<128>(base + xl);
+    xr[5] = lds_read16<160>(base + xl);
+    xr[6] = lds_read16<192>(base + xl);
+    xr[7] = lds_read16<224>(base + xl);
+    lds_done(qa);
+    lds_done(ga);
+    lds_done(qt);
+    lds_done(gtc);
+    lds_done(xr);
+    if (i + 2 < cnt) issue(wave_uniform(myx[i + 2]), i & 1);
+    const f32x16 s = mfma_abt<BF16, KC>(qa, kf);            // lane: key, 16 queries
+    const f32x16 pv = mfma_abt<BF16, KC>(ga, vf);
+    float a[16], ds[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float lq = __uint_as_float(xr[r / 4][r % 4]), dl = __uint_as_float(xr[4 + r / 4][r % 4]);
+      a[r] = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -lq));
+      ds[r] = a[r] * (pv[r] - dl);
+    }
+    uint32_t pa8[8], pd8[8];
+    pack16(a, pa8);
+    pack16(ds, pd8);
+    mfma_acc_bf16<NT>(av, pa8, [&](int c) { return gtc[c]; });
+    mfma_acc_bf16<NT>(ak, pd8, [&](int c) { return qt[c]; });
+  }
+  store_block<BF16, D>(reinterpret_cast<elem*>(dk) + gy * 32 * D, ak, scale,
+                       COARSE ? dkp + gy * D : nullptr);
+  store_block<BF16, D>(reinterpret_cast<elem*>(dv) + gy * 32 * D, av, 1.0f,
+                       COARSE ? dvp + gy * D : nullptr);
+}
+
+// ---------------------------------------------------------------------------
 template <int DT, int D, bool COARSE>
 static void launch_tiles_t(const BwdArgs& A, hipStream_t stream) {
   using Cfg = TileCfg<DT, D>;
@@ -774,7 +1035,15 @@ static void launch_tiles_t(const BwdArgs& A, hipStream_t stream) {
   const size_t smem_dq = (size_t)kBwdTileWaves * A.m * sizeof(int32_t);
   const size_t smem_dkdv = (size_t)kBwdTileWaves * nb * sizeof(int32_t);
   constexpr int W = kBwdTileWaves;
-  if constexpr (Cfg::kKChunks <= 4 && Cfg::kVChunks <= 4) {
+  if constexpr (DT == BF16 && Cfg::kKChunks <= 4 && Cfg::kVChunks <= 4) {
+    bwd_dq_tr_kernel<D, COARSE, W><<<wgs, W * kWave, smem_dq, stream>>>(
+        A.q, A.dout, A.k_row, A.v_row, A.idx, A.ld, A.dqp, A.dq, nb, A.m, rows, scale, scale_log2);
+    // one wave per workgroup: column lists differ in length (a workgroup
+    // keeps its LDS until its longest list is done), rows all have m tiles
+    bwd_dkdv_tr_kernel<D, COARSE, 1><<<(unsigned)rows, kWave, nb * sizeof(int32_t), stream>>>(
+        A.k, A.v, A.q_row, A.g_row, A.bits, A.ld, A.dkp, A.dvp, A.dk, A.dv, nb, rows, scale,
+        scale_log2);
+  } else if constexpr (Cfg::kKChunks <= 4 && Cfg::kVChunks <= 4) {
     bwd_dq_stream_kernel<DT, D, COARSE, W><<<wgs, W * kWave, smem_dq, stream>>>(
         A.q, A.dout, A.k_row, A.v_row, A.k_t, A.idx, A.ld, A.dqp, A.dq, nb, A.m, rows, scale,
         scale_log2);
@@ -813,11 +1082,14 @@ static void launch_bwd_t(const BwdArgs& A, hipStream_t stream) {
 }
 
 hipError_t launch_bwd(const BwdArgs& A, hipStream_t stream) {
-  // pooled rows and packed operands of Q, K, V and G = dZ
-  const PackJob jobs[4] = {{A.q, A.coarse ? A.qp : nullptr, A.q_row, A.q_t},
-                           {A.k, A.coarse ? A.kp : nullptr, A.k_row, A.k_t},
+  // pooled rows and packed operands of Q, K, V and G = dZ; the transposed
+  // copies only where the tile passes read them (not bf16 d <= 64, whose
+  // passes transpose in LDS)
+  const bool tr = A.dtype == BF16 && A.d <= 64;
+  const PackJob jobs[4] = {{A.q, A.coarse ? A.qp : nullptr, A.q_row, tr ? nullptr : A.q_t},
+                           {A.k, A.coarse ? A.kp : nullptr, A.k_row, tr ? nullptr : A.k_t},
                            {A.v, A.coarse ? A.vp : nullptr, A.v_row, nullptr},
-                           {A.dout, nullptr, A.g_row, A.g_t}};
+                           {A.dout, nullptr, A.g_row, tr ? nullptr : A.g_t}};
   const hipError_t e = launch_pack(jobs, 4, A.bh, A.n, A.d, A.dtype, stream);
   if (e != hipSuccess) return e;
   if (A.dtype == BF16) {
