@@ -28,6 +28,10 @@ listed with their reasons in the design notes.
 The sparse-only variant MRA-2-s (Sec. 5: only the scale-1 components over the
 selected blocks, normalised by their own row sums) is ``mra2s_rows``.
 
+Three resolutions R = {s0, b, 1} (Alg. 1 with two refinement levels, budgets
+per block-row at each level) are ``select_multilevel``,
+``mra_multilevel_dense`` and ``mra_multilevel_factored``.
+
 Gradients with the selection held fixed (``mra_grads``) differentiate the
 factored form written with torch float64 CPU operations (``mra_torch``, which
 can also leave out the coarse part: MRA-2-s); ``mra_lse`` gives each query's
@@ -297,6 +301,132 @@ def mra2s_batched(q, k, v, b, m, idx=None):
             Z[bb, h], I[bb, h] = mra2s_rows(q[bb, h], k[bb, h], v[bb, h], b, m,
                                             idx=None if idx is None else idx[bb, h])
     return Z, I
+
+
+# --------------------------------------------------------------------------
+# Sec. 4.2 Alg. 1 and Sec. 4.3 Alg. 2 with three resolutions R = {s0, b, 1}
+# (s0 a multiple of b), budgets per block-row at every scale
+# --------------------------------------------------------------------------
+def select_multilevel(q, k, s0, b, m1, m2):
+    """Alg. 1 for R = {s0, b, 1}, applied row by row: every s0-block-row X
+    keeps the m1 s0-blocks Y with the largest S~0[X, Y] (its refined coarse
+    blocks); every b-block-row x then keeps, among the b-blocks inside its
+    parent row's refined s0-blocks (m1 * s0/b candidates), the m2 with the
+    largest S~[x, y] (those become exact). Ties: lower index first. Returns
+    (idx1 [n/s0, m1], idx2 [n/b, m2]), rows ascending."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    n = q.shape[0]
+    r = s0 // b
+    S0 = coarse_logits(block_mean(q, s0), block_mean(k, s0))
+    idx1 = select_blocks(S0, m1)
+    S1 = coarse_logits(block_mean(q, b), block_mean(k, b))
+    nb = n // b
+    if not 0 <= m2 <= m1 * r:
+        raise ValueError("second-level budget out of range")
+    idx2 = np.empty((nb, m2), dtype=np.int64)
+    for x in range(nb):
+        cand = [int(Y) * r + t for Y in idx1[x // r] for t in range(r)]
+        best = sorted(cand, key=lambda y: (-S1[x, y], y))[:m2]
+        idx2[x] = sorted(best)
+    return idx1, idx2
+
+
+def multilevel_logits_slab(q, k, s0, b, idx1, idx2, x):
+    """The b x n logits of block-row x under eq. actual_approx_mat_form with
+    three scales: exact P_ij inside its refined b-blocks, S~[x, y] inside the
+    other b-blocks of its parent's refined s0-blocks, S~0[X, Y] in the
+    s0-blocks its parent row did not refine."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    n, d = q.shape
+    r = s0 // b
+    X = x // r
+    S0 = coarse_logits(block_mean(q, s0), block_mean(k, s0))
+    S1 = coarse_logits(block_mean(q, b), block_mean(k, b))
+    P = q[x * b:(x + 1) * b] @ k.T / math.sqrt(d)
+    refined0 = set(int(Y) for Y in idx1[X])
+    refined1 = set(int(y) for y in idx2[x])
+    slab = np.empty((b, n))
+    for j in range(n):
+        Y, y = j // s0, j // b
+        if Y not in refined0:
+            slab[:, j] = S0[X, Y]
+        elif y not in refined1:
+            slab[:, j] = S1[x, y]
+        else:
+            slab[:, j] = P[:, j]
+    return slab
+
+
+def mra_multilevel_dense(q, k, v, s0, b, m1, m2, idx1=None, idx2=None):
+    """Z = D^ A^ V for one head with R = {s0, b, 1} (dense slab per
+    block-row). Returns (Z, idx1, idx2)."""
+    if idx1 is None:
+        idx1, idx2 = select_multilevel(q, k, s0, b, m1, m2)
+    v = np.asarray(v, dtype=np.float64)
+    nb = q.shape[0] // b
+    Z = np.vstack([_normalised_rows(multilevel_logits_slab(q, k, s0, b, idx1, idx2, x), v) for x in range(nb)])
+    return Z, idx1, idx2
+
+
+def multilevel_coarse_term(q, k, v, s0, b, idx1, idx2, x):
+    """Alg. 2's low-resolution part of block-row x with three scales, shifted
+    by its largest coarse logit M: (M, c, L) with c = sum of s0 e^{S~0 - M}
+    over the parent row's unrefined s0-blocks plus b e^{S~ - M} over the
+    unrefined b-blocks inside its refined s0-blocks, and L the same sums
+    weighting V~0_Y and V~_y (each coarse block counts the columns it spans)."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    n = q.shape[0]
+    r = s0 // b
+    X = x // r
+    S0 = coarse_logits(block_mean(q, s0), block_mean(k, s0))
+    S1 = coarse_logits(block_mean(q, b), block_mean(k, b))
+    vp0, vp1 = block_mean(v, s0), block_mean(v, b)
+    refined0 = set(int(Y) for Y in idx1[X])
+    refined1 = set(int(y) for y in idx2[x])
+    terms = [(S0[X, Y], s0, vp0[Y]) for Y in range(n // s0) if Y not in refined0]
+    terms += [(S1[x, Y * r + t], b, vp1[Y * r + t]) for Y in sorted(refined0) for t in range(r)
+              if Y * r + t not in refined1]
+    if not terms:
+        return -np.inf, 0.0, np.zeros(v.shape[1])
+    M = max(t[0] for t in terms)
+    c = sum(w * math.exp(lg - M) for lg, w, _ in terms)
+    L = sum(w * math.exp(lg - M) * vv for lg, w, vv in terms)
+    return M, c, L
+
+
+def mra_multilevel_factored(q, k, v, s0, b, m1, m2, idx1=None, idx2=None, rows=None):
+    """The same Z computed as in Alg. 2: exact tiles exp(P) V over the
+    refined b-blocks merged with multilevel_coarse_term. With `rows`, only
+    those block-rows (stacked). Returns (Z, idx1, idx2)."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    n, d = q.shape
+    if idx1 is None:
+        idx1, idx2 = select_multilevel(q, k, s0, b, m1, m2)
+    rows = list(range(n // b)) if rows is None else list(rows)
+    out = np.empty((len(rows) * b, v.shape[1]))
+    for i, x in enumerate(rows):
+        M, c, L = multilevel_coarse_term(q, k, v, s0, b, idx1, idx2, x)
+        sel = [int(y) for y in idx2[x]]
+        qx = q[x * b:(x + 1) * b]
+        if sel:
+            cols = np.concatenate([np.arange(y * b, (y + 1) * b) for y in sel])
+            P = qx @ k[cols].T / math.sqrt(d)
+            mf = P.max(axis=1, keepdims=True)
+        else:
+            cols = np.zeros(0, dtype=np.int64)
+            P = np.zeros((b, 0))
+            mf = np.full((b, 1), -np.inf)
+        top = np.maximum(mf, M)
+        wf = np.exp(P - top)
+        wc = np.exp(M - top) if np.isfinite(M) else np.zeros_like(top)
+        out[i * b:(i + 1) * b] = (wf @ v[cols] + wc * L[None, :]) / (wf.sum(axis=1, keepdims=True) + wc * c)
+    return out, idx1, idx2
 
 
 # --------------------------------------------------------------------------

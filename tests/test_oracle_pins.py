@@ -617,3 +617,102 @@ def test_mra_grads_rows_subset():
             np.testing.assert_allclose(dq_r[blk], dq[blk], rtol=1e-12, atol=1e-13)
         else:
             assert not dq_r[blk].any()
+
+
+# ---------------------------------------------------------------- three resolutions R = {s0, b, 1}
+def _brute_multilevel(q, k, v, s0, b, m1, m2):
+    """Pure-Python loops over the definitions (block means by summation,
+    logits by explicit dot products, selection by full sorting, A^ entry by
+    entry, then row normalisation)."""
+    n, d = len(q), len(q[0])
+    c = 1.0 / math.sqrt(d)
+    def mean_rows(x, s):
+        return [[sum(x[i][t] for i in range(B * s, B * s + s)) / s for t in range(len(x[0]))] for B in range(n // s)]
+    def dot(a, bb):
+        return sum(a[t] * bb[t] for t in range(len(a)))
+    q0, k0, q1, k1 = mean_rows(q, s0), mean_rows(k, s0), mean_rows(q, b), mean_rows(k, b)
+    S0 = [[c * dot(q0[X], k0[Y]) for Y in range(n // s0)] for X in range(n // s0)]
+    S1 = [[c * dot(q1[x], k1[y]) for y in range(n // b)] for x in range(n // b)]
+    r = s0 // b
+    ref0 = [set(sorted(range(n // s0), key=lambda Y: (-S0[X][Y], Y))[:m1]) for X in range(n // s0)]
+    ref1 = []
+    for x in range(n // b):
+        cand = [Y * r + t for Y in ref0[x // r] for t in range(r)]
+        ref1.append(set(sorted(cand, key=lambda y: (-S1[x][y], y))[:m2]))
+    Z = []
+    for i in range(n):
+        x, X = i // b, i // s0
+        row = []
+        for j in range(n):
+            Y, y = j // s0, j // b
+            if Y not in ref0[X]:
+                row.append(math.exp(S0[X][Y]))
+            elif y not in ref1[x]:
+                row.append(math.exp(S1[x][y]))
+            else:
+                row.append(math.exp(c * dot(q[i], k[j])))
+        tot = sum(row)
+        Z.append([sum(row[j] * v[j][t] for j in range(n)) / tot for t in range(len(v[0]))])
+    return np.array(Z)
+
+
+@pytest.mark.parametrize("m1,m2", [(1, 1), (2, 3), (3, 6), (0, 0), (4, 2)])
+def test_multilevel_brute_force(m1, m2):
+    r = _rng(200 + 10 * m1 + m2)
+    n, s0, b, d = 32, 8, 4, 3
+    q, k, v = (r.standard_normal((n, d)) for _ in range(3))
+    want = _brute_multilevel(q.tolist(), k.tolist(), v.tolist(), s0, b, m1, m2)
+    Zd, i1, i2 = O.mra_multilevel_dense(q, k, v, s0, b, m1, m2)
+    Zf, _, _ = O.mra_multilevel_factored(q, k, v, s0, b, m1, m2)
+    np.testing.assert_allclose(Zd, want, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(Zf, want, rtol=1e-12, atol=1e-13)
+
+
+def test_multilevel_reduces_to_two_levels():
+    """All s0-blocks refined: the second level is MRA-2 at block b with budget
+    m2. Every candidate refined: MRA-2 at block s0 with budget m1. Nothing
+    refined: pure coarse at s0."""
+    r = _rng(210)
+    n, s0, b, d = 256, 64, 16, 8
+    q, k, v = (r.standard_normal((n, d)) for _ in range(3))
+    nb0, rr = n // s0, s0 // b
+    Z, _, i2 = O.mra_multilevel_factored(q, k, v, s0, b, nb0, 5)
+    Z2, idx = O.mra_factored(q, k, v, b, 5)
+    np.testing.assert_array_equal(i2, idx)
+    np.testing.assert_allclose(Z, Z2, rtol=1e-12, atol=1e-13)
+    Z, i1, _ = O.mra_multilevel_factored(q, k, v, s0, b, 2, 2 * rr)
+    Z2, idx = O.mra_factored(q, k, v, s0, 2)
+    np.testing.assert_array_equal(i1, idx)
+    np.testing.assert_allclose(Z, Z2, rtol=1e-12, atol=1e-13)
+    Z, _, _ = O.mra_multilevel_factored(q, k, v, s0, b, 0, 0)
+    np.testing.assert_allclose(Z, O.mra_factored(q, k, v, s0, 0)[0], rtol=1e-12, atol=1e-13)
+
+
+def test_multilevel_constant_blocks_exact():
+    """Q and K constant on every s0-block: every mu is exact at every scale, so
+    the result is exact attention for any budgets."""
+    r = _rng(220)
+    n, s0, b, d = 128, 32, 8, 4
+    q = np.repeat(r.standard_normal((n // s0, d)), s0, axis=0)
+    k = np.repeat(r.standard_normal((n // s0, d)), s0, axis=0)
+    v = r.standard_normal((n, d))
+    exact = O.exact_attention(q, k, v)
+    for m1, m2 in ((0, 0), (1, 2), (2, 5), (4, 16)):
+        np.testing.assert_allclose(O.mra_multilevel_factored(q, k, v, s0, b, m1, m2)[0], exact,
+                                   rtol=1e-12, atol=1e-13)
+
+
+def test_multilevel_selection_nested_and_tied():
+    """Level-2 picks lie inside the parent row's level-1 picks; equal scores
+    resolve to lower indices."""
+    r = _rng(230)
+    n, s0, b, d = 128, 32, 8, 4
+    q, k = r.standard_normal((n, d)), r.standard_normal((n, d))
+    i1, i2 = O.select_multilevel(q, k, s0, b, 2, 3)
+    rr = s0 // b
+    for x in range(n // b):
+        assert set(int(y) // rr for y in i2[x]) <= set(int(Y) for Y in i1[x // rr])
+        assert (np.diff(i2[x]) > 0).all()
+    z = np.zeros((n, d))
+    i1, i2 = O.select_multilevel(z, z, s0, b, 2, 3)
+    assert (i1 == [0, 1]).all() and (i2 == [0, 1, 2]).all()
