@@ -232,6 +232,18 @@ def main():
         variants["mra2_global_budget"] = {"ms_per_step": global_ms, "tokens_per_s": w.B * w.n / (global_ms * 1e-3),
                                           "budget_per_head": gb, "prior": "diagonal"}
 
+    # Three resolutions R = {s0, 32, 1} (Alg. 1 with two refinement levels),
+    # the second-level budget the headline's, reported beside it.
+    if not args.no_variants:
+        s0, m1 = inputs.MULTILEVEL[w.name]
+        mws = torch.empty(ops.forward_multilevel_workspace_bytes(w.B, w.H, w.n, w.d, s0, m1, w.budget, tdt),
+                          dtype=torch.uint8, device=dev)
+        ml_ms = time_launches(lambda: ops.attention_forward_multilevel(tq, tk, tv, s0, m1, w.budget, out=out,
+                                                                       idx2_out=idx, workspace=mws),
+                              max(args.steps, 20))
+        variants["mra_multilevel"] = {"ms_per_step": ml_ms, "tokens_per_s": w.B * w.n / (ml_ms * 1e-3),
+                                      "coarse_block": s0, "budget1": m1, "budget2": w.budget}
+
     if not args.no_variants:
         variants["backward"] = backward_leg(w, ops, tq, tk, tv, out, idx, ws, max(args.steps, 20))
 

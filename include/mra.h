@@ -270,6 +270,51 @@ mra_status_t mra_sparse_attention_forward(const void* q, const void* k, const vo
                                           void* stream);
 
 /*
+ * mra_forward_multilevel_workspace_bytes — workspace of
+ * mra_attention_forward_multilevel: that of mra_attention_forward with budget
+ * budget2, plus the scale-s0 means, both coarse-logit grids and the
+ * first-level selection. 0 for invalid or unsupported arguments.
+ */
+size_t mra_forward_multilevel_workspace_bytes(int B, int H, int n, int d, int block,
+                                              int coarse_block, int budget1, int budget2,
+                                              mra_dtype_t dtype);
+
+/*
+ * mra_attention_forward_multilevel — three resolutions R = {s0, 32, 1}
+ * (Sec. 4.2 Alg. 1 with two refinement levels, s0 = coarse_block; Sec. 4.3
+ * Alg. 2 over the resulting J), with a budget per block-row at each level:
+ *   level 1: every s0-block-row X keeps the budget1 s0-blocks Y with the
+ *            largest S~0[X,Y] = c Q~0_X . K~0_Y (Q~0, K~0: means of s0-row
+ *            blocks, taken here as means of the r = s0/32 consecutive 32-row
+ *            means);
+ *   level 2: every 32-block-row x keeps, among the 32-blocks inside its
+ *            parent row's refined s0-blocks (budget1 * r candidates), the
+ *            budget2 with the largest S~[x,y];
+ *   A^_ij = exp(c Q_i.K_j) in the refined 32-blocks, exp(S~[x,y]) in the other
+ *           candidates, exp(S~0[X,Y]) in the unrefined s0-blocks
+ *           (eq. actual_approx_mat_form), Z = D^ A^ V.
+ * Ties go to the lower index at both levels. Launches: pooling (with K/V
+ * packing), scale-s0 means, coarse logits at both scales, the two per-row
+ * selections (the second over the candidates only), the low-resolution term
+ * (s0 e^{S~0} V~0 and 32 e^{S~} V~ over the unrefined blocks), the tile pass.
+ *   coarse_block : s0 = 32 r with r >= 2, dividing n (MRA_ERR_UNSUPPORTED if
+ *                  not a multiple of 32 above 32, MRA_ERR_INVALID_ARG if it
+ *                  does not divide n).
+ *   budget1      : 0 <= budget1 <= n / s0; budget2 : 0 <= budget2 <= budget1 r.
+ *   idx1_out     : optional [B,H,n/s0,budget1] int32, rows ascending.
+ *   idx2_out     : optional [B,H,n/32,budget2] int32, rows ascending.
+ *   lse_out      : optional [B,H,n] float32 log normalisers.
+ *   Other arguments and errors as for mra_attention_forward; workspace of at
+ *   least mra_forward_multilevel_workspace_bytes(...) bytes.
+ */
+mra_status_t mra_attention_forward_multilevel(const void* q, const void* k, const void* v,
+                                              void* out, int32_t* idx1_out, int32_t* idx2_out,
+                                              float* lse_out, void* workspace,
+                                              size_t workspace_bytes, int B, int H, int n, int d,
+                                              int block, int coarse_block, int budget1,
+                                              int budget2, mra_dtype_t dtype, void* stream);
+
+/*
  * mra_backward_workspace_bytes — device workspace of mra_attention_backward:
  * seven rearranged copies of Q, K, V and dZ (7*B*H*n*d*elem bytes), pooled
  * rows and their gradients, two float32 values per query, the selection as a

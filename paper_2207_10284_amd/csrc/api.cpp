@@ -146,6 +146,42 @@ WsBwd ws_bwd(long long bh, int nb, int d, mra_dtype_t dtype) {
   return L;
 }
 
+// The three-resolution forward: the forward's layout with the second-level
+// selection as its rows, plus the scale-s0 means, both coarse-logit grids and
+// the first-level selection.
+struct WsMulti {
+  WsLayout base;
+  size_t qp0, kp0, vp0, S0, idx1, S, total;
+};
+
+WsMulti ws_multi(long long bh, int nb, int nb0, int d, int m1, int m2, mra_dtype_t dtype) {
+  WsMulti W{};
+  W.base = ws_layout(bh, nb, d, m2, dtype);
+  size_t off = W.base.total;
+  const size_t pooled0 = align256((size_t)bh * nb0 * d * sizeof(float));
+  W.qp0 = off; off += pooled0;
+  W.kp0 = off; off += pooled0;
+  W.vp0 = off; off += pooled0;
+  W.S0 = off; off += align256((size_t)bh * nb0 * nb0 * sizeof(float));
+  W.idx1 = off; off += align256((size_t)bh * nb0 * m1 * sizeof(int32_t));
+  W.S = off; off += align256((size_t)bh * nb * nb * sizeof(float));
+  W.total = off;
+  return W;
+}
+
+// coarse_block = 32 r with r >= 2 dividing n / 32; 0 <= m1 <= n / coarse_block;
+// 0 <= m2 <= m1 r.
+mra_status_t check_multi(const Shape& s, int n, int coarse_block, int m1, int m2, int* r, int* nb0) {
+  if (coarse_block <= kBlockSize || coarse_block % kBlockSize != 0) return MRA_ERR_UNSUPPORTED;
+  if (n % coarse_block != 0) return MRA_ERR_INVALID_ARG;
+  *r = coarse_block / kBlockSize;
+  *nb0 = n / coarse_block;
+  if (m1 < 0 || m1 > *nb0) return MRA_ERR_INVALID_ARG;
+  if (m2 < 0 || (long long)m2 > (long long)m1 * *r) return MRA_ERR_INVALID_ARG;
+  (void)s;
+  return MRA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -431,6 +467,66 @@ mra_status_t mra_attention_backward(const void* q, const void* k, const void* v,
   A.gh = f32(L.gh); A.W = f32(L.W); A.dS = f32(L.dS);
   A.dqp = f32(L.dqp); A.dkp = f32(L.dkp); A.dvp = f32(L.dvp);
   return hip_status(mra::launch_bwd(A, static_cast<hipStream_t>(stream)));
+}
+
+size_t mra_forward_multilevel_workspace_bytes(int B, int H, int n, int d, int block,
+                                              int coarse_block, int budget1, int budget2,
+                                              mra_dtype_t dtype) {
+  Shape s;
+  if (check_shape(B, H, n, d, block, true, &s) != MRA_OK) return 0;
+  if (check_dtype(dtype) != MRA_OK) return 0;
+  int r = 0, nb0 = 0;
+  if (check_multi(s, n, coarse_block, budget1, budget2, &r, &nb0) != MRA_OK) return 0;
+  return ws_multi(s.bh, s.nb, nb0, d, budget1, budget2, dtype).total;
+}
+
+mra_status_t mra_attention_forward_multilevel(const void* q, const void* k, const void* v,
+                                              void* out, int32_t* idx1_out, int32_t* idx2_out,
+                                              float* lse_out, void* workspace,
+                                              size_t workspace_bytes, int B, int H, int n, int d,
+                                              int block, int coarse_block, int budget1,
+                                              int budget2, mra_dtype_t dtype, void* stream) {
+  Shape s;
+  MRA_TRY(check_shape(B, H, n, d, block, true, &s));
+  MRA_TRY(check_dtype(dtype));
+  int r = 0, nb0 = 0;
+  MRA_TRY(check_multi(s, n, coarse_block, budget1, budget2, &r, &nb0));
+  if (s.empty) return MRA_OK;
+  MRA_TRY(check_ptr(q));
+  MRA_TRY(check_ptr(k));
+  MRA_TRY(check_ptr(v));
+  MRA_TRY(check_ptr(out));
+  const void* opt[3] = {idx1_out, idx2_out, lse_out};
+  for (const void* p : opt)
+    if (p != nullptr && !aligned16(p)) return MRA_ERR_MISALIGNED;
+  MRA_TRY(check_ptr(workspace));
+  const WsMulti W = ws_multi(s.bh, s.nb, nb0, d, budget1, budget2, dtype);
+  if (workspace_bytes < W.total) return MRA_ERR_WORKSPACE;
+
+  char* ws = static_cast<char*>(workspace);
+  const WsLayout& L = W.base;
+  auto f32 = [&](size_t off) { return reinterpret_cast<float*>(ws + off); };
+  float *qp = f32(L.qp), *kp = f32(L.kp), *vp = f32(L.vp);
+  float *qp0 = f32(W.qp0), *kp0 = f32(W.kp0), *vp0 = f32(W.vp0);
+  float *S0 = f32(W.S0), *S = f32(W.S);
+  void* kvpacked = ws + L.kvpacked;
+  int32_t* idx1 = idx1_out ? idx1_out : reinterpret_cast<int32_t*>(ws + W.idx1);
+  int32_t* idx2 = idx2_out ? idx2_out : reinterpret_cast<int32_t*>(ws + L.idx);
+  float *cmax = f32(L.cmax), *csum = f32(L.csum), *cvec = f32(L.cvec);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int nb = s.nb;
+
+  MRA_TRY(hip_status(mra::launch_pool(q, k, v, qp, kp, vp, kvpacked, s.bh, n, d, (int)dtype, st)));
+  MRA_TRY(hip_status(mra::launch_pool_up(qp, kp, vp, qp0, kp0, vp0, s.bh * nb0, d, r, st)));
+  MRA_TRY(hip_status(mra::launch_coarse(qp0, kp0, S0, s.bh, nb0, d, st)));
+  if (budget1 > 0) MRA_TRY(hip_status(mra::launch_select(S0, idx1, s.bh, nb0, budget1, st)));
+  MRA_TRY(hip_status(mra::launch_coarse(qp, kp, S, s.bh, nb, d, st)));
+  MRA_TRY(hip_status(mra::launch_mask_candidates(S, idx1, s.bh, nb, nb0, r, budget1, st)));
+  if (budget2 > 0) MRA_TRY(hip_status(mra::launch_select(S, idx2, s.bh, nb, budget2, st)));
+  MRA_TRY(hip_status(mra::launch_coarse_term_ml(S0, idx1, S, idx2, vp0, vp, cmax, csum, cvec, s.bh,
+                                                nb, nb0, r, budget1, budget2, d, st)));
+  return hip_status(mra::launch_tile(q, k, v, kvpacked, idx2, cmax, csum, cvec, out, lse_out, s.bh,
+                                     n, d, budget2, (int)dtype, st));
 }
 
 const char* mra_status_str(mra_status_t status) {

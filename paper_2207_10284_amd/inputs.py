@@ -149,3 +149,15 @@ def random_qkv(seed: int, B: int, H: int, n: int, d: int, dtype: str = "f32", sc
     arrs = [rng.standard_normal(shape) * scale for _ in range(3)]
     cast = round_to_bf16 if dtype == "bf16" else (lambda a: a.astype(np.float32))
     return tuple(cast(a) for a in arrs)
+
+# Three-resolution settings R = {coarse_block, 32, 1} per workload:
+# (coarse_block, first-level budget per coarse block-row). The second-level
+# budget is the workload's own; first-level budgets leave at least twice as
+# many candidate 32-blocks as that budget.
+MULTILEVEL = {
+    "tiny-512": (64, 3),
+    "base-512": (64, 8),
+    "small-4096": (128, 4),
+    "base-4096": (128, 8),
+    "long-32768": (256, 8),
+}

@@ -36,6 +36,9 @@ SIGNATURES = {
     "mra_select_global": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, _P]),
     "mra_forward_global_workspace_bytes": (_Z, [_I, _I, _I, _I, _I, _I]),
     "mra_attention_forward_global": (_I, [_P, _P, _P, _P, _P, _P, _P, _Z, _I, _I, _I, _I, _I, _I, _I, _I, _P]),
+    "mra_forward_multilevel_workspace_bytes": (_Z, [_I, _I, _I, _I, _I, _I, _I, _I, _I]),
+    "mra_attention_forward_multilevel": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _Z, _I, _I, _I, _I, _I, _I,
+                                              _I, _I, _I, _P]),
     "mra_backward_workspace_bytes": (_Z, [_I, _I, _I, _I, _I, _I]),
     "mra_attention_backward": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _Z,
                                     _I, _I, _I, _I, _I, _I, _I, _I, _P]),
@@ -265,6 +268,38 @@ def attention_forward_global(q, k, v, budget: int, prior_diagonal: bool = False,
     _call("mra_attention_forward_global", _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(idx_out), _ptr(lse_out),
           _ptr(workspace), workspace.numel() * workspace.element_size(),
           B, H, n, d, BLOCK, budget, int(bool(prior_diagonal)), _dtype_code(ref), _stream(ref.device))
+    return out
+
+
+def forward_multilevel_workspace_bytes(B: int, H: int, n: int, d: int, coarse_block: int, budget1: int,
+                                       budget2: int, dtype=torch.bfloat16) -> int:
+    code = MRA_BF16 if dtype == torch.bfloat16 else MRA_F32
+    return int(load().mra_forward_multilevel_workspace_bytes(B, H, n, d, BLOCK, coarse_block, budget1, budget2,
+                                                             code))
+
+
+def attention_forward_multilevel(q, k, v, coarse_block: int, budget1: int, budget2: int, out=None,
+                                 idx1_out=None, idx2_out=None, lse_out=None, workspace=None):
+    """Three resolutions R = {coarse_block, 32, 1} (Alg. 1 with two refinement
+    levels, per-row budgets). Returns Z; the selections go to ``idx1_out``
+    (int32 [B, H, n/coarse_block, budget1]) and ``idx2_out`` (int32
+    [B, H, n/32, budget2]) when given."""
+    ref = _check_qkv(q, k, v)
+    B, H, n, d = ref.shape
+    if out is None:
+        out = torch.empty_like(ref)
+    if idx1_out is not None:
+        _check_idx(idx1_out, B, H, n // coarse_block if coarse_block else 0, budget1, ref.device)
+    if idx2_out is not None:
+        _check_idx(idx2_out, B, H, n // BLOCK, budget2, ref.device)
+    if lse_out is not None:
+        _check_f32(lse_out, (B, H, n), "lse_out")
+    need = forward_multilevel_workspace_bytes(B, H, n, d, coarse_block, budget1, budget2, ref.dtype)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), device=ref.device, dtype=torch.uint8)
+    _call("mra_attention_forward_multilevel", _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(idx1_out),
+          _ptr(idx2_out), _ptr(lse_out), _ptr(workspace), workspace.numel() * workspace.element_size(),
+          B, H, n, d, BLOCK, coarse_block, budget1, budget2, _dtype_code(ref), _stream(ref.device))
     return out
 
 

@@ -45,7 +45,8 @@ def check_selection(gpu_idx, S_ref, m, band=TIE_BAND):
         differ += 1
         srt = np.sort(S_ref[x])[::-1]
         tau = srt[m - 1]
-        scale = max(abs(tau), np.abs(S_ref[x]).max())
+        fin = S_ref[x][np.isfinite(S_ref[x])]       # -inf marks blocks outside a candidate set
+        scale = max(abs(tau), np.abs(fin).max())
         for y in set(g.tolist()) ^ set(ref[x].tolist()):
             assert abs(S_ref[x, y] - tau) <= band * scale, (x, y, S_ref[x, y], tau)
     return differ

@@ -31,7 +31,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 15, names
+    assert len(names) == 17, names
     for name in names:
         assert hasattr(lib, name), name
     assert set(names) == set(ops.SIGNATURES)
@@ -214,6 +214,41 @@ def test_backward_validation(lib):
     assert bwd(lib, wsb=need - 1) == WORKSPACE
     assert bwd(lib, B=0, q=None, k=None, v=None, out=None, dout=None, lse=None, idx=None, dq=None,
                dk=None, dv=None, ws=None) == OK
+    assert lib.mra_last_hip_error() == 0
+
+
+def mfwd(lib, q=A, out=A, ws=A, wsb=1 << 40, n=256, d=64, cb=64, m1=1, m2=1, dtype=1, i1=None, i2=None, lse=None):
+    return lib.mra_attention_forward_multilevel(q, A, A, out, i1, i2, lse, ws, wsb, 1, 1, n, d, 32, cb, m1, m2,
+                                                dtype, None)
+
+
+def test_multilevel_validation(lib):
+    """R = {s0, 32, 1}: s0 a multiple of 32 above 32 dividing n; budgets
+    0 <= m1 <= n/s0, 0 <= m2 <= m1 * s0/32."""
+    assert mfwd(lib, cb=32) == UNSUPPORTED
+    assert mfwd(lib, cb=48) == UNSUPPORTED
+    assert mfwd(lib, cb=0) == UNSUPPORTED
+    assert mfwd(lib, cb=96) == INVALID        # 256 % 96
+    assert mfwd(lib, m1=5) == INVALID         # n/s0 = 4
+    assert mfwd(lib, m1=-1) == INVALID
+    assert mfwd(lib, m1=1, m2=3) == INVALID   # 1 * 64/32 = 2 candidates
+    assert mfwd(lib, m1=0, m2=1) == INVALID
+    assert mfwd(lib, d=48) == UNSUPPORTED
+    assert mfwd(lib, q=None) == INVALID
+    assert mfwd(lib, i1=MIS) == MISALIGNED
+    assert mfwd(lib, i2=MIS) == MISALIGNED
+    assert mfwd(lib, lse=MIS) == MISALIGNED
+    need = lib.mra_forward_multilevel_workspace_bytes(1, 1, 256, 64, 32, 64, 1, 1, 1)
+    assert need > 0
+    assert mfwd(lib, wsb=need - 1) == WORKSPACE
+    assert mfwd(lib, n=0, m1=0, m2=0, q=None, out=None, ws=None) == OK
+    assert lib.mra_forward_multilevel_workspace_bytes(1, 1, 256, 64, 32, 96, 1, 1, 1) == 0
+    al = lambda x: (x + 255) // 256 * 256
+    B, H, n, d, s0, m1, m2 = 8, 12, 4096, 64, 128, 8, 16
+    bh, nb, nb0 = B * H, n // 32, n // s0
+    want = lib.mra_forward_workspace_bytes(B, H, n, d, 32, m2, 1) + 3 * al(bh * nb0 * d * 4) \
+        + al(bh * nb0 * nb0 * 4) + al(bh * nb0 * m1 * 4) + al(bh * nb * nb * 4)
+    assert lib.mra_forward_multilevel_workspace_bytes(B, H, n, d, 32, s0, m1, m2, 1) == want
     assert lib.mra_last_hip_error() == 0
 
 
