@@ -9,9 +9,9 @@
 //   M = max S~ over unselected blocks, c = sum b e^{S~ - M},
 //   L = sum b e^{S~ - M} V~_y.
 //
-// One workgroup (16 waves) owns 16 consecutive block-rows of one head, one
-// wave per row. Lane l of a row's wave holds the row's scores for blocks
-// y = 64j + l in registers: loaded from S~, or (fused mode) computed in
+// One workgroup owns 16 consecutive block-rows of one head: 8 waves with two
+// rows each (one row per wave for heads of more than 512 blocks). Lane l of a
+// row's wave holds the row's scores for blocks y = 64j + l in registers: loaded from S~, or (fused mode) computed in
 // 64-column chunks on the float64 matrix cores with the same tile routine as
 // the coarse-logit kernel (so the same bits). The selection is a radix search
 // for the m-th largest order-preserving 32-bit key (32 rounds of ballot +
@@ -20,7 +20,7 @@
 // popcounts. Max and sum use DPP / lane-swap reductions (no LDS). L = W V~ is
 // formed chunk by chunk on the float32 matrix cores (16x16x4): the weights
 // b e^{S~ - M} (0 where selected) of the 16 rows pass through LDS one 64-block
-// chunk at a time, and the 16 waves split the dims and the blocks of a chunk
+// chunk at a time, and the waves split the dims and the blocks of a chunk
 // between them, so V~ is read once per workgroup. Workgroups of one head stay
 // on one XCD. Every mode runs the same arithmetic in the same order, so the
 // fused forward step is bit-identical to separate score, select and
@@ -54,12 +54,14 @@ static RowsSmem rows_smem(int d, bool fused) {
   return L;
 }
 
-template <int D, int MODE, int JMAX>
-__global__ __launch_bounds__(1024) void rows_kernel(
+template <int D, int MODE, int JMAX, int RPW>
+__global__ __launch_bounds__(kRows / RPW * kWave) void rows_kernel(
     const float* __restrict__ S, const float* __restrict__ qp, const float* __restrict__ kp,
     int32_t* __restrict__ idx_out, const int32_t* __restrict__ idx_in,
     const float* __restrict__ vp, float* __restrict__ cmax, float* __restrict__ csum,
     float* __restrict__ cvec, int nb, int m, int q_off, int k_off, double scale) {
+  constexpr int NW = kRows / RPW;                                  // waves per workgroup
+  constexpr int NTH = NW * kWave;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   float* Cb = reinterpret_cast<float*>(smem);                      // [16][65] chunk buffer
   constexpr int ldc = kChunk + 1;
@@ -72,21 +74,58 @@ __global__ __launch_bounds__(1024) void rows_kernel(
   const int x0 = (int)(lwg - bh * groups) * kRows;
   const int rows = min(kRows, nb - x0);
   const long long g0 = bh * nb + x0;                               // first global block-row
-  const bool active = w < rows;                                    // this wave owns a row
-  const long long g = g0 + w;
   const int J = (nb + kChunk - 1) / kChunk;
+  // this wave's rows: w + NW * i, i < RPW
+  auto row_of = [&](int i) { return w + NW * i; };
 
-  // ---- phase 1: this row's scores into registers, s[j] for y = 64j + lane
-  float s[JMAX];
+  // Phase 4's B operands (V~ values, NB4 per chunk and lane) are loaded two
+  // chunks ahead, the first two here, so their latency hides behind phases 1-3.
+  constexpr int NTD = D / 16, KQ = NW / NTD, YPW = kChunk / KQ, NB4 = YPW / 4;
+  static_assert(KQ >= 1 && NW % NTD == 0, "waves cover the dim tiles");
+  const int nt = w % NTD, kq = w / NTD;
+  const int ar = lane & 15, ak = lane >> 4;
+  const float* vh = vp + bh * (long long)nb * D;
+  float bv[2][NB4];
+  auto load_b = [&](int j, float (&dst)[NB4]) {
+    const int yb = kChunk * j + kq * YPW;
 #pragma unroll
-  for (int j = 0; j < JMAX; ++j) s[j] = 0.0f;
+    for (int t = 0; t < NB4; ++t) {
+      const int y = yb + 4 * t + ak;
+      dst[t] = y < nb ? vh[(long long)y * D + 16 * nt + ar] : 0.0f;
+    }
+  };
+  if constexpr (MODE == kFused || MODE == kTermOnly) {
+    load_b(0, bv[0]);
+    if (J > 1) load_b(1, bv[1]);
+  }
+
+  // ---- phase 1: the rows' scores into registers, s[i][j] for y = 64j + lane
+  float s[RPW][JMAX];
+#pragma unroll
+  for (int i = 0; i < RPW; ++i)
+#pragma unroll
+    for (int j = 0; j < JMAX; ++j) s[i][j] = 0.0f;
   if constexpr (MODE == kFused || MODE == kFusedSelect) {
     constexpr int ldq = D + 1, ldk = D + 1;
     double* Qd = reinterpret_cast<double*>(smem + q_off);          // [16][D+1]
     float* Kc = reinterpret_cast<float*>(smem + k_off);            // [64][D+1]
     const float* qh = qp + g0 * D;
     const float* kh = kp + bh * (long long)nb * D;
-    for (int i = tid; i < kRows * D; i += 1024) {
+    // a chunk of K~ (64 rows x D) is KV4 float4 per thread
+    constexpr int KV4 = (kChunk * (D / 4) + NTH - 1) / NTH;
+    f32x4 kv[KV4];
+    auto load_k = [&](int j) {
+      const int y0 = kChunk * j;
+#pragma unroll
+      for (int u = 0; u < KV4; ++u) {
+        const int i = tid + NTH * u, r = i / (D / 4), c4 = i % (D / 4);
+        kv[u] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        if (i < kChunk * (D / 4) && y0 + r < nb)
+          kv[u] = *reinterpret_cast<const f32x4*>(kh + (long long)(y0 + r) * D + 4 * c4);
+      }
+    };
+    load_k(0);
+    for (int i = tid; i < kRows * D; i += NTH) {
       const int r = i / D, c = i % D;
       Qd[r * ldq + c] = r < rows ? (double)qh[(long long)r * D + c] : 0.0;
     }
@@ -94,14 +133,15 @@ __global__ __launch_bounds__(1024) void rows_kernel(
     for (int j = 0; j < JMAX; ++j) {
       if (j >= J) break;
       __syncthreads();                                             // Kc, Cb free; Qd ready
-      const int y0 = kChunk * j;
-      for (int i = tid; i < kChunk * (D / 4); i += 1024) {
-        const int r = i / (D / 4), c4 = i % (D / 4);
-        f32x4 v = {0.0f, 0.0f, 0.0f, 0.0f};
-        if (y0 + r < nb) v = *reinterpret_cast<const f32x4*>(kh + (long long)(y0 + r) * D + 4 * c4);
-        float* dst = Kc + r * ldk + 4 * c4;
-        dst[0] = v[0]; dst[1] = v[1]; dst[2] = v[2]; dst[3] = v[3];
+#pragma unroll
+      for (int u = 0; u < KV4; ++u) {
+        const int i = tid + NTH * u, r = i / (D / 4), c4 = i % (D / 4);
+        if (i < kChunk * (D / 4)) {
+          float* dst = Kc + r * ldk + 4 * c4;
+          dst[0] = kv[u][0]; dst[1] = kv[u][1]; dst[2] = kv[u][2]; dst[3] = kv[u][3];
+        }
       }
+      if (j + 1 < J) load_k(j + 1);
       __syncthreads();
       if (w < kChunk / 16) {                                       // waves 0..3: one 16x16 tile each
         f64x4 acc = {0.0, 0.0, 0.0, 0.0};
@@ -111,25 +151,34 @@ __global__ __launch_bounds__(1024) void rows_kernel(
           Cb[coarse_tile_row(lane, e) * ldc + 16 * w + (lane & 15)] = coarse_round(acc[e], scale);
       }
       __syncthreads();
-      if (active && y0 + lane < nb) s[j] = Cb[w * ldc + lane];
+#pragma unroll
+      for (int i = 0; i < RPW; ++i)
+        if (row_of(i) < rows && kChunk * j + lane < nb) s[i][j] = Cb[row_of(i) * ldc + lane];
     }
   } else {
-    if (active) {
+#pragma unroll
+    for (int i = 0; i < RPW; ++i) {
+      if (row_of(i) >= rows) continue;
+      const long long g = g0 + row_of(i);
 #pragma unroll
       for (int j = 0; j < JMAX; ++j) {
         const int y = kChunk * j + lane;
-        if (j < J && y < nb) s[j] = S[g * nb + y];
+        if (j < J && y < nb) s[i][j] = S[g * nb + y];
       }
     }
   }
 
-  // ---- phase 2: selection flags sel (bit j <-> y = 64j + lane)
-  uint32_t sel = 0;
-  if (active) {
+  // ---- phase 2: selection flags sel[i] (bit j <-> y = 64j + lane)
+  uint32_t sel[RPW];
+#pragma unroll
+  for (int i = 0; i < RPW; ++i) {
+    sel[i] = 0;
+    if (row_of(i) >= rows) continue;
+    const long long g = g0 + row_of(i);
     if constexpr (MODE == kTermOnly) {
       // the row's list (any width, entries outside [0, nb) ignored) as a
-      // bitmap in this wave's part of the chunk buffer, 64 entries per step
-      uint32_t* bm = reinterpret_cast<uint32_t*>(Cb) + w * 64;     // nb <= 2048 bits
+      // bitmap in the row's part of the chunk buffer, 64 entries per step
+      uint32_t* bm = reinterpret_cast<uint32_t*>(Cb) + row_of(i) * 64;   // nb <= 2048 bits
       bm[lane] = 0u;
       wave_lds_sync();
       for (int i0 = 0; i0 < m; i0 += kWave) {
@@ -140,12 +189,12 @@ __global__ __launch_bounds__(1024) void rows_kernel(
 #pragma unroll
       for (int j = 0; j < JMAX; ++j) {
         const int y = kChunk * j + lane;
-        if (j < J && y < nb && ((bm[y >> 5] >> (y & 31)) & 1u)) sel |= 1u << j;
+        if (j < J && y < nb && ((bm[y >> 5] >> (y & 31)) & 1u)) sel[i] |= 1u << j;
       }
     } else {
       uint32_t key[JMAX];
 #pragma unroll
-      for (int j = 0; j < JMAX; ++j) key[j] = (j < J && kChunk * j + lane < nb) ? ordered_key(s[j]) : 0u;
+      for (int j = 0; j < JMAX; ++j) key[j] = (j < J && kChunk * j + lane < nb) ? ordered_key(s[i][j]) : 0u;
       uint32_t T = 0;
       int need = 0;
       const bool all = (m == nb), none = (m == 0);
@@ -157,12 +206,13 @@ __global__ __launch_bounds__(1024) void rows_kernel(
           for (int j = 0; j < JMAX; ++j)
             if (j < J) cnt += __popcll(__ballot(key[j] >= cand));
           if (cnt >= m) T = cand;
+          if (cnt == m) break;               // exactly the m largest are >= T
         }
         int gt = 0;
 #pragma unroll
         for (int j = 0; j < JMAX; ++j)
           if (j < J) gt += __popcll(__ballot(key[j] > T));
-        need = m - gt;                       // >= 1 keys equal to T still to take
+        need = m - gt;                       // keys equal to T still to take
       }
       int eq_seen = 0, written = 0;
 #pragma unroll
@@ -185,61 +235,60 @@ __global__ __launch_bounds__(1024) void rows_kernel(
         const uint64_t tm = __ballot(take);
         if (take && idx_out) idx_out[g * m + written + __popcll(tm & lanemask_lt())] = y;
         written += __popcll(tm);
-        if (take) sel |= 1u << j;
+        if (take) sel[i] |= 1u << j;
       }
     }
   }
   if constexpr (MODE == kSelectOnly || MODE == kFusedSelect) return;
 
   // ---- phase 3: max, weights (kept in s[]) and their sum over unselected blocks
-  if (active) {
-    float M = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < JMAX; ++j)
-      if (j < J && kChunk * j + lane < nb && !((sel >> j) & 1u)) M = fmaxf(M, s[j]);
-    M = wave_max(M);
-    const bool any = M != -INFINITY;
-    float c = 0.0f;
+  for (int i = 0; i < RPW; ++i) {
+    if (row_of(i) < rows) {
+      const long long g = g0 + row_of(i);
+      float M = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < JMAX; ++j) {
-      const int y = kChunk * j + lane;
-      const bool unsel = j < J && y < nb && !((sel >> j) & 1u);
-      s[j] = (any && unsel) ? (float)kBlock * expf(s[j] - M) : 0.0f;
-      c += s[j];
+      for (int j = 0; j < JMAX; ++j)
+        if (j < J && kChunk * j + lane < nb && !((sel[i] >> j) & 1u)) M = fmaxf(M, s[i][j]);
+      M = wave_max(M);
+      const bool any = M != -INFINITY;
+      float c = 0.0f;
+#pragma unroll
+      for (int j = 0; j < JMAX; ++j) {
+        const int y = kChunk * j + lane;
+        const bool unsel = j < J && y < nb && !((sel[i] >> j) & 1u);
+        s[i][j] = (any && unsel) ? (float)kBlock * expf(s[i][j] - M) : 0.0f;
+        c += s[i][j];
+      }
+      c = wave_sum(c);
+      if (lane == 0) {
+        cmax[g] = M;
+        csum[g] = c;
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < JMAX; ++j) s[i][j] = 0.0f;
     }
-    c = wave_sum(c);
-    if (lane == 0) {
-      cmax[g] = M;
-      csum[g] = c;
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < JMAX; ++j) s[j] = 0.0f;
   }
 
   // ---- phase 4: L = W V~ on the float32 matrix cores (v_mfma_f32_16x16x4_f32,
   // A = W: 16 rows x 4 blocks, B = V~: 4 blocks x 16 dims). Wave w takes dim
-  // tile nt = w % (D/16) and, inside every chunk, the block range of quarter
+  // tile nt = w % (D/16) and, inside every chunk, the block range of part
   // kq = w / (D/16); the per-wave partial sums are added in kq order at the end.
-  constexpr int NTD = D / 16, KQ = kRows / NTD, YPW = kChunk / KQ;
-  const int nt = w % NTD, kq = w / NTD;
-  const int ar = lane & 15, ak = lane >> 4;
-  const float* vh = vp + bh * (long long)nb * D;
   f32x4v acc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
   for (int j = 0; j < JMAX; ++j) {
     if (j >= J) break;
     __syncthreads();                                               // previous chunk consumed
-    Cb[w * ldc + lane] = s[j];                                     // zero for inactive rows
-    __syncthreads();
-    const int yb = kChunk * j + kq * YPW;
 #pragma unroll
-    for (int t = 0; t < YPW; t += 4) {
-      const int y = yb + t + ak;
-      const float a = Cb[ar * ldc + kq * YPW + t + ak];
-      const float b = y < nb ? vh[(long long)y * D + 16 * nt + ar] : 0.0f;
-      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc, 0, 0, 0);
+    for (int i = 0; i < RPW; ++i) Cb[row_of(i) * ldc + lane] = s[i][j];   // zero for inactive rows
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < NB4; ++t) {
+      const float a = Cb[ar * ldc + kq * YPW + 4 * t + ak];
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[j & 1][t], acc, 0, 0, 0);
     }
+    if (j + 2 < J) load_b(j + 2, bv[j & 1]);
   }
   // partial sums: lane holds rows 4*ak + e of dim 16*nt + ar
   float* part = reinterpret_cast<float*>(smem + k_off);            // [KQ][16][D]
@@ -247,7 +296,7 @@ __global__ __launch_bounds__(1024) void rows_kernel(
 #pragma unroll
   for (int e = 0; e < 4; ++e) part[(kq * kRows + 4 * ak + e) * D + 16 * nt + ar] = acc[e];
   __syncthreads();
-  for (int i = tid; i < rows * D; i += 1024) {
+  for (int i = tid; i < rows * D; i += NTH) {
     const int r = i / D, dm = i % D;
     float sum = part[r * D + dm];
 #pragma unroll
@@ -264,8 +313,10 @@ static void launch_rows_j(const float* S, const float* qp, const float* kp, int3
   const unsigned blocks = (unsigned)(bh * groups);
   const RowsSmem L = rows_smem(d, MODE == kFused || MODE == kFusedSelect);
   const double scale = 1.0 / sqrt((double)d);
+  // two rows per wave (8 waves) while the scores fit: four workgroups per CU
+  constexpr int RPW = JMAX <= 8 ? 2 : 1;
 #define MRA_ROWS_LAUNCH(DD)                                                                     \
-  rows_kernel<DD, MODE, JMAX><<<blocks, 64 * kRows, L.bytes, stream>>>(                       \
+  rows_kernel<DD, MODE, JMAX, RPW><<<blocks, 64 * kRows / RPW, L.bytes, stream>>>(            \
       S, qp, kp, idx_out, idx_in, vp, cmax, csum, cvec, nb, m, (int)L.q_off, (int)L.k_off, scale)
   switch (d) {
     case 32: MRA_ROWS_LAUNCH(32); break;
