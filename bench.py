@@ -49,11 +49,19 @@ def backward_flops(w) -> float:
     return 10.0 * w.B * w.H * w.nb * w.budget * 32 * 32 * w.d
 
 
+def raw_tiles(w) -> bool:
+    """The forward's tile pass reads bfloat16 K/V tiles of d <= 64 from the
+    rows themselves; otherwise pooling also writes a packed copy of K and V."""
+    return w.dtype == "bf16" and w.d <= 64
+
+
 def pool_bytes(w) -> float:
     """Pooling pass as run in the forward: Q, K, V read once, the pooled rows
-    written, and K and V written once more in packed order."""
+    written, and (packed configurations) K and V written once more in packed
+    order."""
     e = 2 if w.dtype == "bf16" else 4
-    return 5.0 * w.B * w.H * w.n * w.d * e + 3.0 * w.B * w.H * w.nb * w.d * 4
+    copies = 3 if raw_tiles(w) else 5
+    return copies * w.B * w.H * w.n * w.d * e + 3 * w.B * w.H * w.nb * w.d * 4
 
 
 TILE_SOURCES = ["paper_2207_10284_amd/csrc/tile.hip", "paper_2207_10284_amd/csrc/tile_ops.h",
@@ -249,14 +257,22 @@ def main():
 
     # Dominant kernel: the tile pass, the same instantiation as inside the
     # forward (packed K/V, coarse term given), on the same inputs; timed alone.
-    qp, kp, vp, kvpk = ops.pool(tq, tk, tv, packed=True)
+    packed = not raw_tiles(w)
+    if packed:
+        qp, kp, vp, kvpk = ops.pool(tq, tk, tv, packed=True)
+    else:
+        (qp, kp, vp), kvpk = ops.pool(tq, tk, tv), None
     S = ops.coarse_scores(qp, kp)
     sel = ops.select(S, w.budget)
     cm, cs, cv = ops.coarse_term(S, sel, vp)
     tile_out = torch.empty_like(tq)
     it = max(args.steps, 20)
-    tile_ms = time_launches(lambda: ops.block_sddmm_spmm(tq, None, None, sel, cm, cs, cv, out=tile_out, kvpacked=kvpk), it)
-    pool_ms = time_launches(lambda: ops.pool(tq, tk, tv, packed=True), it)
+    if packed:
+        tile_ms = time_launches(lambda: ops.block_sddmm_spmm(tq, None, None, sel, cm, cs, cv, out=tile_out,
+                                                             kvpacked=kvpk), it)
+    else:
+        tile_ms = time_launches(lambda: ops.block_sddmm_spmm(tq, tk, tv, sel, cm, cs, cv, out=tile_out), it)
+    pool_ms = time_launches(lambda: ops.pool(tq, tk, tv, packed=packed), it)
     coarse_ms = time_launches(lambda: ops.coarse_scores(qp, kp), it)
     tflops = tile_flops(w) / (tile_ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS

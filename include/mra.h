@@ -188,17 +188,20 @@ mra_status_t mra_block_sddmm_spmm(const void* q, const void* k, const void* v,
 
 /*
  * mra_forward_workspace_bytes — bytes of device workspace mra_attention_forward
- * needs for these sizes and dtype: pooled rows, copies of K and V rearranged
- * into matrix-core operand order, the selection and the coarse term (about
- * 2*B*H*n*d*elem + B*H*(n/32)*(4d + budget + 2)*4 bytes). Returns 0 for
- * invalid or unsupported arguments.
+ * needs for these sizes and dtype: pooled rows, the selection and the coarse
+ * term (B*H*(n/32)*(4d + budget + 2)*4 bytes, each part rounded up to 256),
+ * plus, for float32 inputs and for d = 128, copies of K and V rearranged into
+ * matrix-core operand order (2*B*H*n*d*elem bytes; bfloat16 tiles of
+ * d <= 64 are read straight from K and V). Returns 0 for invalid or
+ * unsupported arguments.
  */
 size_t mra_forward_workspace_bytes(int B, int H, int n, int d, int block, int budget,
                                    mra_dtype_t dtype);
 
 /*
- * mra_attention_forward — the whole MRA-2 forward pass: pooling (which also
- * rearranges K and V for the tile pass), coarse logits with
+ * mra_attention_forward — the whole MRA-2 forward pass: pooling (which, for
+ * float32 inputs and d = 128, also rearranges K and V for the tile pass),
+ * coarse logits with
  * selection and coarse term fused (the logits never leave on-chip memory),
  * then the tile pass. Results are bit-identical to the calls above made in
  * order (mra_pool, mra_coarse_scores, mra_select, mra_coarse_term,

@@ -73,6 +73,10 @@ struct WsLayout {
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
+// The forward's tile pass reads bfloat16 K/V tiles of d <= 64 straight from
+// their rows; other tiles need the packed copy the pooling pass writes.
+bool raw_tiles(int d, mra_dtype_t dtype) { return dtype == MRA_BF16 && d <= 64; }
+
 WsLayout ws_layout(long long bh, int nb, int d, int m, mra_dtype_t dtype) {
   WsLayout L{};
   size_t off = 0;
@@ -81,7 +85,8 @@ WsLayout ws_layout(long long bh, int nb, int d, int m, mra_dtype_t dtype) {
   L.qp = off; off += pooled;
   L.kp = off; off += pooled;
   L.vp = off; off += pooled;
-  L.kvpacked = off; off += align256((size_t)2 * bh * nb * kBlockSize * d * elem);
+  L.kvpacked = off;
+  if (!raw_tiles(d, dtype)) off += align256((size_t)2 * bh * nb * kBlockSize * d * elem);
   L.idx = off; off += align256((size_t)bh * nb * m * sizeof(int32_t));
   L.cmax = off; off += align256((size_t)bh * nb * sizeof(float));
   L.csum = off; off += align256((size_t)bh * nb * sizeof(float));
@@ -312,7 +317,7 @@ mra_status_t mra_attention_forward(const void* q, const void* k, const void* v, 
   float* qp = reinterpret_cast<float*>(ws + L.qp);
   float* kp = reinterpret_cast<float*>(ws + L.kp);
   float* vp = reinterpret_cast<float*>(ws + L.vp);
-  void* kvpacked = ws + L.kvpacked;
+  void* kvpacked = raw_tiles(d, dtype) ? nullptr : ws + L.kvpacked;
   int32_t* idx = idx_out ? idx_out : reinterpret_cast<int32_t*>(ws + L.idx);
   float* cmax = reinterpret_cast<float*>(ws + L.cmax);
   float* csum = reinterpret_cast<float*>(ws + L.csum);
@@ -352,7 +357,7 @@ mra_status_t mra_sparse_attention_forward(const void* q, const void* k, const vo
   float* qp = reinterpret_cast<float*>(ws + L.qp);
   float* kp = reinterpret_cast<float*>(ws + L.kp);
   float* vp = reinterpret_cast<float*>(ws + L.vp);
-  void* kvpacked = ws + L.kvpacked;
+  void* kvpacked = raw_tiles(d, dtype) ? nullptr : ws + L.kvpacked;
   int32_t* idx = idx_out ? idx_out : reinterpret_cast<int32_t*>(ws + L.idx);
   hipStream_t st = static_cast<hipStream_t>(stream);
 
@@ -408,7 +413,7 @@ mra_status_t mra_attention_forward_global(const void* q, const void* k, const vo
   float* qp = reinterpret_cast<float*>(ws + L.qp);
   float* kp = reinterpret_cast<float*>(ws + L.kp);
   float* vp = reinterpret_cast<float*>(ws + L.vp);
-  void* kvpacked = ws + L.kvpacked;
+  void* kvpacked = raw_tiles(d, dtype) ? nullptr : ws + L.kvpacked;
   int32_t* idx = idx_out ? idx_out : reinterpret_cast<int32_t*>(ws + L.idx);
   float* cmax = reinterpret_cast<float*>(ws + L.cmax);
   float* csum = reinterpret_cast<float*>(ws + L.csum);
@@ -509,7 +514,7 @@ mra_status_t mra_attention_forward_multilevel(const void* q, const void* k, cons
   float *qp = f32(L.qp), *kp = f32(L.kp), *vp = f32(L.vp);
   float *qp0 = f32(W.qp0), *kp0 = f32(W.kp0), *vp0 = f32(W.vp0);
   float *S0 = f32(W.S0), *S = f32(W.S);
-  void* kvpacked = ws + L.kvpacked;
+  void* kvpacked = raw_tiles(d, dtype) ? nullptr : ws + L.kvpacked;
   int32_t* idx1 = idx1_out ? idx1_out : reinterpret_cast<int32_t*>(ws + W.idx1);
   int32_t* idx2 = idx2_out ? idx2_out : reinterpret_cast<int32_t*>(ws + L.idx);
   float *cmax = f32(L.cmax), *csum = f32(L.csum), *cvec = f32(L.cvec);

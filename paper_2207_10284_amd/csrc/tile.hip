@@ -387,7 +387,76 @@ __global__ __launch_bounds__((TileCfg<DT, D>::kWaves * kWave)) void tile_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// One wave per block-row, packed K/V staged through a wave-private LDS slot:
+// Raw K/V tiles in LDS (bfloat16, d <= 64). A 32-row tile of K (or V) is 4 KB
+// (d = 64) of consecutive rows in HBM. It is copied with direct-to-LDS loads
+// of whole rows (each 1 KB load covers 1024 / (2d) complete rows, so it
+// touches as many cache lines as a contiguous copy), but each lane fetches
+// the 16-byte block that belongs at its LDS position under an XOR swizzle of
+// the blocks within a row: block b of row r sits at block b ^ f(r). With the
+// swizzles below the matrix-core operand reads are free of bank conflicts
+// (checked with a CPU model of the LDS banks):
+//   K, row layout, ds_read_b128 (16 lanes = 16 rows per pass): lane (h, j)
+//     reads row j, block (d/16) h + s;
+//   V^T, transposed layout, ds_read_b64_tr_b16 (32 lanes per pass): within a
+//     group of 16 lanes, lane 4k + g supplies 4 columns of row key0 + k and
+//     lane i receives element i % 4 of lane (4k + i/4)'s 8 bytes as value k;
+//     two reads (key0 = 16u + 4h and 16u + 8 + 4h) fill the 8 keys of a
+//     chunk in the order the weights of the second product hold them.
+template <int D>
+__host__ __device__ constexpr int raw_swz_k(int r) {
+  return D == 64 ? (r >> 1) & 7 : (r >> 2) & 3;
+}
+template <int D>
+__host__ __device__ constexpr int raw_swz_v(int r) {
+  return D == 64 ? ((r >> 1) & 1) << 2 : 0;
+}
+// byte offset of element (r, c) of a raw bf16 tile in LDS under swizzle F
+template <int D, int (*F)(int)>
+__host__ __device__ constexpr int raw_offset(int r, int c) {
+  return r * (2 * D) + ((((2 * c) >> 4) ^ F(r)) << 4) + ((2 * c) & 15);
+}
+
+// Source byte offset (within the tile) of the 16 bytes lane `lane` copies to
+// LDS byte i * 1024 + 16 lane under swizzle F.
+template <int D, int (*F)(int)>
+__device__ __forceinline__ int raw_copy_offset(int i, int lane) {
+  const int q = i * 1024 + 16 * lane, r = q / (2 * D), blk = (q % (2 * D)) / 16;
+  return r * (2 * D) + ((blk ^ F(r)) << 4);
+}
+
+// The C 1 KB copies of a raw K tile and of a raw V tile. The swizzled source
+// offsets repeat with period KP in the copy index for K (the swizzle of row r
+// depends on r / 2 for d = 64) and period 1 for V, so per lane they are k0
+// (even copies), k1 (odd copies, less 1 KB) and v0, and the load's immediate
+// offset moves the source and the LDS destination together.
+template <int C, int KP>
+__device__ __forceinline__ void copy_raw_tiles(gptr_t k0, gptr_t k1, gptr_t v0, lptr_t ks, lptr_t vs) {
+  if constexpr (C > 0) {
+    copy_raw_tiles<C - 1, KP>(k0, k1, v0, ks, vs);
+    constexpr int i = C - 1;
+    __builtin_amdgcn_global_load_lds((KP == 2 && (i & 1)) ? k1 : k0, ks, 16, i * 1024, 0);
+    __builtin_amdgcn_global_load_lds(v0, vs, 16, i * 1024, 0);
+  }
+}
+
+// Transposed V chunks c = u NT + t (c < VC) of a raw tile: two transposing
+// reads each, 8 rows apart, from this lane's column-tile address vt[t].
+template <int D, int C, int VC>
+struct RawTrChunks {
+  static constexpr int NT = D / 32, RB = 2 * D;
+  static __device__ __forceinline__ void run(const uint32_t* vt, u32x4* v) {
+    if constexpr (C < VC) {
+      constexpr int u = C / NT, t = C % NT;
+      const u32x2 lo = lds_read_tr16<16 * u * RB>(vt[t]);
+      const u32x2 hi = lds_read_tr16<(16 * u + 8) * RB>(vt[t]);
+      v[C] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+      RawTrChunks<D, C + 1, VC>::run(vt, v);
+    }
+  }
+};
+
+// ---------------------------------------------------------------------------
+// One wave per block-row, K/V staged through a wave-private LDS slot:
 // the next selected tile is copied HBM/L2 -> LDS with direct-to-LDS loads
 // while the current one is computed from registers. Prefetching into LDS
 // instead of registers leaves room for four waves per SIMD.
@@ -403,7 +472,7 @@ __device__ __forceinline__ void wait_tiles_in_flight(int keep) {
   else asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * CH) : "memory");
 }
 
-template <int DT, int D, bool COARSE, int WAVES, int SLOTS>
+template <int DT, int D, bool COARSE, int WAVES, int SLOTS, bool RAW>
 __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
     const void* __restrict__ qv, const void* __restrict__ kpk, const void* __restrict__ vpk,
     const int32_t* __restrict__ idx, const float* __restrict__ cmax,
@@ -414,6 +483,7 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
   constexpr int KC = Cfg::kKChunks, VC = Cfg::kVChunks, CH = Cfg::kChunks;
   static_assert(CH <= 8, "operands of a tile are held in registers");
   static_assert(SLOTS >= 1 && SLOTS <= 3, "tiles in flight per wave");
+  static_assert(!RAW || (DT == BF16 && D <= 64), "raw tiles: bfloat16, d <= 64");
   // the slots are their own LDS object, apart from the selection lists, so
   // reading a list does not wait for loads in flight into a slot
   __shared__ __attribute__((aligned(16))) u32x4 slot_all[WAVES][SLOTS][CH * 64];
@@ -438,14 +508,36 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
   // One lane address per operand; its chunks are 1 KB apart in memory and in
   // the slot, and the load's immediate offset moves both addresses.
   static_assert(KC <= 4 && VC <= 4, "chunk offsets fit the immediate field");
+  // raw tiles: this lane's source offsets for the copies (k0, k1, v0: see
+  // copy_raw_tiles) and its LDS read offsets (K chunk c; V^T column tile t)
+  constexpr int NT = TileCfg<DT, D>::kNT, KP = D == 64 ? 2 : 1;
+  int koff0 = 0, koff1 = 0, voff0 = 0, kread[KC], vread[NT];
+  if constexpr (RAW) {
+    koff0 = raw_copy_offset<D, raw_swz_k<D>>(0, lane);
+    koff1 = raw_copy_offset<D, raw_swz_k<D>>(1, lane) - 1024;
+    voff0 = raw_copy_offset<D, raw_swz_v<D>>(0, lane);
+    const int h = lane >> 5, j = lane & 31, i16 = lane & 15;
+#pragma unroll
+    for (int c = 0; c < KC; ++c) kread[c] = raw_offset<D, raw_swz_k<D>>(j, (D / 2) * h + 8 * c);
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+      vread[t] = KC * 1024 +
+                 raw_offset<D, raw_swz_v<D>>(4 * h + i16 / 4, 32 * t + 16 * ((lane >> 4) & 1) + 4 * (i16 & 3));
+  }
   auto issue = [&](int y, int sidx) {
     unsigned char* slot = reinterpret_cast<unsigned char*>(slot_all[w][sidx]);
-    const auto* kp = (const __attribute__((address_space(1))) char*)(kslab + (size_t)y * KC * 1024 + loff);
-    const auto* vp = (const __attribute__((address_space(1))) char*)(vslab + (size_t)y * VC * 1024 + loff);
     auto* ks = (__attribute__((address_space(3))) char*)slot;
     auto* vs = (__attribute__((address_space(3))) char*)(slot + KC * 1024);
-    load_chunks_lds<KC>(kp, ks);
-    load_chunks_lds<VC>(vp, vs);
+    if constexpr (RAW) {
+      const gptr_t kt = (gptr_t)(kslab + (size_t)y * KC * 1024);
+      const gptr_t vt = (gptr_t)(vslab + (size_t)y * VC * 1024);
+      copy_raw_tiles<KC, KP>(kt + koff0, kt + koff1, vt + voff0, ks, vs);
+    } else {
+      const auto* kp = (const __attribute__((address_space(1))) char*)(kslab + (size_t)y * KC * 1024 + loff);
+      const auto* vp = (const __attribute__((address_space(1))) char*)(vslab + (size_t)y * VC * 1024 + loff);
+      load_chunks_lds<KC>(kp, ks);
+      load_chunks_lds<VC>(vp, vs);
+    }
   };
   // entries outside [0, nb) are skipped
   auto next_valid = [&](int j, int& y) {
@@ -470,12 +562,24 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
       }
     while (used < issued) {
       wait_tiles_in_flight<CH>(issued - used - 1);   // tile `used` is in its slot
-      const u32x4* sl = slot_all[w][used % SLOTS] + lane;
       u32x4 kf[KC], vf[VC];
+      if constexpr (RAW) {
+        const uint32_t base = lds_addr(slot_all[w][used % SLOTS]);
 #pragma unroll
-      for (int c = 0; c < KC; ++c) kf[c] = sl[c * 64];
+        for (int c = 0; c < KC; ++c) kf[c] = lds_read16<0>(base + kread[c]);
+        uint32_t va[NT];
 #pragma unroll
-      for (int c = 0; c < VC; ++c) vf[c] = sl[(KC + c) * 64];
+        for (int t = 0; t < NT; ++t) va[t] = base + vread[t];
+        RawTrChunks<D, 0, VC>::run(va, vf);
+        lds_done(kf);
+        lds_done(vf);
+      } else {
+        const u32x4* sl = slot_all[w][used % SLOTS] + lane;
+#pragma unroll
+        for (int c = 0; c < KC; ++c) kf[c] = sl[c * 64];
+#pragma unroll
+        for (int c = 0; c < VC; ++c) vf[c] = sl[(KC + c) * 64];
+      }
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // operands in registers
       ++used;
       if (ni < m) {                                  // refill the slot just read
@@ -496,10 +600,14 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
     for (int i = 0; i < m; ++i) {
       const int yy = wave_uniform(myidx[i]);
       if (yy < 0 || yy >= nb) continue;
-      const u32x4* kt = reinterpret_cast<const u32x4*>(kslab + (size_t)yy * KC * 1024) + lane;
       u32x4 kf[KC];
+      if constexpr (RAW) {
+        load_rows<DT, D>(reinterpret_cast<const elem*>(kslab + (size_t)yy * KC * 1024), kf);
+      } else {
+        const u32x4* kt = reinterpret_cast<const u32x4*>(kslab + (size_t)yy * KC * 1024) + lane;
 #pragma unroll
-      for (int c = 0; c < KC; ++c) kf[c] = kt[c * 64];
+        for (int c = 0; c < KC; ++c) kf[c] = kt[c * 64];
+      }
       mx = __builtin_elementwise_maximum(mx, row.tile_ref(row.scores(kf)));
     }
     row.restart(mx);
@@ -517,15 +625,17 @@ static void launch_tile_t(const void* q, const void* k, const void* v, const int
   const int nb = n / kBlock;
   const long long rows = bh * nb;
   const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
-  // tiles of up to 8 KB (bfloat16 d <= 64, float32 d = 32) stream through LDS
-  if constexpr (PACKED && TileCfg<DT, D>::kChunks <= 8) {
+  // tiles of up to 8 KB (bfloat16 d <= 64, float32 d = 32) stream through LDS:
+  // packed operands, or for bfloat16 the raw rows
+  constexpr bool RAW = !PACKED && DT == BF16 && D <= 64;
+  if constexpr ((PACKED || RAW) && TileCfg<DT, D>::kChunks <= 8) {
     const unsigned blocks = (unsigned)((rows + kStreamWaves - 1) / kStreamWaves);
     const size_t smem = (size_t)kStreamWaves * m * sizeof(int32_t);
     if (cmax)
-      tile_stream_kernel<DT, D, true, kStreamWaves, kStreamSlots><<<blocks, kStreamWaves * kWave, smem, stream>>>(
+      tile_stream_kernel<DT, D, true, kStreamWaves, kStreamSlots, RAW><<<blocks, kStreamWaves * kWave, smem, stream>>>(
           q, k, v, idx, cmax, csum, cvec, out, lse, n, nb, m, rows, scale_log2);
     else
-      tile_stream_kernel<DT, D, false, kStreamWaves, kStreamSlots><<<blocks, kStreamWaves * kWave, smem, stream>>>(
+      tile_stream_kernel<DT, D, false, kStreamWaves, kStreamSlots, RAW><<<blocks, kStreamWaves * kWave, smem, stream>>>(
           q, k, v, idx, cmax, csum, cvec, out, lse, n, nb, m, rows, scale_log2);
     return;
   }

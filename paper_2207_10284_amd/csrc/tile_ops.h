@@ -109,6 +109,61 @@ __device__ __forceinline__ void load_chunks_lds(const __attribute__((address_spa
   }
 }
 
+__device__ __forceinline__ void wait_lds_reads() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+}
+
+// Slot reads are issued as inline assembly: the compiler cannot tell the
+// slot's parts apart and, seeing loads in flight into LDS, would wait for all
+// of them before any slot read. Here the caller's wait_loads<> covers the part
+// being read; lds_done() waits for the reads and ties each value to that wait
+// so that no use is scheduled before it.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+}
+
+template <int OFF>
+__device__ __forceinline__ u32x4 lds_read16(uint32_t addr) {
+  u32x4 v;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF) : "memory");
+  return v;
+}
+
+// v[i] = chunk C0 + i of a part (chunks 1 KB apart) for this lane, i < C
+template <int I, int C, int C0>
+struct LdsChunks {
+  static __device__ __forceinline__ void run(uint32_t addr, u32x4* v) {
+    v[I] = lds_read16<(C0 + I) * 1024>(addr);
+    LdsChunks<I + 1, C, C0>::run(addr, v);
+  }
+};
+template <int C, int C0>
+struct LdsChunks<C, C, C0> {
+  static __device__ __forceinline__ void run(uint32_t, u32x4*) {}
+};
+
+template <int C, int C0 = 0>
+__device__ __forceinline__ void lds_read_chunks(uint32_t addr, u32x4 (&v)[C]) {
+  LdsChunks<0, C, C0>::run(addr, v);
+}
+
+template <int C>
+__device__ __forceinline__ void lds_done(u32x4 (&v)[C]) {
+  wait_lds_reads();
+#pragma unroll
+  for (int c = 0; c < C; ++c) asm volatile("" : "+v"(v[c]));
+}
+
+// gfx950's transposing read (ds_read_b64_tr_b16): within each group of 16
+// lanes, lane i receives as value k (k = 0..3) the 16-bit element i%4 of the
+// 8 bytes at the address that lane 4k + i/4 of the group supplies.
+template <int OFF>
+__device__ __forceinline__ u32x2 lds_read_tr16(uint32_t addr) {
+  u32x2 v;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF) : "memory");
+  return v;
+}
+
 typedef const __attribute__((address_space(1))) char* gptr_t;
 typedef __attribute__((address_space(3))) char* lptr_t;
 
