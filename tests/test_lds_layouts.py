@@ -1,0 +1,117 @@
+"""CPU model of the raw-tile LDS layout of the bfloat16 tile pass (d = 32, 64).
+
+The tile pass copies a raw 32-row K (or V) tile into LDS with direct-to-LDS
+loads of 16 bytes per lane, each 1 KB load covering whole rows; lane p of load
+i writes LDS byte i*1024 + 16p and fetches the block that an XOR swizzle of
+the 16-byte blocks within each row puts there. The matrix-core operands are
+then read with ds_read_b128 (K, row layout) and ds_read_b64_tr_b16 (V^T,
+transposed layout). This model restates the swizzles of csrc/tile.hip
+(raw_swz_k, raw_swz_v) and checks, per lane and value, that the reads deliver
+the operands of v_mfma_f32_32x32x16_bf16 as the tile pass uses them, and that
+no LDS pass has a bank conflict (64 banks of 4 bytes; 16 lanes per
+ds_read_b128 pass, 32 lanes per ds_read_b64 pass). The GPU parity tests check
+the kernels themselves (the raw path is bit-identical to the packed one).
+"""
+import pytest
+
+
+def swz_k(d, r):
+    return (r >> 1) & 7 if d == 64 else (r >> 2) & 3
+
+
+def swz_v(d, r):
+    return ((r >> 1) & 1) << 2 if d == 64 else 0
+
+
+def offset(d, r, c, swz):
+    """LDS byte of element (r, c) of a tile (bf16, d columns)."""
+    rb = 2 * d
+    return r * rb + (((2 * c) // 16 ^ swz(d, r)) * 16) + (2 * c) % 16
+
+
+def conflict_ways(addrs, width):
+    """Largest number of distinct addresses sharing a bank in one pass."""
+    banks = {}
+    for a in addrs:
+        for b in range(width // 4):
+            banks.setdefault((a // 4 + b) % 64, set()).add(a)
+    return max(len(v) for v in banks.values())
+
+
+@pytest.mark.parametrize("d", [32, 64])
+@pytest.mark.parametrize("which", ["k", "v"])
+def test_copies_cover_whole_rows_once(d, which):
+    swz = swz_k if which == "k" else swz_v
+    rb = 2 * d
+    sources = set()
+    for i in range(32 * rb // 1024):
+        rows = set()
+        for p in range(64):
+            q = i * 1024 + 16 * p
+            r, slot = q // rb, (q % rb) // 16
+            blk = slot ^ swz(d, r)
+            assert 0 <= blk < rb // 16
+            rows.add(r)
+            sources.add(r * rb + 16 * blk)
+            assert offset(d, r, 8 * blk, swz) == q           # the block lands where reads expect it
+        assert len(rows) * rb == 1024                         # one load = whole rows
+    assert len(sources) == 32 * rb // 16                      # every block copied once
+
+
+@pytest.mark.parametrize("d", [32, 64])
+def test_k_row_operand_reads(d):
+    """Chunk s of lane (h, j) = K[j][(d/2)h + 8s .. +7] (16 contiguous bytes);
+    no bank conflict in any 16-lane pass."""
+    for s in range(d // 16):
+        addrs = []
+        for lane in range(64):
+            h, j = lane // 32, lane % 32
+            a = offset(d, j, (d // 2) * h + 8 * s, swz_k)
+            for e in range(8):
+                assert offset(d, j, (d // 2) * h + 8 * s + e, swz_k) == a + 2 * e
+            addrs.append(a)
+        for p0 in range(0, 64, 16):
+            assert conflict_ways(addrs[p0:p0 + 16], 16) == 1
+
+
+@pytest.mark.parametrize("d", [32, 64])
+def test_v_transposed_operand_reads(d):
+    """ds_read_b64_tr_b16: within a group of 16 lanes, lane i receives as value
+    k the element i%4 of the 8 bytes addressed by lane 4k + i/4. Each lane
+    supplies 4 columns of one row; two reads (rows 8 apart) must give lane
+    l = 32h + j the 8 values V[16u + 8(e/4) + 4h + e%4][32t + j], e = 0..7 --
+    the key order of the weights in the second product. No bank conflict in
+    any 32-lane pass."""
+    for u in range(2):
+        for t in range(d // 32):
+            for half in range(2):
+                sup = []
+                for lane in range(64):
+                    i = lane % 16
+                    row = 16 * u + 8 * half + 4 * (lane // 32) + i // 4
+                    col = 32 * t + 16 * ((lane // 16) & 1) + 4 * (i % 4)
+                    sup.append((row, col, offset(d, row, col, swz_v)))
+                for lane in range(64):
+                    g0, i = lane - lane % 16, lane % 16
+                    for k in range(4):
+                        row, col, a = sup[g0 + 4 * k + i // 4]
+                        want = (16 * u + 8 * half + 4 * (lane // 32) + k, 32 * t + lane % 32)
+                        assert (row, col + i % 4) == want
+                        assert offset(d, row, col + i % 4, swz_v) == a + 2 * (i % 4)
+                for p0 in range(0, 64, 32):
+                    assert conflict_ways([a for _, _, a in sup[p0:p0 + 32]], 8) == 1
+                # the address of the second read is the first one's plus 8 rows
+                if half == 1:
+                    for lane in range(64):
+                        i = lane % 16
+                        r0 = 16 * u + 4 * (lane // 32) + i // 4
+                        c0 = 32 * t + 16 * ((lane // 16) & 1) + 4 * (i % 4)
+                        assert offset(d, r0 + 8, c0, swz_v) - offset(d, r0, c0, swz_v) == 8 * 2 * d
+
+
+def test_unswizzled_rows_would_conflict():
+    """Without the swizzle the K reads of d = 64 are 8-way conflicted (rows are
+    128 bytes apart): the swizzle is what makes them conflict-free."""
+    none = lambda d, r: 0
+    addrs = [offset(64, lane % 32, 32 * (lane // 32), none) for lane in range(16)]
+    assert conflict_ways(addrs, 16) == 8
