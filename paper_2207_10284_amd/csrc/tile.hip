@@ -192,6 +192,7 @@ struct TileRow {
     const float ao = af * inv, bv = bc * inv;       // z = o * ao + cvec * bv
     elem* orow = Out + (long long)(x * 32 + jq) * D;
     const float* cv = COARSE ? cvec + g * D : nullptr;
+    u32x2 pend = {0u, 0u};                          // bf16: the even group's 4 values
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
 #pragma unroll
@@ -207,7 +208,19 @@ struct TileRow {
           lo[0] = (__bf16)z[0]; lo[1] = (__bf16)z[1];
           hi[0] = (__bf16)z[2]; hi[1] = (__bf16)z[3];
           const u32x2 pr = {__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
-          *reinterpret_cast<u32x2*>(orow + d0) = pr;
+          // lanes l and l^32 hold dims 4h..4h+3 of groups rg (even, odd):
+          // exchange so that lane h = 0 stores the even group's 8 dims and
+          // lane h = 1 the odd group's, 16 contiguous bytes each
+          if ((rg & 1) == 0) {
+            pend = pr;
+          } else {
+            const u32x2 send = h ? pend : pr;          // h = 0 sends its odd group, h = 1 its even one
+            u32x2 recv;
+            recv[0] = (uint32_t)__shfl_xor((int)send[0], 32);
+            recv[1] = (uint32_t)__shfl_xor((int)send[1], 32);
+            const u32x4 st = h ? u32x4{recv[0], recv[1], pr[0], pr[1]} : u32x4{pend[0], pend[1], recv[0], recv[1]};
+            *reinterpret_cast<u32x4*>(orow + 32 * t + 8 * (rg - 1) + 8 * h) = st;
+          }
         } else {
           const f32x4 st = {z[0], z[1], z[2], z[3]};
           *reinterpret_cast<f32x4*>(orow + d0) = st;
@@ -243,10 +256,11 @@ __global__ __launch_bounds__((TileCfg<DT, D>::kWaves * kWave)) void tile_kernel(
   const elem* K = reinterpret_cast<const elem*>(kv) + hoff;
   extern __shared__ int32_t sidx_all[];
   int32_t* myidx = sidx_all + w * m;
-  m = stage_selection(idx + g * m, m, nb, myidx);  // valid entries only, in order
-
+  // Q_x's loads are issued first, so their latency overlaps the staging of
+  // the selection list
   TileRow<DT, D, COARSE> row;
   row.init(reinterpret_cast<const elem*>(qv) + hoff, x, scale_log2);
+  m = stage_selection(idx + g * m, m, nb, myidx);  // valid entries only, in order
   auto clampy = [&](int y) { return (y < 0 || y >= nb) ? 0 : y; };
   auto valid = [&](int y) { return y >= 0 && y < nb; };
 
@@ -498,10 +512,11 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
   const int x = (int)(g - bh * nb);
   const long long hoff = bh * (long long)n * D;
   int32_t* myidx = sidx_all + w * m;
-  m = stage_selection(idx + g * m, m, nb, myidx);  // valid entries only, in order
-
+  // Q_x's loads are issued first, so their latency overlaps the staging of
+  // the selection list
   TileRow<DT, D, COARSE> row;
   row.init(reinterpret_cast<const elem*>(qv) + hoff, x, scale_log2);
+  m = stage_selection(idx + g * m, m, nb, myidx);  // valid entries only, in order
   const char* kslab = static_cast<const char*>(kpk) + (size_t)bh * nb * KC * 1024;
   const char* vslab = static_cast<const char*>(vpk) + (size_t)bh * nb * VC * 1024;
   const unsigned loff = lane * 16u;
