@@ -39,18 +39,32 @@
 
 namespace mra {
 
-constexpr int kBwdRows = 16;              // waves (block-rows or columns) per workgroup
-constexpr int kBwdChunk = 64;             // blocks staged per step
+constexpr int kBwdRows = 16;              // waves (block-rows) per workgroup of the row pass
 constexpr int kBwdTileWaves = 4;          // waves per workgroup of the tile passes
+constexpr int kBwdCols = 16;              // column blocks per workgroup of the column pass
 
 template <int DT>
 __device__ __forceinline__ float elem_lo(uint32_t w) {
   return DT == BF16 ? bf16_to_f32(w & 0xFFFFu) : __uint_as_float(w);
 }
 
+__device__ __forceinline__ f32x4 mfma16x4(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
 // ---------------------------------------------------------------------------
+// Row pass: one wave per block-row x for the per-row terms (the record, the
+// bitmap, G^_x, d^_x), then with the coarse term the 16 rows of the
+// workgroup together, 128 column blocks per step, on the float32 matrix cores
+// (v_mfma_f32_16x16x4_f32; A: 16 rows x 4, B: 4 x 16 columns, lane l holds
+// A[l%16][l/16] and B[l/16][l%16], and D[4(l/16)+r][l%16] in register r):
+//  1. S~ = Q~_x K~_y^T and G^_x V~_y^T: one 16 x 16 tile per wave, the
+//     contraction over dims taken four at a time from 16-byte loads;
+//  2. W and dS~ for the 16 x 128 entries (two per thread), written out;
+//  3. dQ~_x += dS~ K~_y: wave (dim tile, part of the step's columns), the
+//     partial sums added in part order at the end.
 template <int DT, int D, bool COARSE>
-__global__ __launch_bounds__(kBwdRows * kWave) void bwd_rows_kernel(
+__global__ __launch_bounds__(kBwdRows * kWave) __attribute__((amdgpu_waves_per_eu(D <= 64 ? 8 : 1, 8))) void bwd_rows_kernel(
     const void* __restrict__ gin, const void* __restrict__ zin, const float* __restrict__ lse,
     const int32_t* __restrict__ idx, const float* __restrict__ qp, const float* __restrict__ kp,
     const float* __restrict__ vp, float* __restrict__ ld, uint32_t* __restrict__ bits, float* __restrict__ gh, float* __restrict__ Wout,
@@ -58,13 +72,17 @@ __global__ __launch_bounds__(kBwdRows * kWave) void bwd_rows_kernel(
   using Cfg = TileCfg<DT, D>;
   using elem = typename Cfg::elem;
   constexpr int KC = Cfg::kKChunks;                        // 16-byte chunks per half row
-  constexpr int PK = D + 1;                                 // LDS pitch of staged rows
-  __shared__ float Kc[COARSE ? kBwdChunk * PK : 1];
-  __shared__ float Vc[COARSE ? kBwdChunk * PK : 1];
-  __shared__ float Qx[kBwdRows][D];
-  __shared__ float Gx[kBwdRows][D];
+  constexpr int PQ = D + 4;                                 // LDS pitch of the Q~, G^ rows
+  constexpr int YC = 128;                                   // column blocks per step
+  constexpr int PP = YC + 1, PD = YC + 4;
+  constexpr int NTD = D / 16, KQ = kBwdRows / NTD, YK = YC / KQ;
+  static_assert(KQ * kBwdRows * D <= 2 * kBwdRows * PP, "dQ~ partials fit the step buffer");
+  __shared__ __attribute__((aligned(16))) float Qx[COARSE ? kBwdRows * PQ : 1];
+  __shared__ __attribute__((aligned(16))) float Gx[COARSE ? kBwdRows * PQ : 1];
+  __shared__ float Pst[COARSE ? 2 * kBwdRows * PP : 1];    // a step's S~, G^V~^T; then dQ~ partials
+  __shared__ float Ds[COARSE ? kBwdRows * PD : 1];
   __shared__ float wq[kBwdRows][32];
-  __shared__ float dsl[kBwdRows][kBwdChunk];
+  __shared__ float rowm[kBwdRows], rowd[kBwdRows];
   __shared__ uint32_t bm_all[kBwdRows][64];                 // nb <= 2048 bits
 
   const int tid = threadIdx.x;
@@ -79,8 +97,11 @@ __global__ __launch_bounds__(kBwdRows * kWave) void bwd_rows_kernel(
   const int nbw = (nb + 31) / 32;
   uint32_t* bm = bm_all[w];
 
-  float mref = 0.0f, dhat = 0.0f;
   if (active) {
+    // the first 64 selection entries and the log normaliser are requested
+    // first, so their latency overlaps the delta's loads
+    const int ysel0 = lane < m ? idx[g * m + lane] : -1;
+    const float L = lse[g * 32 + j];
     // delta_i = G_i . Z_i: lane (h, j) takes half h of row j
     const long long roff = (g * 32 + j) * D + (D / 2) * h;
     const u32x4* gp = reinterpret_cast<const u32x4*>(reinterpret_cast<const elem*>(gin) + roff);
@@ -96,7 +117,6 @@ __global__ __launch_bounds__(kBwdRows * kWave) void bwd_rows_kernel(
       }
     }
     const float dl = halves_sum(part);
-    const float L = lse[g * 32 + j];
     if (h == 0) {                                           // the block-row's record
       ld[g * 64 + j] = L * kLog2e;
       ld[g * 64 + 32 + j] = dl;
@@ -104,17 +124,22 @@ __global__ __launch_bounds__(kBwdRows * kWave) void bwd_rows_kernel(
     // the selection as a bitmap (entries outside [0, nb) ignored)
     for (int i = lane; i < nbw; i += kWave) bm[i] = 0u;
     wave_lds_sync();
-    for (int i0 = 0; i0 < m; i0 += kWave) {
+    if (ysel0 >= 0 && ysel0 < nb) atomicOr(&bm[ysel0 >> 5], 1u << (ysel0 & 31));
+    for (int i0 = kWave; i0 < m; i0 += kWave) {
       const int y = i0 + lane < m ? idx[g * m + i0 + lane] : -1;
       if (y >= 0 && y < nb) atomicOr(&bm[y >> 5], 1u << (y & 31));
     }
     wave_lds_sync();
     for (int i = lane; i < nbw; i += kWave) bits[g * nbw + i] = bm[i];
     if constexpr (COARSE) {
-      mref = -wave_max(-L);                                 // min over the 32 queries
+      const float mref = -wave_max(-L);                     // min over the 32 queries
       const float wi = exp2f((mref - L) * kLog2e);
-      dhat = wave_sum(h == 0 ? wi * dl : 0.0f);
+      const float dhat = wave_sum(h == 0 ? wi * dl : 0.0f);
       if (h == 0) wq[w][j] = wi;
+      if (lane == 0) {
+        rowm[w] = mref;
+        rowd[w] = dhat;
+      }
       wave_lds_sync();
       // G^_x: lanes over the dims, rows in order
       const elem* G = reinterpret_cast<const elem*>(gin) + g * 32 * D;
@@ -126,138 +151,129 @@ __global__ __launch_bounds__(kBwdRows * kWave) void bwd_rows_kernel(
           else gv = G[i * D + dd];
           acc = fmaf(wq[w][i], gv, acc);
         }
-        Gx[w][dd] = acc;
+        Gx[w * PQ + dd] = acc;
         gh[g * D + dd] = acc;
-        Qx[w][dd] = qp[g * D + dd];
+        Qx[w * PQ + dd] = qp[g * D + dd];
       }
-      wave_lds_sync();
     }
+  } else if constexpr (COARSE) {
+    for (int dd = lane; dd < D; dd += kWave) Gx[w * PQ + dd] = Qx[w * PQ + dd] = 0.0f;
   }
   if constexpr (!COARSE) return;
+  __syncthreads();                                          // Q~, G^, rowm, rowd, bitmaps
 
-  // ---- coarse row terms, 64 column blocks per step
   const float* kh = kp + bh * (long long)nb * D;
   const float* vh = vp + bh * (long long)nb * D;
-  constexpr int DQ = (D + kWave - 1) / kWave;
-  float accq[DQ];
+  const int lr = lane & 15, lg = lane >> 4;
+  const int kind = w >> 3, t = w & 7;                       // step 1: S~ (0) or G^V~^T (1), columns 16t..
+  const float* arow = (kind ? Gx : Qx) + lr * PQ + 4 * lg;
+  const float* bsrc = kind ? vh : kh;
+  const int nt = w % NTD, kq = w / NTD;                     // step 3: dims 16nt.., columns kq*YK..
+  f32x4 accq = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int y0 = 0; y0 < nb; y0 += YC) {
+    const int yb = y0 + 16 * t + lr;
+    f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+    constexpr int UG = D / 16 < 4 ? D / 16 : 4;             // 16-byte loads in flight per group
 #pragma unroll
-  for (int q = 0; q < DQ; ++q) accq[q] = 0.0f;
-  for (int y0 = 0; y0 < nb; y0 += kBwdChunk) {
-    __syncthreads();                                        // previous chunk consumed
-    for (int i = tid; i < kBwdChunk * D; i += kBwdRows * kWave) {
-      const int r = i / D, c = i % D;
-      const bool in = y0 + r < nb;
-      Kc[r * PK + c] = in ? kh[(long long)(y0 + r) * D + c] : 0.0f;
-      Vc[r * PK + c] = in ? vh[(long long)(y0 + r) * D + c] : 0.0f;
+    for (int u0 = 0; u0 < D / 16; u0 += UG) {
+      f32x4 bq[UG];
+#pragma unroll
+      for (int u = 0; u < UG; ++u)
+        bq[u] = yb < nb ? *reinterpret_cast<const f32x4*>(bsrc + (long long)yb * D + 16 * (u0 + u) + 4 * lg)
+                        : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int u = 0; u < UG; ++u) {
+        const f32x4 a = *reinterpret_cast<const f32x4*>(arow + 16 * (u0 + u));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc = mfma16x4(a[e], bq[u][e], acc);   // dims 16(u0+u) + 4(l/16) + e
+      }
+    }
+    __syncthreads();                                        // the previous step's Pst, Ds consumed
+#pragma unroll
+    for (int r = 0; r < 4; ++r) Pst[(kind * kBwdRows + 4 * lg + r) * PP + 16 * t + lr] = acc[r];
+    __syncthreads();
+    for (int e = tid; e < kBwdRows * YC; e += kBwdRows * kWave) {
+      const int i = e / YC, yl = e % YC, y = y0 + yl;
+      float dsv = 0.0f;
+      if (x0 + i < nb && y < nb) {
+        float wv = 0.0f;
+        if (!((bm_all[i][y >> 5] >> (y & 31)) & 1u)) {
+          wv = (float)kBlock * exp2f(fmaf(Pst[i * PP + yl], scale, -rowm[i]) * kLog2e);
+          dsv = wv * (Pst[(kBwdRows + i) * PP + yl] - rowd[i]);
+        }
+        const long long gi = bh * nb + x0 + i;
+        Wout[gi * nb + y] = wv;
+        dSout[gi * nb + y] = dsv;
+      }
+      Ds[i * PD + yl] = dsv;
     }
     __syncthreads();
-    if (active) {
-      const int y = y0 + lane;
-      float dsv = 0.0f;
-      if (y < nb) {
-        const bool sel = (bm[y >> 5] >> (y & 31)) & 1u;
-        float wv = 0.0f;
-        if (!sel) {
-          float s = 0.0f, vg = 0.0f;
-#pragma unroll 8
-          for (int c = 0; c < D; ++c) {
-            s = fmaf(Qx[w][c], Kc[lane * PK + c], s);
-            vg = fmaf(Gx[w][c], Vc[lane * PK + c], vg);
-          }
-          wv = (float)kBlock * exp2f(fmaf(s, scale, -mref) * kLog2e);
-          dsv = wv * (vg - dhat);
-        }
-        Wout[g * nb + y] = wv;
-        dSout[g * nb + y] = dsv;
-      }
-      dsl[w][lane] = dsv;
-      wave_lds_sync();
 #pragma unroll
-      for (int q = 0; q < DQ; ++q) {
-        const int dd = lane + kWave * q;
-        if (dd < D) {
-          float a = accq[q];
-          for (int t = 0; t < kBwdChunk; ++t) a = fmaf(dsl[w][t], Kc[t * PK + dd], a);
-          accq[q] = a;
-        }
-      }
+    for (int s = 0; s < YK / 4; ++s) {
+      const int yl = kq * YK + 4 * s + lg, y = y0 + yl;
+      const float b = y < nb ? kh[(long long)y * D + 16 * nt + lr] : 0.0f;
+      accq = mfma16x4(Ds[lr * PD + yl], b, accq);
     }
   }
-  if (active) {
+  __syncthreads();
 #pragma unroll
-    for (int q = 0; q < DQ; ++q) {
-      const int dd = lane + kWave * q;
-      if (dd < D) dqp[g * D + dd] = accq[q] * scale;
+  for (int r = 0; r < 4; ++r) Pst[(kq * kBwdRows + 4 * lg + r) * D + 16 * nt + lr] = accq[r];
+  __syncthreads();
+  if (active) {
+    for (int dd = lane; dd < D; dd += kWave) {
+      float sum = Pst[w * D + dd];
+#pragma unroll
+      for (int q = 1; q < KQ; ++q) sum += Pst[(q * kBwdRows + w) * D + dd];
+      dqp[g * D + dd] = sum * scale;
     }
   }
 }
 
 // ---------------------------------------------------------------------------
-// dK~_y = c sum_x dS~[x,y] Q~_x, dV~_y = sum_x W[x,y] G^_x: one wave per
-// column block, 16 per workgroup; Q~, G^ and the columns of W and dS~ staged
-// through LDS 64 block-rows at a time; rows summed in ascending order.
+// Column pass: dK~_y = c sum_x dS~[x,y] Q~_x and dV~_y = sum_x W[x,y] G^_x for
+// 16 column blocks per workgroup on the float32 matrix cores; one output tile
+// (quantity, 16 dims) per wave and step, the contraction over the block-rows
+// x in ascending order, four per matrix-core step.
 template <int D>
-__global__ __launch_bounds__(kBwdRows * kWave) void bwd_cols_kernel(
+struct ColsCfg {
+  static constexpr int kTiles = 2 * (D / 16);
+  static constexpr int kWaves = kTiles < 8 ? kTiles : 8;
+  static constexpr int kTilesPerWave = kTiles / kWaves;
+};
+
+template <int D>
+__global__ __launch_bounds__(ColsCfg<D>::kWaves * kWave) void bwd_cols_kernel(
     const float* __restrict__ qp, const float* __restrict__ gh, const float* __restrict__ W,
     const float* __restrict__ dS, float* __restrict__ dkp, float* __restrict__ dvp, int nb,
     float scale) {
-  constexpr int PC = kBwdRows + 1;
-  __shared__ float Qc[kBwdChunk][D];
-  __shared__ float Gc[kBwdChunk][D];
-  __shared__ float Wc[kBwdChunk * PC];
-  __shared__ float Sc[kBwdChunk * PC];
-  const int tid = threadIdx.x;
-  const int w = wave_uniform(tid / kWave);
-  const int lane = lane_id();
-  const int groups = (nb + kBwdRows - 1) / kBwdRows;
+  constexpr int NTD = D / 16, TPW = ColsCfg<D>::kTilesPerWave;
+  const int w = wave_uniform(threadIdx.x / kWave);
+  const int lane = lane_id(), lr = lane & 15, lg = lane >> 4;
+  const int groups = (nb + kBwdCols - 1) / kBwdCols;
   const long long lwg = xcd_remap(blockIdx.x, gridDim.x);
   const long long bh = lwg / groups;
-  const int y0 = (int)(lwg - bh * groups) * kBwdRows;
-  const bool active = y0 + w < nb;
+  const int y0 = (int)(lwg - bh * groups) * kBwdCols;
   const long long hb = bh * nb;                             // first block of the head
-  constexpr int DQ = (D + kWave - 1) / kWave;
-  float ak[DQ], av[DQ];
+  const int y = y0 + lr;
 #pragma unroll
-  for (int q = 0; q < DQ; ++q) ak[q] = av[q] = 0.0f;
-  for (int r0 = 0; r0 < nb; r0 += kBwdChunk) {
-    __syncthreads();
-    for (int i = tid; i < kBwdChunk * D; i += kBwdRows * kWave) {
-      const int r = i / D, c = i % D;
-      const bool in = r0 + r < nb;
-      Qc[r][c] = in ? qp[(hb + r0 + r) * D + c] : 0.0f;
-      Gc[r][c] = in ? gh[(hb + r0 + r) * D + c] : 0.0f;
+  for (int tp = 0; tp < TPW; ++tp) {
+    const int tile = w * TPW + tp, kind = tile / NTD, nt = tile % NTD;
+    const float* A = kind ? W : dS;                         // A[y][x] = A[x * nb + y] (column y)
+    const float* B = (kind ? gh : qp) + 16 * nt + lr;
+    f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll 8
+    for (int xs = 0; xs < nb; xs += 4) {
+      const int x = xs + lg;
+      const float a = (x < nb && y < nb) ? A[(hb + x) * nb + y] : 0.0f;
+      const float b = x < nb ? B[(hb + x) * D] : 0.0f;
+      acc = mfma16x4(a, b, acc);
     }
-    for (int i = tid; i < kBwdChunk * kBwdRows; i += kBwdRows * kWave) {
-      const int r = i / kBwdRows, c = i % kBwdRows;
-      const bool in = r0 + r < nb && y0 + c < nb;
-      Wc[r * PC + c] = in ? W[(hb + r0 + r) * nb + y0 + c] : 0.0f;
-      Sc[r * PC + c] = in ? dS[(hb + r0 + r) * nb + y0 + c] : 0.0f;
-    }
-    __syncthreads();
-    if (active) {
+    float* out = kind ? dvp : dkp;
+    const float f = kind ? 1.0f : scale;
 #pragma unroll
-      for (int q = 0; q < DQ; ++q) {
-        const int dd = lane + kWave * q;
-        if (dd < D) {
-          float a = ak[q], b = av[q];
-          for (int r = 0; r < kBwdChunk; ++r) {
-            a = fmaf(Sc[r * PC + w], Qc[r][dd], a);
-            b = fmaf(Wc[r * PC + w], Gc[r][dd], b);
-          }
-          ak[q] = a;
-          av[q] = b;
-        }
-      }
-    }
-  }
-  if (active) {
-#pragma unroll
-    for (int q = 0; q < DQ; ++q) {
-      const int dd = lane + kWave * q;
-      if (dd < D) {
-        dkp[(hb + y0 + w) * D + dd] = ak[q] * scale;
-        dvp[(hb + y0 + w) * D + dd] = av[q];
-      }
+    for (int r = 0; r < 4; ++r) {
+      const int yy = y0 + 4 * lg + r;
+      if (yy < nb) out[(hb + yy) * D + 16 * nt + lr] = acc[r] * f;
     }
   }
 }
@@ -1018,8 +1034,9 @@ static void launch_bwd_t(const BwdArgs& A, hipStream_t stream) {
     bwd_rows_kernel<DT, D, true><<<wg_rows, kBwdRows * kWave, 0, stream>>>(
         A.dout, A.out, A.lse, A.idx, A.qp, A.kp, A.vp, A.ld, A.bits, A.gh, A.W, A.dS, A.dqp, nb,
         A.m, scale);
-    bwd_cols_kernel<D><<<wg_rows, kBwdRows * kWave, 0, stream>>>(A.qp, A.gh, A.W, A.dS, A.dkp,
-                                                                 A.dvp, nb, scale);
+    const unsigned wg_cols = (unsigned)(A.bh * ((nb + kBwdCols - 1) / kBwdCols));
+    bwd_cols_kernel<D><<<wg_cols, ColsCfg<D>::kWaves * kWave, 0, stream>>>(
+        A.qp, A.gh, A.W, A.dS, A.dkp, A.dvp, nb, scale);
     launch_tiles_t<DT, D, true>(A, stream);
   } else {
     bwd_rows_kernel<DT, D, false><<<wg_rows, kBwdRows * kWave, 0, stream>>>(
