@@ -3,9 +3,11 @@
 // pairwise halvings of a 32-row block equal its plain mean).
 //
 // HBM-bound: every input byte is read once, 1/32 of it is written back.
-// One thread owns one 16-byte column chunk of one 32-row block and walks its
-// 32 rows; a wave's load covers whole 128-byte row segments of consecutive
-// blocks, so every HBM line fetched is fully used. No LDS, no barriers.
+// Two threads own one 16-byte column chunk of one 32-row block: one sums rows
+// 0..15, the other rows 16..31 (each in row order, float32), and the mean is
+// (first half + second half) / 32. A wave's load covers whole 128-byte row
+// segments, so every HBM line fetched is fully used; two threads per chunk
+// keep enough waves in flight to fill the GPU. No LDS, no barriers.
 //
 // Optionally K and V are also written in the tile kernel's matrix-core operand
 // order ("packed K/V", layout in kernels.h), so every operand load of the tile
@@ -31,37 +33,44 @@ __global__ __launch_bounds__(256) void pool_kernel(const void* __restrict__ x0,
   if (y == nullptr) return;
   constexpr int kPer = DT == BF16 ? 8 : 4;        // elements per 16-byte chunk
   const long long t = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= chunks) return;
   const int cpr = d / kPer;                        // chunks per row
-  const long long blk = t / cpr;
-  const int c = (int)(t - blk * cpr);
-  const long long row0 = blk * kBlock;             // first row of the block (all heads flattened)
-  const u32x4* base = reinterpret_cast<const u32x4*>(x) + row0 * cpr + c;
-
+  // thread t: block t / (2 cpr); within it, half (rows 16 half ..) and chunk
+  const long long blk = t / (2 * cpr);
+  const int i = (int)(t - blk * 2 * cpr), half = i / cpr, c = i - half * cpr;
+  const bool active = t < 2 * chunks;              // whole (block, chunk) pairs: 2 cpr divides 64
   float acc[kPer];
 #pragma unroll
   for (int e = 0; e < kPer; ++e) acc[e] = 0.0f;
+  if (active) {
+    const long long row0 = blk * kBlock + 16 * half;   // all heads flattened
+    const u32x4* base = reinterpret_cast<const u32x4*>(x) + row0 * cpr + c;
 #pragma unroll 8
-  for (int r = 0; r < kBlock; ++r) {
-    const u32x4 w = base[(long long)r * cpr];
-    if constexpr (DT == BF16) {
+    for (int r = 0; r < 16; ++r) {
+      const u32x4 w = base[(long long)r * cpr];
+      if constexpr (DT == BF16) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        acc[2 * e] += bf16_to_f32(w[e] & 0xFFFFu);
-        acc[2 * e + 1] += bf16_to_f32(w[e] >> 16);
+        for (int e = 0; e < 4; ++e) {
+          acc[2 * e] += bf16_to_f32(w[e] & 0xFFFFu);
+          acc[2 * e + 1] += bf16_to_f32(w[e] >> 16);
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[e] += __uint_as_float(w[e]);
       }
-    } else {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) acc[e] += __uint_as_float(w[e]);
     }
   }
+  // the second half's sums, from lane + cpr of the same wave
+  float hi[kPer];
+#pragma unroll
+  for (int e = 0; e < kPer; ++e) hi[e] = __shfl_down(acc[e], cpr);
+  if (!active || half != 0) return;
   constexpr float inv = 1.0f / kBlock;             // exact: power of two
   f32x4* out = reinterpret_cast<f32x4*>(y + blk * d + c * kPer);
 #pragma unroll
   for (int v = 0; v < kPer / 4; ++v) {
     f32x4 o;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) o[e] = acc[4 * v + e] * inv;
+    for (int e = 0; e < 4; ++e) o[e] = (acc[4 * v + e] + hi[4 * v + e]) * inv;
     out[v] = o;
   }
 }
@@ -96,34 +105,39 @@ __global__ __launch_bounds__(256) void pool_pack_kernel(PackJobs jobs, long long
     for (int ci = tid; ci < NBLK * CPB; ci += 256)
       if (ci < nblk * CPB) tile[ci] = src[b0 * CPB + ci];
     __syncthreads();
-    // block means: one thread per (block, column chunk), rows in order
+    // block means: one thread per (block, column chunk); rows 0..15 and
+    // 16..31 summed in order, then added (pool_kernel's arithmetic)
     if (pooled != nullptr) {
       for (int pc = tid; pc < nblk * CPR; pc += 256) {
         const int bl = pc / CPR, c = pc % CPR;
-        float acc[kPer];
+        float acc[2][kPer];
 #pragma unroll
-        for (int e = 0; e < kPer; ++e) acc[e] = 0.0f;
+        for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+          for (int e = 0; e < kPer; ++e) acc[hh][e] = 0.0f;
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
 #pragma unroll 8
-        for (int r = 0; r < kBlock; ++r) {
-          const u32x4 w = tile[bl * CPB + r * CPR + c];
-          if constexpr (DT == BF16) {
+          for (int r = 16 * hh; r < 16 * hh + 16; ++r) {
+            const u32x4 w = tile[bl * CPB + r * CPR + c];
+            if constexpr (DT == BF16) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              acc[2 * e] += bf16_to_f32(w[e] & 0xFFFFu);
-              acc[2 * e + 1] += bf16_to_f32(w[e] >> 16);
+              for (int e = 0; e < 4; ++e) {
+                acc[hh][2 * e] += bf16_to_f32(w[e] & 0xFFFFu);
+                acc[hh][2 * e + 1] += bf16_to_f32(w[e] >> 16);
+              }
+            } else {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) acc[hh][e] += __uint_as_float(w[e]);
             }
-          } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) acc[e] += __uint_as_float(w[e]);
           }
-        }
         constexpr float inv = 1.0f / kBlock;
         f32x4* out = reinterpret_cast<f32x4*>(pooled + (b0 + bl) * D + c * kPer);
 #pragma unroll
         for (int q = 0; q < kPer / 4; ++q) {
           f32x4 o;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) o[e] = acc[4 * q + e] * inv;
+          for (int e = 0; e < 4; ++e) o[e] = (acc[0][4 * q + e] + acc[1][4 * q + e]) * inv;
           out[q] = o;
         }
       }
@@ -202,7 +216,7 @@ hipError_t launch_pool(const void* q, const void* k, const void* v, float* qp, f
   const int per = dtype == BF16 ? 8 : 4;
   const long long chunks = bh * (n / kBlock) * (d / per);
   const int threads = 256;
-  const long long blocks = (chunks + threads - 1) / threads;
+  const long long blocks = (2 * chunks + threads - 1) / threads;   // two threads per chunk
   dim3 grid((unsigned)blocks, 3);
   if (dtype == BF16)
     pool_kernel<BF16><<<grid, threads, 0, stream>>>(q, k, v, qp, kp, vp, chunks, d);

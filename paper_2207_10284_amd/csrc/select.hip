@@ -199,19 +199,33 @@ __global__ __launch_bounds__(kRows / RPW * kWave) void rows_kernel(
       int need = 0;
       const bool all = (m == nb), none = (m == 0);
       if (!all && !none) {
-        for (int bit = 31; bit >= 0; --bit) {
+        // Every valid key shares the bits above the highest bit in which the
+        // row's largest and smallest keys differ, so the search starts there
+        // with those bits set. Unused registers hold key 0, below every
+        // candidate, so the counts need no range checks.
+        float smax = -INFINITY, smin = INFINITY;
+#pragma unroll
+        for (int j = 0; j < JMAX; ++j)
+          if (j < J && kChunk * j + lane < nb) {
+            smax = fmaxf(smax, s[i][j]);
+            smin = fminf(smin, s[i][j]);
+          }
+        const uint32_t kmax = __builtin_amdgcn_readfirstlane(ordered_key(wave_max(smax)));
+        const uint32_t kmin = __builtin_amdgcn_readfirstlane(ordered_key(-wave_max(-smin)));
+        const uint32_t diff = kmax ^ kmin;
+        const int top = diff ? 31 - __builtin_clz(diff) : -1;
+        T = top >= 0 ? kmax & ~((2u << top) - 1u) : kmax;
+        for (int bit = top; bit >= 0; --bit) {
           const uint32_t cand = T | (1u << bit);
           int cnt = 0;
 #pragma unroll
-          for (int j = 0; j < JMAX; ++j)
-            if (j < J) cnt += __popcll(__ballot(key[j] >= cand));
+          for (int j = 0; j < JMAX; ++j) cnt += __popcll(__ballot(key[j] >= cand));
           if (cnt >= m) T = cand;
           if (cnt == m) break;               // exactly the m largest are >= T
         }
         int gt = 0;
 #pragma unroll
-        for (int j = 0; j < JMAX; ++j)
-          if (j < J) gt += __popcll(__ballot(key[j] > T));
+        for (int j = 0; j < JMAX; ++j) gt += __popcll(__ballot(key[j] > T));
         need = m - gt;                       // keys equal to T still to take
       }
       int eq_seen = 0, written = 0;
