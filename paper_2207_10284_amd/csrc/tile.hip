@@ -42,13 +42,19 @@ namespace mra {
 // are exp2(s * c * log2(e) - mrun) for the row's reference mrun, which need
 // not be the running max: any reference works as long as weights and
 // accumulators stay finite, because the final normalisation uses the same
-// reference. mrun is set to the exact max of the row's first tile; later tiles
-// only check that their weights sum to at most 2^kWeightCap per lane (far
-// inside float32 and bfloat16 range, 2^128, even summed over 65536 keys). If
-// a tile exceeds it, the row is computed again with the exact max over all its
-// tiles as the reference, where no weight exceeds 1. The loop body thus has no
-// 16-way max, no cross-lane exchange and no branch that rescales O.
+// reference. mrun is set to the exact max of the row's first tile plus
+// kRefMargin; later tiles only check that their weights sum to at most
+// 2^kWeightCap per lane (far inside float32 and bfloat16 range, 2^128, even
+// summed over 65536 keys). If a tile exceeds it, the row is computed again with
+// the exact max over all its tiles as the reference, where no weight exceeds 1.
+// The loop body thus has no 16-way max, no cross-lane exchange and no branch
+// that rescales O. The margin makes that restart rare: a later logit must
+// exceed the first tile's max by 96 (log2 units, 66.5 nats) to trigger it,
+// while the row's largest weight stays at least 2^-32, far above the float32
+// and bfloat16 underflow threshold 2^-126 (and bfloat16 rounding is relative,
+// so the precision of the weights does not change).
 constexpr float kWeightCap = 0x1p64f;
+constexpr float kRefMargin = 32.0f;
 
 __device__ __forceinline__ float tile_max(const f32x16& s) {
   float a = s[0];
@@ -144,7 +150,7 @@ struct TileRow {
   template <class VA>
   __device__ __forceinline__ bool accumulate(const f32x16& s, bool use, bool check, VA va) {
     if (first && use) {                              // wave-uniform: the row's first tile
-      mrun = tile_ref(s);
+      mrun = tile_ref(s) + kRefMargin;
       first = false;
     }
     float t;
