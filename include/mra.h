@@ -319,7 +319,8 @@ mra_status_t mra_attention_forward_multilevel(const void* q, const void* k, cons
 
 /*
  * mra_backward_workspace_bytes — device workspace of mra_attention_backward:
- * seven rearranged copies of Q, K, V and dZ (7*B*H*n*d*elem bytes), pooled
+ * seven rearranged copies of Q, K, V and dZ (7*B*H*n*d*elem bytes; none for
+ * bfloat16 with d <= 64, whose gradient passes read the inputs' rows), pooled
  * rows and their gradients, two float32 values per query, the selection as a
  * bitmap and two float32 nb x nb grids per head (W and dS~ below). 0 for
  * invalid or unsupported arguments.

@@ -127,7 +127,9 @@ WsBwd ws_bwd(long long bh, int nb, int d, mra_dtype_t dtype) {
   WsBwd L{};
   size_t off = 0;
   const size_t pooled = align256((size_t)bh * nb * d * sizeof(float));
-  const size_t packed = align256((size_t)bh * nb * kBlockSize * d * (dtype == MRA_BF16 ? 2 : 4));
+  // packed operand copies: not for bfloat16 with d <= 64 (raw tiles)
+  const bool raw = dtype == MRA_BF16 && d <= 64;
+  const size_t packed = raw ? 0 : align256((size_t)bh * nb * kBlockSize * d * (dtype == MRA_BF16 ? 2 : 4));
   const size_t grid = align256((size_t)bh * nb * nb * sizeof(float));
   L.qp = off; off += pooled;
   L.kp = off; off += pooled;

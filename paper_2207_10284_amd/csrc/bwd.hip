@@ -808,20 +808,100 @@ struct TrChunks {
   }
 };
 
-// dQ (bf16): one wave per block-row; a slot holds K_y and V_y in the row
-// layout (K^T is read transposed from the K part).
+// bfloat16, d <= 64: the passes read raw 32-row tiles of the inputs
+// themselves, no packed copies. A tile (32 consecutive rows, 2d bytes each) is
+// copied with direct-to-LDS loads of whole rows, every lane fetching the
+// 16-byte block that belongs at its LDS position under an XOR swizzle of the
+// blocks within a row (raw_offset / raw_copy_offset), and read both in the row
+// layout (ds_read_b128: 16 lanes = 16 rows per pass) and transposed
+// (ds_read_b64_tr_b16: 32 lanes = 4 rows x 64 bytes per pass). One swizzle
+// serves both: for d = 64 the even rows of 16 consecutive rows take 8
+// different block positions, and so do the odd ones (row reads), and rows r
+// and r + 2 of a group of four take positions in opposite halves of the row
+// (transposed reads); for d = 32 rows r, r + 4, r + 8, r + 12 take 4
+// different positions. The swizzle has period 16 in the row, so the
+// transposed reads 16 rows further use the same lane address plus an
+// immediate offset; reads 8 rows further need a second address. The copy
+// offsets repeat with period 2 (d = 64) or 1 (d = 32) in the copy index.
+template <int D>
+__host__ __device__ constexpr int raw_swz_b(int r) {
+  return D == 64 ? 4 * ((r >> 1) & 1) + ((r >> 2) & 3) : (r >> 2) & 3;
+}
+
+// This lane's offsets for the raw tiles of the gradient passes.
+template <int D>
+struct RawB {
+  static constexpr int KC = D / 16, NT = D / 32;
+  static constexpr int TB = 64 * D;                           // bytes of a 32-row tile
+  static constexpr int KP = D == 64 ? 2 : 1;                  // period of the copy offsets
+  int c0, c1;                                                 // copy sources: even, odd copies (less 1 KB)
+  uint32_t rr[KC];                                            // row-layout chunk c
+  uint32_t tr[NT][2];                                         // transposed column tile t, half e
+  __device__ __forceinline__ void init() {
+    const int lane = lane_id(), h = lane >> 5, j = lane & 31, i16 = lane & 15;
+    c0 = raw_copy_offset<D, raw_swz_b<D>>(0, lane);
+    c1 = KP == 2 ? raw_copy_offset<D, raw_swz_b<D>>(1, lane) - 1024 : c0;
+#pragma unroll
+    for (int c = 0; c < KC; ++c) rr[c] = (uint32_t)raw_offset<D, raw_swz_b<D>>(j, (D / 2) * h + 8 * c);
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int e = 0; e < 2; ++e)
+        tr[t][e] = (uint32_t)raw_offset<D, raw_swz_b<D>>(4 * h + i16 / 4 + 8 * e,
+                                                         32 * t + 16 * ((lane >> 4) & 1) + 4 * (i16 & 3));
+  }
+};
+
+// Two raw tiles (sources a and b, LDS destinations as and bs), C 1 KB copies each.
+template <int C, int KP>
+__device__ __forceinline__ void copy_raw_pair(gptr_t a0, gptr_t a1, gptr_t b0, gptr_t b1, lptr_t as,
+                                              lptr_t bs) {
+  if constexpr (C > 0) {
+    copy_raw_pair<C - 1, KP>(a0, a1, b0, b1, as, bs);
+    constexpr int i = C - 1;
+    __builtin_amdgcn_global_load_lds((KP == 2 && (i & 1)) ? a1 : a0, as, 16, i * 1024, 0);
+    __builtin_amdgcn_global_load_lds((KP == 2 && (i & 1)) ? b1 : b0, bs, 16, i * 1024, 0);
+  }
+}
+
+// Row-layout chunks of the raw tile at base + OFF.
+template <int OFF, int KC>
+__device__ __forceinline__ void raw_rows(uint32_t base, const uint32_t (&rr)[KC], u32x4 (&v)[KC]) {
+#pragma unroll
+  for (int c = 0; c < KC; ++c) v[c] = lds_read16<OFF>(base + rr[c]);
+}
+
+// Transposed chunks c = u*NT + t (c < VC) of the raw tile at base + OFF: two
+// transposing reads each, the halves 8 rows apart, 16 u rows further on.
+template <int D, int OFF, int C, int VC>
+struct RawTrB {
+  static constexpr int NT = D / 32;
+  static __device__ __forceinline__ void run(uint32_t base, const uint32_t (&tr)[NT][2], u32x4* v) {
+    if constexpr (C < VC) {
+      constexpr int u = C / NT, t = C % NT, o = OFF + 16 * u * 2 * D;
+      const u32x2 a = lds_read_tr16<o>(base + tr[t][0]);
+      const u32x2 b = lds_read_tr16<o>(base + tr[t][1]);
+      v[C] = u32x4{a[0], a[1], b[0], b[1]};
+      RawTrB<D, OFF, C + 1, VC>::run(base, tr, v);
+    }
+  }
+};
+
+// dQ (bf16, d <= 64): one wave per block-row; a slot holds the raw tiles K_y
+// and V_y (K^T is read transposed from the K tile).
 template <int D, bool COARSE, int WAVES>
 __global__ __launch_bounds__(WAVES * kWave) void bwd_dq_tr_kernel(
-    const void* __restrict__ qin, const void* __restrict__ gin, const void* __restrict__ krow,
-    const void* __restrict__ vrow, const int32_t* __restrict__ idx,
+    const void* __restrict__ qin, const void* __restrict__ gin, const void* __restrict__ kin,
+    const void* __restrict__ vin, const int32_t* __restrict__ idx,
     const float* __restrict__ ld, const float* __restrict__ dqp, void* __restrict__ dq, int nb,
     int m, long long rows, float scale, float scale_log2) {
   using Cfg = TileCfg<BF16, D>;
   using elem = typename Cfg::elem;
+  using R = RawB<D>;
   constexpr int KC = Cfg::kKChunks, VC = Cfg::kVChunks, NT = Cfg::kNT;
-  constexpr int N = 2 * KC;                                 // loads per tile
-  constexpr int SLOT = N * kChunkStride;
-  static_assert(KC <= 4 && VC <= 4, "chunk offsets fit the immediate field");
+  constexpr int TB = R::TB, N = 2 * KC;                     // loads per tile
+  constexpr int SLOT = 2 * TB;
+  static_assert(KC == R::KC && KC <= 4 && VC <= 4, "raw tiles of d <= 64");
   __shared__ __attribute__((aligned(16))) unsigned char slots[WAVES][2][SLOT];
   extern __shared__ int32_t sidx_all[];
   const int w = wave_uniform(threadIdx.x / kWave);
@@ -842,15 +922,15 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dq_tr_kernel(
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[t][r] = 0.0f;
 
-  const unsigned loff = lane * 16u;
-  const char* ks = static_cast<const char*>(krow) + (size_t)bh * nb * KC * 1024 + loff;
-  const char* vs = static_cast<const char*>(vrow) + (size_t)bh * nb * KC * 1024 + loff;
+  R ro;
+  ro.init();
+  const char* kh = static_cast<const char*>(kin) + (size_t)bh * nb * TB;
+  const char* vh = static_cast<const char*>(vin) + (size_t)bh * nb * TB;
   const uint32_t a0 = lds_addr(slots[w][0]);
-  const uint32_t trl = tr_lane_offset<D>();
   auto issue = [&](int y, int sl) {
     const lptr_t dst = (lptr_t)slots[w][sl];
-    load_chunks_lds_padded<KC>((gptr_t)(ks + (size_t)y * KC * 1024), dst);
-    load_chunks_lds_padded<KC>((gptr_t)(vs + (size_t)y * KC * 1024), dst + KC * kChunkStride);
+    const gptr_t kt = (gptr_t)(kh + (size_t)y * TB), vt = (gptr_t)(vh + (size_t)y * TB);
+    copy_raw_pair<KC, R::KP>(kt + ro.c0, kt + ro.c1, vt + ro.c0, vt + ro.c1, dst, dst + TB);
   };
   if (cnt > 0) issue(wave_uniform(myidx[0]), 0);
   if (cnt > 1) issue(wave_uniform(myidx[1]), 1);
@@ -859,9 +939,9 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dq_tr_kernel(
     else wait_loads<0>();
     const uint32_t base = a0 + (uint32_t)((i & 1) * SLOT);
     u32x4 kf[KC], vf[KC], tf[VC];
-    LdsChunksPadded<0, KC, 0>::run(base + loff, kf);
-    LdsChunksPadded<0, KC, KC>::run(base + loff, vf);
-    TrChunks<D, 0, VC>::run(base + trl, tf);
+    raw_rows<0>(base, ro.rr, kf);
+    raw_rows<TB>(base, ro.rr, vf);
+    RawTrB<D, 0, 0, VC>::run(base, ro.tr, tf);
     lds_done(kf);
     lds_done(vf);
     lds_done(tf);
@@ -880,21 +960,23 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dq_tr_kernel(
                        COARSE ? dqp + g * D : nullptr);
 }
 
-// dK, dV (bf16): one wave per column block; a slot holds Q_x and G_x in the
-// row layout and block-row x's record (Q^T and G^T are read transposed).
+// dK, dV (bf16, d <= 64): one wave per column block; a slot holds the raw
+// tiles Q_x and G_x and block-row x's record (Q^T and G^T are read
+// transposed).
 template <int D, bool COARSE, int WAVES>
 __global__ __launch_bounds__(WAVES * kWave) void bwd_dkdv_tr_kernel(
-    const void* __restrict__ kin, const void* __restrict__ vin, const void* __restrict__ qrow,
-    const void* __restrict__ grow, const uint32_t* __restrict__ bits,
+    const void* __restrict__ kin, const void* __restrict__ vin, const void* __restrict__ qin,
+    const void* __restrict__ gin, const uint32_t* __restrict__ bits,
     const float* __restrict__ ld, const float* __restrict__ dkp, const float* __restrict__ dvp,
     void* __restrict__ dk, void* __restrict__ dv, int nb, long long rows, float scale,
     float scale_log2) {
   using Cfg = TileCfg<BF16, D>;
   using elem = typename Cfg::elem;
+  using R = RawB<D>;
   constexpr int KC = Cfg::kKChunks, VC = Cfg::kVChunks, NT = Cfg::kNT;
-  constexpr int N = 2 * KC + 1;                             // loads per tile
-  constexpr int SLOT = 2 * KC * kChunkStride + 256;
-  static_assert(KC <= 4 && VC <= 4, "chunk offsets fit the immediate field");
+  constexpr int TB = R::TB, N = 2 * KC + 1;                 // loads per tile
+  constexpr int SLOT = 2 * TB + 256;
+  static_assert(KC == R::KC && KC <= 4 && VC <= 4, "raw tiles of d <= 64");
   __shared__ __attribute__((aligned(16))) unsigned char slots[WAVES][2][SLOT];
   extern __shared__ int32_t sidx_all[];
   const int w = wave_uniform(threadIdx.x / kWave);
@@ -928,18 +1010,18 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dkdv_tr_kernel(
 #pragma unroll
     for (int r = 0; r < 16; ++r) ak[t][r] = av[t][r] = 0.0f;
 
-  const unsigned loff = lane * 16u;
-  const char* qs = static_cast<const char*>(qrow) + (size_t)hb * KC * 1024 + loff;
-  const char* gs = static_cast<const char*>(grow) + (size_t)hb * KC * 1024 + loff;
+  R ro;
+  ro.init();
+  const char* qh = static_cast<const char*>(qin) + (size_t)hb * TB;
+  const char* gh = static_cast<const char*>(gin) + (size_t)hb * TB;
   const char* xs = reinterpret_cast<const char*>(ld + hb * 64) + lane * 4u;
   const uint32_t a0 = lds_addr(slots[w][0]);
-  const uint32_t trl = tr_lane_offset<D>();
-  const uint32_t xl = (uint32_t)(2 * KC * kChunkStride) + 16u * h;   // this half's queries in the record
+  const uint32_t xl = (uint32_t)(2 * TB) + 16u * h;        // this half's queries in the record
   auto issue = [&](int x, int sl) {
     const lptr_t dst = (lptr_t)slots[w][sl];
-    load_chunks_lds_padded<KC>((gptr_t)(qs + (size_t)x * KC * 1024), dst);
-    load_chunks_lds_padded<KC>((gptr_t)(gs + (size_t)x * KC * 1024), dst + KC * kChunkStride);
-    __builtin_amdgcn_global_load_lds((gptr_t)(xs + (size_t)x * 256), dst + 2 * KC * kChunkStride, 4, 0, 0);
+    const gptr_t qt = (gptr_t)(qh + (size_t)x * TB), gt = (gptr_t)(gh + (size_t)x * TB);
+    copy_raw_pair<KC, R::KP>(qt + ro.c0, qt + ro.c1, gt + ro.c0, gt + ro.c1, dst, dst + TB);
+    __builtin_amdgcn_global_load_lds((gptr_t)(xs + (size_t)x * 256), dst + 2 * TB, 4, 0, 0);
   };
   if (cnt > 0) issue(wave_uniform(myx[0]), 0);
   if (cnt > 1) issue(wave_uniform(myx[1]), 1);
@@ -948,10 +1030,10 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dkdv_tr_kernel(
     else wait_loads<0>();
     const uint32_t base = a0 + (uint32_t)((i & 1) * SLOT);
     u32x4 qa[KC], ga[KC], qt[VC], gtc[VC], xr[8];
-    LdsChunksPadded<0, KC, 0>::run(base + loff, qa);
-    LdsChunksPadded<0, KC, KC>::run(base + loff, ga);
-    TrChunks<D, 0, VC>::run(base + trl, qt);
-    TrChunks<D, 0, VC>::run(base + KC * kChunkStride + trl, gtc);
+    raw_rows<0>(base, ro.rr, qa);
+    raw_rows<TB>(base, ro.rr, ga);
+    RawTrB<D, 0, 0, VC>::run(base, ro.tr, qt);
+    RawTrB<D, TB, 0, VC>::run(base, ro.tr, gtc);
     xr[0] = lds_read16<0>(base + xl);
     xr[1] = lds_read16<32>(base + xl);
     xr[2] = lds_read16<64>(base + xl);
@@ -1001,11 +1083,11 @@ static void launch_tiles_t(const BwdArgs& A, hipStream_t stream) {
   constexpr int W = kBwdTileWaves;
   if constexpr (DT == BF16 && Cfg::kKChunks <= 4 && Cfg::kVChunks <= 4) {
     bwd_dq_tr_kernel<D, COARSE, W><<<wgs, W * kWave, smem_dq, stream>>>(
-        A.q, A.dout, A.k_row, A.v_row, A.idx, A.ld, A.dqp, A.dq, nb, A.m, rows, scale, scale_log2);
+        A.q, A.dout, A.k, A.v, A.idx, A.ld, A.dqp, A.dq, nb, A.m, rows, scale, scale_log2);
     // one wave per workgroup: column lists differ in length (a workgroup
     // keeps its LDS until its longest list is done), rows all have m tiles
     bwd_dkdv_tr_kernel<D, COARSE, 1><<<(unsigned)rows, kWave, nb * sizeof(int32_t), stream>>>(
-        A.k, A.v, A.q_row, A.g_row, A.bits, A.ld, A.dkp, A.dvp, A.dk, A.dv, nb, rows, scale,
+        A.k, A.v, A.q, A.dout, A.bits, A.ld, A.dkp, A.dvp, A.dk, A.dv, nb, rows, scale,
         scale_log2);
   } else if constexpr (Cfg::kKChunks <= 4 && Cfg::kVChunks <= 4) {
     bwd_dq_stream_kernel<DT, D, COARSE, W><<<wgs, W * kWave, smem_dq, stream>>>(
@@ -1047,15 +1129,19 @@ static void launch_bwd_t(const BwdArgs& A, hipStream_t stream) {
 }
 
 hipError_t launch_bwd(const BwdArgs& A, hipStream_t stream) {
-  // pooled rows and packed operands of Q, K, V and G = dZ; the transposed
-  // copies only where the tile passes read them (not bf16 d <= 64, whose
-  // passes transpose in LDS)
-  const bool tr = A.dtype == BF16 && A.d <= 64;
-  const PackJob jobs[4] = {{A.q, A.coarse ? A.qp : nullptr, A.q_row, tr ? nullptr : A.q_t},
-                           {A.k, A.coarse ? A.kp : nullptr, A.k_row, tr ? nullptr : A.k_t},
-                           {A.v, A.coarse ? A.vp : nullptr, A.v_row, nullptr},
-                           {A.dout, nullptr, A.g_row, tr ? nullptr : A.g_t}};
-  const hipError_t e = launch_pack(jobs, 4, A.bh, A.n, A.d, A.dtype, stream);
+  hipError_t e = hipSuccess;
+  if (A.dtype == BF16 && A.d <= 64) {
+    // the tile passes read raw tiles of Q, K, V and G = dZ: only the pooled
+    // rows of the coarse term
+    if (A.coarse) e = launch_pool(A.q, A.k, A.v, A.qp, A.kp, A.vp, nullptr, A.bh, A.n, A.d, A.dtype, stream);
+  } else {
+    // pooled rows and packed operands of Q, K, V and G = dZ
+    const PackJob jobs[4] = {{A.q, A.coarse ? A.qp : nullptr, A.q_row, A.q_t},
+                             {A.k, A.coarse ? A.kp : nullptr, A.k_row, A.k_t},
+                             {A.v, A.coarse ? A.vp : nullptr, A.v_row, nullptr},
+                             {A.dout, nullptr, A.g_row, A.g_t}};
+    e = launch_pack(jobs, 4, A.bh, A.n, A.d, A.dtype, stream);
+  }
   if (e != hipSuccess) return e;
   if (A.dtype == BF16) {
     if (A.d == 32) launch_bwd_t<BF16, 32>(A, stream);

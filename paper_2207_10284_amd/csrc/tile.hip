@@ -430,19 +430,6 @@ template <int D>
 __host__ __device__ constexpr int raw_swz_v(int r) {
   return D == 64 ? ((r >> 1) & 1) << 2 : 0;
 }
-// byte offset of element (r, c) of a raw bf16 tile in LDS under swizzle F
-template <int D, int (*F)(int)>
-__host__ __device__ constexpr int raw_offset(int r, int c) {
-  return r * (2 * D) + ((((2 * c) >> 4) ^ F(r)) << 4) + ((2 * c) & 15);
-}
-
-// Source byte offset (within the tile) of the 16 bytes lane `lane` copies to
-// LDS byte i * 1024 + 16 lane under swizzle F.
-template <int D, int (*F)(int)>
-__device__ __forceinline__ int raw_copy_offset(int i, int lane) {
-  const int q = i * 1024 + 16 * lane, r = q / (2 * D), blk = (q % (2 * D)) / 16;
-  return r * (2 * D) + ((blk ^ F(r)) << 4);
-}
 
 // The C 1 KB copies of a raw K tile and of a raw V tile. The swizzled source
 // offsets repeat with period KP in the copy index for K (the swizzle of row r

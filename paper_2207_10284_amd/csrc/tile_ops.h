@@ -167,6 +167,24 @@ __device__ __forceinline__ u32x2 lds_read_tr16(uint32_t addr) {
 typedef const __attribute__((address_space(1))) char* gptr_t;
 typedef __attribute__((address_space(3))) char* lptr_t;
 
+// Raw bfloat16 tiles in LDS (d <= 64): a 32-row tile of consecutive rows
+// (2d bytes each) copied with direct-to-LDS loads whose lanes each fetch the
+// 16-byte block that belongs at their LDS position under an XOR swizzle F of
+// the blocks within a row: block b of row r sits at block b ^ F(r).
+// Byte offset of element (r, c) of such a tile in LDS:
+template <int D, int (*F)(int)>
+__host__ __device__ constexpr int raw_offset(int r, int c) {
+  return r * (2 * D) + ((((2 * c) >> 4) ^ F(r)) << 4) + ((2 * c) & 15);
+}
+
+// Source byte offset (within the tile) of the 16 bytes lane `lane` copies to
+// LDS byte i * 1024 + 16 lane under swizzle F.
+template <int D, int (*F)(int)>
+__device__ __forceinline__ int raw_copy_offset(int i, int lane) {
+  const int q = i * 1024 + 16 * lane, r = q / (2 * D), blk = (q % (2 * D)) / 16;
+  return r * (2 * D) + ((blk ^ F(r)) << 4);
+}
+
 // Copies a list of m block ids into LDS keeping only the entries in [0, nb),
 // in their order, and returns how many there are (wave-uniform). Reading the
 // ids from LDS keeps them off the vector-memory counter, so prefetched loads

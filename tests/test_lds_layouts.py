@@ -115,3 +115,99 @@ def test_unswizzled_rows_would_conflict():
     none = lambda d, r: 0
     addrs = [offset(64, lane % 32, 32 * (lane // 32), none) for lane in range(16)]
     assert conflict_ways(addrs, 16) == 8
+
+
+# ---------------------------------------------------------------------------
+# The gradient passes read each raw tile twice: in the row layout
+# (ds_read_b128, as K above) and transposed (ds_read_b64_tr_b16, as V above).
+# One swizzle serves both (csrc/bwd.hip, raw_swz_b): for d = 64 block b of row
+# r sits at b ^ (4 ((r >> 1) & 1) + ((r >> 2) & 3)), for d = 32 at
+# b ^ ((r >> 2) & 3).
+
+def swz_b(d, r):
+    return 4 * ((r >> 1) & 1) + ((r >> 2) & 3) if d == 64 else (r >> 2) & 3
+
+
+@pytest.mark.parametrize("d", [32, 64])
+def test_b_copies_cover_whole_rows_once(d):
+    rb = 2 * d
+    sources = set()
+    for i in range(32 * rb // 1024):
+        rows = set()
+        for p in range(64):
+            q = i * 1024 + 16 * p
+            r, slot = q // rb, (q % rb) // 16
+            blk = slot ^ swz_b(d, r)
+            assert 0 <= blk < rb // 16
+            rows.add(r)
+            sources.add(r * rb + 16 * blk)
+            assert offset(d, r, 8 * blk, swz_b) == q
+        assert len(rows) * rb == 1024
+    assert len(sources) == 32 * rb // 16
+    # the per-lane source offsets repeat with period 2 (d = 64) or 1 (d = 32)
+    # in the copy index, up to the 1 KB step of the load's immediate offset
+    period = 2 if d == 64 else 1
+    for i in range(period, 32 * rb // 1024):
+        for p in range(64):
+            def src(ii):
+                q = ii * 1024 + 16 * p
+                r, slot = q // rb, (q % rb) // 16
+                return r * rb + 16 * (slot ^ swz_b(d, r))
+            assert src(i) - src(i - period) == period * 1024
+
+
+@pytest.mark.parametrize("d", [32, 64])
+def test_b_row_reads(d):
+    """Chunk s of lane (h, j) = X[j][(d/2)h + 8s .. +7], conflict-free."""
+    for s in range(d // 16):
+        addrs = []
+        for lane in range(64):
+            h, j = lane // 32, lane % 32
+            a = offset(d, j, (d // 2) * h + 8 * s, swz_b)
+            for e in range(8):
+                assert offset(d, j, (d // 2) * h + 8 * s + e, swz_b) == a + 2 * e
+            addrs.append(a)
+        for p0 in range(0, 64, 16):
+            assert conflict_ways(addrs[p0:p0 + 16], 16) == 1
+
+
+@pytest.mark.parametrize("d", [32, 64])
+def test_b_transposed_reads(d):
+    """Transposed chunk (u, t) of lane l = 32h + j: X[16u + 8(s/4) + 4h + s%4]
+    [32t + j], s = 0..7, from two transposing reads (half e = s/4). Each lane
+    supplies row 4h + (l%16)/4 + 8e (+16u), columns 32t + 16((l/16)&1) +
+    4(l%4) .. +3; the address for +16 rows is the one for +0 plus 16 rows'
+    bytes (an immediate offset), the two halves need one address each.
+    Conflict-free in every 32-lane pass."""
+    rb = 2 * d
+    for u in range(2):
+        for t in range(d // 32):
+            for e in range(2):
+                sup = []
+                for lane in range(64):
+                    i = lane % 16
+                    row = 16 * u + 8 * e + 4 * (lane // 32) + i // 4
+                    col = 32 * t + 16 * ((lane // 16) & 1) + 4 * (i % 4)
+                    a = offset(d, row, col, swz_b)
+                    assert a == offset(d, row - 16 * u, col, swz_b) + 16 * u * rb
+                    for c in range(4):
+                        assert offset(d, row, col + c, swz_b) == a + 2 * c
+                    sup.append((row, col, a))
+                for lane in range(64):
+                    g0, i = lane - lane % 16, lane % 16
+                    for k in range(4):
+                        row, col, _ = sup[g0 + 4 * k + i // 4]
+                        assert (row, col + i % 4) == (16 * u + 8 * e + 4 * (lane // 32) + k, 32 * t + lane % 32)
+                for p0 in range(0, 64, 32):
+                    assert conflict_ways([a for _, _, a in sup[p0:p0 + 32]], 8) == 1
+
+
+def test_forward_swizzles_do_not_serve_both_reads():
+    """Why the gradient passes need their own swizzle: with the forward's K
+    swizzle the transposed reads of d = 64 are 2-way conflicted, with its V
+    swizzle the row reads are."""
+    d = 64
+    sup = [offset(d, 4 * (l // 32) + (l % 16) // 4, 16 * ((l // 16) & 1) + 4 * (l % 4), swz_k) for l in range(32)]
+    assert conflict_ways(sup, 8) == 2
+    addrs = [offset(d, l % 32, 8 * 0, swz_v) for l in range(16)]
+    assert conflict_ways(addrs, 16) > 1
