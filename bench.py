@@ -173,7 +173,9 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=20)
+    # about 0.3 s of forward steps: the GPU reaches its sustained clock only
+    # after some milliseconds of work (20 warm-up steps measure ~9% slower)
+    ap.add_argument("--warmup", type=int, default=2000)
     ap.add_argument("--workload", default=None)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-baseline leg")
     ap.add_argument("--no-variants", action="store_true",
