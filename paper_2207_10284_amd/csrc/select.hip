@@ -340,7 +340,8 @@ static void launch_rows_j(const float* S, const float* qp, const float* kp, int3
 #undef MRA_ROWS_LAUNCH
 }
 
-// Score registers per lane: up to 2 (nb <= 128), 8 (nb <= 512) or 32 (nb <= 2048).
+// Score registers per lane: up to 2 (nb <= 128), 8 (nb <= 512), 16 (nb <= 1024)
+// or 32 (nb <= 2048).
 template <int MODE>
 static hipError_t launch_rows(const float* S, const float* qp, const float* kp, int32_t* idx_out,
                               const int32_t* idx_in, const float* vp, float* cmax, float* csum,
@@ -349,6 +350,8 @@ static hipError_t launch_rows(const float* S, const float* qp, const float* kp, 
     launch_rows_j<MODE, 2>(S, qp, kp, idx_out, idx_in, vp, cmax, csum, cvec, bh, nb, d, m, stream);
   else if (nb <= 512)
     launch_rows_j<MODE, 8>(S, qp, kp, idx_out, idx_in, vp, cmax, csum, cvec, bh, nb, d, m, stream);
+  else if (nb <= 1024)
+    launch_rows_j<MODE, 16>(S, qp, kp, idx_out, idx_in, vp, cmax, csum, cvec, bh, nb, d, m, stream);
   else
     launch_rows_j<MODE, 32>(S, qp, kp, idx_out, idx_in, vp, cmax, csum, cvec, bh, nb, d, m, stream);
   return hipGetLastError();
