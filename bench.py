@@ -49,6 +49,28 @@ def backward_flops(w) -> float:
     return 10.0 * w.B * w.H * w.nb * w.budget * 32 * 32 * w.d
 
 
+# MI355X unit counts and clock used for the tile pass's model floors
+CUS, SIMDS_PER_CU, CLOCK_HZ = 256, 4, 2.4e9
+L1_BYTES_PER_CLK_CU = 59.0     # measured ceiling of L2 -> CU loads (direct-to-LDS or VGPR)
+
+
+def tile_floors(w) -> dict:
+    """Lower bounds (µs) of the tile pass from unit counts and clock, one per
+    resource: matrix cores (the MFMA roofline), the vector ALU (per selected
+    tile and lane: 16 exponentials at quarter rate plus, for bfloat16, 16 FMA,
+    8 conversions and 8 row-sum dot products at full rate; float32: 16 FMA and
+    16 adds), and the per-CU vector-memory path (the tile's K and V bytes at
+    the measured L2 -> CU ceiling). The measured pass exceeds the largest."""
+    tiles = w.B * w.H * w.nb * w.budget
+    e = 2 if w.dtype == "bf16" else 4
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    mfma = tile_flops(w) / (peak * 1e12) * 1e6
+    valu_cycles = 16 * 16 + 32 * 4                          # per tile, one SIMD (wave64 on 16 lanes)
+    valu = tiles * valu_cycles / (CUS * SIMDS_PER_CU * CLOCK_HZ) * 1e6
+    vmem = tiles * 2 * 32 * w.d * e / (CUS * L1_BYTES_PER_CLK_CU * CLOCK_HZ) * 1e6
+    return {"mfma_us": mfma, "valu_us": valu, "vector_memory_us": vmem}
+
+
 def raw_tiles(w) -> bool:
     """The forward's tile pass reads bfloat16 K/V tiles of d <= 64 from the
     rows themselves; otherwise pooling also writes a packed copy of K and V."""
@@ -295,6 +317,7 @@ def main():
         "stages_us": {"pool": pool_ms * 1e3, "tile": tile_ms * 1e3,
                       "select_and_coarse_term_fused": (ms - pool_ms - tile_ms) * 1e3,
                       "coarse_scores_stepwise": coarse_ms * 1e3},
+        "tile_floors": tile_floors(w),
         "pool_roofline": {"bound": "hbm", "achieved": pool_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                           "frac": pool_gbs / PEAK_HBM_GBS, "bytes_per_launch": pool_bytes(w)},
         **variants,
