@@ -314,8 +314,9 @@ def main():
                      "traffic": recorded_traffic(), "traffic_unit": "bytes per launch",
                      "launch_us": tile_ms * 1e3,
                      "flops_per_launch": tile_flops(w)},
+        # each stage launched alone, back to back (inputs warm in the caches);
+        # in-step durations of the three forward kernels are in the profiles
         "stages_us": {"pool": pool_ms * 1e3, "tile": tile_ms * 1e3,
-                      "select_and_coarse_term_fused": (ms - pool_ms - tile_ms) * 1e3,
                       "coarse_scores_stepwise": coarse_ms * 1e3},
         "tile_floors": tile_floors(w),
         "pool_roofline": {"bound": "hbm", "achieved": pool_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
