@@ -40,14 +40,20 @@ struct RowsSmem {
   size_t c_off, q_off, k_off, bytes;      // chunk buffer, Q~ (f64), K~ chunk / partials
 };
 
-static RowsSmem rows_smem(int d, bool fused) {
+// Columns per pass of the coarse logits and per step of the coarse term:
+// 128 for heads of more than 128 blocks (half the barriers and load waits of
+// 64-column passes), else 64.
+__host__ __device__ constexpr int pass_cols(int jmax) { return jmax >= 8 ? 128 : kChunk; }
+
+static RowsSmem rows_smem(int d, bool fused, int jmax) {
   RowsSmem L{};
   size_t off = 0;
-  L.c_off = off; off += (size_t)kRows * (kChunk + 1) * sizeof(float);
+  const int pc = pass_cols(jmax);
+  L.c_off = off; off += (size_t)kRows * (pc + 1) * sizeof(float);
   off = (off + 15) & ~size_t(15);
   L.q_off = off; if (fused) off += (size_t)kRows * (d + 1) * sizeof(double);
   L.k_off = off;
-  const size_t kbuf = fused ? (size_t)kChunk * (d + 1) * sizeof(float) : 0;
+  const size_t kbuf = fused ? (size_t)pc * (d + 1) * sizeof(float) : 0;
   const size_t part = (size_t)4096 * sizeof(float);   // partial sums of L: (256/d) x 16 x d
   off += kbuf > part ? kbuf : part;
   L.bytes = off;
@@ -64,7 +70,6 @@ __global__ __launch_bounds__(kRows / RPW * kWave) void rows_kernel(
   constexpr int NTH = NW * kWave;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   float* Cb = reinterpret_cast<float*>(smem);                      // [16][65] chunk buffer
-  constexpr int ldc = kChunk + 1;
   const int tid = threadIdx.x;
   const int w = wave_uniform(tid / kWave);
   const int lane = lane_id();
@@ -78,16 +83,20 @@ __global__ __launch_bounds__(kRows / RPW * kWave) void rows_kernel(
   // this wave's rows: w + NW * i, i < RPW
   auto row_of = [&](int i) { return w + NW * i; };
 
-  // Phase 4's B operands (V~ values, NB4 per chunk and lane) are loaded two
-  // chunks ahead, the first two here, so their latency hides behind phases 1-3.
-  constexpr int NTD = D / 16, KQ = NW / NTD, YPW = kChunk / KQ, NB4 = YPW / 4;
+  // Phase 4's B operands (V~ values, NB4 per step and lane) are loaded 128
+  // columns ahead (two 64-column steps or one 128-column step), the first
+  // here, so their latency hides behind phases 1-3.
+  constexpr int PC = pass_cols(JMAX), SUB = PC / kChunk, ldp = PC + 1;
+  constexpr int NTD = D / 16, KQ = NW / NTD, YPW = PC / KQ, NB4 = YPW / 4;
   static_assert(KQ >= 1 && NW % NTD == 0, "waves cover the dim tiles");
   const int nt = w % NTD, kq = w / NTD;
   const int ar = lane & 15, ak = lane >> 4;
   const float* vh = vp + bh * (long long)nb * D;
-  float bv[2][NB4];
+  const int JS = (nb + PC - 1) / PC;                               // column steps
+  constexpr int PF = SUB == 2 ? 1 : 2;                             // steps of look-ahead
+  float bv[PF][NB4];
   auto load_b = [&](int j, float (&dst)[NB4]) {
-    const int yb = kChunk * j + kq * YPW;
+    const int yb = PC * j + kq * YPW;
 #pragma unroll
     for (int t = 0; t < NB4; ++t) {
       const int y = yb + 4 * t + ak;
@@ -96,7 +105,7 @@ __global__ __launch_bounds__(kRows / RPW * kWave) void rows_kernel(
   };
   if constexpr (MODE == kFused || MODE == kTermOnly) {
     load_b(0, bv[0]);
-    if (J > 1) load_b(1, bv[1]);
+    if (PF == 2 && JS > 1) load_b(1, bv[PF - 1]);
   }
 
   // ---- phase 1: the rows' scores into registers, s[i][j] for y = 64j + lane
@@ -107,20 +116,21 @@ __global__ __launch_bounds__(kRows / RPW * kWave) void rows_kernel(
     for (int j = 0; j < JMAX; ++j) s[i][j] = 0.0f;
   if constexpr (MODE == kFused || MODE == kFusedSelect) {
     constexpr int ldq = D + 1, ldk = D + 1;
+    static_assert(PC / 16 <= NW, "one 16x16 tile per wave and pass");
     double* Qd = reinterpret_cast<double*>(smem + q_off);          // [16][D+1]
-    float* Kc = reinterpret_cast<float*>(smem + k_off);            // [64][D+1]
+    float* Kc = reinterpret_cast<float*>(smem + k_off);            // [PC][D+1]
     const float* qh = qp + g0 * D;
     const float* kh = kp + bh * (long long)nb * D;
-    // a chunk of K~ (64 rows x D) is KV4 float4 per thread
-    constexpr int KV4 = (kChunk * (D / 4) + NTH - 1) / NTH;
+    // a pass of K~ (PC rows x D) is KV4 float4 per thread
+    constexpr int KV4 = (PC * (D / 4) + NTH - 1) / NTH;
     f32x4 kv[KV4];
-    auto load_k = [&](int j) {
-      const int y0 = kChunk * j;
+    auto load_k = [&](int js) {
+      const int y0 = PC * js;
 #pragma unroll
       for (int u = 0; u < KV4; ++u) {
         const int i = tid + NTH * u, r = i / (D / 4), c4 = i % (D / 4);
         kv[u] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-        if (i < kChunk * (D / 4) && y0 + r < nb)
+        if (i < PC * (D / 4) && y0 + r < nb)
           kv[u] = *reinterpret_cast<const f32x4*>(kh + (long long)(y0 + r) * D + 4 * c4);
       }
     };
@@ -130,30 +140,35 @@ __global__ __launch_bounds__(kRows / RPW * kWave) void rows_kernel(
       Qd[r * ldq + c] = r < rows ? (double)qh[(long long)r * D + c] : 0.0;
     }
 #pragma unroll
-    for (int j = 0; j < JMAX; ++j) {
-      if (j >= J) break;
+    for (int js = 0; js < (JMAX + SUB - 1) / SUB; ++js) {
+      if (js >= JS) break;
       __syncthreads();                                             // Kc, Cb free; Qd ready
 #pragma unroll
       for (int u = 0; u < KV4; ++u) {
         const int i = tid + NTH * u, r = i / (D / 4), c4 = i % (D / 4);
-        if (i < kChunk * (D / 4)) {
+        if (i < PC * (D / 4)) {
           float* dst = Kc + r * ldk + 4 * c4;
           dst[0] = kv[u][0]; dst[1] = kv[u][1]; dst[2] = kv[u][2]; dst[3] = kv[u][3];
         }
       }
-      if (j + 1 < J) load_k(j + 1);
+      if (js + 1 < JS) load_k(js + 1);
       __syncthreads();
-      if (w < kChunk / 16) {                                       // waves 0..3: one 16x16 tile each
+      if (w < PC / 16) {                                           // one 16x16 tile per wave
         f64x4 acc = {0.0, 0.0, 0.0, 0.0};
         coarse_tile_f64(acc, Qd, ldq, Kc + 16 * w * ldk, ldk, D);
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          Cb[coarse_tile_row(lane, e) * ldc + 16 * w + (lane & 15)] = coarse_round(acc[e], scale);
+          Cb[coarse_tile_row(lane, e) * ldp + 16 * w + (lane & 15)] = coarse_round(acc[e], scale);
       }
       __syncthreads();
 #pragma unroll
-      for (int i = 0; i < RPW; ++i)
-        if (row_of(i) < rows && kChunk * j + lane < nb) s[i][j] = Cb[row_of(i) * ldc + lane];
+      for (int sb = 0; sb < SUB; ++sb) {
+        const int j = js * SUB + sb;
+        if (j >= JMAX) break;
+#pragma unroll
+        for (int i = 0; i < RPW; ++i)
+          if (row_of(i) < rows && kChunk * j + lane < nb) s[i][j] = Cb[row_of(i) * ldp + kChunk * sb + lane];
+      }
     }
   } else {
 #pragma unroll
@@ -291,18 +306,23 @@ __global__ __launch_bounds__(kRows / RPW * kWave) void rows_kernel(
   // kq = w / (D/16); the per-wave partial sums are added in kq order at the end.
   f32x4v acc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-  for (int j = 0; j < JMAX; ++j) {
-    if (j >= J) break;
-    __syncthreads();                                               // previous chunk consumed
+  for (int js = 0; js < (JMAX + SUB - 1) / SUB; ++js) {
+    if (js >= JS) break;
+    __syncthreads();                                               // previous step consumed
 #pragma unroll
-    for (int i = 0; i < RPW; ++i) Cb[row_of(i) * ldc + lane] = s[i][j];   // zero for inactive rows
+    for (int sb = 0; sb < SUB; ++sb) {
+      const int j = js * SUB + sb;
+      if (j >= JMAX) break;
+#pragma unroll
+      for (int i = 0; i < RPW; ++i) Cb[row_of(i) * ldp + kChunk * sb + lane] = s[i][j];   // zero for inactive rows
+    }
     __syncthreads();
 #pragma unroll
     for (int t = 0; t < NB4; ++t) {
-      const float a = Cb[ar * ldc + kq * YPW + 4 * t + ak];
-      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[j & 1][t], acc, 0, 0, 0);
+      const float a = Cb[ar * ldp + kq * YPW + 4 * t + ak];
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[js % PF][t], acc, 0, 0, 0);
     }
-    if (j + 2 < J) load_b(j + 2, bv[j & 1]);
+    if (js + PF < JS) load_b(js + PF, bv[js % PF]);
   }
   // partial sums: lane holds rows 4*ak + e of dim 16*nt + ar
   float* part = reinterpret_cast<float*>(smem + k_off);            // [KQ][16][D]
@@ -325,7 +345,7 @@ static void launch_rows_j(const float* S, const float* qp, const float* kp, int3
                           float* cvec, long long bh, int nb, int d, int m, hipStream_t stream) {
   const long long groups = (nb + kRows - 1) / kRows;
   const unsigned blocks = (unsigned)(bh * groups);
-  const RowsSmem L = rows_smem(d, MODE == kFused || MODE == kFusedSelect);
+  const RowsSmem L = rows_smem(d, MODE == kFused || MODE == kFusedSelect, JMAX);
   const double scale = 1.0 / sqrt((double)d);
   // two rows per wave (8 waves) while the scores fit: four workgroups per CU
   constexpr int RPW = JMAX <= 8 ? 2 : 1;
