@@ -32,7 +32,9 @@
 //    dQ^T += K_y^T dP^T.
 //  * bwd_dkdv_(stream_)kernel: per column block (a wave), over the block-rows that
 //    refined it (ascending): dV^T += G_x^T A, dK^T += c Q_x^T dP.
-// Tile operands come from packed copies in the layouts of tile_ops.h.
+// Tile operands: for bfloat16 with d <= 64 raw 32-row tiles of the inputs
+// (copied into LDS under a swizzle that serves row and transposed reads);
+// otherwise packed copies in the layouts of tile_ops.h.
 #include "common.h"
 #include "kernels.h"
 #include "tile_ops.h"
