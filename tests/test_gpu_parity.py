@@ -168,6 +168,38 @@ def test_forward_small(gpu, dtype, d, B, H, n, m):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("d", [32, 64, 128])
+@pytest.mark.parametrize("n,m", [(6400, 9), (22400, 12)])
+def test_forward_wide_heads(gpu, dtype, d, n, m):
+    """Heads of 200 and 700 blocks: the fused selection kernel's 8- and
+    16-register tiers, whose coarse logits and coarse term go 128 columns per
+    pass (here with a ragged last pass)."""
+    _say("forward wide", dtype, d, n, m)
+    q, k, v = inputs.random_qkv(3000 + n + d, 1, 2 if n < 10000 else 1, n, d, dtype, scale=1.2)
+    _, _, err, differ = _forward_and_check(gpu, q, k, v, m, dtype)
+    _say("  err", err, "rows with tie swaps", differ)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("n,m", [(6400, 9), (22400, 12)])
+def test_forward_matches_stepwise_bitwise_wide(gpu, dtype, n, m):
+    """The fused forward equals the step-wise calls bit for bit on wide heads
+    too (selection, coarse term and output)."""
+    q, k, v = inputs.random_qkv(78 + n, 1, 2, n, 64, dtype)
+    nb = n // 32
+    tq, tk, tv = dev(q, dtype), dev(k, dtype), dev(v, dtype)
+    idx_f = torch.empty(1, 2, nb, m, dtype=torch.int32, device="cuda")
+    out_f = gpu.attention_forward(tq, tk, tv, m, idx_out=idx_f)
+    qp, kp, vp = gpu.pool(tq, tk, tv)
+    S = gpu.coarse_scores(qp, kp)
+    idx = gpu.select(S, m)
+    cm, cs, cv = gpu.coarse_term(S, idx, vp)
+    out = gpu.block_sddmm_spmm(tq, tk, tv, idx, cm, cs, cv)
+    assert torch.equal(idx, idx_f)
+    assert torch.equal(out, out_f)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_forward_matches_stepwise_bitwise(gpu, dtype):
     q, k, v = inputs.random_qkv(77, 2, 2, 640, 64, dtype)
     m = 4
