@@ -1,6 +1,6 @@
 // One 16 x 16 tile of the coarse logits on the float64 matrix cores, shared by
 // the coarse-logit kernel and the fused selection kernel so that both produce
-// the same bits (same operands, same instruction sequence, k ascending).
+// the same bits (same operands, same instruction sequence).
 #pragma once
 
 #include "common.h"
@@ -9,21 +9,37 @@ namespace mra {
 
 typedef double f64x4 __attribute__((ext_vector_type(4)));
 
-// acc += sum_{k < klen} qd[i][k] * kf[j][k] for the tile rows i (queries) and
-// columns j (keys), k in steps of four, one v_mfma_f64_16x16x4_f64 per step.
-// qd: float64 rows in LDS (row stride ldq); kf: float32 rows in LDS (row
-// stride ldk), converted exactly to float64. Lane l supplies A[l%16][l/16]
-// and B[l/16][l%16]; result register e of lane l is row coarse_tile_row(l, e)
-// of column l%16 (the float64 16x16x4 instruction interleaves rows across the
-// four lane groups, unlike its float32 counterpart).
-__device__ __forceinline__ void coarse_tile_f64(f64x4& acc, const double* qd, int ldq,
-                                                const float* kf, int ldk, int klen) {
-  const int lane = lane_id(), r = lane & 15, kq = lane >> 4;
-  const double* qa = qd + r * ldq + kq;
-  const float* kb = kf + r * ldk + kq;
-#pragma unroll 4
-  for (int k0 = 0; k0 < klen; k0 += 4)
-    acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[k0], (double)kb[k0], acc, 0, 0, 0);
+// Operands of a tile in registers. Lane l = 16g + r holds row r of the tile
+// (a query row of Q~ or a key row of K~) at columns 16s + 4g .. 16s + 4g + 3
+// for s < d/16, one float4 per s, loaded straight from the row-major pooled
+// rows (the 16 lanes of a group read 16 rows, the four groups 64 contiguous
+// bytes of each). Callers clamp rows past the end to a valid row and ignore
+// the results in those rows and columns.
+template <int D>
+__device__ __forceinline__ void coarse_load(const float* __restrict__ row, f32x4 (&v)[D / 16]) {
+  const int g = lane_id() >> 4;
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s) v[s] = *reinterpret_cast<const f32x4*>(row + 16 * s + 4 * g);
+}
+
+// acc = sum over the d columns of q[i][k] * kf[j][k] (tile rows i = queries,
+// columns j = keys), one v_mfma_f64_16x16x4_f64 per step. Step 4s + e takes
+// column 16s + 4g + e in lane group g (the instruction's contraction index is
+// the lane group), so the d columns are each used once, in this fixed order;
+// the float32 values convert exactly to float64. Two chains (s even, s odd)
+// keep two products in flight; their sums are added at the end. Result
+// register e of lane l is row coarse_tile_row(l, e) of column l%16 (the
+// float64 16x16x4 instruction interleaves rows across the four lane groups,
+// unlike its float32 counterpart).
+template <int D>
+__device__ __forceinline__ f64x4 coarse_tile_f64(const f32x4 (&q)[D / 16], const f32x4 (&kf)[D / 16]) {
+  f64x4 acc[2] = {{0.0, 0.0, 0.0, 0.0}, {0.0, 0.0, 0.0, 0.0}};
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s)
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      acc[s & 1] = __builtin_amdgcn_mfma_f64_16x16x4f64((double)q[s][e], (double)kf[s][e], acc[s & 1], 0, 0, 0);
+  return acc[0] + acc[1];
 }
 
 __device__ __forceinline__ int coarse_tile_row(int lane, int e) { return 4 * e + (lane >> 4); }

@@ -11,16 +11,17 @@
 //
 // One workgroup owns 16 consecutive block-rows of one head: 8 waves with two
 // rows each (one row per wave for heads of more than 512 blocks). Lane l of a
-// row's wave holds the row's scores for blocks y = 64j + l in registers: loaded from S~, or (fused mode) computed in
-// 64-column chunks on the float64 matrix cores with the same tile routine as
-// the coarse-logit kernel (so the same bits). The selection is a radix search
-// for the m-th largest order-preserving 32-bit key (32 rounds of ballot +
-// popcount over the registers), then one ascending sweep that resolves ties
-// at the threshold by index and compacts the kept indices with prefix
-// popcounts. Max and sum use DPP / lane-swap reductions (no LDS). L = W V~ is
-// formed chunk by chunk on the float32 matrix cores (16x16x4): the weights
-// b e^{S~ - M} (0 where selected) of the 16 rows pass through LDS one 64-block
-// chunk at a time, and the waves split the dims and the blocks of a chunk
+// row's wave holds the row's scores for blocks y = 64j + l in registers:
+// loaded from S~, or (fused modes) computed as 16 x 16 tiles on the float64
+// matrix cores with the same tile routine as the coarse-logit kernel (so the
+// same bits), the waves taking tiles in turn with their operands in
+// registers, then passed through LDS. The selection is a radix search for the
+// m-th largest order-preserving 32-bit key (32 rounds of ballot + popcount
+// over the registers), then one ascending sweep that resolves ties at the
+// threshold by index and compacts the kept indices with prefix popcounts. Max
+// and sum use DPP / lane-swap reductions (no LDS). L = W V~ is formed on the
+// float32 matrix cores (16x16x4): the weights b e^{S~ - M} (0 where selected)
+// of the 16 rows go to LDS once, and the waves split the dims and the blocks
 // between them, so V~ is read once per workgroup. Workgroups of one head stay
 // on one XCD. Every mode runs the same arithmetic in the same order, so the
 // fused forward step is bit-identical to separate score, select and
@@ -32,31 +33,26 @@ namespace mra {
 
 enum RowsMode { kSelectOnly = 0, kTermOnly = 1, kFused = 2, kFusedSelect = 3 };
 constexpr int kRows = 16;                 // block-rows (waves) per workgroup
-constexpr int kChunk = 64;                // score columns per chunk
+constexpr int kChunk = 64;                // score columns per register
+constexpr int kU = 8;                     // coarse-term steps per batch of V~ loads (two float4 of weights)
 
 typedef float f32x4v __attribute__((ext_vector_type(4)));
 
+// LDS of a workgroup: the 16 rows' scores (fused modes) and then their
+// weights, [16][ldc] floats with ldc = 64 JMAX + 4 (zero past nb; the pad of
+// 4 keeps the reads of the coarse term's operands and of the scores free of
+// bank conflicts), followed by the partial sums of L ((16 / (d/16)) x 16 x d
+// floats).
+__host__ __device__ constexpr int rows_ldc(int jmax) { return 64 * jmax + 4; }
+
 struct RowsSmem {
-  size_t c_off, q_off, k_off, bytes;      // chunk buffer, Q~ (f64), K~ chunk / partials
+  size_t part_off, bytes;
 };
 
-// Columns per pass of the coarse logits and per step of the coarse term:
-// 128 for heads of more than 128 blocks (half the barriers and load waits of
-// 64-column passes), else 64.
-__host__ __device__ constexpr int pass_cols(int jmax) { return jmax >= 8 ? 128 : kChunk; }
-
-static RowsSmem rows_smem(int d, bool fused, int jmax) {
+static RowsSmem rows_smem(int jmax, int nw) {
   RowsSmem L{};
-  size_t off = 0;
-  const int pc = pass_cols(jmax);
-  L.c_off = off; off += (size_t)kRows * (pc + 1) * sizeof(float);
-  off = (off + 15) & ~size_t(15);
-  L.q_off = off; if (fused) off += (size_t)kRows * (d + 1) * sizeof(double);
-  L.k_off = off;
-  const size_t kbuf = fused ? (size_t)pc * (d + 1) * sizeof(float) : 0;
-  const size_t part = (size_t)4096 * sizeof(float);   // partial sums of L: (256/d) x 16 x d
-  off += kbuf > part ? kbuf : part;
-  L.bytes = off;
+  L.part_off = ((size_t)kRows * rows_ldc(jmax) * sizeof(float) + 15) & ~size_t(15);
+  L.bytes = L.part_off + (size_t)nw * 16 * 16 * sizeof(float);
   return L;
 }
 
@@ -65,11 +61,11 @@ __global__ __launch_bounds__(kRows / RPW * kWave) void rows_kernel(
     const float* __restrict__ S, const float* __restrict__ qp, const float* __restrict__ kp,
     int32_t* __restrict__ idx_out, const int32_t* __restrict__ idx_in,
     const float* __restrict__ vp, float* __restrict__ cmax, float* __restrict__ csum,
-    float* __restrict__ cvec, int nb, int m, int q_off, int k_off, double scale) {
+    float* __restrict__ cvec, int nb, int m, int part_off, double scale) {
   constexpr int NW = kRows / RPW;                                  // waves per workgroup
   constexpr int NTH = NW * kWave;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  float* Cb = reinterpret_cast<float*>(smem);                      // [16][65] chunk buffer
+  float* Cb = reinterpret_cast<float*>(smem);                      // [16][ldc] scores, then weights
   const int tid = threadIdx.x;
   const int w = wave_uniform(tid / kWave);
   const int lane = lane_id();
@@ -83,30 +79,26 @@ __global__ __launch_bounds__(kRows / RPW * kWave) void rows_kernel(
   // this wave's rows: w + NW * i, i < RPW
   auto row_of = [&](int i) { return w + NW * i; };
 
-  // Phase 4's B operands (V~ values, NB4 per step and lane) are loaded 128
-  // columns ahead (two 64-column steps or one 128-column step), the first
-  // here, so their latency hides behind phases 1-3.
-  constexpr int PC = pass_cols(JMAX), SUB = PC / kChunk, ldp = PC + 1;
-  constexpr int NTD = D / 16, KQ = NW / NTD, YPW = PC / KQ, NB4 = YPW / 4;
+  // Phase 4's B operands (V~ values, kU steps per batch): for heads of up to
+  // 512 blocks the first batch is loaded here so its latency hides behind
+  // phases 1-3 (larger heads keep those registers for phase 1).
+  constexpr bool kEarlyB = JMAX <= 8;
+  constexpr int NTD = D / 16, KQ = NW / NTD;
   static_assert(KQ >= 1 && NW % NTD == 0, "waves cover the dim tiles");
   const int nt = w % NTD, kq = w / NTD;
   const int ar = lane & 15, ak = lane >> 4;
-  const float* vh = vp + bh * (long long)nb * D;
-  const int JS = (nb + PC - 1) / PC;                               // column steps
-  constexpr int PF = SUB == 2 ? 1 : 2;                             // steps of look-ahead
-  float bv[PF][NB4];
-  auto load_b = [&](int j, float (&dst)[NB4]) {
-    const int yb = PC * j + kq * YPW;
+  constexpr int ldc = rows_ldc(JMAX), BPW = 2 * JMAX / KQ;            // batches per wave
+  static_assert(BPW * KQ == 2 * JMAX, "whole batches");
+  const float* vcol = vp + bh * (long long)nb * D + 16 * nt + ar;
+  float ba[kU];
+  // V~ rows of this wave's batch u: blocks 32 (kq + KQ u) + 8 ak + e, e < kU
+  // (rows past nb are read at nb - 1; their weights are zero)
+  auto load_b = [&](int u, float (&b)[kU]) {
+    const int y0 = 4 * kU * (kq + KQ * u) + kU * ak;
 #pragma unroll
-    for (int t = 0; t < NB4; ++t) {
-      const int y = yb + 4 * t + ak;
-      dst[t] = y < nb ? vh[(long long)y * D + 16 * nt + ar] : 0.0f;
-    }
+    for (int e = 0; e < kU; ++e) b[e] = vcol[min(y0 + e, nb - 1) * D];
   };
-  if constexpr (MODE == kFused || MODE == kTermOnly) {
-    load_b(0, bv[0]);
-    if (PF == 2 && JS > 1) load_b(1, bv[PF - 1]);
-  }
+  if constexpr ((MODE == kFused || MODE == kTermOnly) && kEarlyB) load_b(0, ba);
 
   // ---- phase 1: the rows' scores into registers, s[i][j] for y = 64j + lane
   float s[RPW][JMAX];
@@ -115,60 +107,60 @@ __global__ __launch_bounds__(kRows / RPW * kWave) void rows_kernel(
 #pragma unroll
     for (int j = 0; j < JMAX; ++j) s[i][j] = 0.0f;
   if constexpr (MODE == kFused || MODE == kFusedSelect) {
-    constexpr int ldq = D + 1, ldk = D + 1;
-    static_assert(PC / 16 <= NW, "one 16x16 tile per wave and pass");
-    double* Qd = reinterpret_cast<double*>(smem + q_off);          // [16][D+1]
-    float* Kc = reinterpret_cast<float*>(smem + k_off);            // [PC][D+1]
-    const float* qh = qp + g0 * D;
+    // 16 x 16 tiles of S~ (the 16 rows x 16 keys) on the float64 matrix
+    // cores, tile t by wave t % NW, operands in registers straight from the
+    // pooled rows, results through LDS
+    constexpr int NQ = D / 16;
+    const int r = lane & 15;
     const float* kh = kp + bh * (long long)nb * D;
-    // a pass of K~ (PC rows x D) is KV4 float4 per thread
-    constexpr int KV4 = (PC * (D / 4) + NTH - 1) / NTH;
-    f32x4 kv[KV4];
-    auto load_k = [&](int js) {
-      const int y0 = PC * js;
-#pragma unroll
-      for (int u = 0; u < KV4; ++u) {
-        const int i = tid + NTH * u, r = i / (D / 4), c4 = i % (D / 4);
-        kv[u] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-        if (i < PC * (D / 4) && y0 + r < nb)
-          kv[u] = *reinterpret_cast<const f32x4*>(kh + (long long)(y0 + r) * D + 4 * c4);
-      }
+    f32x4 qv[NQ];
+    coarse_load<D>(qp + (g0 + min(r, rows - 1)) * D, qv);       // rows past the group: ignored
+    const int ntile = (nb + 15) / 16;
+    auto load_k = [&](int t, f32x4 (&kv)[NQ]) {                   // keys past nb: ignored columns
+      coarse_load<D>(kh + (long long)min(16 * min(t, ntile - 1) + r, nb - 1) * D, kv);
     };
-    load_k(0);
-    for (int i = tid; i < kRows * D; i += NTH) {
-      const int r = i / D, c = i % D;
-      Qd[r * ldq + c] = r < rows ? (double)qh[(long long)r * D + c] : 0.0;
+    auto tile = [&](int t, const f32x4 (&kv)[NQ]) {
+      // Q~ stays in float32 registers (converted at each use): room for the
+      // next tile's K~
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) asm volatile("" : "+v"(qv[q]));
+      const f64x4 acc = coarse_tile_f64<D>(qv, kv);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) Cb[coarse_tile_row(lane, e) * ldc + 16 * t + r] = coarse_round(acc[e], scale);
+    };
+    // K~ one tile ahead where a wave takes several tiles and the registers
+    // allow it (not at d = 128 with two rows per wave)
+    if constexpr (4 * JMAX <= NW || (D == 128 && RPW == 2)) {
+      for (int t = w; t < ntile; t += NW) {
+        f32x4 kv[NQ];
+        load_k(t, kv);
+        tile(t, kv);
+      }
+    } else {
+      f32x4 ka[NQ], kb[NQ];
+      int t = w;
+      if (t < ntile) load_k(t, ka);
+      // unconditional loads (past the last tile: the last tile again), so the
+      // load-counter waits stay exact
+      while (t < ntile) {
+        load_k(t + NW, kb);
+        asm volatile("" ::: "memory");                            // loads stay ahead of the products
+        tile(t, ka);
+        t += NW;
+        if (t >= ntile) break;
+        load_k(t + NW, ka);
+        asm volatile("" ::: "memory");
+        tile(t, kb);
+        t += NW;
+      }
     }
+    __syncthreads();
 #pragma unroll
-    for (int js = 0; js < (JMAX + SUB - 1) / SUB; ++js) {
-      if (js >= JS) break;
-      __syncthreads();                                             // Kc, Cb free; Qd ready
+    for (int j = 0; j < JMAX; ++j) {
+      if (j >= J) break;
 #pragma unroll
-      for (int u = 0; u < KV4; ++u) {
-        const int i = tid + NTH * u, r = i / (D / 4), c4 = i % (D / 4);
-        if (i < PC * (D / 4)) {
-          float* dst = Kc + r * ldk + 4 * c4;
-          dst[0] = kv[u][0]; dst[1] = kv[u][1]; dst[2] = kv[u][2]; dst[3] = kv[u][3];
-        }
-      }
-      if (js + 1 < JS) load_k(js + 1);
-      __syncthreads();
-      if (w < PC / 16) {                                           // one 16x16 tile per wave
-        f64x4 acc = {0.0, 0.0, 0.0, 0.0};
-        coarse_tile_f64(acc, Qd, ldq, Kc + 16 * w * ldk, ldk, D);
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          Cb[coarse_tile_row(lane, e) * ldp + 16 * w + (lane & 15)] = coarse_round(acc[e], scale);
-      }
-      __syncthreads();
-#pragma unroll
-      for (int sb = 0; sb < SUB; ++sb) {
-        const int j = js * SUB + sb;
-        if (j >= JMAX) break;
-#pragma unroll
-        for (int i = 0; i < RPW; ++i)
-          if (row_of(i) < rows && kChunk * j + lane < nb) s[i][j] = Cb[row_of(i) * ldp + kChunk * sb + lane];
-      }
+      for (int i = 0; i < RPW; ++i)
+        if (row_of(i) < rows && kChunk * j + lane < nb) s[i][j] = Cb[row_of(i) * ldc + kChunk * j + lane];
     }
   } else {
 #pragma unroll
@@ -301,32 +293,50 @@ __global__ __launch_bounds__(kRows / RPW * kWave) void rows_kernel(
   }
 
   // ---- phase 4: L = W V~ on the float32 matrix cores (v_mfma_f32_16x16x4_f32,
-  // A = W: 16 rows x 4 blocks, B = V~: 4 blocks x 16 dims). Wave w takes dim
-  // tile nt = w % (D/16) and, inside every chunk, the block range of part
-  // kq = w / (D/16); the per-wave partial sums are added in kq order at the end.
+  // A = W: 16 rows x 4 blocks from LDS, B = V~: 4 blocks x 16 dims straight
+  // from the pooled rows, two batches of kU steps ahead). Wave w takes dim tile
+  // nt = w % (D/16) and the 32-block batches kq + KQ u, u < BPW, for
+  // kq = w / (D/16) (all 64 JMAX columns; the weights past nb are zero); the
+  // per-wave partial sums are added in kq order at the end.
+  __syncthreads();                                                 // every wave has read its scores
+#pragma unroll
+  for (int j = 0; j < JMAX; ++j) {
+    if (j >= J) break;
+#pragma unroll
+    for (int i = 0; i < RPW; ++i) Cb[row_of(i) * ldc + kChunk * j + lane] = s[i][j];   // zero: inactive rows, blocks >= nb
+  }
+  for (int c = kChunk * J + lane; c < kChunk * JMAX; c += kWave)   // columns past the scores
+    for (int i = 0; i < RPW; ++i) Cb[row_of(i) * ldc + c] = 0.0f;
+  __syncthreads();
+  if constexpr (!kEarlyB) load_b(0, ba);
+  const float* wrow = Cb + ar * ldc + kU * ak;
   f32x4v acc = {0.0f, 0.0f, 0.0f, 0.0f};
+  // batch u: step e takes block 32 (kq + KQ u) + 8 ak + e in lane group ak,
+  // so each lane reads its kU weights as two 16-byte LDS reads
+  auto steps = [&](int u, const float (&b)[kU]) {
+    const f32x4v* wp = reinterpret_cast<const f32x4v*>(wrow + 4 * kU * (kq + KQ * u));
+    const f32x4v a0 = wp[0], a1 = wp[1];
 #pragma unroll
-  for (int js = 0; js < (JMAX + SUB - 1) / SUB; ++js) {
-    if (js >= JS) break;
-    __syncthreads();                                               // previous step consumed
+    for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[e], b[e], acc, 0, 0, 0);
 #pragma unroll
-    for (int sb = 0; sb < SUB; ++sb) {
-      const int j = js * SUB + sb;
-      if (j >= JMAX) break;
+    for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[e], b[4 + e], acc, 0, 0, 0);
+  };
+  // All BPW batches unrolled (no loop state for the compiler's load-counter
+  // waits to merge), loads two batches ahead; the empty asm keeps the
+  // compiler from sinking them below the products, which would expose their
+  // latency.
+  float bv[3][kU];
 #pragma unroll
-      for (int i = 0; i < RPW; ++i) Cb[row_of(i) * ldp + kChunk * sb + lane] = s[i][j];   // zero for inactive rows
-    }
-    __syncthreads();
+  for (int e = 0; e < kU; ++e) bv[0][e] = ba[e];
+  if constexpr (BPW > 1) load_b(1, bv[1]);
 #pragma unroll
-    for (int t = 0; t < NB4; ++t) {
-      const float a = Cb[ar * ldp + kq * YPW + 4 * t + ak];
-      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[js % PF][t], acc, 0, 0, 0);
-    }
-    if (js + PF < JS) load_b(js + PF, bv[js % PF]);
+  for (int u = 0; u < BPW; ++u) {
+    if (u + 2 < BPW) load_b(u + 2, bv[(u + 2) % 3]);
+    asm volatile("" ::: "memory");
+    steps(u, bv[u % 3]);
   }
   // partial sums: lane holds rows 4*ak + e of dim 16*nt + ar
-  float* part = reinterpret_cast<float*>(smem + k_off);            // [KQ][16][D]
-  __syncthreads();
+  float* part = reinterpret_cast<float*>(smem + part_off);         // [KQ][16][D]
 #pragma unroll
   for (int e = 0; e < 4; ++e) part[(kq * kRows + 4 * ak + e) * D + 16 * nt + ar] = acc[e];
   __syncthreads();
@@ -345,13 +355,13 @@ static void launch_rows_j(const float* S, const float* qp, const float* kp, int3
                           float* cvec, long long bh, int nb, int d, int m, hipStream_t stream) {
   const long long groups = (nb + kRows - 1) / kRows;
   const unsigned blocks = (unsigned)(bh * groups);
-  const RowsSmem L = rows_smem(d, MODE == kFused || MODE == kFusedSelect, JMAX);
+  constexpr int RPW = JMAX <= 8 ? 2 : 1;
+  const RowsSmem L = rows_smem(JMAX, kRows / RPW);
   const double scale = 1.0 / sqrt((double)d);
   // two rows per wave (8 waves) while the scores fit: four workgroups per CU
-  constexpr int RPW = JMAX <= 8 ? 2 : 1;
 #define MRA_ROWS_LAUNCH(DD)                                                                     \
   rows_kernel<DD, MODE, JMAX, RPW><<<blocks, 64 * kRows / RPW, L.bytes, stream>>>(            \
-      S, qp, kp, idx_out, idx_in, vp, cmax, csum, cvec, nb, m, (int)L.q_off, (int)L.k_off, scale)
+      S, qp, kp, idx_out, idx_in, vp, cmax, csum, cvec, nb, m, (int)L.part_off, scale)
   switch (d) {
     case 32: MRA_ROWS_LAUNCH(32); break;
     case 64: MRA_ROWS_LAUNCH(64); break;
