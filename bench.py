@@ -135,6 +135,39 @@ def time_launches(fn, iters: int, warmup: int = 3) -> float:
     return s.elapsed_time(e) / iters
 
 
+def time_graph(fn, reps: int = 50, replays: int = 5) -> float:
+    """Average duration (ms) of `fn` for kernels too short for Python to keep
+    the GPU busy launch by launch: `reps` calls captured in one HIP graph,
+    replayed, timed with HIP events on the capturing stream."""
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    st = torch.cuda.Stream()
+    st.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(st):
+        with torch.cuda.graph(g, stream=st):
+            for _ in range(reps):
+                fn()
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    cur = torch.cuda.current_stream()
+    s.record(cur)
+    for _ in range(replays):
+        g.replay()
+    e.record(cur)
+    torch.cuda.synchronize()
+    return s.elapsed_time(e) / (replays * reps)
+
+
+def select_bytes(w) -> float:
+    """The step-wise selection (mra_select): reads the coarse logits, writes
+    the selected indices."""
+    return 4.0 * w.B * w.H * w.nb * w.nb + 4.0 * w.B * w.H * w.nb * w.budget
+
+
 def backward_leg(w, ops, tq, tk, tv, out, idx, ws, iters):
     """The gradient pass on the workload: mra_attention_backward alone, and a
     forward that also writes the log normalisers followed by the backward
@@ -298,6 +331,8 @@ def main():
         tile_ms = time_launches(lambda: ops.block_sddmm_spmm(tq, tk, tv, sel, cm, cs, cv, out=tile_out), it)
     pool_ms = time_launches(lambda: ops.pool(tq, tk, tv, packed=packed), it)
     coarse_ms = time_launches(lambda: ops.coarse_scores(qp, kp), it)
+    select_ms = time_graph(lambda: ops.select(S, w.budget))
+    select_gbs = select_bytes(w) / (select_ms * 1e-3) / 1e9
     tflops = tile_flops(w) / (tile_ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     pool_gbs = pool_bytes(w) / (pool_ms * 1e-3) / 1e9
@@ -321,6 +356,12 @@ def main():
         "tile_floors": tile_floors(w),
         "pool_roofline": {"bound": "hbm", "achieved": pool_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                           "frac": pool_gbs / PEAK_HBM_GBS, "bytes_per_launch": pool_bytes(w)},
+        # the step-wise selection alone (the forward fuses it with the coarse
+        # logits and the coarse term, so S~ never reaches HBM there)
+        "select_roofline": {"bound": "hbm", "kernel": "rows_kernel, select-only mode (mra_select)",
+                            "achieved": select_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                            "frac": select_gbs / PEAK_HBM_GBS, "bytes_per_launch": select_bytes(w),
+                            "launch_us": select_ms * 1e3},
         **variants,
         "tflops_step": (tile_flops(w) + coarse_flops(w)) / (ms * 1e-3) / 1e12,
         "wall_s_timed": wall,

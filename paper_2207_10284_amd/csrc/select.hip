@@ -49,10 +49,13 @@ struct RowsSmem {
   size_t part_off, bytes;
 };
 
-static RowsSmem rows_smem(int jmax, int nw) {
+// The select-only mode uses no LDS; the fused select-only mode only the
+// score rows.
+static RowsSmem rows_smem(int jmax, int nw, int mode) {
   RowsSmem L{};
+  if (mode == kSelectOnly) return L;
   L.part_off = ((size_t)kRows * rows_ldc(jmax) * sizeof(float) + 15) & ~size_t(15);
-  L.bytes = L.part_off + (size_t)nw * 16 * 16 * sizeof(float);
+  L.bytes = mode == kFusedSelect ? L.part_off : L.part_off + (size_t)nw * 16 * 16 * sizeof(float);
   return L;
 }
 
@@ -356,7 +359,7 @@ static void launch_rows_j(const float* S, const float* qp, const float* kp, int3
   const long long groups = (nb + kRows - 1) / kRows;
   const unsigned blocks = (unsigned)(bh * groups);
   constexpr int RPW = JMAX <= 8 ? 2 : 1;
-  const RowsSmem L = rows_smem(JMAX, kRows / RPW);
+  const RowsSmem L = rows_smem(JMAX, kRows / RPW, MODE);
   const double scale = 1.0 / sqrt((double)d);
   // two rows per wave (8 waves) while the scores fit: four workgroups per CU
 #define MRA_ROWS_LAUNCH(DD)                                                                     \
