@@ -169,11 +169,11 @@ def test_forward_small(gpu, dtype, d, B, H, n, m):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("d", [32, 64, 128])
-@pytest.mark.parametrize("n,m", [(6400, 9), (22400, 12)])
+@pytest.mark.parametrize("n,m", [(6400, 9), (22400, 12), (48000, 10)])
 def test_forward_wide_heads(gpu, dtype, d, n, m):
-    """Heads of 200 and 700 blocks: the fused selection kernel's 8- and
-    16-register tiers, whose coarse logits and coarse term go 128 columns per
-    pass (here with a ragged last pass)."""
+    """Heads of 200, 700 and 1500 blocks: the fused selection kernel's 8-, 16-
+    and 32-register tiers (16-key logit tiles spread over the waves with a
+    ragged last tile, coarse-term batches past the head's last block)."""
     _say("forward wide", dtype, d, n, m)
     q, k, v = inputs.random_qkv(3000 + n + d, 1, 2 if n < 10000 else 1, n, d, dtype, scale=1.2)
     _, _, err, differ = _forward_and_check(gpu, q, k, v, m, dtype)
@@ -181,7 +181,7 @@ def test_forward_wide_heads(gpu, dtype, d, n, m):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("n,m", [(6400, 9), (22400, 12)])
+@pytest.mark.parametrize("n,m", [(6400, 9), (22400, 12), (48000, 10)])
 def test_forward_matches_stepwise_bitwise_wide(gpu, dtype, n, m):
     """The fused forward equals the step-wise calls bit for bit on wide heads
     too (selection, coarse term and output)."""
