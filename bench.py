@@ -72,9 +72,9 @@ def tile_floors(w) -> dict:
 
 
 def raw_tiles(w) -> bool:
-    """The forward's tile pass reads bfloat16 K/V tiles of d <= 64 from the
-    rows themselves; otherwise pooling also writes a packed copy of K and V."""
-    return w.dtype == "bf16" and w.d <= 64
+    """The forward's tile pass reads bfloat16 K/V tiles from the rows
+    themselves; for float32 pooling also writes a packed copy of K and V."""
+    return w.dtype == "bf16"
 
 
 def pool_bytes(w) -> float:

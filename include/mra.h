@@ -190,10 +190,9 @@ mra_status_t mra_block_sddmm_spmm(const void* q, const void* k, const void* v,
  * mra_forward_workspace_bytes — bytes of device workspace mra_attention_forward
  * needs for these sizes and dtype: pooled rows, the selection and the coarse
  * term (B*H*(n/32)*(4d + budget + 2)*4 bytes, each part rounded up to 256),
- * plus, for float32 inputs and for d = 128, copies of K and V rearranged into
- * matrix-core operand order (2*B*H*n*d*elem bytes; bfloat16 tiles of
- * d <= 64 are read straight from K and V). Returns 0 for invalid or
- * unsupported arguments.
+ * plus, for float32 inputs, copies of K and V rearranged into matrix-core
+ * operand order (2*B*H*n*d*elem bytes; bfloat16 tiles are read straight
+ * from K and V). Returns 0 for invalid or unsupported arguments.
  */
 size_t mra_forward_workspace_bytes(int B, int H, int n, int d, int block, int budget,
                                    mra_dtype_t dtype);

@@ -73,9 +73,9 @@ struct WsLayout {
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-// The forward's tile pass reads bfloat16 K/V tiles of d <= 64 straight from
-// their rows; other tiles need the packed copy the pooling pass writes.
-bool raw_tiles(int d, mra_dtype_t dtype) { return dtype == MRA_BF16 && d <= 64; }
+// The forward's tile pass reads bfloat16 K/V tiles straight from their rows;
+// float32 tiles need the packed copy the pooling pass writes.
+bool raw_tiles(int d, mra_dtype_t dtype) { (void)d; return dtype == MRA_BF16; }
 
 WsLayout ws_layout(long long bh, int nb, int d, int m, mra_dtype_t dtype) {
   WsLayout L{};

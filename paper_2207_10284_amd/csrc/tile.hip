@@ -424,11 +424,11 @@ __global__ __launch_bounds__((TileCfg<DT, D>::kWaves * kWave)) void tile_kernel(
 //     chunk in the order the weights of the second product hold them.
 template <int D>
 __host__ __device__ constexpr int raw_swz_k(int r) {
-  return D == 64 ? (r >> 1) & 7 : (r >> 2) & 3;
+  return D == 128 ? r & 15 : (D == 64 ? (r >> 1) & 7 : (r >> 2) & 3);
 }
 template <int D>
 __host__ __device__ constexpr int raw_swz_v(int r) {
-  return D == 64 ? ((r >> 1) & 1) << 2 : 0;
+  return D == 128 ? 4 * (r & 3) : (D == 64 ? ((r >> 1) & 1) << 2 : 0);
 }
 
 // The C 1 KB copies of a raw K tile and of a raw V tile. The swizzled source
@@ -443,6 +443,24 @@ __device__ __forceinline__ void copy_raw_tiles(gptr_t k0, gptr_t k1, gptr_t v0, 
     constexpr int i = C - 1;
     __builtin_amdgcn_global_load_lds((KP == 2 && (i & 1)) ? k1 : k0, ks, 16, i * 1024, 0);
     __builtin_amdgcn_global_load_lds(v0, vs, 16, i * 1024, 0);
+  }
+}
+
+// d = 128: a raw tile is 8 KB (eight 1 KB copies of four 256-byte rows each),
+// copied with buffer loads to LDS: the tile's offset in the head goes in the
+// scalar offset, the lane's swizzled source offset in the vector offset, so a
+// copy costs no vector instructions. The K swizzle of row r depends on r mod 16,
+// so copy i uses the lane offset of copy i mod 4 (koff) and moves the source by
+// i KB like the destination; the V swizzle depends on r mod 4 only (voff).
+template <int I>
+__device__ __forceinline__ void copy_raw_tiles_buf(i32x4 krs, i32x4 vrs, unsigned ktile, unsigned vtile,
+                                                   const unsigned (&koff)[4], unsigned voff, lptr_t ks,
+                                                   lptr_t vs) {
+  if constexpr (I > 0) {
+    copy_raw_tiles_buf<I - 1>(krs, vrs, ktile, vtile, koff, voff, ks, vs);
+    constexpr int i = I - 1;
+    buffer_load_lds16(krs, ks + i * 1024, koff[i & 3], ktile + i * 1024);
+    buffer_load_lds16(vrs, vs + i * 1024, voff, vtile + i * 1024);
   }
 }
 
@@ -488,9 +506,9 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
   using Cfg = TileCfg<DT, D>;
   using elem = typename Cfg::elem;
   constexpr int KC = Cfg::kKChunks, VC = Cfg::kVChunks, CH = Cfg::kChunks;
-  static_assert(CH <= 8, "operands of a tile are held in registers");
+  static_assert(CH <= (RAW && D == 128 ? 16 : 8), "operands of a tile are held in registers");
   static_assert(SLOTS >= 1 && SLOTS <= 3, "tiles in flight per wave");
-  static_assert(!RAW || (DT == BF16 && D <= 64), "raw tiles: bfloat16, d <= 64");
+  static_assert(!RAW || DT == BF16, "raw tiles: bfloat16");
   // the slots are their own LDS object, apart from the selection lists, so
   // reading a list does not wait for loads in flight into a slot
   __shared__ __attribute__((aligned(16))) u32x4 slot_all[WAVES][SLOTS][CH * 64];
@@ -515,12 +533,23 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
   const unsigned loff = lane * 16u;
   // One lane address per operand; its chunks are 1 KB apart in memory and in
   // the slot, and the load's immediate offset moves both addresses.
-  static_assert(KC <= 4 && VC <= 4, "chunk offsets fit the immediate field");
+  static_assert((RAW && D == 128) || (KC <= 4 && VC <= 4), "chunk offsets fit the immediate field");
   // raw tiles: this lane's source offsets for the copies (k0, k1, v0: see
   // copy_raw_tiles) and its LDS read offsets (K chunk c; V^T column tile t)
   constexpr int NT = TileCfg<DT, D>::kNT, KP = D == 64 ? 2 : 1;
-  int koff0 = 0, koff1 = 0, voff0 = 0, kread[KC], vread[NT];
+  unsigned koffq[4] = {0u, 0u, 0u, 0u};             // d = 128: K source offsets of copies i mod 4
+  i32x4 krs = {0, 0, 0, 0}, vrs = {0, 0, 0, 0};     // d = 128: the head's K and V rows
+  // (unsigned: a uniform tile base plus a zero-extended per-lane offset lets
+  // the copies use scalar-base addressing, with no per-copy address arithmetic)
+  unsigned koff0 = 0, koff1 = 0, voff0 = 0;
+  int kread[KC], vread[NT];
   if constexpr (RAW) {
+    if constexpr (D == 128) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) koffq[q] = raw_copy_offset<D, raw_swz_k<D>>(q, lane) - q * 1024;
+      krs = buffer_rsrc(kslab, (unsigned)nb * KC * 1024u);
+      vrs = buffer_rsrc(vslab, (unsigned)nb * VC * 1024u);
+    }
     koff0 = raw_copy_offset<D, raw_swz_k<D>>(0, lane);
     koff1 = raw_copy_offset<D, raw_swz_k<D>>(1, lane) - 1024;
     voff0 = raw_copy_offset<D, raw_swz_v<D>>(0, lane);
@@ -536,7 +565,9 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
     unsigned char* slot = reinterpret_cast<unsigned char*>(slot_all[w][sidx]);
     auto* ks = (__attribute__((address_space(3))) char*)slot;
     auto* vs = (__attribute__((address_space(3))) char*)(slot + KC * 1024);
-    if constexpr (RAW) {
+    if constexpr (RAW && D == 128) {
+      copy_raw_tiles_buf<KC>(krs, vrs, (unsigned)y * KC * 1024u, (unsigned)y * VC * 1024u, koffq, voff0, ks, vs);
+    } else if constexpr (RAW) {
       const gptr_t kt = (gptr_t)(kslab + (size_t)y * KC * 1024);
       const gptr_t vt = (gptr_t)(vslab + (size_t)y * VC * 1024);
       copy_raw_tiles<KC, KP>(kt + koff0, kt + koff1, vt + voff0, ks, vs);
@@ -635,8 +666,8 @@ static void launch_tile_t(const void* q, const void* k, const void* v, const int
   const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
   // tiles of up to 8 KB (bfloat16 d <= 64, float32 d = 32) stream through LDS:
   // packed operands, or for bfloat16 the raw rows
-  constexpr bool RAW = !PACKED && DT == BF16 && D <= 64;
-  if constexpr ((PACKED || RAW) && TileCfg<DT, D>::kChunks <= 8) {
+  constexpr bool RAW = !PACKED && DT == BF16;
+  if constexpr (RAW || (PACKED && TileCfg<DT, D>::kChunks <= 8)) {
     const unsigned blocks = (unsigned)((rows + kStreamWaves - 1) / kStreamWaves);
     const size_t smem = (size_t)kStreamWaves * m * sizeof(int32_t);
     if (cmax)

@@ -1,4 +1,4 @@
-"""CPU model of the raw-tile LDS layout of the bfloat16 tile pass (d = 32, 64).
+"""CPU model of the raw-tile LDS layout of the bfloat16 tile pass (d = 32, 64, 128).
 
 The tile pass copies a raw 32-row K (or V) tile into LDS with direct-to-LDS
 loads of 16 bytes per lane, each 1 KB load covering whole rows; lane p of load
@@ -16,11 +16,11 @@ import pytest
 
 
 def swz_k(d, r):
-    return (r >> 1) & 7 if d == 64 else (r >> 2) & 3
+    return {128: r & 15, 64: (r >> 1) & 7, 32: (r >> 2) & 3}[d]
 
 
 def swz_v(d, r):
-    return ((r >> 1) & 1) << 2 if d == 64 else 0
+    return {128: 4 * (r & 3), 64: ((r >> 1) & 1) << 2, 32: 0}[d]
 
 
 def offset(d, r, c, swz):
@@ -38,7 +38,7 @@ def conflict_ways(addrs, width):
     return max(len(v) for v in banks.values())
 
 
-@pytest.mark.parametrize("d", [32, 64])
+@pytest.mark.parametrize("d", [32, 64, 128])
 @pytest.mark.parametrize("which", ["k", "v"])
 def test_copies_cover_whole_rows_once(d, which):
     swz = swz_k if which == "k" else swz_v
@@ -58,7 +58,7 @@ def test_copies_cover_whole_rows_once(d, which):
     assert len(sources) == 32 * rb // 16                      # every block copied once
 
 
-@pytest.mark.parametrize("d", [32, 64])
+@pytest.mark.parametrize("d", [32, 64, 128])
 def test_k_row_operand_reads(d):
     """Chunk s of lane (h, j) = K[j][(d/2)h + 8s .. +7] (16 contiguous bytes);
     no bank conflict in any 16-lane pass."""
@@ -74,7 +74,7 @@ def test_k_row_operand_reads(d):
             assert conflict_ways(addrs[p0:p0 + 16], 16) == 1
 
 
-@pytest.mark.parametrize("d", [32, 64])
+@pytest.mark.parametrize("d", [32, 64, 128])
 def test_v_transposed_operand_reads(d):
     """ds_read_b64_tr_b16: within a group of 16 lanes, lane i receives as value
     k the element i%4 of the 8 bytes addressed by lane 4k + i/4. Each lane
@@ -107,6 +107,24 @@ def test_v_transposed_operand_reads(d):
                         r0 = 16 * u + 4 * (lane // 32) + i // 4
                         c0 = 32 * t + 16 * ((lane // 16) & 1) + 4 * (i % 4)
                         assert offset(d, r0 + 8, c0, swz_v) - offset(d, r0, c0, swz_v) == 8 * 2 * d
+
+
+def test_d128_copy_offsets_repeat():
+    """d = 128: the source offset of copy i less i KB repeats with period 4 in i
+    for K (its swizzle depends on the row mod 16, four rows per copy) and is
+    the same for every copy for V (row mod 4), so four lane offsets (K) and
+    one (V) serve all eight copies of a tile."""
+    d, rb = 128, 256
+
+    def src(i, p, swz):
+        q = i * 1024 + 16 * p
+        r, slot = q // rb, (q % rb) // 16
+        return r * rb + 16 * (slot ^ swz(d, r))
+    for p in range(64):
+        for i in range(8):
+            assert src(i, p, swz_k) - 1024 * i == src(i % 4, p, swz_k) - 1024 * (i % 4)
+            assert src(i, p, swz_v) - 1024 * i == src(0, p, swz_v)
+            assert 0 <= src(i % 4, p, swz_k) - 1024 * (i % 4) < 1024
 
 
 def test_unswizzled_rows_would_conflict():
