@@ -431,27 +431,14 @@ __host__ __device__ constexpr int raw_swz_v(int r) {
   return D == 128 ? 4 * (r & 3) : (D == 64 ? ((r >> 1) & 1) << 2 : 0);
 }
 
-// The C 1 KB copies of a raw K tile and of a raw V tile. The swizzled source
-// offsets repeat with period KP in the copy index for K (the swizzle of row r
-// depends on r / 2 for d = 64) and period 1 for V, so per lane they are k0
-// (even copies), k1 (odd copies, less 1 KB) and v0, and the load's immediate
-// offset moves the source and the LDS destination together.
-template <int C, int KP>
-__device__ __forceinline__ void copy_raw_tiles(gptr_t k0, gptr_t k1, gptr_t v0, lptr_t ks, lptr_t vs) {
-  if constexpr (C > 0) {
-    copy_raw_tiles<C - 1, KP>(k0, k1, v0, ks, vs);
-    constexpr int i = C - 1;
-    __builtin_amdgcn_global_load_lds((KP == 2 && (i & 1)) ? k1 : k0, ks, 16, i * 1024, 0);
-    __builtin_amdgcn_global_load_lds(v0, vs, 16, i * 1024, 0);
-  }
-}
-
-// d = 128: a raw tile is 8 KB (eight 1 KB copies of four 256-byte rows each),
-// copied with buffer loads to LDS: the tile's offset in the head goes in the
-// scalar offset, the lane's swizzled source offset in the vector offset, so a
-// copy costs no vector instructions. The K swizzle of row r depends on r mod 16,
-// so copy i uses the lane offset of copy i mod 4 (koff) and moves the source by
-// i KB like the destination; the V swizzle depends on r mod 4 only (voff).
+// The 1 KB copies of a raw K tile and of a raw V tile (32 x d bfloat16: d/16
+// copies each), buffer loads to LDS: the head's rows are one buffer resource,
+// the tile's offset goes in the scalar offset and the lane's swizzled source
+// offset in the vector offset, so a copy costs no vector instruction. Copy i
+// moves source and destination by i KB; the swizzled lane offsets repeat with
+// period 2 (K, d = 64: the swizzle of row r depends on r / 2), 4 (K, d = 128:
+// r mod 16) or 1 in the copy index, so koff holds the offsets of copies
+// i mod 4 and voff the V offset.
 template <int I>
 __device__ __forceinline__ void copy_raw_tiles_buf(i32x4 krs, i32x4 vrs, unsigned ktile, unsigned vtile,
                                                    const unsigned (&koff)[4], unsigned voff, lptr_t ks,
@@ -531,27 +518,23 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
   const char* kslab = static_cast<const char*>(kpk) + (size_t)bh * nb * KC * 1024;
   const char* vslab = static_cast<const char*>(vpk) + (size_t)bh * nb * VC * 1024;
   const unsigned loff = lane * 16u;
-  // One lane address per operand; its chunks are 1 KB apart in memory and in
-  // the slot, and the load's immediate offset moves both addresses.
-  static_assert((RAW && D == 128) || (KC <= 4 && VC <= 4), "chunk offsets fit the immediate field");
-  // raw tiles: this lane's source offsets for the copies (k0, k1, v0: see
-  // copy_raw_tiles) and its LDS read offsets (K chunk c; V^T column tile t)
-  constexpr int NT = TileCfg<DT, D>::kNT, KP = D == 64 ? 2 : 1;
-  unsigned koffq[4] = {0u, 0u, 0u, 0u};             // d = 128: K source offsets of copies i mod 4
-  i32x4 krs = {0, 0, 0, 0}, vrs = {0, 0, 0, 0};     // d = 128: the head's K and V rows
-  // (unsigned: a uniform tile base plus a zero-extended per-lane offset lets
-  // the copies use scalar-base addressing, with no per-copy address arithmetic)
-  unsigned koff0 = 0, koff1 = 0, voff0 = 0;
+  // Packed operands: one lane address per operand; its chunks are 1 KB apart
+  // in memory and in the slot, and the load's immediate offset moves both
+  // addresses.
+  static_assert(RAW || (KC <= 4 && VC <= 4), "chunk offsets fit the immediate field");
+  // raw tiles: this lane's source offsets for the copies (see
+  // copy_raw_tiles_buf) and its LDS read offsets (K chunk c; V^T column tile t)
+  constexpr int NT = TileCfg<DT, D>::kNT;
+  constexpr int KPB = D == 128 ? 4 : (D == 64 ? 2 : 1);   // period of the K copy offsets
+  unsigned koffq[4] = {0u, 0u, 0u, 0u};             // K source offsets of copies i mod 4
+  i32x4 krs = {0, 0, 0, 0}, vrs = {0, 0, 0, 0};     // the head's K and V rows
+  unsigned voff0 = 0;
   int kread[KC], vread[NT];
   if constexpr (RAW) {
-    if constexpr (D == 128) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) koffq[q] = raw_copy_offset<D, raw_swz_k<D>>(q, lane) - q * 1024;
-      krs = buffer_rsrc(kslab, (unsigned)nb * KC * 1024u);
-      vrs = buffer_rsrc(vslab, (unsigned)nb * VC * 1024u);
-    }
-    koff0 = raw_copy_offset<D, raw_swz_k<D>>(0, lane);
-    koff1 = raw_copy_offset<D, raw_swz_k<D>>(1, lane) - 1024;
+    for (int q = 0; q < 4; ++q) koffq[q] = raw_copy_offset<D, raw_swz_k<D>>(q % KPB, lane) - (q % KPB) * 1024;
+    krs = buffer_rsrc(kslab, (unsigned)nb * KC * 1024u);
+    vrs = buffer_rsrc(vslab, (unsigned)nb * VC * 1024u);
     voff0 = raw_copy_offset<D, raw_swz_v<D>>(0, lane);
     const int h = lane >> 5, j = lane & 31, i16 = lane & 15;
 #pragma unroll
@@ -565,12 +548,8 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
     unsigned char* slot = reinterpret_cast<unsigned char*>(slot_all[w][sidx]);
     auto* ks = (__attribute__((address_space(3))) char*)slot;
     auto* vs = (__attribute__((address_space(3))) char*)(slot + KC * 1024);
-    if constexpr (RAW && D == 128) {
+    if constexpr (RAW) {
       copy_raw_tiles_buf<KC>(krs, vrs, (unsigned)y * KC * 1024u, (unsigned)y * VC * 1024u, koffq, voff0, ks, vs);
-    } else if constexpr (RAW) {
-      const gptr_t kt = (gptr_t)(kslab + (size_t)y * KC * 1024);
-      const gptr_t vt = (gptr_t)(vslab + (size_t)y * VC * 1024);
-      copy_raw_tiles<KC, KP>(kt + koff0, kt + koff1, vt + voff0, ks, vs);
     } else {
       const auto* kp = (const __attribute__((address_space(1))) char*)(kslab + (size_t)y * KC * 1024 + loff);
       const auto* vp = (const __attribute__((address_space(1))) char*)(vslab + (size_t)y * VC * 1024 + loff);
