@@ -241,25 +241,26 @@ __global__ __launch_bounds__(kRows / RPW * kWave) void rows_kernel(
       int eq_seen = 0, written = 0;
 #pragma unroll
       for (int j = 0; j < JMAX; ++j) {
-        if (j >= J) break;
-        const int y = kChunk * j + lane;
-        const bool valid = y < nb;
-        bool take;
-        if (all) {
-          take = valid;
-        } else if (none) {
-          take = false;
-        } else {
-          const bool eq = valid && key[j] == T;
-          const uint64_t eqm = __ballot(eq);
-          const int rank = eq_seen + __popcll(eqm & lanemask_lt());
-          eq_seen += __popcll(eqm);
-          take = valid && (key[j] > T || (eq && rank < need));
+        if (j < J) {                         // wave-uniform: unrolls fully
+          const int y = kChunk * j + lane;
+          const bool valid = y < nb;
+          bool take;
+          if (all) {
+            take = valid;
+          } else if (none) {
+            take = false;
+          } else {
+            const bool eq = valid && key[j] == T;
+            const uint64_t eqm = __ballot(eq);
+            const int rank = eq_seen + __popcll(eqm & lanemask_lt());
+            eq_seen += __popcll(eqm);
+            take = valid && (key[j] > T || (eq && rank < need));
+          }
+          const uint64_t tm = __ballot(take);
+          if (take && idx_out) idx_out[g * m + written + __popcll(tm & lanemask_lt())] = y;
+          written += __popcll(tm);
+          if (take) sel[i] |= 1u << j;
         }
-        const uint64_t tm = __ballot(take);
-        if (take && idx_out) idx_out[g * m + written + __popcll(tm & lanemask_lt())] = y;
-        written += __popcll(tm);
-        if (take) sel[i] |= 1u << j;
       }
     }
   }
