@@ -49,13 +49,19 @@ struct RowsSmem {
   size_t part_off, bytes;
 };
 
-// The select-only mode uses no LDS; the fused select-only mode only the
-// score rows.
-static RowsSmem rows_smem(int jmax, int nw, int mode) {
+// The select-only mode uses no LDS. In the fused modes the region after the
+// score rows first holds the 16 query rows in float64 ([16][d + 2]; the pad
+// of 16 bytes keeps their reads free of bank conflicts), then the partial
+// sums of L.
+__host__ __device__ constexpr int rows_ldq(int d) { return d + 2; }
+
+static RowsSmem rows_smem(int jmax, int nw, int mode, int d) {
   RowsSmem L{};
   if (mode == kSelectOnly) return L;
   L.part_off = ((size_t)kRows * rows_ldc(jmax) * sizeof(float) + 15) & ~size_t(15);
-  L.bytes = mode == kFusedSelect ? L.part_off : L.part_off + (size_t)nw * 16 * 16 * sizeof(float);
+  const size_t part = mode == kTermOnly || mode == kFused ? (size_t)nw * 16 * 16 * sizeof(float) : 0;
+  const size_t qd = mode == kFused || mode == kFusedSelect ? (size_t)kRows * rows_ldq(d) * sizeof(double) : 0;
+  L.bytes = L.part_off + (part > qd ? part : qd);
   return L;
 }
 
@@ -116,18 +122,22 @@ __global__ __launch_bounds__(kRows / RPW * kWave) void rows_kernel(
     constexpr int NQ = D / 16;
     const int r = lane & 15;
     const float* kh = kp + bh * (long long)nb * D;
-    f32x4 qv[NQ];
-    coarse_load<D>(qp + (g0 + min(r, rows - 1)) * D, qv);       // rows past the group: ignored
+    // the 16 query rows in float64, converted once (rows past the group
+    // repeat the last one; their results are ignored)
+    constexpr int LDQ = rows_ldq(D);
+    double* Qd = reinterpret_cast<double*>(smem + part_off);
+    for (int i = tid; i < kRows * D; i += NTH) {
+      const int rr = i / D, c = i % D;
+      Qd[rr * LDQ + c] = (double)qp[(g0 + min(rr, rows - 1)) * D + c];
+    }
+    __syncthreads();
+    const double* qrow = Qd + r * LDQ + 4 * (lane >> 4);
     const int ntile = (nb + 15) / 16;
     auto load_k = [&](int t, f32x4 (&kv)[NQ]) {                   // keys past nb: ignored columns
       coarse_load<D>(kh + (long long)min(16 * min(t, ntile - 1) + r, nb - 1) * D, kv);
     };
     auto tile = [&](int t, const f32x4 (&kv)[NQ]) {
-      // Q~ stays in float32 registers (converted at each use): room for the
-      // next tile's K~
-#pragma unroll
-      for (int q = 0; q < NQ; ++q) asm volatile("" : "+v"(qv[q]));
-      const f64x4 acc = coarse_tile_f64<D>(qv, kv);
+      const f64x4 acc = coarse_tile_f64_qd<D>(qrow, kv);
 #pragma unroll
       for (int e = 0; e < 4; ++e) Cb[coarse_tile_row(lane, e) * ldc + 16 * t + r] = coarse_round(acc[e], scale);
     };
@@ -360,7 +370,7 @@ static void launch_rows_j(const float* S, const float* qp, const float* kp, int3
   const long long groups = (nb + kRows - 1) / kRows;
   const unsigned blocks = (unsigned)(bh * groups);
   constexpr int RPW = JMAX <= 8 ? 2 : 1;
-  const RowsSmem L = rows_smem(JMAX, kRows / RPW, MODE);
+  const RowsSmem L = rows_smem(JMAX, kRows / RPW, MODE, d);
   const double scale = 1.0 / sqrt((double)d);
   // two rows per wave (8 waves) while the scores fit: four workgroups per CU
 #define MRA_ROWS_LAUNCH(DD)                                                                     \
