@@ -1,6 +1,6 @@
 """Throughput of the MRA-2 forward pass on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--all] [--no-cpu]
 
 One step = one mra_attention_forward call (pool, coarse logits, selection with
 the coarse term, tile pass) over the whole workload, inputs resident in HBM.
@@ -9,6 +9,12 @@ tile pass, timed with HIP events on the stream it runs on) and the float64
 oracle timed on the host as a reported CPU baseline. Beside the headline it
 reports MRA-2-s, the head-wide budget and the gradient pass (forward with log
 normalisers, then mra_attention_backward) on the same inputs.
+
+The CPU leg also compares the GPU's output with the oracle's on the heads it
+computed (max row-normwise error, rows whose selection differs by a near-tie)
+and reports the approximation error of MRA-2 against exact softmax attention,
+||Z_MRA - Z||_F / ||Z||_F (the paper's accuracy measure, Sec. 5), on one head.
+With --all the same numbers are given for every workload in "workloads".
 """
 from __future__ import annotations
 
@@ -77,12 +83,14 @@ def raw_tiles(w) -> bool:
     return w.dtype == "bf16"
 
 
-def pool_bytes(w) -> float:
-    """Pooling pass as run in the forward: Q, K, V read once, the pooled rows
-    written, and (packed configurations) K and V written once more in packed
-    order."""
+def pool_bytes(w, packed=None) -> float:
+    """Pooling pass: Q, K, V read once and the pooled rows written; in the
+    forward for float32 (packed=None follows the forward) K and V are written
+    once more in matrix-core operand order."""
     e = 2 if w.dtype == "bf16" else 4
-    copies = 3 if raw_tiles(w) else 5
+    if packed is None:
+        packed = not raw_tiles(w)
+    copies = 5 if packed else 3
     return copies * w.B * w.H * w.n * w.d * e + 3 * w.B * w.H * w.nb * w.d * 4
 
 
@@ -197,31 +205,120 @@ def backward_leg(w, ops, tq, tk, tv, out, idx, ws, iters):
             "workspace_bytes": bws.numel()}
 
 
-def cpu_baseline(w, q, k, v):
-    """The float64 oracle (factored form, as it stands) over every head of the
-    workload, timed on the host. Returns the JSON object."""
+def cpu_baseline(w, q, k, v, gpu_out=None, gpu_idx=None, budget_s=25.0):
+    """The float64 oracle (factored form, as it stands) over the heads of the
+    workload, timed on the host until about `budget_s` seconds have passed.
+    Returns (the cpu_baseline object, a parity object or None).
+
+    Parity (outside the timed region): for every head the oracle computed,
+    the GPU's selection against the oracle's (rows that differ, each
+    difference a near-tie of the m-th score within 1e-6 relative) and the
+    GPU's output against the oracle evaluated under the GPU's selection (max
+    row-normwise relative error)."""
     from oracle import mra_oracle as O
     try:
         import threadpoolctl
         threads = max(i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()) or 1
     except Exception:                                  # pragma: no cover
         threads = os.cpu_count() or 1
-    budget_s = 25.0
     t0 = time.perf_counter()
-    heads = 0
+    done = []
     for b in range(w.B):
         for h in range(w.H):
-            O.mra_factored(q[b, h], k[b, h], v[b, h], 32, w.budget)
-            heads += 1
+            Z, I = O.mra_factored(q[b, h], k[b, h], v[b, h], 32, w.budget)
+            done.append((b, h, Z, I))
             if time.perf_counter() - t0 > budget_s:
                 break
         else:
             continue
         break
     dt = time.perf_counter() - t0
+    heads = len(done)
     tokens = heads / w.H * w.n                         # tokens of a full H-head layer
-    return {"value": tokens / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{heads} of {w.B * w.H} heads ({w.name}), float64 factored form, {dt:.1f} s"}
+    cpu = {"value": tokens / dt, "unit": "tokens/s", "cores": int(threads), "host_cpus": os.cpu_count(),
+           "kind": "oracle",
+           "sample": f"{heads} of {w.B * w.H} heads ({w.name}), float64 factored form, {dt:.1f} s"}
+    if gpu_out is None:
+        return cpu, None
+    worst, tie_rows, rows = 0.0, 0, 0
+    for b, h, Z, I in done:
+        gi = gpu_idx[b, h]
+        differ = [x for x in range(w.nb) if not np.array_equal(gi[x], I[x])]
+        if differ:
+            S = O.coarse_logits(O.block_mean(q[b, h], 32), O.block_mean(k[b, h], 32))
+            for x in differ:
+                tau = np.sort(S[x])[::-1][w.budget - 1]
+                scale = max(abs(tau), np.abs(S[x]).max())
+                for y in set(gi[x].tolist()) ^ set(I[x].tolist()):
+                    if not abs(S[x, y] - tau) <= 1e-6 * scale:
+                        raise AssertionError(f"{w.name}: selection of head ({b},{h}) row {x} differs beyond a tie")
+            Z, _, _ = O.mra_factored_rows(q[b, h], k[b, h], v[b, h], 32, w.budget, idx=gi)
+        tie_rows += len(differ)
+        rows += w.nb
+        got = gpu_out[b, h].astype(np.float64)
+        num = np.abs(got - Z).max(axis=-1)
+        den = np.maximum(np.abs(Z).max(axis=-1), 1e-30)
+        worst = max(worst, float((num / den).max()))
+    parity = {"max_row_rel_err": worst, "bar": 1e-5 if w.dtype == "f32" else 2e-2, "block_rows": rows,
+              "heads": heads, "tie_swap_rows": tie_rows,
+              "reference": "float64 oracle under the GPU's selection"}
+    return cpu, parity
+
+
+def approximation_error(w, q, k, v, gpu_out, b=0, h=0):
+    """||Z_MRA - Z_exact||_F / ||Z_exact||_F of one head, Z_MRA the GPU's
+    output and Z_exact softmax attention computed by the float64 oracle in
+    slabs of rows (part of the CPU leg)."""
+    from oracle import mra_oracle as O
+    qh, kh, vh = (a[b, h].astype(np.float64) for a in (q, k, v))
+    num = den = 0.0
+    step = 1024
+    for i0 in range(0, w.n, step):
+        Ze = O.exact_attention_rows(qh, kh, vh, i0, min(i0 + step, w.n))
+        dz = gpu_out[b, h, i0:i0 + step].astype(np.float64) - Ze
+        num += float((dz ** 2).sum())
+        den += float((Ze ** 2).sum())
+    return {"value": float(np.sqrt(num / den)), "head": [b, h],
+            "measure": "||Z_MRA-2 - softmax(QK^T/sqrt(d))V||_F / ||softmax(QK^T/sqrt(d))V||_F"}
+
+
+def workload_line(w, ops, steps, warmup, cpu):
+    """Forward, tile pass and pooling of one workload (its own inputs), and
+    with `cpu` the CPU leg: oracle time, parity and approximation error."""
+    import torch
+    from paper_2207_10284_amd import inputs
+    q, k, v = inputs.make_qkv(w)
+    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    dev = torch.device("cuda:0")
+    tq, tk, tv = (torch.from_numpy(a).to(dev).to(tdt) for a in (q, k, v))
+    out = torch.empty_like(tq)
+    idx = torch.empty(w.B, w.H, w.nb, w.budget, dtype=torch.int32, device=dev)
+    ws = torch.empty(ops.forward_workspace_bytes(w.B, w.H, w.n, w.d, w.budget, tdt), dtype=torch.uint8, device=dev)
+    step = lambda: ops.attention_forward(tq, tk, tv, w.budget, out=out, idx_out=idx, workspace=ws)
+    ms = time_launches(step, steps, warmup)
+    qp, kp, vp = ops.pool(tq, tk, tv)
+    S = ops.coarse_scores(qp, kp)
+    sel = ops.select(S, w.budget)
+    cm, cs, cv = ops.coarse_term(S, sel, vp)
+    tile_out = torch.empty_like(tq)
+    it = max(steps, 20)
+    tile_ms = time_launches(lambda: ops.block_sddmm_spmm(tq, tk, tv, sel, cm, cs, cv, out=tile_out), it)
+    pool_ms = time_launches(lambda: ops.pool(tq, tk, tv), it)
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    line = {"B": w.B, "H": w.H, "n": w.n, "d": w.d, "dtype": w.dtype, "budget": w.budget,
+            "forward_us": ms * 1e3, "tokens_per_s": w.B * w.n / (ms * 1e-3),
+            "tile_us": tile_ms * 1e3, "tile_frac_of_peak": tile_flops(w) / (tile_ms * 1e-3) / 1e12 / peak,
+            "tile_peak_tflops": peak,
+            "pool_frac_of_hbm": pool_bytes(w, packed=False) / (pool_ms * 1e-3) / 1e9 / PEAK_HBM_GBS}
+    if cpu:
+        torch.cuda.synchronize()
+        out_h = out.float().cpu().numpy()
+        gi = idx.cpu().numpy().astype(np.int64)
+        c, par = cpu_baseline(w, q, k, v, out_h, gi, budget_s=10.0)
+        line["cpu_baseline"] = c
+        line["parity"] = par
+        line["approximation_error"] = approximation_error(w, q, k, v, out_h, w.B - 1, w.H - 1)
+    return line
 
 
 def main():
@@ -232,6 +329,8 @@ def main():
     # after some milliseconds of work (20 warm-up steps measure ~9% slower)
     ap.add_argument("--warmup", type=int, default=2000)
     ap.add_argument("--workload", default=None)
+    ap.add_argument("--all", action="store_true",
+                    help="also measure every other workload (forward, tile pass, pooling, CPU leg) into 'workloads'")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-baseline leg")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip timing MRA-2-s, the head-wide budget and the backward (profiling runs)")
@@ -312,30 +411,24 @@ def main():
     if not args.no_variants:
         variants["backward"] = backward_leg(w, ops, tq, tk, tv, out, idx, ws, max(args.steps, 20))
 
-    # Dominant kernel: the tile pass, the same instantiation as inside the
-    # forward (packed K/V, coarse term given), on the same inputs; timed alone.
-    packed = not raw_tiles(w)
-    if packed:
-        qp, kp, vp, kvpk = ops.pool(tq, tk, tv, packed=True)
-    else:
-        (qp, kp, vp), kvpk = ops.pool(tq, tk, tv), None
+    # Dominant kernel: the tile pass on the same inputs, timed alone. For
+    # bfloat16 this is the forward's own instantiation (raw K/V tiles); for
+    # float32 the step-wise call reads row-major K/V while the forward's reads
+    # the packed copy its pooling pass writes.
+    qp, kp, vp = ops.pool(tq, tk, tv)
     S = ops.coarse_scores(qp, kp)
     sel = ops.select(S, w.budget)
     cm, cs, cv = ops.coarse_term(S, sel, vp)
     tile_out = torch.empty_like(tq)
     it = max(args.steps, 20)
-    if packed:
-        tile_ms = time_launches(lambda: ops.block_sddmm_spmm(tq, None, None, sel, cm, cs, cv, out=tile_out,
-                                                             kvpacked=kvpk), it)
-    else:
-        tile_ms = time_launches(lambda: ops.block_sddmm_spmm(tq, tk, tv, sel, cm, cs, cv, out=tile_out), it)
-    pool_ms = time_launches(lambda: ops.pool(tq, tk, tv, packed=packed), it)
+    tile_ms = time_launches(lambda: ops.block_sddmm_spmm(tq, tk, tv, sel, cm, cs, cv, out=tile_out), it)
+    pool_ms = time_launches(lambda: ops.pool(tq, tk, tv), it)
     coarse_ms = time_launches(lambda: ops.coarse_scores(qp, kp), it)
     select_ms = time_graph(lambda: ops.select(S, w.budget))
     select_gbs = select_bytes(w) / (select_ms * 1e-3) / 1e9
     tflops = tile_flops(w) / (tile_ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
-    pool_gbs = pool_bytes(w) / (pool_ms * 1e-3) / 1e9
+    pool_gbs = pool_bytes(w, packed=False) / (pool_ms * 1e-3) / 1e9
 
     res = {
         "metric": "MRA-2 attention fwd tokens/s at n=4096,d=64 bf16; % MFMA peak on tile path",
@@ -355,7 +448,7 @@ def main():
                       "coarse_scores_stepwise": coarse_ms * 1e3},
         "tile_floors": tile_floors(w),
         "pool_roofline": {"bound": "hbm", "achieved": pool_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                          "frac": pool_gbs / PEAK_HBM_GBS, "bytes_per_launch": pool_bytes(w)},
+                          "frac": pool_gbs / PEAK_HBM_GBS, "bytes_per_launch": pool_bytes(w, packed=False)},
         # the step-wise selection alone (the forward fuses it with the coarse
         # logits and the coarse term, so S~ never reaches HBM there)
         "select_roofline": {"bound": "hbm", "kernel": "rows_kernel, select-only mode (mra_select)",
@@ -367,7 +460,18 @@ def main():
         "wall_s_timed": wall,
     }
     if not args.no_cpu:
-        res["cpu_baseline"] = cpu_baseline(w, q, k, v)
+        torch.cuda.synchronize()
+        out_h = out.float().cpu().numpy()
+        gi = idx.cpu().numpy().astype(np.int64)
+        res["cpu_baseline"], res["parity"] = cpu_baseline(w, q, k, v, out_h, gi)
+        res["approximation_error"] = approximation_error(w, q, k, v, out_h, w.B - 1, w.H - 1)
+    if args.all:
+        res["workloads"] = {}
+        for name, ow in inputs.WORKLOADS.items():
+            if name == w.name:
+                continue
+            print(f"# workload {name}", file=sys.stderr, flush=True)
+            res["workloads"][name] = workload_line(ow, ops, max(args.steps, 20), 200, not args.no_cpu)
     print(json.dumps(res), flush=True)
 
 

@@ -18,7 +18,7 @@
  *                         exp(S~[block(i), block(j)]) otherwise
  *                              (Sec. 4.2 eq. actual_approx_mat_form)
  *   output        Z = D^ A^ V, D^ normalising each row of A^ to sum 1
- *                              (Sec. 3.1 eq. softmax-attention applied to A^;
+ *                              (Sec. 2.1 eq. softmax-attention applied to A^;
  *                              computed as in Sec. 4.3 Alg. 2)
  *
  * Conventions shared by every call
@@ -82,15 +82,11 @@ typedef enum {
  *   qp, kp, vp : [B,H,nb,d] float32 outputs. A pair (x, xp) may be NULL
  *                together, in which case that tensor is skipped; at least one
  *                pair must be given.
- *   kvpacked   : optional output (NULL to skip; needs k, v, kp, vp):
- *                2*B*H*n*d elements of `dtype`, K and V rearranged block by
- *                block into the operand order of the tile pass's matrix-core
- *                products (an opaque layout, only meant for
- *                mra_block_sddmm_spmm).
- * Each mean is summed in float32 in row order and multiplied by 1/32.
+ * Each mean is summed in float32 (rows 0..15 and 16..31 of a block each in
+ * row order, then added) and multiplied by 1/32.
  */
 mra_status_t mra_pool(const void* q, const void* k, const void* v,
-                      float* qp, float* kp, float* vp, void* kvpacked,
+                      float* qp, float* kp, float* vp,
                       int B, int H, int n, int d, int block,
                       mra_dtype_t dtype, void* stream);
 
@@ -153,7 +149,7 @@ mra_status_t mra_coarse_term(const float* scores, const int32_t* idx, const floa
 /*
  * mra_block_sddmm_spmm — the high-resolution part and the output (Sec. 4.2
  * eq. actual_approx_mat_form with mu_{1,i,j} = exp(P_ij); Sec. 4.3 Alg. 2 at
- * scale 1; Sec. 3.1 normalisation D^). For every block-row x and every
+ * scale 1; Sec. 2.1 normalisation D^). For every block-row x and every
  * y in T_x it computes the 32x32 tile exp(c Q_x K_y^T) (block-sparse SDDMM),
  * multiplies it by V_y (block-sparse SpMM), merges the result with the coarse
  * term and normalises:
@@ -161,9 +157,6 @@ mra_status_t mra_coarse_term(const float* scores, const int32_t* idx, const floa
  *         (sum_{j in T} e^{P_ij}     + e^{M_x} csum[x])
  * (evaluated with max shifts; nothing overflows for finite inputs).
  *   q, k, v : [B,H,n,d] of `dtype`.
- *   kvpacked: optional: the packed K and V written by mra_pool from these same
- *             k and v. If not NULL it is read instead of k and v (which may
- *             then be NULL); the result is identical either way.
  *   idx     : [B,H,nb,budget] int32, rows strictly ascending in [0, nb);
  *             entries outside [0, nb) are skipped.
  *   cmax, csum, cvec : the coarse term from mra_coarse_term. All three may be
@@ -180,7 +173,7 @@ mra_status_t mra_coarse_term(const float* scores, const int32_t* idx, const floa
  *             mra_attention_backward takes it.
  */
 mra_status_t mra_block_sddmm_spmm(const void* q, const void* k, const void* v,
-                                  const void* kvpacked, const int32_t* idx,
+                                  const int32_t* idx,
                                   const float* cmax, const float* csum, const float* cvec,
                                   void* out, float* lse_out,
                                   int B, int H, int n, int d, int block, int budget,
@@ -330,7 +323,7 @@ size_t mra_backward_workspace_bytes(int B, int H, int n, int d, int block, mra_d
  * mra_attention_backward — gradients dQ, dK, dV of a scalar loss through one
  * MRA-2 (or MRA-2-s) forward, given dZ, with the selection held fixed (the
  * selection is a discrete choice with no gradient). The forward is the
- * softmax of Sec. 3.1 over the approximation A^ of Sec. 4.2
+ * softmax of Sec. 2.1 over the approximation A^ of Sec. 4.2
  * (eq. actual_approx_mat_form): each query's logits are the fine c Q_i.K_j
  * of its refined blocks and, with the low-resolution term, the coarse
  * S~[x,y] + ln b of the others, applied to V_j and V~_y. The coarse logits

@@ -18,7 +18,7 @@ two-resolution scheme R = {b, 1} ("MRA-2", Sec. 5, b = 32):
   every entry is exp(P_ij) (the scale-1 components), every other block is the
   constant exp(S~_xy) (the scale-b component it was not replaced by);
 * Z = D^ A^ V with D^ the diagonal that makes every row of A^ sum to one
-  (Sec. 3.1, eq. softmax-attention, applied to A^).
+  (Sec. 2.1, eq. softmax-attention, applied to A^).
 
 Readings of points the paper leaves open (scale 1/sqrt(d) kept in both fine and
 coarse logits, per-row budget, replacement rather than addition, factor b on
@@ -376,22 +376,32 @@ def multilevel_coarse_term(q, k, v, s0, b, idx1, idx2, x):
     over the parent row's unrefined s0-blocks plus b e^{S~ - M} over the
     unrefined b-blocks inside its refined s0-blocks, and L the same sums
     weighting V~0_Y and V~_y (each coarse block counts the columns it spans)."""
+    return _multilevel_term(_multilevel_means(q, k, v, s0, b), s0, b, idx1, idx2, x)
+
+
+def _multilevel_means(q, k, v, s0, b):
+    """(S~0, S~, V~0, V~) of one head: the coarse logits and pooled values at
+    both scales."""
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
     v = np.asarray(v, dtype=np.float64)
-    n = q.shape[0]
-    r = s0 // b
-    X = x // r
     S0 = coarse_logits(block_mean(q, s0), block_mean(k, s0))
     S1 = coarse_logits(block_mean(q, b), block_mean(k, b))
-    vp0, vp1 = block_mean(v, s0), block_mean(v, b)
+    return S0, S1, block_mean(v, s0), block_mean(v, b)
+
+
+def _multilevel_term(means, s0, b, idx1, idx2, x):
+    """multilevel_coarse_term from the head's precomputed means."""
+    S0, S1, vp0, vp1 = means
+    r = s0 // b
+    X = x // r
     refined0 = set(int(Y) for Y in idx1[X])
     refined1 = set(int(y) for y in idx2[x])
-    terms = [(S0[X, Y], s0, vp0[Y]) for Y in range(n // s0) if Y not in refined0]
+    terms = [(S0[X, Y], s0, vp0[Y]) for Y in range(S0.shape[1]) if Y not in refined0]
     terms += [(S1[x, Y * r + t], b, vp1[Y * r + t]) for Y in sorted(refined0) for t in range(r)
               if Y * r + t not in refined1]
     if not terms:
-        return -np.inf, 0.0, np.zeros(v.shape[1])
+        return -np.inf, 0.0, np.zeros(vp1.shape[1])
     M = max(t[0] for t in terms)
     c = sum(w * math.exp(lg - M) for lg, w, _ in terms)
     L = sum(w * math.exp(lg - M) * vv for lg, w, vv in terms)
@@ -410,8 +420,9 @@ def mra_multilevel_factored(q, k, v, s0, b, m1, m2, idx1=None, idx2=None, rows=N
         idx1, idx2 = select_multilevel(q, k, s0, b, m1, m2)
     rows = list(range(n // b)) if rows is None else list(rows)
     out = np.empty((len(rows) * b, v.shape[1]))
+    means = _multilevel_means(q, k, v, s0, b)
     for i, x in enumerate(rows):
-        M, c, L = multilevel_coarse_term(q, k, v, s0, b, idx1, idx2, x)
+        M, c, L = _multilevel_term(means, s0, b, idx1, idx2, x)
         sel = [int(y) for y in idx2[x]]
         qx = q[x * b:(x + 1) * b]
         if sel:
@@ -488,7 +499,7 @@ def mra_lse(q, k, b, idx, coarse=True):
     """Each query's log normaliser L_i = ln(sum of row i of A^): the fine
     terms exp(P_ij) of its refined blocks plus, with coarse=True, b exp(S~)
     for every other block (eq. actual_approx_mat_form; the row sums that
-    D^ of Sec. 3.1 divides by). Taken with a max shift; float64 [n]."""
+    D^ of Sec. 2.1 divides by). Taken with a max shift; float64 [n]."""
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
     n, d = q.shape
@@ -512,13 +523,22 @@ def mra_lse(q, k, b, idx, coarse=True):
 
 
 # --------------------------------------------------------------------------
-# Sec. 3.1, eq. softmax-attention: exact attention (scale 1/sqrt(d))
+# Sec. 2.1, eq. softmax-attention: exact attention (scale 1/sqrt(d))
 # --------------------------------------------------------------------------
 def exact_attention(q, k, v):
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
     v = np.asarray(v, dtype=np.float64)
     return _normalised_rows(q @ k.T / math.sqrt(q.shape[1]), v)
+
+
+def exact_attention_rows(q, k, v, i0, i1):
+    """Rows i0 .. i1-1 of exact_attention(q, k, v), without forming the other
+    rows' logits (for long sequences)."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    return _normalised_rows(q[i0:i1] @ k.T / math.sqrt(q.shape[1]), v)
 
 
 # --------------------------------------------------------------------------

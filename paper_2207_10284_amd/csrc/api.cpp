@@ -191,11 +191,62 @@ mra_status_t check_multi(const Shape& s, int n, int coarse_block, int m1, int m2
 
 }  // namespace
 
+namespace mra {
+
+mra_status_t hip_error_status(hipError_t e) { return hip_status(e); }
+
+mra_status_t forward_check(const void* q, const void* k, const void* v, const void* out,
+                           const int32_t* idx_out, const float* lse_out, int B, int H, int n,
+                           int d, int block, int budget, mra_dtype_t dtype, size_t* need,
+                           bool* empty) {
+  Shape s;
+  MRA_TRY(check_shape(B, H, n, d, block, true, &s));
+  MRA_TRY(check_dtype(dtype));
+  if (budget < 0 || budget > s.nb) return MRA_ERR_INVALID_ARG;
+  *empty = s.empty;
+  *need = 0;
+  if (s.empty) return MRA_OK;
+  MRA_TRY(check_ptr(q));
+  MRA_TRY(check_ptr(k));
+  MRA_TRY(check_ptr(v));
+  MRA_TRY(check_ptr(out));
+  if (idx_out != nullptr && !aligned16(idx_out)) return MRA_ERR_MISALIGNED;
+  if (lse_out != nullptr && !aligned16(lse_out)) return MRA_ERR_MISALIGNED;
+  *need = ws_layout(s.bh, s.nb, d, budget, dtype).total;
+  return MRA_OK;
+}
+
+mra_status_t forward_enqueue(const void* q, const void* k, const void* v, void* out,
+                             int32_t* idx_out, float* lse_out, void* workspace, int B, int H,
+                             int n, int d, int budget, mra_dtype_t dtype, void* stream) {
+  const long long bh = (long long)B * H;
+  const int nb = n / kBlockSize;
+  const WsLayout L = ws_layout(bh, nb, d, budget, dtype);
+  char* ws = static_cast<char*>(workspace);
+  float* qp = reinterpret_cast<float*>(ws + L.qp);
+  float* kp = reinterpret_cast<float*>(ws + L.kp);
+  float* vp = reinterpret_cast<float*>(ws + L.vp);
+  void* kvpacked = raw_tiles(d, dtype) ? nullptr : ws + L.kvpacked;
+  int32_t* idx = idx_out ? idx_out : reinterpret_cast<int32_t*>(ws + L.idx);
+  float* cmax = reinterpret_cast<float*>(ws + L.cmax);
+  float* csum = reinterpret_cast<float*>(ws + L.csum);
+  float* cvec = reinterpret_cast<float*>(ws + L.cvec);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+
+  MRA_TRY(hip_status(launch_pool(q, k, v, qp, kp, vp, kvpacked, bh, n, d, (int)dtype, st)));
+  MRA_TRY(hip_status(launch_select_term_fused(qp, kp, idx, vp, cmax, csum, cvec, bh, nb, d, budget,
+                                              st)));
+  return hip_status(launch_tile(q, k, v, kvpacked, idx, cmax, csum, cvec, out, lse_out, bh, n, d,
+                                budget, (int)dtype, st));
+}
+
+}  // namespace mra
+
 extern "C" {
 
 mra_status_t mra_pool(const void* q, const void* k, const void* v, float* qp, float* kp,
-                      float* vp, void* kvpacked, int B, int H, int n, int d, int block,
-                      mra_dtype_t dtype, void* stream) {
+                      float* vp, int B, int H, int n, int d, int block, mra_dtype_t dtype,
+                      void* stream) {
   Shape s;
   MRA_TRY(check_shape(B, H, n, d, block, true, &s));
   MRA_TRY(check_dtype(dtype));
@@ -203,12 +254,11 @@ mra_status_t mra_pool(const void* q, const void* k, const void* v, float* qp, fl
       (v == nullptr) != (vp == nullptr))
     return MRA_ERR_INVALID_ARG;
   if (q == nullptr && k == nullptr && v == nullptr) return MRA_ERR_INVALID_ARG;
-  if (kvpacked != nullptr && (k == nullptr || v == nullptr)) return MRA_ERR_INVALID_ARG;
   if (s.empty) return MRA_OK;
-  const void* ptrs[7] = {q, k, v, qp, kp, vp, kvpacked};
+  const void* ptrs[6] = {q, k, v, qp, kp, vp};
   for (const void* p : ptrs)
     if (p != nullptr && !aligned16(p)) return MRA_ERR_MISALIGNED;
-  return hip_status(mra::launch_pool(q, k, v, qp, kp, vp, kvpacked, s.bh, n, d, (int)dtype,
+  return hip_status(mra::launch_pool(q, k, v, qp, kp, vp, nullptr, s.bh, n, d, (int)dtype,
                                      static_cast<hipStream_t>(stream)));
 }
 
@@ -254,8 +304,7 @@ mra_status_t mra_coarse_term(const float* scores, const int32_t* idx, const floa
 }
 
 mra_status_t mra_block_sddmm_spmm(const void* q, const void* k, const void* v,
-                                  const void* kvpacked, const int32_t* idx,
-                                  const float* cmax, const float* csum,
+                                  const int32_t* idx, const float* cmax, const float* csum,
                                   const float* cvec, void* out, float* lse_out, int B, int H,
                                   int n, int d, int block, int budget, mra_dtype_t dtype,
                                   void* stream) {
@@ -268,12 +317,8 @@ mra_status_t mra_block_sddmm_spmm(const void* q, const void* k, const void* v,
   if (given == 0 && budget == 0) return MRA_ERR_INVALID_ARG;   // nothing to normalise
   if (s.empty) return MRA_OK;
   MRA_TRY(check_ptr(q));
-  if (kvpacked) {
-    MRA_TRY(check_ptr(kvpacked));
-  } else {
-    MRA_TRY(check_ptr(k));
-    MRA_TRY(check_ptr(v));
-  }
+  MRA_TRY(check_ptr(k));
+  MRA_TRY(check_ptr(v));
   MRA_TRY(check_ptr(out));
   if (lse_out != nullptr && !aligned16(lse_out)) return MRA_ERR_MISALIGNED;
   if (budget > 0) MRA_TRY(check_ptr(idx));
@@ -282,7 +327,7 @@ mra_status_t mra_block_sddmm_spmm(const void* q, const void* k, const void* v,
     MRA_TRY(check_ptr(csum));
     MRA_TRY(check_ptr(cvec));
   }
-  return hip_status(mra::launch_tile(q, k, v, kvpacked, idx, cmax, csum, cvec, out, lse_out, s.bh,
+  return hip_status(mra::launch_tile(q, k, v, nullptr, idx, cmax, csum, cvec, out, lse_out, s.bh,
                                      n, d, budget, (int)dtype, static_cast<hipStream_t>(stream)));
 }
 
@@ -300,37 +345,15 @@ mra_status_t mra_attention_forward(const void* q, const void* k, const void* v, 
                                    size_t workspace_bytes,
                                    int B, int H, int n, int d, int block, int budget,
                                    mra_dtype_t dtype, void* stream) {
-  Shape s;
-  MRA_TRY(check_shape(B, H, n, d, block, true, &s));
-  MRA_TRY(check_dtype(dtype));
-  if (budget < 0 || budget > s.nb) return MRA_ERR_INVALID_ARG;
-  if (s.empty) return MRA_OK;
-  MRA_TRY(check_ptr(q));
-  MRA_TRY(check_ptr(k));
-  MRA_TRY(check_ptr(v));
-  MRA_TRY(check_ptr(out));
-  if (idx_out != nullptr && !aligned16(idx_out)) return MRA_ERR_MISALIGNED;
-  if (lse_out != nullptr && !aligned16(lse_out)) return MRA_ERR_MISALIGNED;
+  size_t need = 0;
+  bool empty = true;
+  MRA_TRY(mra::forward_check(q, k, v, out, idx_out, lse_out, B, H, n, d, block, budget, dtype, &need,
+                             &empty));
+  if (empty) return MRA_OK;
   MRA_TRY(check_ptr(workspace));
-  const WsLayout L = ws_layout(s.bh, s.nb, d, budget, dtype);
-  if (workspace_bytes < L.total) return MRA_ERR_WORKSPACE;
-
-  char* ws = static_cast<char*>(workspace);
-  float* qp = reinterpret_cast<float*>(ws + L.qp);
-  float* kp = reinterpret_cast<float*>(ws + L.kp);
-  float* vp = reinterpret_cast<float*>(ws + L.vp);
-  void* kvpacked = raw_tiles(d, dtype) ? nullptr : ws + L.kvpacked;
-  int32_t* idx = idx_out ? idx_out : reinterpret_cast<int32_t*>(ws + L.idx);
-  float* cmax = reinterpret_cast<float*>(ws + L.cmax);
-  float* csum = reinterpret_cast<float*>(ws + L.csum);
-  float* cvec = reinterpret_cast<float*>(ws + L.cvec);
-  hipStream_t st = static_cast<hipStream_t>(stream);
-
-  MRA_TRY(hip_status(mra::launch_pool(q, k, v, qp, kp, vp, kvpacked, s.bh, n, d, (int)dtype, st)));
-  MRA_TRY(hip_status(mra::launch_select_term_fused(qp, kp, idx, vp, cmax, csum, cvec, s.bh, s.nb,
-                                                   d, budget, st)));
-  return hip_status(mra::launch_tile(q, k, v, kvpacked, idx, cmax, csum, cvec, out, lse_out, s.bh,
-                                     n, d, budget, (int)dtype, st));
+  if (workspace_bytes < need) return MRA_ERR_WORKSPACE;
+  return mra::forward_enqueue(q, k, v, out, idx_out, lse_out, workspace, B, H, n, d, budget, dtype,
+                              stream);
 }
 
 mra_status_t mra_sparse_attention_forward(const void* q, const void* k, const void* v,

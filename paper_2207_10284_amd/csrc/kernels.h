@@ -4,9 +4,30 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
 
+#include "mra.h"
+
 namespace mra {
+
+// The forward's host-side half, shared by mra_attention_forward and the entry
+// point without a workspace argument (api.cpp). forward_check runs every
+// argument check of mra_attention_forward except those of the workspace,
+// makes no HIP call, and on MRA_OK sets *need to the workspace bytes and
+// *empty when there is nothing to compute. forward_enqueue enqueues the three
+// launches of the forward with the given workspace (at least *need bytes,
+// 16-byte aligned) for arguments that passed forward_check.
+mra_status_t forward_check(const void* q, const void* k, const void* v, const void* out,
+                           const int32_t* idx_out, const float* lse_out, int B, int H, int n,
+                           int d, int block, int budget, mra_dtype_t dtype, size_t* need,
+                           bool* empty);
+mra_status_t forward_enqueue(const void* q, const void* k, const void* v, void* out,
+                             int32_t* idx_out, float* lse_out, void* workspace, int B, int H,
+                             int n, int d, int budget, mra_dtype_t dtype, void* stream);
+// MRA_OK for hipSuccess; otherwise records e as the calling thread's last HIP
+// error (mra_last_hip_error) and returns MRA_ERR_HIP.
+mra_status_t hip_error_status(hipError_t e);
 
 // Packed K/V (written by the pooling pass, read by the tile pass): for every
 // head and 32-key block y, the tile's matrix-core operands in lane order, 16

@@ -1,6 +1,6 @@
 // High-resolution part of MRA-2 and the output (Sec. 4.2 eq.
 // actual_approx_mat_form with mu_{1,i,j} = exp(P_ij); Sec. 4.3 Alg. 2 at
-// scale 1; Sec. 3.1 row normalisation D^).
+// scale 1; Sec. 2.1 row normalisation D^).
 //
 // One wave owns one block-row x (32 queries). For every selected column block
 // y, in ascending order, it computes the 32x32 tile S = c Q_x K_y^T on the

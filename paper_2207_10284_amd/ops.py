@@ -25,11 +25,11 @@ STATUS = {0: "MRA_OK", 1: "MRA_ERR_INVALID_ARG", 2: "MRA_ERR_UNSUPPORTED",
 # name -> (restype, argtypes); mirrors include/mra.h
 _P, _I, _Z = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
 SIGNATURES = {
-    "mra_pool": (_I, [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P]),
+    "mra_pool": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P]),
     "mra_coarse_scores": (_I, [_P, _P, _P, _I, _I, _I, _I, _I, _P]),
     "mra_select": (_I, [_P, _P, _I, _I, _I, _I, _I, _P]),
     "mra_coarse_term": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _P]),
-    "mra_block_sddmm_spmm": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _P]),
+    "mra_block_sddmm_spmm": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _P]),
     "mra_forward_workspace_bytes": (_Z, [_I, _I, _I, _I, _I, _I, _I]),
     "mra_attention_forward": (_I, [_P, _P, _P, _P, _P, _P, _P, _Z, _I, _I, _I, _I, _I, _I, _I, _P]),
     "mra_sparse_attention_forward": (_I, [_P, _P, _P, _P, _P, _P, _P, _Z, _I, _I, _I, _I, _I, _I, _I, _P]),
@@ -115,18 +115,16 @@ def _check_f32(t, shape, name):
         raise ValueError(f"{name} must be a contiguous float32 device tensor of shape {tuple(shape)}")
 
 
-def pool(q, k=None, v=None, packed=False):
+def pool(q, k=None, v=None):
     """Block means (Sec. 4.1/4.3): returns (qp, kp, vp), float32 [B, H, n/32, d]
-    (None for a tensor not given); with ``packed=True`` also the packed copies
-    of k and v for the tile pass, as a fourth element (opaque, [2, B, H, n, d])."""
+    (None for a tensor not given)."""
     ref = _check_qkv(q, k, v)
     B, H, n, d = ref.shape
     outs = [None if t is None else torch.empty(B, H, n // BLOCK, d, device=ref.device, dtype=torch.float32)
             for t in (q, k, v)]
-    kvpk = torch.empty((2,) + tuple(ref.shape), device=ref.device, dtype=ref.dtype) if packed else None
-    _call("mra_pool", _ptr(q), _ptr(k), _ptr(v), *(_ptr(o) for o in outs), _ptr(kvpk),
+    _call("mra_pool", _ptr(q), _ptr(k), _ptr(v), *(_ptr(o) for o in outs),
           B, H, n, d, BLOCK, _dtype_code(ref), _stream(ref.device))
-    return tuple(outs) + ((kvpk,) if packed else ())
+    return tuple(outs)
 
 
 def coarse_scores(qp, kp):
@@ -181,12 +179,11 @@ def coarse_term(scores, idx, vp):
     return cmax, csum, cvec
 
 
-def block_sddmm_spmm(q, k, v, idx, cmax=None, csum=None, cvec=None, out=None, kvpacked=None, lse_out=None):
+def block_sddmm_spmm(q, k, v, idx, cmax=None, csum=None, cvec=None, out=None, lse_out=None):
     """Selected tiles exp(c Q_x K_y^T) V_y, merged with the coarse term (if
     given) and normalised: the output Z, [B, H, n, d] in the input dtype.
-    ``kvpacked`` (from ``pool(..., packed=True)``) replaces k and v when given;
     ``lse_out`` (float32 [B, H, n]) receives each query's log normaliser."""
-    ref = _check_qkv(q, *((k, v) if kvpacked is None else (kvpacked[0], kvpacked[1])))
+    ref = _check_qkv(q, k, v)
     B, H, n, d = ref.shape
     nb = n // BLOCK
     budget = idx.shape[-1]
@@ -199,7 +196,7 @@ def block_sddmm_spmm(q, k, v, idx, cmax=None, csum=None, cvec=None, out=None, kv
         out = torch.empty_like(ref)
     if lse_out is not None:
         _check_f32(lse_out, (B, H, n), "lse_out")
-    _call("mra_block_sddmm_spmm", _ptr(q), _ptr(k), _ptr(v), _ptr(kvpacked), _ptr(idx), _ptr(cmax), _ptr(csum),
+    _call("mra_block_sddmm_spmm", _ptr(q), _ptr(k), _ptr(v), _ptr(idx), _ptr(cmax), _ptr(csum),
           _ptr(cvec), _ptr(out), _ptr(lse_out), B, H, n, d, BLOCK, budget, _dtype_code(ref), _stream(ref.device))
     return out
 

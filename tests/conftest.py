@@ -12,6 +12,29 @@ def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
 
 
+def pytest_sessionfinish(session, exitstatus):
+    """With MRA_PARITY_LOG set, write the full-size parity results the GPU
+    tests collected (tests/parity.py RECORDS) to that file as a table."""
+    path = os.environ.get("MRA_PARITY_LOG")
+    if not path:
+        return
+    from tests import parity
+    if not parity.RECORDS:
+        return
+    lines = ["| variant | workload | dtype | heads | block-rows checked | max row-normwise rel. err | "
+             "max abs err / max abs ref | rel. Frobenius err | bar | rows with tie swaps | note |",
+             "|---|---|---|---|---|---|---|---|---|---|---|"]
+    for r in parity.RECORDS:
+        lines.append(f"| {r['variant']} | {r['workload']} | {r['dtype']} | {r['heads']} | {r['rows']} | "
+                     f"{r['row_err']:.3e} | {r['global_err']:.3e} | {r['fro_err']:.3e} | {r['tol']:.0e} | "
+                     f"{r['tie_rows']} | {r['note']} |")
+    d = os.path.dirname(path)
+    if d:
+        os.makedirs(d, exist_ok=True)
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 @pytest.fixture(scope="session")
 def gpu():
     """The HIP library bound to cuda:0. GPU tests fail (not skip) without a GPU,

@@ -80,3 +80,28 @@ def check_selection_global(gpu_idx, S_ref, budget, prior_diagonal, band=TIE_BAND
         for f in diff:
             assert abs(S_ref.ravel()[f] - tau) <= band * scale, (f, S_ref.ravel()[f], tau)
     return len(diff)
+
+
+def err_stats(Z, Zref):
+    """Error measures of an output against the oracle's (rows = last axis):
+    the max row-normwise relative error (the bar), the largest elementwise
+    error over the largest reference magnitude, and the relative Frobenius
+    error."""
+    Z = np.asarray(Z, dtype=np.float64)
+    Zref = np.asarray(Zref, dtype=np.float64)
+    diff = np.abs(Z - Zref)
+    fro = float(np.sqrt((diff ** 2).sum()) / max(np.sqrt((Zref ** 2).sum()), 1e-300)) if Z.size else 0.0
+    glob = float(diff.max() / max(np.abs(Zref).max(), 1e-300)) if Z.size else 0.0
+    return {"row": row_rel_err(Z, Zref), "global": glob, "fro": fro}
+
+
+# Parity results of the full-size tests, one dict per (variant, workload);
+# conftest.py writes them as a table at the end of the session when the
+# environment variable MRA_PARITY_LOG names a file.
+RECORDS = []
+
+
+def record(variant, workload, dtype, heads, rows, stats, tol, tie_rows, note=""):
+    RECORDS.append({"variant": variant, "workload": workload, "dtype": dtype, "heads": heads, "rows": rows,
+                    "row_err": stats["row"], "global_err": stats["global"], "fro_err": stats["fro"],
+                    "tol": tol, "tie_rows": tie_rows, "note": note})

@@ -162,13 +162,13 @@ def test_global_selection_validation(lib):
 def test_step_validation(lib):
     # pool: pairs must be given together, at least one pair
     p = lib.mra_pool
-    assert p(A, None, None, None, None, None, None, 1, 1, 64, 64, 32, 1, None) == INVALID
-    assert p(None, None, None, None, None, None, None, 1, 1, 64, 64, 32, 1, None) == INVALID
-    assert p(A, None, None, MIS, None, None, None, 1, 1, 64, 64, 32, 1, None) == MISALIGNED
-    assert p(A, A, A, A, A, A, None, 1, 1, 64, 64, 32, 5, None) == UNSUPPORTED
-    assert p(A, None, None, A, None, None, A, 1, 1, 64, 64, 32, 1, None) == INVALID   # packing needs k and v
-    assert p(A, A, None, A, A, None, A, 1, 1, 64, 64, 32, 1, None) == INVALID
-    assert p(A, A, A, A, A, A, MIS, 1, 1, 64, 64, 32, 1, None) == MISALIGNED
+    assert p(A, None, None, None, None, None, 1, 1, 64, 64, 32, 1, None) == INVALID
+    assert p(None, None, None, None, None, None, 1, 1, 64, 64, 32, 1, None) == INVALID
+    assert p(A, None, None, MIS, None, None, 1, 1, 64, 64, 32, 1, None) == MISALIGNED
+    assert p(A, A, A, A, A, A, 1, 1, 64, 64, 32, 5, None) == UNSUPPORTED
+    assert p(A, A, None, A, None, None, 1, 1, 64, 64, 32, 1, None) == INVALID        # k without kp
+    assert p(A, A, A, A, A, MIS, 1, 1, 64, 64, 32, 1, None) == MISALIGNED
+    assert p(None, None, None, None, None, None, 0, 1, 64, 64, 32, 1, None) == INVALID
     # coarse scores
     assert lib.mra_coarse_scores(A, A, None, 1, 1, 64, 64, 32, None) == INVALID
     assert lib.mra_coarse_scores(A, A, A, 1, 1, 64, 100, 32, None) == UNSUPPORTED
@@ -180,18 +180,18 @@ def test_step_validation(lib):
     assert lib.mra_coarse_term(A, None, A, A, A, A, 1, 1, 64, 64, 32, 1, None) == INVALID
     assert lib.mra_coarse_term(A, A, A, A, A, MIS, 1, 1, 64, 64, 32, 1, None) == MISALIGNED
     # tile pass: coarse term all-or-nothing; sparse-only needs budget >= 1
-    t = lambda q, k, v, kv, idx, cm, cs, cv, out, B, H, n, d, blk, m, dt, lse=None: \
-        lib.mra_block_sddmm_spmm(q, k, v, kv, idx, cm, cs, cv, out, lse, B, H, n, d, blk, m, dt, None)
-    assert t(A, A, A, None, A, A, None, A, A, 1, 1, 64, 64, 32, 1, 1) == INVALID
-    assert t(A, A, A, None, None, None, None, None, A, 1, 1, 64, 64, 32, 0, 1) == INVALID
-    assert t(A, A, A, None, A, A, A, A, A, 1, 1, 64, 64, 32, 3, 1) == INVALID
-    assert t(A, A, A, None, A, A, A, A, MIS, 1, 1, 64, 64, 32, 1, 1) == MISALIGNED
-    assert t(A, A, A, None, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 1, lse=MIS) == MISALIGNED
-    assert t(A, A, A, None, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 2) == UNSUPPORTED
-    assert t(A, A, None, None, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 1) == INVALID   # no v at all
-    assert t(A, None, A, None, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 1) == INVALID   # no k
-    assert t(A, None, None, MIS, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 1) == MISALIGNED
-    assert t(None, None, None, None, None, A, A, A, None, 0, 1, 64, 64, 32, 1, 1) == OK
+    t = lambda q, k, v, idx, cm, cs, cv, out, B, H, n, d, blk, m, dt, lse=None: \
+        lib.mra_block_sddmm_spmm(q, k, v, idx, cm, cs, cv, out, lse, B, H, n, d, blk, m, dt, None)
+    assert t(A, A, A, A, A, None, A, A, 1, 1, 64, 64, 32, 1, 1) == INVALID
+    assert t(A, A, A, None, None, None, None, A, 1, 1, 64, 64, 32, 0, 1) == INVALID
+    assert t(A, A, A, A, A, A, A, A, 1, 1, 64, 64, 32, 3, 1) == INVALID
+    assert t(A, A, A, A, A, A, A, MIS, 1, 1, 64, 64, 32, 1, 1) == MISALIGNED
+    assert t(A, A, A, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 1, lse=MIS) == MISALIGNED
+    assert t(A, A, A, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 2) == UNSUPPORTED
+    assert t(A, A, None, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 1) == INVALID   # no v
+    assert t(A, None, A, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 1) == INVALID   # no k
+    assert t(A, MIS, A, A, A, A, A, A, 1, 1, 64, 64, 32, 1, 1) == MISALIGNED
+    assert t(None, None, None, None, A, A, A, None, 0, 1, 64, 64, 32, 1, 1) == OK
 
 
 def bwd(lib, q=A, k=A, v=A, out=A, dout=A, lse=A, idx=A, dq=A, dk=A, dv=A, ws=A, wsb=1 << 40,

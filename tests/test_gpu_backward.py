@@ -4,23 +4,32 @@ the C ABI, against the float64 oracle on the same seeded inputs:
 ``O.mra_grads`` (torch float64 autograd of the factored form) and
 ``O.mra_lse``, both evaluated under the GPU's own selection.
 
-Metrics, per head and tensor: gradients max|err| / max|ref| <= 2e-5 (float32
-inputs: float32 products and sums over at most n terms) or 2e-2 (bfloat16
-inputs, whose probabilities and logit gradients are rounded to bfloat16
-before the matrix-core products, 2^-9 relative each); log normalisers
-|err| <= 1e-5 (float32) or 4e-3 (bfloat16: rounded weights change the row sum
-by at most 2^-9 relative) times max(1, |L|)."""
+Metrics, per head and tensor:
+* floored row-normwise error: max over rows i of ||err_i||_inf /
+  max(||ref_i||_inf, f), the floor f = 1/8 of the head's median row norm, so
+  that rows of ordinary size are judged against their own magnitude and only
+  rows far below it against the floor;
+* max|err| / max|ref| over the whole tensor (<= 2e-5 float32, 2e-2 bfloat16).
+Gradient rows are sums of many signed terms (the logit gradients
+p (G.v - delta) sum to zero over a row), so a row's relative error is the
+rounding of its terms times the ratio of the sum of their magnitudes to the
+magnitude of the sum. Float32 inputs: float32 products and sums; bfloat16
+inputs: probabilities and logit gradients rounded to bfloat16 (2^-9 relative
+each) before the matrix-core products. Log normalisers: |err| <= 1e-5
+(float32) or 4e-3 (bfloat16: rounded weights change the row sum by at most
+2^-9 relative) times max(1, |L|)."""
 import numpy as np
 import pytest
 import torch
 
 from oracle import mra_oracle as O
 from paper_2207_10284_amd import inputs
-from tests.parity import dev, host
+from tests.parity import dev, host, record
 
 pytestmark = pytest.mark.gpu
 
-GRAD_TOL = {"f32": 2e-5, "bf16": 2e-2}
+GRAD_TOL = {"f32": 2e-5, "bf16": 2e-2}        # max|err| / max|ref|
+GRAD_ROW_TOL = {"f32": 1e-3, "bf16": 1e-1}    # floored row-normwise
 LSE_TOL = {"f32": 1e-5, "bf16": 4e-3}
 
 
@@ -41,6 +50,17 @@ def _case(index, B, H, n, d, dtype, budget, kind="ar1"):
 
 def _rel(a, ref):
     return float(np.abs(a - ref).max() / max(np.abs(ref).max(), 1e-30))
+
+
+def _rowerr(a, ref):
+    """Floored row-normwise relative error (rows = tokens)."""
+    rn = np.abs(ref).max(axis=-1)
+    floor = max(np.median(rn) / 8.0, 1e-30)
+    return float((np.abs(a - ref).max(axis=-1) / np.maximum(rn, floor)).max())
+
+
+def _fro(a, ref):
+    return float(np.sqrt(((a - ref) ** 2).sum()) / max(np.sqrt((ref ** 2).sum()), 1e-300))
 
 
 def _forward(gpu, variant, tq, tk, tv, budget, prior=False):
@@ -70,7 +90,8 @@ def _check(gpu, variant, q, k, v, g, budget, dtype, prior=False, heads=None):
     grads = [host(t) for t in (dq, dk, dv)]
     B, H = q.shape[:2]
     heads = [(b, h) for b in range(B) for h in range(H)] if heads is None else heads
-    worst = {"lse": 0.0, "dq": 0.0, "dk": 0.0, "dv": 0.0}
+    worst = {"lse": 0.0, "dq": 0.0, "dk": 0.0, "dv": 0.0, "dq_row": 0.0, "dk_row": 0.0, "dv_row": 0.0,
+             "dq_fro": 0.0, "dk_fro": 0.0, "dv_fro": 0.0}
     for b, h in heads:
         qh, kh, vh, gh = (a[b, h].astype(np.float64) for a in (q, k, v, g))
         Lref = O.mra_lse(qh, kh, 32, gi[b, h], coarse)
@@ -78,11 +99,21 @@ def _check(gpu, variant, q, k, v, g, budget, dtype, prior=False, heads=None):
         ref = O.mra_grads(qh, kh, vh, gh, 32, gi[b, h], coarse)
         for name, got, want in zip(("dq", "dk", "dv"), grads, ref):
             worst[name] = max(worst[name], _rel(got[b, h], want))
+            worst[name + "_row"] = max(worst[name + "_row"], _rowerr(got[b, h], want))
+            worst[name + "_fro"] = max(worst[name + "_fro"], _fro(got[b, h], want))
     _say(" ", variant, q.shape, dtype, budget, {k_: f"{e:.2e}" for k_, e in worst.items()})
     assert worst["lse"] <= LSE_TOL[dtype], worst
     for name in ("dq", "dk", "dv"):
         assert worst[name] <= GRAD_TOL[dtype], (name, worst)
+        assert worst[name + "_row"] <= GRAD_ROW_TOL[dtype], (name, worst)
     return worst
+
+
+def _record_grads(label, w, heads, worst):
+    for name in ("dq", "dk", "dv"):
+        record(f"backward {name} ({label})", w.name, w.dtype, len(heads), len(heads) * w.nb,
+               {"row": worst[name + "_row"], "global": worst[name], "fro": worst[name + "_fro"]},
+               GRAD_ROW_TOL[w.dtype], "-", note="floored row-normwise; whole heads")
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -177,13 +208,16 @@ def test_backward_workload_full_size(gpu, name):
     g = np.random.Generator(np.random.PCG64(w.seed + 7)).standard_normal(q.shape)
     g = inputs.round_to_bf16(g) if w.dtype == "bf16" else g.astype(np.float32)
     heads = sorted({(0, 0), (w.B - 1, w.H - 1)})
-    _check(gpu, "mra2", q, k, v, g, w.budget, w.dtype, heads=heads)
+    worst = _check(gpu, "mra2", q, k, v, g, w.budget, w.dtype, heads=heads)
+    _record_grads("MRA-2", w, heads, worst)
 
 
-def test_backward_long_sequence_sampled_rows(gpu):
-    """The 32768-token workload at its real shape: dQ of sampled block-rows of
-    one head against the oracle restricted to those rows (exact there), the
-    log normalisers of the whole head, and finite dK, dV everywhere."""
+def test_backward_long_sequence_full_head(gpu):
+    """The 32768-token workload at its real shape (forward and backward of
+    all 16 heads on the GPU): dQ, dK, dV and the log normalisers of one whole
+    head against the oracle (Sec. 4.3 Alg. 2 differentiated through
+    eq. actual_approx_mat_form with the selection held fixed), and finite
+    gradients everywhere."""
     w = inputs.WORKLOADS["long-32768"]
     _say("backward workload", w.name)
     q, k, v = inputs.make_qkv(w)
@@ -193,17 +227,21 @@ def test_backward_long_sequence_sampled_rows(gpu):
     out, idx, lse = _forward(gpu, "mra2", tq, tk, tv, w.budget)
     dq, dk, dv = gpu.attention_backward(tq, tk, tv, out, tg, lse, idx)
     torch.cuda.synchronize()
-    assert torch.isfinite(dk).all() and torch.isfinite(dv).all()
+    for t in (dq, dk, dv):
+        assert torch.isfinite(t).all()
     b, h = w.B - 1, w.H - 1
     gi = host(idx[b, h]).astype(np.int64)
     qh, kh, vh, gh = (a[b, h].astype(np.float64) for a in (q, k, v, g))
     Lref = O.mra_lse(qh, kh, 32, gi)
     lerr = float((np.abs(host(lse[b, h]) - Lref) / np.maximum(1.0, np.abs(Lref))).max())
-    r = np.random.Generator(np.random.PCG64(w.seed + 11))
-    rows = sorted({0, w.nb - 1} | set(int(x) for x in r.choice(w.nb, 6, replace=False)))
-    dq_ref, _, _ = O.mra_grads(qh, kh, vh, gh, 32, gi, rows=rows)
-    blk = np.concatenate([np.arange(x * 32, x * 32 + 32) for x in rows])
-    err = _rel(host(dq[b, h])[blk], dq_ref[blk])
-    _say("  long-32768 lse", f"{lerr:.2e}", "dq rows", rows, f"{err:.2e}")
+    ref = O.mra_grads(qh, kh, vh, gh, 32, gi)
+    worst = {"lse": lerr}
+    for name, got, want in zip(("dq", "dk", "dv"), (dq, dk, dv), ref):
+        gh_ = host(got[b, h])
+        worst[name], worst[name + "_row"], worst[name + "_fro"] = _rel(gh_, want), _rowerr(gh_, want), _fro(gh_, want)
+    _say("  long-32768", {k_: f"{e:.2e}" for k_, e in worst.items()})
+    _record_grads("MRA-2", w, [(b, h)], worst)
     assert lerr <= LSE_TOL[w.dtype]
-    assert err <= GRAD_TOL[w.dtype]
+    for name in ("dq", "dk", "dv"):
+        assert worst[name] <= GRAD_TOL[w.dtype], (name, worst)
+        assert worst[name + "_row"] <= GRAD_ROW_TOL[w.dtype], (name, worst)

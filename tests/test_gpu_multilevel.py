@@ -12,7 +12,7 @@ import torch
 
 from oracle import mra_oracle as O
 from paper_2207_10284_amd import inputs
-from tests.parity import TOL, check_selection, dev, host, row_rel_err
+from tests.parity import TOL, check_selection, dev, err_stats, host, record, row_rel_err
 
 pytestmark = pytest.mark.gpu
 
@@ -22,16 +22,17 @@ def _say(*a):
 
 
 def _check_selections(i1, i2, q, k, s0, m1, m2):
-    """i1 [nb0, m1], i2 [nb, m2] of one head against the oracle's scores."""
+    """i1 [nb0, m1], i2 [nb, m2] of one head against the oracle's scores.
+    Returns the number of rows (of both levels) that differ by near-ties."""
     r = s0 // 32
     S0 = O.coarse_logits(O.block_mean(q, s0), O.block_mean(k, s0))
-    check_selection(i1, S0, m1)
+    differ = check_selection(i1, S0, m1)
     S1 = O.coarse_logits(O.block_mean(q, 32), O.block_mean(k, 32))
     masked = np.full_like(S1, -np.inf)
     for x in range(S1.shape[0]):
         cand = [int(Y) * r + t for Y in i1[x // r] for t in range(r)]
         masked[x, cand] = S1[x, cand]
-    check_selection(i2, masked, m2)
+    return differ + check_selection(i2, masked, m2)
 
 
 def _run(gpu, q, k, v, s0, m1, m2, dtype):
@@ -104,8 +105,8 @@ def test_multilevel_repeat_and_smaller_call(gpu, dtype):
 @pytest.mark.parametrize("name", list(inputs.WORKLOADS))
 def test_multilevel_workload_full_size(gpu, name):
     """Each workload at its real shape with its three-resolution setting;
-    sampled block-rows of sampled heads checked against the oracle under the
-    GPU's selections, which are checked against the oracle's scores."""
+    every block-row of every head checked against the oracle under the GPU's
+    selections, which are checked against the oracle's scores."""
     w = inputs.WORKLOADS[name]
     s0, m1 = inputs.MULTILEVEL[name]
     m2 = w.budget
@@ -113,17 +114,16 @@ def test_multilevel_workload_full_size(gpu, name):
     q, k, v = inputs.make_qkv(w)
     out, i1, i2 = _run(gpu, q, k, v, s0, m1, m2, w.dtype)
     out_h = host(out)
-    r = np.random.Generator(np.random.PCG64(w.seed + 3))
-    heads = {(0, 0), (w.B - 1, w.H - 1)}
-    while len(heads) < min(3, w.B * w.H):
-        heads.add((int(r.integers(w.B)), int(r.integers(w.H))))
-    worst = 0.0
-    for b, h in sorted(heads):
-        qh, kh, vh = q[b, h].astype(np.float64), k[b, h].astype(np.float64), v[b, h].astype(np.float64)
-        _check_selections(i1[b, h], i2[b, h], qh, kh, s0, m1, m2)
-        rows = sorted({0, w.nb - 1, *[int(x) for x in r.integers(w.nb, size=6)]})
-        Z, _, _ = O.mra_multilevel_factored(qh, kh, vh, s0, 32, m1, m2, idx1=i1[b, h], idx2=i2[b, h], rows=rows)
-        got = np.concatenate([out_h[b, h, x * 32:(x + 1) * 32] for x in rows])
-        worst = max(worst, row_rel_err(got, Z))
-    _say("  multilevel", name, "worst", worst)
-    assert worst <= TOL[w.dtype]
+    del out
+    Zall = np.empty(out_h.shape)
+    differ = 0
+    for b in range(w.B):
+        for h in range(w.H):
+            qh, kh, vh = q[b, h].astype(np.float64), k[b, h].astype(np.float64), v[b, h].astype(np.float64)
+            differ += _check_selections(i1[b, h], i2[b, h], qh, kh, s0, m1, m2)
+            Zall[b, h], _, _ = O.mra_multilevel_factored(qh, kh, vh, s0, 32, m1, m2, idx1=i1[b, h], idx2=i2[b, h])
+    st = err_stats(out_h, Zall)
+    record(f"three resolutions R = {{{s0}, 32, 1}}, budgets {m1}/{m2}", name, w.dtype, w.B * w.H,
+           w.B * w.H * w.nb, st, TOL[w.dtype], differ, note="tie rows at both levels")
+    _say("  multilevel", name, "worst", st["row"])
+    assert st["row"] <= TOL[w.dtype]

@@ -87,6 +87,9 @@ def test_full_budget_is_torch_softmax(n, b, d, scale):
     Z, _ = O.mra_dense(q, k, v, b, n // b)
     np.testing.assert_allclose(Z, ref, rtol=1e-11, atol=1e-12)
     np.testing.assert_allclose(O.exact_attention(q, k, v), ref, rtol=1e-11, atol=1e-12)
+    # any slab of rows, computed alone (the benchmark's accuracy measure uses it)
+    for i0, i1 in ((0, n), (0, 1), (5, 37), (n - 3, n)):
+        np.testing.assert_allclose(O.exact_attention_rows(q, k, v, i0, i1), ref[i0:i1], rtol=1e-11, atol=1e-12)
 
 
 def _constant_block_qk(r, n, b, d, scale=1.0):
@@ -129,7 +132,7 @@ def test_constant_blocks_mixed_v_nonconstant():
 # ---------------------------------------------------------------- invariants
 @pytest.mark.parametrize("m", [0, 1, 3, 8])
 def test_rows_sum_to_one(m):
-    """D^ normalises every row of A^ (Sec. 3.1): with V = 1 the output is 1."""
+    """D^ normalises every row of A^ (Sec. 2.1): with V = 1 the output is 1."""
     r = _rng(5)
     n, b, d = 256, 32, 16
     q, k = r.standard_normal((n, d)) * 3, r.standard_normal((n, d)) * 3
