@@ -495,6 +495,68 @@ def mra_grads(q, k, v, g, b, idx, coarse=True, rows=None):
     return tq.grad.numpy(), tk.grad.numpy(), tv.grad.numpy()
 
 
+def mra_grad_terms(q, k, v, g, b, idx, coarse=True, absolute=False):
+    """The gradients of sum(g * Z) for one head under the fixed selection idx,
+    written out by the chain rule in numpy (an independent formulation of
+    mra_grads), or with absolute=True the sums of the magnitudes of the terms
+    each gradient element is a sum of: the size against which a rounding of
+    those terms is measured (a first-order error bound).
+
+    Per block-row x (queries i, softmax p over the fine logits c Q_i.K_j of
+    the refined columns and the coarse logits S~[x,y] + ln b of the other
+    blocks, delta_i = g_i . Z_i):
+      logit gradient  dl = p (g_i . value - delta_i)
+      dq_i += c sum_j dl_ij k_j,  dk_j += c sum_i dl_ij q_i,  dv_j += sum_i p_ij g_i
+      dS~[x,y] = sum_i dl_iy (the 32 queries share S~[x,y]),  dV~_y += sum_i p_iy g_i
+    then dQ~ = c dS~ K~, dK~ = c dS~^T Q~, each reaching the b rows of its
+    block divided by b (the pooled rows are block means). With
+    absolute=True every sum is taken over the magnitudes of its terms, down to
+    the inputs (|Z| = p |v|, |delta| = |g| . |Z|, |g . v| = |g| . |v|, and the
+    difference in dl becomes a sum), so each element bounds what rounding
+    any of the intermediate terms can move it by, relative to that
+    rounding."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    g = np.asarray(g, dtype=np.float64)
+    f = np.abs if absolute else (lambda a: a)
+    n, d = q.shape
+    nb = n // b
+    c = 1.0 / math.sqrt(d)
+    qp, kp, vp = block_mean(q, b), block_mean(k, b), block_mean(v, b)
+    S = coarse_logits(qp, kp)
+    dq, dk, dv = np.zeros_like(q), np.zeros_like(k), np.zeros_like(v)
+    dS = np.zeros((nb, nb))
+    dvp = np.zeros_like(vp)
+    for x in range(nb):
+        sel = [int(y) for y in idx[x] if 0 <= int(y) < nb]
+        chosen = set(sel)
+        rest = [y for y in range(nb) if y not in chosen] if coarse else []
+        cols = np.array([j for y in sel for j in range(y * b, (y + 1) * b)], dtype=np.int64)
+        rows = slice(x * b, (x + 1) * b)
+        logits = np.concatenate([q[rows] @ k[cols].T * c,
+                                 np.broadcast_to(S[x, rest] + math.log(b), (b, len(rest)))], axis=1)
+        e = np.exp(logits - logits.max(axis=1, keepdims=True))
+        p = e / e.sum(axis=1, keepdims=True)
+        pf, pc = p[:, :len(cols)], p[:, len(cols):]
+        Z = pf @ f(v[cols]) + pc @ f(vp[rest])
+        delta = (f(g[rows]) * Z).sum(axis=1, keepdims=True)
+        gvf, gvc = f(g[rows]) @ f(v[cols]).T, f(g[rows]) @ f(vp[rest]).T
+        # absolute: every factor is already a magnitude, and the difference
+        # of the two sums becomes their sum
+        sgn = 1.0 if absolute else -1.0
+        af, ac = pf * (gvf + sgn * delta), pc * (gvc + sgn * delta)
+        dq[rows] += c * af @ f(k[cols])
+        dk[cols] += c * af.T @ f(q[rows])
+        dv[cols] += pf.T @ f(g[rows])
+        dS[x, rest] += ac.sum(axis=0)
+        dvp[rest] += pc.T @ f(g[rows])
+    dq += np.repeat(c * dS @ f(kp), b, axis=0) / b
+    dk += np.repeat(c * dS.T @ f(qp), b, axis=0) / b
+    dv += np.repeat(dvp, b, axis=0) / b
+    return dq, dk, dv
+
+
 def mra_lse(q, k, b, idx, coarse=True):
     """Each query's log normaliser L_i = ln(sum of row i of A^): the fine
     terms exp(P_ij) of its refined blocks plus, with coarse=True, b exp(S~)

@@ -719,3 +719,47 @@ def test_multilevel_selection_nested_and_tied():
     z = np.zeros((n, d))
     i1, i2 = O.select_multilevel(z, z, s0, b, 2, 3)
     assert (i1 == [0, 1]).all() and (i2 == [0, 1, 2]).all()
+
+
+@pytest.mark.parametrize("case", ["mra2", "mra2_budget0", "mra2_full", "mra2s", "global"])
+def test_grad_terms_signed_equal_autograd(case):
+    """The chain rule written out (mra_grad_terms) equals torch's autograd of
+    the factored form (mra_grads, itself pinned by finite differences and by
+    softmax attention at full budget): per-row, empty, full, sparse-only and
+    head-wide (ragged, with empty rows) selections."""
+    r = _rng(190)
+    n, b, d = 128, 16, 8
+    q, k, v, g = (r.standard_normal((n, d)) for _ in range(4))
+    S = O.coarse_logits(O.block_mean(q, b), O.block_mean(k, b))
+    coarse = case != "mra2s"
+    idx = {"mra2": O.select_blocks(S, 3), "mra2_budget0": O.select_blocks(S, 0),
+           "mra2_full": O.select_blocks(S, n // b), "mra2s": O.select_blocks(S, 2),
+           "global": O.select_global(S, 13, True)}[case]
+    want = O.mra_grads(q, k, v, g, b, idx, coarse)
+    got = O.mra_grad_terms(q, k, v, g, b, idx, coarse)
+    for a, w in zip(got, want):
+        np.testing.assert_allclose(a, w, rtol=1e-10, atol=1e-12)
+
+
+def test_grad_terms_magnitudes_bound_gradients():
+    """The term magnitudes bound every gradient element (triangle inequality)
+    and, where every term of dv is nonnegative (g >= 0), equal |dv|; they do
+    not depend on the sign of g and scale with it as the gradients do."""
+    r = _rng(191)
+    n, b, d = 128, 16, 8
+    q, k, v, g = (r.standard_normal((n, d)) for _ in range(4))
+    idx = O.select_blocks(O.coarse_logits(O.block_mean(q, b), O.block_mean(k, b)), 3)
+    grads = O.mra_grad_terms(q, k, v, g, b, idx)
+    mags = O.mra_grad_terms(q, k, v, g, b, idx, absolute=True)
+    for a, m_ in zip(grads, mags):
+        assert (m_ >= np.abs(a) * (1 - 1e-12)).all()
+    # cancellation: the logit gradients of a row sum to zero, so dq is much
+    # smaller than its term magnitudes somewhere
+    assert (np.abs(grads[0]).max(axis=1) < 0.5 * mags[0].max(axis=1)).any()
+    gp = np.abs(g)
+    _, _, dv = O.mra_grad_terms(q, k, v, gp, b, idx)
+    _, _, mv = O.mra_grad_terms(q, k, v, gp, b, idx, absolute=True)
+    np.testing.assert_allclose(mv, dv, rtol=1e-12, atol=1e-14)
+    m2 = O.mra_grad_terms(q, k, v, -2.0 * g, b, idx, absolute=True)
+    for a, m_ in zip(m2, mags):
+        np.testing.assert_allclose(a, 2.0 * m_, rtol=1e-12, atol=1e-14)
