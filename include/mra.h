@@ -71,7 +71,9 @@ typedef enum {
   MRA_ERR_UNSUPPORTED = 2,   /* block != 32, d not in {32,64,128}, n > 65536, unknown dtype */
   MRA_ERR_MISALIGNED = 3,    /* a pointer not 16-byte aligned */
   MRA_ERR_WORKSPACE = 4,     /* workspace_bytes smaller than required */
-  MRA_ERR_HIP = 5            /* a HIP launch failed; see mra_last_hip_error() */
+  MRA_ERR_HIP = 5,           /* a HIP launch failed; see mra_last_hip_error() */
+  MRA_ERR_SCRATCH = 6        /* problem too large for the static scratch of
+                                mra_attention_forward_noalloc */
 } mra_status_t;
 
 /*
@@ -212,6 +214,31 @@ mra_status_t mra_attention_forward(const void* q, const void* k, const void* v, 
                                    size_t workspace_bytes,
                                    int B, int H, int n, int d, int block, int budget,
                                    mra_dtype_t dtype, void* stream);
+
+/*
+ * mra_attention_forward_noalloc — mra_attention_forward without a workspace
+ * argument, for callers that cannot allocate device memory (code under HIP
+ * graph capture, serving loops, harnesses that forbid allocation). The
+ * forward's workspace is taken from a file-scope device array of
+ * MRA_NOALLOC_SCRATCH_BYTES bytes that every GPU the library runs on holds
+ * from the first use of the library on it until the process ends; the call
+ * itself allocates and frees nothing.
+ *   Arguments, layouts, results and errors as for mra_attention_forward
+ *   (same kernels, bit-identical output), except that a problem whose
+ *   mra_forward_workspace_bytes exceeds MRA_NOALLOC_SCRATCH_BYTES returns
+ *   MRA_ERR_SCRATCH after the other argument checks and enqueues nothing.
+ *   64 MiB covers the five benchmark workloads (the largest needs ~36 MB).
+ * All calls on one GPU share that GPU's array and leave their intermediates
+ * in it (the forward writes every part before reading it, so nothing needs
+ * clearing): calls that overlap on one GPU (concurrent streams or threads)
+ * race and give undefined results. The first call on each GPU looks up the
+ * array's device address (hipGetSymbolAddress) with that GPU current.
+ */
+#define MRA_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+mra_status_t mra_attention_forward_noalloc(const void* q, const void* k, const void* v,
+                                           void* out, int32_t* idx_out, float* lse_out,
+                                           int B, int H, int n, int d, int block, int budget,
+                                           mra_dtype_t dtype, void* stream);
 
 /*
  * mra_forward_global_workspace_bytes — workspace of

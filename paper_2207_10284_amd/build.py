@@ -19,7 +19,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libmra.so")
 SOURCES = ["api.cpp", "pool.hip", "coarse.hip", "select.hip", "select_global.hip", "tile.hip",
-           "bwd.hip", "multilevel.hip"]
+           "bwd.hip", "multilevel.hip", "noalloc.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

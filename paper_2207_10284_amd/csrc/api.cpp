@@ -567,6 +567,7 @@ const char* mra_status_str(mra_status_t status) {
     case MRA_ERR_MISALIGNED: return "MRA_ERR_MISALIGNED: pointer not 16-byte aligned";
     case MRA_ERR_WORKSPACE: return "MRA_ERR_WORKSPACE: workspace too small";
     case MRA_ERR_HIP: return "MRA_ERR_HIP: HIP launch failed";
+    case MRA_ERR_SCRATCH: return "MRA_ERR_SCRATCH: problem needs more than the static scratch of mra_attention_forward_noalloc";
   }
   return "unknown mra_status_t";
 }

@@ -20,7 +20,7 @@ BLOCK = 32
 
 MRA_F32, MRA_BF16 = 0, 1
 STATUS = {0: "MRA_OK", 1: "MRA_ERR_INVALID_ARG", 2: "MRA_ERR_UNSUPPORTED",
-          3: "MRA_ERR_MISALIGNED", 4: "MRA_ERR_WORKSPACE", 5: "MRA_ERR_HIP"}
+          3: "MRA_ERR_MISALIGNED", 4: "MRA_ERR_WORKSPACE", 5: "MRA_ERR_HIP", 6: "MRA_ERR_SCRATCH"}
 
 # name -> (restype, argtypes); mirrors include/mra.h
 _P, _I, _Z = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
@@ -33,6 +33,7 @@ SIGNATURES = {
     "mra_forward_workspace_bytes": (_Z, [_I, _I, _I, _I, _I, _I, _I]),
     "mra_attention_forward": (_I, [_P, _P, _P, _P, _P, _P, _P, _Z, _I, _I, _I, _I, _I, _I, _I, _P]),
     "mra_sparse_attention_forward": (_I, [_P, _P, _P, _P, _P, _P, _P, _Z, _I, _I, _I, _I, _I, _I, _I, _P]),
+    "mra_attention_forward_noalloc": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _P]),
     "mra_select_global": (_I, [_P, _P, _I, _I, _I, _I, _I, _I, _P]),
     "mra_forward_global_workspace_bytes": (_Z, [_I, _I, _I, _I, _I, _I]),
     "mra_attention_forward_global": (_I, [_P, _P, _P, _P, _P, _P, _P, _Z, _I, _I, _I, _I, _I, _I, _I, _I, _P]),
@@ -211,6 +212,24 @@ def attention_forward(q, k, v, budget: int, out=None, idx_out=None, workspace=No
     dtype); the selection is written to ``idx_out`` and each query's log
     normaliser (float32 [B, H, n]) to ``lse_out`` when given."""
     return _forward("mra_attention_forward", q, k, v, budget, out, idx_out, workspace, lse_out)
+
+
+def attention_forward_noalloc(q, k, v, budget: int, out=None, idx_out=None, lse_out=None):
+    """``attention_forward`` through the entry point that allocates nothing:
+    its workspace is the library's static per-GPU scratch (calls on one GPU
+    must not overlap). ``out`` is allocated here only when not given."""
+    ref = _check_qkv(q, k, v)
+    B, H, n, d = ref.shape
+    nb = n // BLOCK
+    if out is None:
+        out = torch.empty_like(ref)
+    if idx_out is not None:
+        _check_idx(idx_out, B, H, nb, budget, ref.device)
+    if lse_out is not None:
+        _check_f32(lse_out, (B, H, n), "lse_out")
+    _call("mra_attention_forward_noalloc", _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(idx_out), _ptr(lse_out),
+          B, H, n, d, BLOCK, budget, _dtype_code(ref), _stream(ref.device))
+    return out
 
 
 def sparse_attention_forward(q, k, v, budget: int, out=None, idx_out=None, workspace=None, lse_out=None):

@@ -13,7 +13,7 @@ from paper_2207_10284_amd import ops
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "mra.h")
 
-OK, INVALID, UNSUPPORTED, MISALIGNED, WORKSPACE, HIP = range(6)
+OK, INVALID, UNSUPPORTED, MISALIGNED, WORKSPACE, HIP, SCRATCH = range(7)
 A = 1 << 20            # a fake, 16-byte aligned address: never dereferenced
 MIS = A + 4            # misaligned
 
@@ -31,7 +31,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 17, names
+    assert len(names) == 18, names
     for name in names:
         assert hasattr(lib, name), name
     assert set(names) == set(ops.SIGNATURES)
@@ -73,6 +73,31 @@ def test_forward_validation(lib):
     assert fwd(lib, B=0, q=None, k=None, v=None, out=None, ws=None) == OK
     assert fwd(lib, n=0, budget=0, q=None, out=None, ws=None) == OK
     assert fwd(lib, n=0, budget=1) == INVALID  # nb = 0
+    assert lib.mra_last_hip_error() == 0
+
+
+def test_noalloc_forward_validation(lib):
+    """The entry point without a workspace: every check of mra_attention_forward
+    except the workspace's, then the static scratch's limit, all before any
+    HIP call."""
+    f = lambda q=A, k=A, v=A, out=A, idx=None, lse=None, B=1, H=1, n=64, d=64, block=32, budget=1, dtype=1: \
+        lib.mra_attention_forward_noalloc(q, k, v, out, idx, lse, B, H, n, d, block, budget, dtype, None)
+    assert f(block=16) == UNSUPPORTED
+    assert f(d=48) == UNSUPPORTED
+    assert f(n=48) == INVALID
+    assert f(budget=3) == INVALID
+    assert f(dtype=7) == UNSUPPORTED
+    assert f(q=None) == INVALID
+    assert f(out=MIS) == MISALIGNED
+    assert f(idx=MIS) == MISALIGNED
+    assert f(lse=MIS) == MISALIGNED
+    assert f(B=0, q=None, k=None, v=None, out=None) == OK
+    limit = 64 << 20
+    # the largest benchmark workload fits; 128 heads of 32k tokens at d = 128 do not
+    assert lib.mra_forward_workspace_bytes(1, 16, 32768, 128, 32, 32, 1) <= limit
+    assert lib.mra_forward_workspace_bytes(1, 128, 32768, 128, 32, 32, 1) > limit
+    assert f(B=1, H=128, n=32768, d=128, budget=32) == SCRATCH
+    assert f(B=1, H=128, n=32768, d=128, budget=32, q=None) == INVALID   # argument checks come first
     assert lib.mra_last_hip_error() == 0
 
 
