@@ -6,6 +6,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <cstdlib>
 
 #include "kernels.h"
 
@@ -61,11 +62,41 @@ mra_status_t hip_status(hipError_t e) {
   return MRA_ERR_HIP;
 }
 
+// Debug aid: with MRA_DEBUG_NANFILL=1 in the environment, every call that
+// computes fills its outputs and the part of the workspace it uses with quiet
+// NaN before its kernels run (bfloat16 outputs with bfloat16 NaNs; index
+// outputs with the same bits, an id outside every block range). An element
+// the call fails to write then stays NaN (or an invalid id), and a value read
+// before the call wrote it turns the results that depend on it into NaN.
+bool nanfill_enabled() {
+  const char* e = std::getenv("MRA_DEBUG_NANFILL");
+  return e != nullptr && e[0] == '1';
+}
+
+constexpr uint32_t kNanF32 = 0x7FC00000u;        // float32 quiet NaN
+constexpr uint32_t kNanBf16x2 = 0x7FC07FC0u;     // two bfloat16 quiet NaNs
+
+uint32_t nan_pattern(mra_dtype_t dt) { return dt == MRA_BF16 ? kNanBf16x2 : kNanF32; }
+
 #define MRA_TRY(expr)                 \
   do {                                \
     const mra_status_t st_ = (expr);  \
     if (st_ != MRA_OK) return st_;    \
   } while (0)
+
+// Fills the (pointer, bytes, pattern) buffers when the debug flag is set.
+struct Fill {
+  void* p;
+  size_t bytes;
+  uint32_t pattern;
+};
+template <int N>
+mra_status_t debug_fill(const Fill (&f)[N], void* stream) {
+  if (!nanfill_enabled()) return MRA_OK;
+  for (const Fill& x : f)
+    MRA_TRY(hip_status(mra::launch_fill(x.p, x.bytes, x.pattern, static_cast<hipStream_t>(stream))));
+  return MRA_OK;
+}
 
 struct WsLayout {
   size_t qp, kp, vp, kvpacked, idx, cmax, csum, cvec, total;
@@ -232,6 +263,12 @@ mra_status_t forward_enqueue(const void* q, const void* k, const void* v, void* 
   float* csum = reinterpret_cast<float*>(ws + L.csum);
   float* cvec = reinterpret_cast<float*>(ws + L.cvec);
   hipStream_t st = static_cast<hipStream_t>(stream);
+  const size_t elem = dtype == MRA_BF16 ? 2 : 4;
+  const Fill fills[4] = {{out, (size_t)bh * n * d * elem, nan_pattern(dtype)},
+                         {idx_out, (size_t)bh * nb * budget * 4, kNanF32},
+                         {lse_out, (size_t)bh * n * 4, kNanF32},
+                         {workspace, L.total, kNanF32}};
+  MRA_TRY(debug_fill(fills, stream));
 
   MRA_TRY(hip_status(launch_pool(q, k, v, qp, kp, vp, kvpacked, bh, n, d, (int)dtype, st)));
   MRA_TRY(hip_status(launch_select_term_fused(qp, kp, idx, vp, cmax, csum, cvec, bh, nb, d, budget,
@@ -258,6 +295,9 @@ mra_status_t mra_pool(const void* q, const void* k, const void* v, float* qp, fl
   const void* ptrs[6] = {q, k, v, qp, kp, vp};
   for (const void* p : ptrs)
     if (p != nullptr && !aligned16(p)) return MRA_ERR_MISALIGNED;
+  const size_t pooled = (size_t)s.bh * s.nb * d * 4;
+  const Fill fills[3] = {{qp, pooled, kNanF32}, {kp, pooled, kNanF32}, {vp, pooled, kNanF32}};
+  MRA_TRY(debug_fill(fills, stream));
   return hip_status(mra::launch_pool(q, k, v, qp, kp, vp, nullptr, s.bh, n, d, (int)dtype,
                                      static_cast<hipStream_t>(stream)));
 }
@@ -270,6 +310,8 @@ mra_status_t mra_coarse_scores(const float* qp, const float* kp, float* scores, 
   MRA_TRY(check_ptr(qp));
   MRA_TRY(check_ptr(kp));
   MRA_TRY(check_ptr(scores));
+  const Fill fills[1] = {{scores, (size_t)s.bh * s.nb * s.nb * 4, kNanF32}};
+  MRA_TRY(debug_fill(fills, stream));
   return hip_status(mra::launch_coarse(qp, kp, scores, s.bh, s.nb, d,
                                        static_cast<hipStream_t>(stream)));
 }
@@ -282,6 +324,8 @@ mra_status_t mra_select(const float* scores, int32_t* idx, int B, int H, int n, 
   if (s.empty || budget == 0) return MRA_OK;
   MRA_TRY(check_ptr(scores));
   MRA_TRY(check_ptr(idx));
+  const Fill fills[1] = {{idx, (size_t)s.bh * s.nb * budget * 4, kNanF32}};
+  MRA_TRY(debug_fill(fills, stream));
   return hip_status(mra::launch_select(scores, idx, s.bh, s.nb, budget,
                                        static_cast<hipStream_t>(stream)));
 }
@@ -299,6 +343,10 @@ mra_status_t mra_coarse_term(const float* scores, const int32_t* idx, const floa
   MRA_TRY(check_ptr(cmax));
   MRA_TRY(check_ptr(csum));
   MRA_TRY(check_ptr(cvec));
+  const Fill fills[3] = {{cmax, (size_t)s.bh * s.nb * 4, kNanF32},
+                         {csum, (size_t)s.bh * s.nb * 4, kNanF32},
+                         {cvec, (size_t)s.bh * s.nb * d * 4, kNanF32}};
+  MRA_TRY(debug_fill(fills, stream));
   return hip_status(mra::launch_coarse_term(scores, idx, vp, cmax, csum, cvec, s.bh, s.nb, d,
                                             budget, static_cast<hipStream_t>(stream)));
 }
@@ -327,6 +375,9 @@ mra_status_t mra_block_sddmm_spmm(const void* q, const void* k, const void* v,
     MRA_TRY(check_ptr(csum));
     MRA_TRY(check_ptr(cvec));
   }
+  const Fill fills[2] = {{out, (size_t)s.bh * n * d * (dtype == MRA_BF16 ? 2 : 4), nan_pattern(dtype)},
+                         {lse_out, (size_t)s.bh * n * 4, kNanF32}};
+  MRA_TRY(debug_fill(fills, stream));
   return hip_status(mra::launch_tile(q, k, v, nullptr, idx, cmax, csum, cvec, out, lse_out, s.bh,
                                      n, d, budget, (int)dtype, static_cast<hipStream_t>(stream)));
 }
@@ -385,6 +436,11 @@ mra_status_t mra_sparse_attention_forward(const void* q, const void* k, const vo
   void* kvpacked = raw_tiles(d, dtype) ? nullptr : ws + L.kvpacked;
   int32_t* idx = idx_out ? idx_out : reinterpret_cast<int32_t*>(ws + L.idx);
   hipStream_t st = static_cast<hipStream_t>(stream);
+  const Fill fills[4] = {{out, (size_t)s.bh * n * d * (dtype == MRA_BF16 ? 2 : 4), nan_pattern(dtype)},
+                         {idx_out, (size_t)s.bh * s.nb * budget * 4, kNanF32},
+                         {lse_out, (size_t)s.bh * n * 4, kNanF32},
+                         {workspace, L.total, kNanF32}};
+  MRA_TRY(debug_fill(fills, stream));
 
   MRA_TRY(hip_status(mra::launch_pool(q, k, v, qp, kp, vp, kvpacked, s.bh, n, d, (int)dtype, st)));
   MRA_TRY(hip_status(mra::launch_select_fused(qp, kp, idx, s.bh, s.nb, d, budget, st)));
@@ -400,6 +456,8 @@ mra_status_t mra_select_global(const float* scores, int32_t* idx, int B, int H, 
   if (s.empty) return MRA_OK;
   MRA_TRY(check_ptr(scores));
   MRA_TRY(check_ptr(idx));
+  const Fill fills[1] = {{idx, (size_t)s.bh * s.nb * s.nb * 4, kNanF32}};
+  MRA_TRY(debug_fill(fills, stream));
   return hip_status(mra::launch_select_global(scores, idx, s.bh, s.nb, budget, prior_diagonal,
                                               static_cast<hipStream_t>(stream)));
 }
@@ -446,6 +504,11 @@ mra_status_t mra_attention_forward_global(const void* q, const void* k, const vo
   float* S = reinterpret_cast<float*>(ws + G.scores);
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int nb = s.nb;
+  const Fill fills[4] = {{out, (size_t)s.bh * n * d * (dtype == MRA_BF16 ? 2 : 4), nan_pattern(dtype)},
+                         {idx_out, (size_t)s.bh * nb * nb * 4, kNanF32},
+                         {lse_out, (size_t)s.bh * n * 4, kNanF32},
+                         {workspace, G.total, kNanF32}};
+  MRA_TRY(debug_fill(fills, stream));
 
   MRA_TRY(hip_status(mra::launch_pool(q, k, v, qp, kp, vp, kvpacked, s.bh, n, d, (int)dtype, st)));
   MRA_TRY(hip_status(mra::launch_coarse(qp, kp, S, s.bh, nb, d, st)));
@@ -496,6 +559,10 @@ mra_status_t mra_attention_backward(const void* q, const void* k, const void* v,
   A.bits = reinterpret_cast<uint32_t*>(ws + L.bits);
   A.gh = f32(L.gh); A.W = f32(L.W); A.dS = f32(L.dS);
   A.dqp = f32(L.dqp); A.dkp = f32(L.dkp); A.dvp = f32(L.dvp);
+  const size_t gbytes = (size_t)s.bh * n * d * (dtype == MRA_BF16 ? 2 : 4);
+  const Fill fills[4] = {{dq, gbytes, nan_pattern(dtype)}, {dk, gbytes, nan_pattern(dtype)},
+                         {dv, gbytes, nan_pattern(dtype)}, {workspace, L.total, kNanF32}};
+  MRA_TRY(debug_fill(fills, stream));
   return hip_status(mra::launch_bwd(A, static_cast<hipStream_t>(stream)));
 }
 
@@ -545,6 +612,12 @@ mra_status_t mra_attention_forward_multilevel(const void* q, const void* k, cons
   float *cmax = f32(L.cmax), *csum = f32(L.csum), *cvec = f32(L.cvec);
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int nb = s.nb;
+  const Fill fills[5] = {{out, (size_t)s.bh * n * d * (dtype == MRA_BF16 ? 2 : 4), nan_pattern(dtype)},
+                         {idx1_out, (size_t)s.bh * nb0 * budget1 * 4, kNanF32},
+                         {idx2_out, (size_t)s.bh * nb * budget2 * 4, kNanF32},
+                         {lse_out, (size_t)s.bh * n * 4, kNanF32},
+                         {workspace, W.total, kNanF32}};
+  MRA_TRY(debug_fill(fills, stream));
 
   MRA_TRY(hip_status(mra::launch_pool(q, k, v, qp, kp, vp, kvpacked, s.bh, n, d, (int)dtype, st)));
   MRA_TRY(hip_status(mra::launch_pool_up(qp, kp, vp, qp0, kp0, vp0, s.bh * nb0, d, r, st)));

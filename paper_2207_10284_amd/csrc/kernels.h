@@ -67,6 +67,9 @@ hipError_t launch_pool(const void* q, const void* k, const void* v, float* qp, f
 hipError_t launch_coarse(const float* qp, const float* kp, float* S, long long bh, int nb, int d,
                          hipStream_t stream);
 
+// Debug aid: every 32-bit word of p[0 .. bytes/4) set to `pattern`.
+hipError_t launch_fill(void* p, size_t bytes, uint32_t pattern, hipStream_t stream);
+
 // Top-m column blocks per row of S, ascending, into idx [bh, nb, m].
 hipError_t launch_select(const float* S, int32_t* idx, long long bh, int nb, int m,
                          hipStream_t stream);

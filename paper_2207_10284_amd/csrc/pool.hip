@@ -225,4 +225,21 @@ hipError_t launch_pool(const void* q, const void* k, const void* v, float* qp, f
   return hipGetLastError();
 }
 
+// Debug aid (MRA_DEBUG_NANFILL, api.cpp): every 32-bit word of a buffer set to
+// one pattern, grid-stride, plain vector stores.
+__global__ void fill_u32_kernel(uint32_t* __restrict__ p, long long words, uint32_t pattern) {
+  const long long stride = (long long)gridDim.x * blockDim.x;
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < words; i += stride) p[i] = pattern;
+}
+
+hipError_t launch_fill(void* p, size_t bytes, uint32_t pattern, hipStream_t stream) {
+  const long long words = (long long)(bytes / 4);
+  if (p == nullptr || words == 0) return hipSuccess;
+  const int threads = 256;
+  long long blocks = (words + threads - 1) / threads;
+  if (blocks > 65536) blocks = 65536;
+  fill_u32_kernel<<<(unsigned)blocks, threads, 0, stream>>>(static_cast<uint32_t*>(p), words, pattern);
+  return hipGetLastError();
+}
+
 }  // namespace mra

@@ -186,8 +186,12 @@ __device__ __forceinline__ int raw_copy_offset(int i, int lane) {
 }
 
 // Buffer loads straight to LDS (16 bytes per lane): a raw buffer resource for
-// `bytes` bytes from `base` (reads past the end return zero), and one load
-// of the 16 bytes at base + soff + voff into LDS byte dst + 16 lane.
+// `bytes` bytes from `base`, and one load of the 16 bytes at base + soff +
+// voff into LDS byte dst + 16 lane. The hardware range check covers the
+// vector and immediate offsets only, not the scalar offset, so a load is in
+// bounds only because every caller validates the block it copies first (the
+// tile passes take only block ids in [0, nb), filtered when the selection is
+// staged); the resource's size is not a safety net for the scalar offset.
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 __device__ void mra_raw_buffer_load_lds(i32x4 rsrc, __attribute__((address_space(3))) void* lds, int size,
                                         int voffset, int soffset, int offset,

@@ -1,0 +1,201 @@
+"""CPU models of the kernels' index and bounds arithmetic (no GPU).
+
+Each test restates the index math of one kernel from the HIP sources and
+checks, exhaustively over the lanes, copies and sizes it uses, that every
+global and LDS access stays inside its buffer or LDS region and that work is
+covered exactly once:
+* xcd_remap (common.h): a permutation of the workgroups, each XCD receiving a
+  contiguous range;
+* pool_kernel (pool.hip): two threads per 16-byte column chunk of a 32-row
+  block, the second half's partner lane inside the same wave, reads and
+  writes inside the tensors;
+* the raw-tile copies and operand reads of tile_stream_kernel (tile.hip,
+  tile_ops.h): buffer-load offsets inside the copied block (the scalar offset
+  is outside the hardware range check, so this is the bound that matters),
+  the period of the lanes' copy offsets the kernel relies on, LDS writes and
+  reads inside the wave's slot, and the workgroup's LDS within the budget of
+  its occupancy;
+* rows_kernel (select.hip): the score/weight rows, the partial sums of the
+  coarse term and the float64 query rows inside the dynamic LDS it requests,
+  for every register tier, head dim and mode, within 160 KB.
+"""
+import pytest
+
+LDS_PER_CU = 160 * 1024
+
+
+# ------------------------------------------------------------------ common.h
+def xcd_remap(p, total, xcds=8):
+    xcd, slot = p % xcds, p // xcds
+    q, r = total // xcds, total % xcds
+    return xcd * (q + 1) + slot if xcd < r else r * (q + 1) + (xcd - r) * q + slot
+
+
+@pytest.mark.parametrize("total", [1, 7, 8, 9, 64, 100, 1023, 1024, 1536, 3072, 4099])
+def test_xcd_remap_is_a_permutation_with_contiguous_ranges(total):
+    logical = [xcd_remap(p, total) for p in range(total)]
+    assert sorted(logical) == list(range(total))
+    for x in range(8):
+        mine = sorted(logical[p] for p in range(x, total, 8))
+        if mine:
+            assert mine == list(range(mine[0], mine[0] + len(mine)))
+
+
+# ------------------------------------------------------------------ pool.hip
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("d", [32, 64, 128])
+def test_pool_thread_map(dtype, d):
+    per = 8 if dtype == "bf16" else 4
+    bh, n = 3, 160
+    cpr = d // per
+    chunks = bh * (n // 32) * cpr
+    threads = 256
+    blocks = (2 * chunks + threads - 1) // threads
+    covered = {}
+    rows_total = bh * n
+    for t in range(blocks * threads):
+        blk = t // (2 * cpr)
+        i = t - blk * 2 * cpr
+        half, c = i // cpr, i % cpr
+        if t >= 2 * chunks:
+            continue
+        row0 = blk * 32 + 16 * half
+        for r in range(16):
+            u = (row0 + r) * cpr + c                    # 16-byte unit read
+            assert 0 <= u < rows_total * cpr
+        if half == 0:
+            partner = t + cpr
+            assert partner // 64 == t // 64             # the shuffle stays in the wave
+            pb = partner // (2 * cpr)
+            assert pb == blk and (partner - pb * 2 * cpr) // cpr == 1 and (partner - pb * 2 * cpr) % cpr == c
+            lo, hi = blk * d + c * per, blk * d + c * per + per
+            assert 0 <= lo and hi <= bh * (n // 32) * d
+            for e in range(lo, hi):
+                assert e not in covered
+                covered[e] = t
+    assert len(covered) == bh * (n // 32) * d
+
+
+# ------------------------------------------------------------------ tile.hip (raw bf16 tiles)
+def swz_k(d, r):
+    return {128: r & 15, 64: (r >> 1) & 7, 32: (r >> 2) & 3}[d]
+
+
+def swz_v(d, r):
+    return {128: 4 * (r & 3), 64: ((r >> 1) & 1) << 2, 32: 0}[d]
+
+
+def raw_offset(d, swz, r, c):
+    return r * (2 * d) + ((((2 * c) >> 4) ^ swz(d, r)) << 4) + ((2 * c) & 15)
+
+
+def raw_copy_offset(d, swz, i, lane):
+    q = i * 1024 + 16 * lane
+    r, blk = q // (2 * d), (q % (2 * d)) // 16
+    return r * (2 * d) + ((blk ^ swz(d, r)) << 4)
+
+
+def tile_cfg(d):
+    kc = d // 16                    # 16-byte row-layout chunks (= 1 KB copies of a K tile)
+    nt = d // 32
+    vc = 2 * nt
+    return kc, vc, kc + vc, nt
+
+
+@pytest.mark.parametrize("d", [32, 64, 128])
+def test_raw_tile_copies_stay_in_the_block(d):
+    """Copy i of block y: scalar offset y*KC*1K + i*1K, vector offset the
+    lane's swizzled source offset of copy i mod period, minus its own copy's
+    1 KB step. The sum must be the lane's source inside block y for every
+    copy (this is what keeps the loads in bounds: the scalar offset is not
+    range-checked), and the LDS destination inside the slot."""
+    kc, vc, ch, nt = tile_cfg(d)
+    kpb = {128: 4, 64: 2, 32: 1}[d]
+    tile = kc * 1024
+    for nb in (1, 3, 128):
+        for y in (0, nb - 1):
+            for i in range(kc):
+                for lane in range(64):
+                    koff = raw_copy_offset(d, swz_k, i % kpb, lane) - (i % kpb) * 1024
+                    src = y * tile + i * 1024 + koff
+                    assert src == y * tile + raw_copy_offset(d, swz_k, i, lane)
+                    assert y * tile <= src and src + 16 <= (y + 1) * tile <= nb * tile
+                    voff = raw_copy_offset(d, swz_v, 0, lane)
+                    vsrc = y * tile + i * 1024 + voff
+                    assert vsrc == y * tile + raw_copy_offset(d, swz_v, i, lane)
+                    assert y * tile <= vsrc and vsrc + 16 <= (y + 1) * tile
+                    assert i * 1024 + 16 * lane + 16 <= kc * 1024        # K part of the slot
+                    assert kc * 1024 + i * 1024 + 16 * lane + 16 <= ch * 1024
+
+
+@pytest.mark.parametrize("d", [32, 64, 128])
+def test_raw_tile_operand_reads_stay_in_the_slot(d):
+    kc, vc, ch, nt = tile_cfg(d)
+    rb = 2 * d
+    for lane in range(64):
+        h, j, i16 = lane >> 5, lane & 31, lane & 15
+        for c in range(kc):
+            a = raw_offset(d, swz_k, j, (d // 2) * h + 8 * c)
+            assert 0 <= a and a + 16 <= kc * 1024
+        for t in range(nt):
+            vr = kc * 1024 + raw_offset(d, swz_v, 4 * h + i16 // 4, 32 * t + 16 * ((lane >> 4) & 1) + 4 * (i16 & 3))
+            for cc in range(vc):
+                u = cc // nt
+                for imm in (16 * u * rb, (16 * u + 8) * rb):   # the two transposing reads of a chunk
+                    assert kc * 1024 <= vr + imm and vr + imm + 8 <= ch * 1024
+
+
+@pytest.mark.parametrize("d,waves_per_cu,m", [(32, 16, 8), (64, 16, 16), (64, 16, 64), (128, 8, 32), (128, 8, 128)])
+def test_tile_stream_lds_fits_its_occupancy(d, waves_per_cu, m):
+    """tile_stream_kernel: 4 waves per workgroup, one slot of CH KB per wave
+    plus the waves' selection lists (m ints each); the workgroups a CU holds
+    at the kernel's occupancy (16 waves for d <= 64, 8 for d = 128, set by
+    registers) must fit its LDS."""
+    kc, vc, ch, nt = tile_cfg(d)
+    waves, slots = 4, 1
+    per_wg = waves * slots * ch * 1024 + waves * m * 4
+    assert (waves_per_cu // waves) * per_wg <= LDS_PER_CU
+
+
+# ------------------------------------------------------------------ select.hip (rows_kernel)
+K_ROWS, K_CHUNK, K_U = 16, 64, 8
+
+
+def rows_smem(jmax, nw, mode, d):
+    if mode == 0:
+        return 0, 0
+    ldc = 64 * jmax + 4
+    part_off = (K_ROWS * ldc * 4 + 15) & ~15
+    part = nw * 16 * 16 * 4 if mode in (1, 2) else 0
+    qd = K_ROWS * (d + 2) * 8 if mode in (2, 3) else 0
+    return part_off, part_off + max(part, qd)
+
+
+@pytest.mark.parametrize("jmax", [2, 8, 16, 32])
+@pytest.mark.parametrize("d", [32, 64, 128])
+@pytest.mark.parametrize("mode", [1, 2, 3])
+def test_rows_kernel_lds_regions(jmax, d, mode):
+    rpw = 2 if jmax <= 8 else 1
+    nw = K_ROWS // rpw
+    ntd = d // 16
+    kq = nw // ntd
+    assert kq >= 1 and nw % ntd == 0
+    bpw = 2 * jmax // kq
+    assert bpw * kq == 2 * jmax
+    ldc = 64 * jmax + 4
+    part_off, total = rows_smem(jmax, nw, mode, d)
+    assert total <= LDS_PER_CU
+    # score / weight rows: row r < 16, column c < 64 JMAX
+    assert (K_ROWS - 1) * ldc + 64 * jmax - 1 < part_off // 4
+    if mode in (1, 2):
+        # partial sums part[(kq' * 16 + 4 ak + e) * D + 16 nt + ar]
+        top = ((kq - 1) * K_ROWS + 4 * 3 + 3) * d + 16 * (ntd - 1) + 15
+        assert part_off + 4 * (top + 1) <= total
+        # phase 4's weight reads: two 16-byte reads per batch u < BPW
+        for kqi in range(kq):
+            for u in range(bpw):
+                for ak in range(4):
+                    col = K_U * ak + 4 * K_U * (kqi + kq * u)
+                    assert col + 8 <= 64 * jmax          # inside the row (zero past nb)
+    if mode in (2, 3):
+        assert part_off + K_ROWS * (d + 2) * 8 <= total
