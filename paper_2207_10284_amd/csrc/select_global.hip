@@ -8,7 +8,10 @@
 // One workgroup (16 waves) per head. The threshold key T (the budget-th
 // largest order-preserving 32-bit key among the non-prior blocks) is found
 // with four 8-bit radix passes over the head's scores, each building a
-// 256-bin histogram in LDS of the keys that share the digits fixed so far.
+// 256-bin histogram in LDS of the keys that share the digits fixed so far
+// (heads of up to 256 x 256 blocks keep their keys in registers, whole rows
+// per wave, so the ties are counted and the rows compacted without reading S
+// again).
 // The keys equal to T are taken in flat-index order: per-row counts of such
 // keys, an exclusive scan over rows, and a rank inside the row give every one
 // its position. A last sweep, one wave per row, compacts the row's refined
@@ -21,13 +24,75 @@ namespace mra {
 constexpr int kGWaves = 16;
 constexpr int kGThreads = kGWaves * kWave;
 
-__global__ __launch_bounds__(kGThreads) void select_global_kernel(const float* __restrict__ S,
-                                                                   int32_t* __restrict__ idx,
-                                                                   int nb, int budget,
-                                                                   int prior_diagonal) {
+// The digit of the `remaining`-th largest key from a 256-bin histogram (wave
+// 0; lane l holds bins 255-4l .. 252-4l, descending) into shared_vals[0] and
+// the count of larger digits into shared_vals[1].
+__device__ __forceinline__ void pick_digit(const uint32_t* hist, int remaining, int lane, int* shared_vals) {
+  uint32_t c[4];
+  uint32_t mine = 0;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    c[e] = hist[255 - 4 * lane - e];
+    mine += c[e];
+  }
+  uint32_t incl = mine;                                      // inclusive prefix over lanes
+  for (int off = 1; off < kWave; off <<= 1) {
+    const uint32_t other = __shfl_up(incl, off);
+    if (lane >= off) incl += other;
+  }
+  const uint32_t excl = incl - mine;
+  const bool here = excl < (uint32_t)remaining && incl >= (uint32_t)remaining;
+  const uint64_t hm = __ballot(here);
+  const int src = __builtin_ctzll(hm);                       // exactly one lane
+  if (lane == src) {
+    uint32_t acc = excl;
+    int digit = 0, before = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (acc + c[e] >= (uint32_t)remaining) {
+        digit = 255 - 4 * lane - e;
+        before = (int)acc;
+        break;
+      }
+      acc += c[e];
+    }
+    shared_vals[0] = digit;
+    shared_vals[1] = before;
+  }
+}
+
+// Exclusive scan of ties[0 .. nb) in place (wave 0; contiguous rows per lane).
+__device__ __forceinline__ void scan_rows(int* ties, int nb, int lane) {
+  const int per = (nb + kWave - 1) / kWave;
+  int mine = 0;
+  for (int r = lane * per; r < min(nb, (lane + 1) * per); ++r) mine += ties[r];
+  int incl = mine;
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int other = __shfl_up(incl, off);
+    if (lane >= off) incl += other;
+  }
+  int run = incl - mine;
+  for (int r = lane * per; r < min(nb, (lane + 1) * per); ++r) {
+    const int t = ties[r];
+    ties[r] = run;
+    run += t;
+  }
+}
+
+// Heads of up to 16 RW rows and 64 CW columns: wave w keeps the keys of rows
+// x = w + 16 i (i < RW), columns y = lane + 64 c (c < CW) in registers, read
+// from S once; the radix passes count them into one 256-bin histogram per wave
+// (fewer same-address LDS atomics across waves, added up per bin afterwards),
+// the rows' ties are counted with ballots and the rows are compacted from
+// the same registers.
+template <int RW, int CW>
+__global__ __launch_bounds__(kGThreads) void select_global_rows_kernel(const float* __restrict__ S,
+                                                                        int32_t* __restrict__ idx,
+                                                                        int nb, int budget,
+                                                                        int prior_diagonal) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  uint32_t* hist = reinterpret_cast<uint32_t*>(smem);          // [256]
-  int* ties = reinterpret_cast<int*>(hist + 256);              // [nb] keys == T per row, then exclusive scan
+  uint32_t* hist = reinterpret_cast<uint32_t*>(smem);          // [16][256], then the sum in hist[0 .. 256)
+  int* ties = reinterpret_cast<int*>(hist + kGWaves * 256);    // [nb] keys == T per row, then exclusive scan
   int* shared_vals = ties + nb;                                // [4] broadcast slots
   const long long head = blockIdx.x;
   const float* Sh = S + head * (long long)nb * nb;
@@ -35,63 +100,48 @@ __global__ __launch_bounds__(kGThreads) void select_global_kernel(const float* _
   const int tid = threadIdx.x;
   const int w = wave_uniform(tid / kWave);
   const int lane = lane_id();
-  const long long N = (long long)nb * nb;
-  const long long nfree = N - (prior_diagonal ? nb : 0);
-  auto is_prior = [&](long long f) { return prior_diagonal && (f / nb) == (f % nb); };
+  const long long nfree = (long long)nb * nb - (prior_diagonal ? nb : 0);
+  const bool none = budget == 0, all = (long long)budget >= nfree;
 
-  // ---- threshold: the budget-th largest key among the non-prior blocks
+  // key 0: a block that does not take part (a prior, or outside the head);
+  // every finite score's key is at least 0x00800000
+  uint32_t key[RW][CW];
+#pragma unroll
+  for (int i = 0; i < RW; ++i) {
+    const int x = w + kGWaves * i;
+#pragma unroll
+    for (int c = 0; c < CW; ++c) {
+      const int y = lane + kWave * c;
+      const bool in = x < nb && y < nb && !(prior_diagonal && x == y);
+      key[i][c] = in ? ordered_key(Sh[(long long)x * nb + y]) : 0u;
+    }
+  }
+
   uint32_t T = 0;
   int need = 0;                        // keys equal to T to take (flat order)
-  const bool none = budget == 0, all = (long long)budget >= nfree;
   if (!none && !all) {
     uint32_t prefix = 0;
     int remaining = budget;
+    uint32_t* wh = hist + w * 256;
     for (int shift = 24; shift >= 0; shift -= 8) {
-      for (int i = tid; i < 256; i += kGThreads) hist[i] = 0u;
+      for (int i = tid; i < kGWaves * 256; i += kGThreads) hist[i] = 0u;
       __syncthreads();
       const uint32_t hi_mask = shift == 24 ? 0u : ~((1u << (shift + 8)) - 1u);
-      for (long long f = tid; f < N; f += kGThreads) {
-        if (is_prior(f)) continue;
-        const uint32_t key = ordered_key(Sh[f]);
-        if ((key & hi_mask) == (prefix & hi_mask)) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+#pragma unroll
+      for (int i = 0; i < RW; ++i)
+#pragma unroll
+        for (int c = 0; c < CW; ++c)
+          if (key[i][c] != 0u && (key[i][c] & hi_mask) == (prefix & hi_mask))
+            atomicAdd(&wh[(key[i][c] >> shift) & 255u], 1u);
+      __syncthreads();
+      if (tid < 256) {
+        uint32_t sum = 0;
+#pragma unroll
+        for (int q = 0; q < kGWaves; ++q) sum += hist[q * 256 + tid];
+        hist[tid] = sum;                                       // row 0 holds the total
       }
       __syncthreads();
-      if (w == 0) {
-        // lane l holds bins 255-4l .. 252-4l (descending); find the digit
-        // where the count of larger-or-equal digits first reaches `remaining`
-        uint32_t c[4];
-        uint32_t mine = 0;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          c[e] = hist[255 - 4 * lane - e];
-          mine += c[e];
-        }
-        // inclusive prefix over lanes (descending digits)
-        uint32_t incl = mine;
-        for (int off = 1; off < kWave; off <<= 1) {
-          const uint32_t other = __shfl_up(incl, off);
-          if (lane >= off) incl += other;
-        }
-        const uint32_t excl = incl - mine;
-        const bool here = excl < (uint32_t)remaining && incl >= (uint32_t)remaining;
-        const uint64_t hm = __ballot(here);
-        const int src = __builtin_ctzll(hm);                  // exactly one lane
-        if (lane == src) {
-          uint32_t acc = excl;
-          int digit = 0, before = 0;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            if (acc + c[e] >= (uint32_t)remaining) {
-              digit = 255 - 4 * lane - e;
-              before = (int)acc;
-              break;
-            }
-            acc += c[e];
-          }
-          shared_vals[0] = digit;
-          shared_vals[1] = before;
-        }
-      }
+      if (w == 0) pick_digit(hist, remaining, lane, shared_vals);
       __syncthreads();
       prefix |= (uint32_t)shared_vals[0] << shift;
       remaining -= shared_vals[1];
@@ -99,60 +149,262 @@ __global__ __launch_bounds__(kGThreads) void select_global_kernel(const float* _
     }
     T = prefix;
     need = remaining;                                        // >= 1
-    // keys equal to T per row, then their exclusive scan over rows
-    for (int i = tid; i < nb; i += kGThreads) ties[i] = 0;
-    __syncthreads();
-    for (long long f = tid; f < N; f += kGThreads)
-      if (!is_prior(f) && ordered_key(Sh[f]) == T) atomicAdd(&ties[f / nb], 1);
-    __syncthreads();
-    if (w == 0) {
-      const int per = (nb + kWave - 1) / kWave;               // rows per lane, contiguous
-      int mine = 0;
-      for (int r = lane * per; r < min(nb, (lane + 1) * per); ++r) mine += ties[r];
-      int incl = mine;
-      for (int off = 1; off < kWave; off <<= 1) {
-        const int other = __shfl_up(incl, off);
-        if (lane >= off) incl += other;
-      }
-      int run = incl - mine;
-      for (int r = lane * per; r < min(nb, (lane + 1) * per); ++r) {
-        const int t = ties[r];
-        ties[r] = run;
-        run += t;
-      }
+    // keys equal to T per row (ballots), then their exclusive scan over rows
+#pragma unroll
+    for (int i = 0; i < RW; ++i) {
+      const int x = w + kGWaves * i;
+      int t = 0;
+#pragma unroll
+      for (int c = 0; c < CW; ++c) t += __popcll(__ballot(key[i][c] != 0u && key[i][c] == T));
+      if (x < nb && lane == 0) ties[x] = t;
     }
+    __syncthreads();
+    if (w == 0) scan_rows(ties, nb, lane);
     __syncthreads();
   }
 
-  // ---- rows: one wave per row, blocks in ascending order
-  for (int x = w; x < nb; x += kGWaves) {
-    const float* row = Sh + (long long)x * nb;
+  // ---- rows: compacted from the registers, blocks in ascending order
+#pragma unroll
+  for (int i = 0; i < RW; ++i) {
+    const int x = w + kGWaves * i;
+    if (x >= nb) break;
     int32_t* orow = out + (long long)x * nb;
     int written = 0, tie_seen = (!none && !all) ? ties[x] : 0;
-    for (int y0 = 0; y0 < nb; y0 += kWave) {
-      const int y = y0 + lane;
+#pragma unroll
+    for (int c = 0; c < CW; ++c) {
+      const int y = lane + kWave * c;
       const bool valid = y < nb;
       const bool prior = valid && prior_diagonal && y == x;
-      const bool cand = valid && !prior && !none && !all;    // decided by the threshold
-      const uint32_t key = cand ? ordered_key(row[y]) : 0u;
-      const bool eq = cand && key == T;
-      const uint64_t em = __ballot(eq);                      // whole wave: tie_seen stays uniform
+      const bool cand = valid && !prior && !none && !all;
+      const bool eq = cand && key[i][c] == T;
+      const uint64_t em = __ballot(eq);
       const int rank = tie_seen + __popcll(em & lanemask_lt());
       tie_seen += __popcll(em);
-      const bool take = prior || (valid && !prior && all) || (cand && (key > T || (eq && rank < need)));
+      const bool take = prior || (valid && !prior && all) || (cand && (key[i][c] > T || (eq && rank < need)));
       const uint64_t tm = __ballot(take);
       if (take) orow[written + __popcll(tm & lanemask_lt())] = y;
       written += __popcll(tm);
     }
-    for (int i = written + lane; i < nb; i += kWave) orow[i] = -1;
+    for (int k = written + lane; k < nb; k += kWave) orow[k] = -1;
   }
+}
+
+// Heads of more than 256 blocks per side: the four radix passes, the ties per
+// row and the compaction run as separate launches over many workgroups per
+// head (one workgroup per head would take milliseconds at 1024 x 1024
+// blocks). Scratch per head in the first words of its own idx output
+// (written last, by the compaction, after everything was read): the four
+// 256-bin histograms, then the ties per row. Every launch recomputes the
+// digits chosen so far from the histograms of the earlier passes, so no
+// other state is kept.
+constexpr int kSgThreads = 256;
+constexpr int kSgKeysPerThread = 16;
+constexpr int kSgTies = 4 * 256;                              // word offset of the ties per row
+
+// prefix and remaining count after `passes` digits (wave 0 of the workgroup;
+// the result broadcast through shared_vals[2..3]).
+__device__ __forceinline__ void digits_so_far(const uint32_t* hists, int passes, int budget, int w, int lane,
+                                              int* shared_vals) {
+  if (w == 0) {
+    uint32_t prefix = 0;
+    int remaining = budget;
+    for (int p = 0; p < passes; ++p) {
+      pick_digit(hists + 256 * p, remaining, lane, shared_vals);
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      prefix |= (uint32_t)shared_vals[0] << (24 - 8 * p);
+      remaining -= shared_vals[1];
+      __builtin_amdgcn_wave_barrier();
+    }
+    if (lane == 0) {
+      shared_vals[2] = (int)prefix;
+      shared_vals[3] = remaining;
+    }
+  }
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(kSgThreads) void sg_zero_kernel(int32_t* __restrict__ idx, long long N) {
+  uint32_t* h = reinterpret_cast<uint32_t*>(idx + blockIdx.x * N);
+  for (int i = threadIdx.x; i < 4 * 256; i += kSgThreads) h[i] = 0u;
+}
+
+// Pass `pass` (digit bits 24 - 8 pass ..): every workgroup counts the keys of
+// its slice that carry the digits chosen so far into histogram `pass`.
+__global__ __launch_bounds__(kSgThreads) void sg_pass_kernel(const float* __restrict__ S, int32_t* __restrict__ idx,
+                                                             int nb, int budget, int prior_diagonal, int pass) {
+  __shared__ uint32_t hist[256];
+  __shared__ int shared_vals[4];
+  const long long N = (long long)nb * nb;
+  const long long head = blockIdx.y;
+  const float* Sh = S + head * N;
+  uint32_t* hists = reinterpret_cast<uint32_t*>(idx + head * N);
+  const int tid = threadIdx.x, w = tid / kWave, lane = lane_id();
+  for (int i = tid; i < 256; i += kSgThreads) hist[i] = 0u;
+  digits_so_far(hists, pass, budget, w, lane, shared_vals);
+  const uint32_t prefix = (uint32_t)shared_vals[2];
+  const int shift = 24 - 8 * pass;
+  const uint32_t hi_mask = pass == 0 ? 0u : ~((1u << (shift + 8)) - 1u);
+  const long long f0 = (long long)blockIdx.x * kSgThreads * kSgKeysPerThread;
+#pragma unroll
+  for (int r = 0; r < kSgKeysPerThread; ++r) {
+    const long long f = f0 + tid + (long long)kSgThreads * r;
+    if (f >= N || (prior_diagonal && f / nb == f % nb)) continue;
+    const uint32_t k = ordered_key(Sh[f]);
+    if ((k & hi_mask) == (prefix & hi_mask)) atomicAdd(&hist[(k >> shift) & 255u], 1u);
+  }
+  __syncthreads();
+  for (int i = tid; i < 256; i += kSgThreads)
+    if (hist[i] != 0u) atomicAdd(&hists[256 * pass + i], hist[i]);
+}
+
+// The keys equal to the threshold per row (one wave per row).
+__global__ __launch_bounds__(kSgThreads) void sg_ties_kernel(const float* __restrict__ S, int32_t* __restrict__ idx,
+                                                             int nb, int budget, int prior_diagonal) {
+  __shared__ int shared_vals[4];
+  const long long N = (long long)nb * nb;
+  const long long head = blockIdx.y;
+  const float* Sh = S + head * N;
+  uint32_t* hists = reinterpret_cast<uint32_t*>(idx + head * N);
+  const int tid = threadIdx.x, w = tid / kWave, lane = lane_id();
+  digits_so_far(hists, 4, budget, w, lane, shared_vals);
+  const uint32_t T = (uint32_t)shared_vals[2];
+  const int x = blockIdx.x * (kSgThreads / kWave) + w;
+  if (x >= nb) return;
+  const float* row = Sh + (long long)x * nb;
+  int t = 0;
+  for (int y0 = 0; y0 < nb; y0 += kWave) {
+    const int y = y0 + lane;
+    const bool cand = y < nb && !(prior_diagonal && y == x);
+    t += __popcll(__ballot(cand && ordered_key(row[y]) == T));
+  }
+  if (lane == 0) reinterpret_cast<int*>(hists)[kSgTies + x] = t;
+}
+
+// Compaction of row x (one wave): priors, every key above the threshold T,
+// and the keys equal to T whose flat rank (tie_before: such keys in earlier
+// rows) is below `need`; then -1 up to nb entries.
+__device__ __forceinline__ void compact_row(const float* __restrict__ row, int32_t* __restrict__ orow, int x, int nb,
+                                            bool prior_diagonal, bool none, bool all, uint32_t T, int need,
+                                            int tie_before, int lane) {
+  int written = 0, tie_seen = tie_before;
+  for (int y0 = 0; y0 < nb; y0 += kWave) {
+    const int y = y0 + lane;
+    const bool valid = y < nb;
+    const bool prior = valid && prior_diagonal && y == x;
+    const bool cand = valid && !prior && !none && !all;
+    const uint32_t key = cand ? ordered_key(row[y]) : 0u;
+    const bool eq = cand && key == T;
+    const uint64_t em = __ballot(eq);
+    const int rank = tie_seen + __popcll(em & lanemask_lt());
+    tie_seen += __popcll(em);
+    const bool take = prior || (valid && !prior && all) || (cand && (key > T || (eq && rank < need)));
+    const uint64_t tm = __ballot(take);
+    if (take) orow[written + __popcll(tm & lanemask_lt())] = y;
+    written += __popcll(tm);
+  }
+  for (int i = written + lane; i < nb; i += kWave) orow[i] = -1;
+}
+
+// Rows that hold no scratch (x >= first): one wave per row; the row's tie
+// offset is the sum of the ties of the rows before it.
+__global__ __launch_bounds__(kSgThreads) void sg_rows_kernel(const float* __restrict__ S, int32_t* __restrict__ idx,
+                                                             int nb, int budget, int prior_diagonal, int first) {
+  __shared__ int shared_vals[4];
+  const long long N = (long long)nb * nb;
+  const long long head = blockIdx.y;
+  int32_t* out = idx + head * N;
+  const uint32_t* hists = reinterpret_cast<const uint32_t*>(out);
+  const int tid = threadIdx.x, w = tid / kWave, lane = lane_id();
+  const long long nfree = N - (prior_diagonal ? nb : 0);
+  const bool none = budget == 0, all = (long long)budget >= nfree;
+  uint32_t T = 0;
+  int need = 0;
+  if (!none && !all) {
+    digits_so_far(hists, 4, budget, w, lane, shared_vals);
+    T = (uint32_t)shared_vals[2];
+    need = shared_vals[3];
+  }
+  const int x = first + blockIdx.x * (kSgThreads / kWave) + w;
+  if (x >= nb) return;
+  int before = 0;
+  if (!none && !all) {
+    const int* ties = reinterpret_cast<const int*>(hists) + kSgTies;
+    for (int r = lane; r < x; r += kWave) before += ties[r];
+    before = (int)wave_sum((float)before);                   // exact: counts below 2^24
+  }
+  compact_row(S + head * N + (long long)x * nb, out + (long long)x * nb, x, nb, prior_diagonal, none, all, T, need,
+              before, lane);
+}
+
+// The rows that hold the scratch (x < first), one workgroup per head, which
+// reads all the scratch it needs before writing a row.
+__global__ __launch_bounds__(kSgThreads) void sg_first_rows_kernel(const float* __restrict__ S,
+                                                                   int32_t* __restrict__ idx, int nb, int budget,
+                                                                   int prior_diagonal, int first) {
+  __shared__ int shared_vals[4];
+  __shared__ int before_all[kSgThreads / kWave * 8];
+  const long long N = (long long)nb * nb;
+  const long long head = blockIdx.x;
+  int32_t* out = idx + head * N;
+  const uint32_t* hists = reinterpret_cast<const uint32_t*>(out);
+  const int tid = threadIdx.x, w = tid / kWave, lane = lane_id();
+  const long long nfree = N - (prior_diagonal ? nb : 0);
+  const bool none = budget == 0, all = (long long)budget >= nfree;
+  uint32_t T = 0;
+  int need = 0;
+  if (!none && !all) {
+    digits_so_far(hists, 4, budget, w, lane, shared_vals);
+    T = (uint32_t)shared_vals[2];
+    need = shared_vals[3];
+    const int* ties = reinterpret_cast<const int*>(hists) + kSgTies;
+    for (int x = w; x < first; x += kSgThreads / kWave) {
+      int before = 0;
+      for (int r = lane; r < x; r += kWave) before += ties[r];
+      before = (int)wave_sum((float)before);
+      if (lane == 0) before_all[x] = before;
+    }
+  }
+  __syncthreads();                                             // all scratch read: its rows may be written
+  for (int x = w; x < first; x += kSgThreads / kWave)
+    compact_row(S + head * N + (long long)x * nb, out + (long long)x * nb, x, nb, prior_diagonal, none, all, T, need,
+                (!none && !all) ? before_all[x] : 0, lane);
 }
 
 hipError_t launch_select_global(const float* S, int32_t* idx, long long bh, int nb, int budget,
                                 int prior_diagonal, hipStream_t stream) {
-  const size_t smem = (256 + (size_t)nb + 4) * sizeof(int);
-  select_global_kernel<<<(unsigned)bh, kGThreads, smem, stream>>>(S, idx, nb, budget,
-                                                                   prior_diagonal);
+  const size_t tail = ((size_t)nb + 4) * sizeof(int);
+  const size_t hist16 = (size_t)kGWaves * 256 * sizeof(int);
+#define MRA_SG_ROWS(RW, CW) \
+  select_global_rows_kernel<RW, CW><<<(unsigned)bh, kGThreads, hist16 + tail, stream>>>(S, idx, nb, budget, prior_diagonal)
+  if (nb <= 16) MRA_SG_ROWS(1, 1);
+  else if (nb <= 32) MRA_SG_ROWS(2, 1);
+  else if (nb <= 64) MRA_SG_ROWS(4, 1);
+  else if (nb <= 128) MRA_SG_ROWS(8, 2);
+  else if (nb <= 256) MRA_SG_ROWS(16, 4);
+  else {
+    // heads of more than 256 blocks per side: passes spread over workgroups
+    const long long N = (long long)nb * nb;
+    const long long nfree = N - (prior_diagonal ? nb : 0);
+    if (budget > 0 && (long long)budget < nfree) {
+      const unsigned slices = (unsigned)((N + (long long)kSgThreads * kSgKeysPerThread - 1) /
+                                         ((long long)kSgThreads * kSgKeysPerThread));
+      sg_zero_kernel<<<(unsigned)bh, kSgThreads, 0, stream>>>(idx, N);
+      for (int pass = 0; pass < 4; ++pass)
+        sg_pass_kernel<<<dim3(slices, (unsigned)bh), kSgThreads, 0, stream>>>(S, idx, nb, budget, prior_diagonal,
+                                                                            pass);
+      const unsigned tiegroups = (unsigned)((nb + kSgThreads / kWave - 1) / (kSgThreads / kWave));
+      sg_ties_kernel<<<dim3(tiegroups, (unsigned)bh), kSgThreads, 0, stream>>>(S, idx, nb, budget, prior_diagonal);
+    }
+    // rows holding the scratch (its first kSgTies + nb words) are written last
+    const int first = (kSgTies + nb + nb - 1) / nb;
+    const unsigned rowgroups = (unsigned)((nb - first + kSgThreads / kWave - 1) / (kSgThreads / kWave));
+    sg_rows_kernel<<<dim3(rowgroups, (unsigned)bh), kSgThreads, 0, stream>>>(S, idx, nb, budget, prior_diagonal,
+                                                                            first);
+    sg_first_rows_kernel<<<(unsigned)bh, kSgThreads, 0, stream>>>(S, idx, nb, budget, prior_diagonal, first);
+  }
+#undef MRA_SG_ROWS
   return hipGetLastError();
 }
 

@@ -22,11 +22,14 @@ def _say(*a):
 
 @pytest.mark.parametrize("nb,budget,prior", [(1, 1, False), (1, 0, True), (4, 5, False), (7, 20, True),
                                              (16, 0, False), (16, 0, True), (16, 256, False), (16, 240, True),
-                                             (64, 100, False), (128, 2048, True), (300, 4500, False),
+                                             (64, 100, False), (128, 2048, True), (129, 900, False),
+                                             (150, 3000, True), (181, 5000, False), (300, 4500, False),
                                              (1024, 32768, False)])
 def test_select_global_exact(gpu, nb, budget, prior):
     """Scores with many exact ties (multiples of 1/4, both signs of zero): the
-    GPU selection equals the oracle's on the same float32 values."""
+    GPU selection equals the oracle's on the same float32 values. Heads of up
+    to 128 and 181 blocks keep their keys in registers (16 and 32 per thread),
+    larger ones re-read the scores in every pass."""
     r = np.random.Generator(np.random.PCG64(9000 + nb + budget))
     S = np.round(r.standard_normal((2, 3, nb, nb)) * 4) / 4
     S[S == 0] = np.where(r.random(S[S == 0].shape) < 0.5, 0.0, -0.0)
