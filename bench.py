@@ -78,9 +78,10 @@ def tile_floors(w) -> dict:
 
 
 def raw_tiles(w) -> bool:
-    """The forward's tile pass reads bfloat16 K/V tiles from the rows
-    themselves; for float32 pooling also writes a packed copy of K and V."""
-    return w.dtype == "bf16"
+    """The forward's tile pass reads K/V tiles from the rows themselves
+    (bfloat16, float32 with d <= 64); for float32 with d = 128 pooling also
+    writes a packed copy of K and V."""
+    return w.dtype == "bf16" or w.d <= 64
 
 
 def pool_bytes(w, packed=None) -> float:
@@ -411,10 +412,8 @@ def main():
     if not args.no_variants:
         variants["backward"] = backward_leg(w, ops, tq, tk, tv, out, idx, ws, max(args.steps, 20))
 
-    # Dominant kernel: the tile pass on the same inputs, timed alone. For
-    # bfloat16 this is the forward's own instantiation (raw K/V tiles); for
-    # float32 the step-wise call reads row-major K/V while the forward's reads
-    # the packed copy its pooling pass writes.
+    # Dominant kernel: the tile pass on the same inputs, timed alone: the
+    # forward's own instantiation (raw K/V tiles) for every workload here.
     qp, kp, vp = ops.pool(tq, tk, tv)
     S = ops.coarse_scores(qp, kp)
     sel = ops.select(S, w.budget)

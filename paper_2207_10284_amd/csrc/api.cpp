@@ -104,9 +104,10 @@ struct WsLayout {
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-// The forward's tile pass reads bfloat16 K/V tiles straight from their rows;
-// float32 tiles need the packed copy the pooling pass writes.
-bool raw_tiles(int d, mra_dtype_t dtype) { (void)d; return dtype == MRA_BF16; }
+// The forward's tile pass reads K/V tiles straight from their rows (bfloat16,
+// and float32 with d <= 64); float32 tiles of d = 128 need the copy in
+// matrix-core operand order that the pooling pass writes.
+bool raw_tiles(int d, mra_dtype_t dtype) { return dtype == MRA_BF16 || d <= 64; }
 
 WsLayout ws_layout(long long bh, int nb, int d, int m, mra_dtype_t dtype) {
   WsLayout L{};

@@ -23,12 +23,14 @@
 //
 // Two kernels share that per-row arithmetic (struct TileRow), so their results
 // are bit-identical:
-//  * tile_stream_kernel (packed K/V, tiles up to 8 KB): the next selected tile
-//    is copied HBM/L2 -> a wave-private LDS slot with direct-to-LDS loads
-//    while the current one is computed from registers.
-//  * tile_kernel: raw K/V (K rows read directly, V_y through a wave-private
-//    LDS tile stored transposed with the key permutation applied), and packed
-//    K/V with larger tiles (next tile's loads in flight in registers).
+//  * tile_stream_kernel (raw K/V rows: bfloat16, and float32 with d <= 64;
+//    packed K/V, tiles up to 8 KB): the next selected tile is copied HBM/L2 ->
+//    a wave-private LDS slot with direct-to-LDS loads while the current one is
+//    computed from registers.
+//  * tile_kernel: raw float32 K/V with d = 128 (K rows read directly, V_y
+//    through a wave-private LDS tile stored transposed with the key
+//    permutation applied), and packed K/V with larger tiles (next tile's loads
+//    in flight in registers).
 // The softmax reference is set once per row (restart on overflow). Workgroup order
 // is remapped so each XCD processes a contiguous range of heads and keeps
 // their K/V tiles in its L2.
@@ -467,6 +469,63 @@ struct RawTrChunks {
   }
 };
 
+// Raw float32 tiles (d <= 64). K: 4d-byte rows, the byte geometry of a
+// bfloat16 tile of 2d columns, so its copies, swizzle and row-layout reads are
+// those above with D2 = 2d (element (r, c) at raw_offset<D2>(r, 2c)). V is read
+// transposed, four consecutive keys of one column per 16-byte operand chunk,
+// with two ds_read2st64_b32 (keys 8a + 4h + e, e = 0, 1 and 2, 3, 256 bytes
+// apart in LDS); rows are placed so that neither read has a bank conflict
+// (CPU-modelled): d = 32 (128-byte rows): row r of each group of eight at
+// slot 2 (r mod 4) + (r / 4 mod 2), so rows r and r + 4 fall in opposite bank
+// halves; d = 64 (256-byte rows): the two 128-byte halves of rows with
+// r / 4 odd swapped.
+template <int D>
+__host__ __device__ constexpr int f32v_slot(int r) {
+  return D == 32 ? 8 * (r >> 3) + 2 * (r & 3) + ((r >> 2) & 1) : r;
+}
+template <int D>
+__host__ __device__ constexpr int f32v_offset(int r, int c) {
+  return f32v_slot<D>(r) * (4 * D) + 16 * ((c >> 2) ^ (D == 64 ? 8 * ((r >> 2) & 1) : 0)) + 4 * (c & 3);
+}
+// Source byte offset (within the V tile) of the 16 bytes lane `lane` copies to
+// LDS byte i * 1024 + 16 lane.
+template <int D>
+__device__ __forceinline__ int f32v_copy_offset(int i, int lane) {
+  const int rb = 4 * D, q = i * 1024 + 16 * lane, sl = q / rb, b = (q % rb) / 16;
+  if (D == 32) return (8 * (sl >> 3) + 4 * (sl & 1) + ((sl >> 1) & 3)) * rb + 16 * b;
+  return sl * rb + 16 * (b ^ (8 * ((sl >> 2) & 1)));
+}
+
+// The K copies (KPB-periodic lane offsets, as copy_raw_tiles_buf) and the V
+// copies of a raw float32 tile (period 1 for d = 32, 2 for d = 64).
+template <int I>
+__device__ __forceinline__ void copy_raw_f32_buf(i32x4 krs, i32x4 vrs, unsigned ktile, unsigned vtile,
+                                                 const unsigned (&koff)[4], const unsigned (&voff)[2], lptr_t ks,
+                                                 lptr_t vs) {
+  if constexpr (I > 0) {
+    copy_raw_f32_buf<I - 1>(krs, vrs, ktile, vtile, koff, voff, ks, vs);
+    constexpr int i = I - 1;
+    buffer_load_lds16(krs, ks + i * 1024, koff[i & 3], ktile + i * 1024);
+    buffer_load_lds16(vrs, vs + i * 1024, voff[i & 1], vtile + i * 1024);
+  }
+}
+
+// Transposed V chunks c = 4 t + a (c < VC) of a raw float32 tile: keys
+// 8a + 4h + e of column 32 t + i, from this lane's column-tile address vt[t].
+template <int D, int C, int VC>
+struct RawF32TrChunks {
+  static constexpr int K64 = D == 32 ? 4 : 8;          // 256-byte units between key groups a
+  static __device__ __forceinline__ void run(const uint32_t* vt, u32x4* v) {
+    if constexpr (C < VC) {
+      constexpr int t = C / 4, a = C % 4;
+      const u32x2 lo = lds_read2st64<K64 * a, K64 * a + 1>(vt[t]);
+      const u32x2 hi = lds_read2st64<K64 * a + 2, K64 * a + 3>(vt[t]);
+      v[C] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+      RawF32TrChunks<D, C + 1, VC>::run(vt, v);
+    }
+  }
+};
+
 // ---------------------------------------------------------------------------
 // One wave per block-row, K/V staged through a wave-private LDS slot:
 // the next selected tile is copied HBM/L2 -> LDS with direct-to-LDS loads
@@ -484,18 +543,20 @@ __device__ __forceinline__ void wait_tiles_in_flight(int keep) {
   else asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * CH) : "memory");
 }
 
-template <int DT, int D, bool COARSE, int WAVES, int SLOTS, bool RAW>
+template <int DT, int D, bool COARSE, int WAVES, int SLOTS>
 __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
-    const void* __restrict__ qv, const void* __restrict__ kpk, const void* __restrict__ vpk,
+    const void* __restrict__ qv, const void* __restrict__ kv, const void* __restrict__ vv,
     const int32_t* __restrict__ idx, const float* __restrict__ cmax,
     const float* __restrict__ csum, const float* __restrict__ cvec, void* __restrict__ outv,
     float* __restrict__ lse, int n, int nb, int m, long long rows, float scale_log2) {
   using Cfg = TileCfg<DT, D>;
   using elem = typename Cfg::elem;
   constexpr int KC = Cfg::kKChunks, VC = Cfg::kVChunks, CH = Cfg::kChunks;
-  static_assert(CH <= (RAW && D == 128 ? 16 : 8), "operands of a tile are held in registers");
+  static_assert(CH <= 16, "operands of a tile are held in registers");
   static_assert(SLOTS >= 1 && SLOTS <= 3, "tiles in flight per wave");
-  static_assert(!RAW || DT == BF16, "raw tiles: bfloat16");
+  static_assert(DT == BF16 || D <= 64, "raw tiles: bfloat16, or float32 with d <= 64");
+  constexpr bool F32RAW = DT == F32;
+  constexpr int D2 = F32RAW ? 2 * D : D;             // the bfloat16 geometry of the K tile
   // the slots are their own LDS object, apart from the selection lists, so
   // reading a list does not wait for loads in flight into a slot
   __shared__ __attribute__((aligned(16))) u32x4 slot_all[WAVES][SLOTS][CH * 64];
@@ -515,30 +576,30 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
   TileRow<DT, D, COARSE> row;
   row.init(reinterpret_cast<const elem*>(qv) + hoff, x, scale_log2);
   m = stage_selection(idx + g * m, m, nb, myidx);  // valid entries only, in order
-  const char* kslab = static_cast<const char*>(kpk) + (size_t)bh * nb * KC * 1024;
-  const char* vslab = static_cast<const char*>(vpk) + (size_t)bh * nb * VC * 1024;
-  const unsigned loff = lane * 16u;
-  // Packed operands: one lane address per operand; its chunks are 1 KB apart
-  // in memory and in the slot, and the load's immediate offset moves both
-  // addresses.
-  static_assert(RAW || (KC <= 4 && VC <= 4), "chunk offsets fit the immediate field");
-  // raw tiles: this lane's source offsets for the copies (see
-  // copy_raw_tiles_buf) and its LDS read offsets (K chunk c; V^T column tile t)
+  // the head's K and V rows (tile y at byte y * 32 d e)
+  const char* kslab = static_cast<const char*>(kv) + (size_t)bh * nb * KC * 1024;
+  const char* vslab = static_cast<const char*>(vv) + (size_t)bh * nb * VC * 1024;
+  // this lane's source offsets for the copies (see copy_raw_tiles_buf) and its
+  // LDS read offsets (K chunk c; V^T column tile t)
   constexpr int NT = TileCfg<DT, D>::kNT;
-  constexpr int KPB = D == 128 ? 4 : (D == 64 ? 2 : 1);   // period of the K copy offsets
-  unsigned koffq[4] = {0u, 0u, 0u, 0u};             // K source offsets of copies i mod 4
-  i32x4 krs = {0, 0, 0, 0}, vrs = {0, 0, 0, 0};     // the head's K and V rows
-  unsigned voff0 = 0;
+  constexpr int KPB = D2 == 128 ? 4 : (D2 == 64 ? 2 : 1);  // period of the K copy offsets
+  unsigned koffq[4];                                 // K source offsets of copies i mod 4
+#pragma unroll
+  for (int q = 0; q < 4; ++q) koffq[q] = raw_copy_offset<D2, raw_swz_k<D2>>(q % KPB, lane) - (q % KPB) * 1024;
+  const i32x4 krs = buffer_rsrc(kslab, (unsigned)nb * KC * 1024u);
+  const i32x4 vrs = buffer_rsrc(vslab, (unsigned)nb * VC * 1024u);
+  const int h = lane >> 5, j = lane & 31, i16 = lane & 15;
   int kread[KC], vread[NT];
-  if constexpr (RAW) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) koffq[q] = raw_copy_offset<D, raw_swz_k<D>>(q % KPB, lane) - (q % KPB) * 1024;
-    krs = buffer_rsrc(kslab, (unsigned)nb * KC * 1024u);
-    vrs = buffer_rsrc(vslab, (unsigned)nb * VC * 1024u);
+  for (int c = 0; c < KC; ++c) kread[c] = raw_offset<D2, raw_swz_k<D2>>(j, (D2 / 2) * h + 8 * c);
+  unsigned voff0 = 0, voffq[2] = {0u, 0u};
+  if constexpr (F32RAW) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) voffq[q] = f32v_copy_offset<D>(q, lane) - q * 1024;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) vread[t] = KC * 1024 + f32v_offset<D>(4 * h, 32 * t + j);
+  } else {
     voff0 = raw_copy_offset<D, raw_swz_v<D>>(0, lane);
-    const int h = lane >> 5, j = lane & 31, i16 = lane & 15;
-#pragma unroll
-    for (int c = 0; c < KC; ++c) kread[c] = raw_offset<D, raw_swz_k<D>>(j, (D / 2) * h + 8 * c);
 #pragma unroll
     for (int t = 0; t < NT; ++t)
       vread[t] = KC * 1024 +
@@ -548,14 +609,10 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
     unsigned char* slot = reinterpret_cast<unsigned char*>(slot_all[w][sidx]);
     auto* ks = (__attribute__((address_space(3))) char*)slot;
     auto* vs = (__attribute__((address_space(3))) char*)(slot + KC * 1024);
-    if constexpr (RAW) {
+    if constexpr (F32RAW)
+      copy_raw_f32_buf<KC>(krs, vrs, (unsigned)y * KC * 1024u, (unsigned)y * VC * 1024u, koffq, voffq, ks, vs);
+    else
       copy_raw_tiles_buf<KC>(krs, vrs, (unsigned)y * KC * 1024u, (unsigned)y * VC * 1024u, koffq, voff0, ks, vs);
-    } else {
-      const auto* kp = (const __attribute__((address_space(1))) char*)(kslab + (size_t)y * KC * 1024 + loff);
-      const auto* vp = (const __attribute__((address_space(1))) char*)(vslab + (size_t)y * VC * 1024 + loff);
-      load_chunks_lds<KC>(kp, ks);
-      load_chunks_lds<VC>(vp, vs);
-    }
   };
   // entries outside [0, nb) are skipped
   auto next_valid = [&](int j, int& y) {
@@ -581,23 +638,16 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
     while (used < issued) {
       wait_tiles_in_flight<CH>(issued - used - 1);   // tile `used` is in its slot
       u32x4 kf[KC], vf[VC];
-      if constexpr (RAW) {
-        const uint32_t base = lds_addr(slot_all[w][used % SLOTS]);
+      const uint32_t base = lds_addr(slot_all[w][used % SLOTS]);
 #pragma unroll
-        for (int c = 0; c < KC; ++c) kf[c] = lds_read16<0>(base + kread[c]);
-        uint32_t va[NT];
+      for (int c = 0; c < KC; ++c) kf[c] = lds_read16<0>(base + kread[c]);
+      uint32_t va[NT];
 #pragma unroll
-        for (int t = 0; t < NT; ++t) va[t] = base + vread[t];
-        RawTrChunks<D, 0, VC>::run(va, vf);
-        lds_done(kf);
-        lds_done(vf);
-      } else {
-        const u32x4* sl = slot_all[w][used % SLOTS] + lane;
-#pragma unroll
-        for (int c = 0; c < KC; ++c) kf[c] = sl[c * 64];
-#pragma unroll
-        for (int c = 0; c < VC; ++c) vf[c] = sl[(KC + c) * 64];
-      }
+      for (int t = 0; t < NT; ++t) va[t] = base + vread[t];
+      if constexpr (F32RAW) RawF32TrChunks<D, 0, VC>::run(va, vf);
+      else RawTrChunks<D, 0, VC>::run(va, vf);
+      lds_done(kf);
+      lds_done(vf);
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // operands in registers
       ++used;
       if (ni < m) {                                  // refill the slot just read
@@ -619,13 +669,7 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
       const int yy = wave_uniform(myidx[i]);
       if (yy < 0 || yy >= nb) continue;
       u32x4 kf[KC];
-      if constexpr (RAW) {
-        load_rows<DT, D>(reinterpret_cast<const elem*>(kslab + (size_t)yy * KC * 1024), kf);
-      } else {
-        const u32x4* kt = reinterpret_cast<const u32x4*>(kslab + (size_t)yy * KC * 1024) + lane;
-#pragma unroll
-        for (int c = 0; c < KC; ++c) kf[c] = kt[c * 64];
-      }
+      load_rows<DT, D>(reinterpret_cast<const elem*>(kslab + (size_t)yy * KC * 1024), kf);
       mx = __builtin_elementwise_maximum(mx, row.tile_ref(row.scores(kf)));
     }
     row.restart(mx);
@@ -635,62 +679,62 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
 }
 
 // ---------------------------------------------------------------------------
-template <int DT, int D, bool PACKED>
-static void launch_tile_t(const void* q, const void* k, const void* v, const int32_t* idx,
+// Raw K/V tiles of up to 8 KB (bfloat16; float32 with d <= 64) stream through
+// LDS.
+template <int DT, int D>
+static void launch_stream(const void* q, const void* k, const void* v, const int32_t* idx,
                           const float* cmax, const float* csum, const float* cvec, void* out,
-                          float* lse, long long bh, int n, int m, hipStream_t stream) {
-  constexpr int W = TileCfg<DT, D>::kWaves;
+                          float* lse, long long bh, int n, int m, float scale_log2, hipStream_t stream) {
   const int nb = n / kBlock;
   const long long rows = bh * nb;
-  const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
-  // tiles of up to 8 KB (bfloat16 d <= 64, float32 d = 32) stream through LDS:
-  // packed operands, or for bfloat16 the raw rows
-  constexpr bool RAW = !PACKED && DT == BF16;
-  if constexpr (RAW || (PACKED && TileCfg<DT, D>::kChunks <= 8)) {
-    const unsigned blocks = (unsigned)((rows + kStreamWaves - 1) / kStreamWaves);
-    const size_t smem = (size_t)kStreamWaves * m * sizeof(int32_t);
-    if (cmax)
-      tile_stream_kernel<DT, D, true, kStreamWaves, kStreamSlots, RAW><<<blocks, kStreamWaves * kWave, smem, stream>>>(
-          q, k, v, idx, cmax, csum, cvec, out, lse, n, nb, m, rows, scale_log2);
-    else
-      tile_stream_kernel<DT, D, false, kStreamWaves, kStreamSlots, RAW><<<blocks, kStreamWaves * kWave, smem, stream>>>(
-          q, k, v, idx, cmax, csum, cvec, out, lse, n, nb, m, rows, scale_log2);
-    return;
-  }
+  const unsigned blocks = (unsigned)((rows + kStreamWaves - 1) / kStreamWaves);
+  const size_t smem = (size_t)kStreamWaves * m * sizeof(int32_t);  // per-wave selection lists
+  if (cmax)
+    tile_stream_kernel<DT, D, true, kStreamWaves, kStreamSlots><<<blocks, kStreamWaves * kWave, smem, stream>>>(
+        q, k, v, idx, cmax, csum, cvec, out, lse, n, nb, m, rows, scale_log2);
+  else
+    tile_stream_kernel<DT, D, false, kStreamWaves, kStreamSlots><<<blocks, kStreamWaves * kWave, smem, stream>>>(
+        q, k, v, idx, cmax, csum, cvec, out, lse, n, nb, m, rows, scale_log2);
+}
+
+// float32 tiles of d = 128 (16 KB): the packed copy, or the raw rows
+template <bool PACKED>
+static void launch_tile_f32_128(const void* q, const void* k, const void* v, const int32_t* idx,
+                                const float* cmax, const float* csum, const float* cvec, void* out,
+                                float* lse, long long bh, int n, int m, float scale_log2, hipStream_t stream) {
+  constexpr int W = TileCfg<F32, 128>::kWaves;
+  const int nb = n / kBlock;
+  const long long rows = bh * nb;
   const unsigned blocks = (unsigned)((rows + W - 1) / W);
   const size_t smem = (size_t)W * m * sizeof(int32_t);     // per-wave selection lists
   if (cmax)
-    tile_kernel<DT, D, true, PACKED><<<blocks, W * kWave, smem, stream>>>(q, k, v, idx, cmax, csum, cvec, out, lse, n, nb, m, rows, scale_log2);
+    tile_kernel<F32, 128, true, PACKED><<<blocks, W * kWave, smem, stream>>>(q, k, v, idx, cmax, csum, cvec, out, lse, n, nb, m, rows, scale_log2);
   else
-    tile_kernel<DT, D, false, PACKED><<<blocks, W * kWave, smem, stream>>>(q, k, v, idx, cmax, csum, cvec, out, lse, n, nb, m, rows, scale_log2);
-}
-
-template <bool PACKED>
-static void launch_tile_p(const void* q, const void* k, const void* v, const int32_t* idx,
-                          const float* cmax, const float* csum, const float* cvec, void* out,
-                          float* lse, long long bh, int n, int d, int m, int dtype, hipStream_t stream) {
-  if (dtype == BF16) {
-    if (d == 32) launch_tile_t<BF16, 32, PACKED>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, m, stream);
-    else if (d == 64) launch_tile_t<BF16, 64, PACKED>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, m, stream);
-    else launch_tile_t<BF16, 128, PACKED>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, m, stream);
-  } else {
-    if (d == 32) launch_tile_t<F32, 32, PACKED>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, m, stream);
-    else if (d == 64) launch_tile_t<F32, 64, PACKED>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, m, stream);
-    else launch_tile_t<F32, 128, PACKED>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, m, stream);
-  }
+    tile_kernel<F32, 128, false, PACKED><<<blocks, W * kWave, smem, stream>>>(q, k, v, idx, cmax, csum, cvec, out, lse, n, nb, m, rows, scale_log2);
 }
 
 hipError_t launch_tile(const void* q, const void* k, const void* v, const void* kvpacked,
                        const int32_t* idx, const float* cmax, const float* csum,
                        const float* cvec, void* out, float* lse, long long bh, int n, int d,
                        int m, int dtype, hipStream_t stream) {
+  const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)d));
   if (kvpacked) {
-    const size_t half = (size_t)bh * n * d * (dtype == BF16 ? 2 : 4);
+    // only float32 tiles of d = 128 are read from the packed copy
+    if (dtype != F32 || d != 128) return hipErrorInvalidValue;
+    const size_t half = (size_t)bh * n * d * 4;
     const void* kpk = kvpacked;
     const void* vpk = static_cast<const char*>(kvpacked) + half;
-    launch_tile_p<true>(q, kpk, vpk, idx, cmax, csum, cvec, out, lse, bh, n, d, m, dtype, stream);
+    launch_tile_f32_128<true>(q, kpk, vpk, idx, cmax, csum, cvec, out, lse, bh, n, m, scale_log2, stream);
+    return hipGetLastError();
+  }
+  if (dtype == BF16) {
+    if (d == 32) launch_stream<BF16, 32>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, m, scale_log2, stream);
+    else if (d == 64) launch_stream<BF16, 64>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, m, scale_log2, stream);
+    else launch_stream<BF16, 128>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, m, scale_log2, stream);
   } else {
-    launch_tile_p<false>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, d, m, dtype, stream);
+    if (d == 32) launch_stream<F32, 32>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, m, scale_log2, stream);
+    else if (d == 64) launch_stream<F32, 64>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, m, scale_log2, stream);
+    else launch_tile_f32_128<false>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, m, scale_log2, stream);
   }
   return hipGetLastError();
 }

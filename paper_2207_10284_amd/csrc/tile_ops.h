@@ -164,6 +164,15 @@ __device__ __forceinline__ u32x2 lds_read_tr16(uint32_t addr) {
   return v;
 }
 
+// Two dwords per lane from addr + 256 OFF0 and addr + 256 OFF1 bytes
+// (ds_read2st64_b32: offsets in units of 64 dwords).
+template <int OFF0, int OFF1>
+__device__ __forceinline__ u32x2 lds_read2st64(uint32_t addr) {
+  u32x2 v;
+  asm volatile("ds_read2st64_b32 %0, %1 offset0:%2 offset1:%3" : "=v"(v) : "v"(addr), "i"(OFF0), "i"(OFF1) : "memory");
+  return v;
+}
+
 typedef const __attribute__((address_space(1))) char* gptr_t;
 typedef __attribute__((address_space(3))) char* lptr_t;
 

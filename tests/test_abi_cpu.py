@@ -136,8 +136,8 @@ def test_workspace_bytes(lib):
     bh, nb = B * H, n // 32
     for dd in (32, 64, 128):
         for dt, e in ((0, 4), (1, 2)):
-            # packed K/V copy only where the tile pass cannot read raw rows (float32)
-            packed = al(2 * bh * n * dd * e) if dt == 0 else 0
+            # packed K/V copy only where the tile pass cannot read raw rows (float32, d = 128)
+            packed = al(2 * bh * n * dd * e) if dt == 0 and dd == 128 else 0
             want = 3 * al(bh * nb * dd * 4) + packed + al(bh * nb * m * 4) \
                 + 2 * al(bh * nb * 4) + al(bh * nb * dd * 4)
             assert f(B, H, n, dd, 32, m, dt) == want, (dd, dt)

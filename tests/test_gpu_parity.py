@@ -266,7 +266,8 @@ def test_reference_restart(gpu, dtype, d):
     selected block has logits of 120: relative to the first block's max the
     later weights would overflow, so the tile pass computes the row again
     relative to its exact max. The result matches the oracle, is finite, and
-    the packed-operand and row-major paths agree bitwise."""
+    the forward agrees bitwise with the step-wise calls (for float32 d = 128
+    that compares the packed-operand path with the row-major one)."""
     _say("restart", dtype, d)
     n, m = 256, 4
     r = np.random.Generator(np.random.PCG64(4242 + d))

@@ -229,3 +229,71 @@ def test_forward_swizzles_do_not_serve_both_reads():
     assert conflict_ways(sup, 8) == 2
     addrs = [offset(d, l % 32, 8 * 0, swz_v) for l in range(16)]
     assert conflict_ways(addrs, 16) > 1
+
+
+# ---------------------------------------------------------------- raw float32 tiles (d <= 64)
+def f32v_slot(d, r):
+    return 8 * (r >> 3) + 2 * (r & 3) + ((r >> 2) & 1) if d == 32 else r
+
+
+def f32v_offset(d, r, c):
+    """LDS byte of element (r, c) of a raw float32 V tile."""
+    return f32v_slot(d, r) * (4 * d) + 16 * ((c >> 2) ^ (8 * ((r >> 2) & 1) if d == 64 else 0)) + 4 * (c & 3)
+
+
+def f32v_copy_offset(d, i, lane):
+    rb = 4 * d
+    q = i * 1024 + 16 * lane
+    sl, b = q // rb, (q % rb) // 16
+    if d == 32:
+        return (8 * (sl >> 3) + 4 * (sl & 1) + ((sl >> 1) & 3)) * rb + 16 * b
+    return sl * rb + 16 * (b ^ (8 * ((sl >> 2) & 1)))
+
+
+@pytest.mark.parametrize("d", [32, 64])
+def test_f32_k_tile_is_the_bf16_geometry_of_twice_the_width(d):
+    """A float32 K tile of d columns has the bytes of a bfloat16 tile of 2d
+    columns; element (r, c) sits at the bfloat16 offset of (r, 2c), and the
+    row-layout chunk s of lane (h, j), float32 columns (d/2) h + 4s .. + 3,
+    is the bfloat16 chunk of the same lane."""
+    d2 = 2 * d
+    for lane in range(64):
+        h, j = lane // 32, lane % 32
+        for s_ in range(d // 8):
+            a = offset(d2, j, (d2 // 2) * h + 8 * s_, swz_k)
+            for e in range(4):
+                assert offset(d2, j, 2 * ((d // 2) * h + 4 * s_ + e), swz_k) == a + 4 * e
+
+
+@pytest.mark.parametrize("d", [32, 64])
+def test_f32_v_copies_and_transposed_reads(d):
+    """Copies place every 16-byte block of the row-major V tile once where
+    f32v_offset expects it (with lane offsets of period 1 or 2 in the copy
+    index); chunk (t, a) of lane (h, i) holds V[8a + 4h + e][32t + i], e < 4,
+    read with two ds_read2st64_b32 from one address per column tile at
+    offsets of 256 bytes, each dword pass over 64 lanes hitting 64 banks."""
+    rb = 4 * d
+    seen = set()
+    for i in range(32 * rb // 1024):
+        for lane in range(64):
+            src = f32v_copy_offset(d, i, lane)
+            r, c = src // rb, (src % rb) // 4
+            assert 0 <= src and src + 16 <= 32 * rb             # inside the block's V tile
+            assert f32v_offset(d, r, c) == i * 1024 + 16 * lane
+            per = 1 if d == 32 else 2
+            assert src - i * 1024 == f32v_copy_offset(d, i % per, lane) - (i % per) * 1024
+            seen.add(src)
+    assert len(seen) == 32 * rb // 16
+    k64 = 4 if d == 32 else 8
+    for t in range(d // 32):
+        for a in range(4):
+            for e0 in (0, 2):
+                for e in (e0, e0 + 1):
+                    addrs = []
+                    for lane in range(64):
+                        h, i = lane // 32, lane % 32
+                        base = f32v_offset(d, 4 * h, 32 * t + i)
+                        got = base + 256 * (k64 * a + e)
+                        assert got == f32v_offset(d, 8 * a + 4 * h + e, 32 * t + i)
+                        addrs.append(got)
+                    assert conflict_ways(addrs, 4) == 1
