@@ -151,8 +151,8 @@ mra_status_t check_global_budget(const Shape& s, int budget, int prior_diagonal)
 
 // Workspace of the gradient pass (pointer roles in kernels.h, BwdArgs).
 struct WsBwd {
-  size_t qp, kp, vp, q_row, q_t, k_row, k_t, v_row, g_row, g_t, ld, bits, gh, W, dS, dqp, dkp,
-      dvp, total;
+  size_t qp, kp, vp, q_row, q_t, k_row, k_t, v_row, g_row, g_t, ld, bias, bits, gh, W, dS, dqp,
+      dkp, dvp, total;
 };
 
 WsBwd ws_bwd(long long bh, int nb, int d, mra_dtype_t dtype) {
@@ -174,6 +174,7 @@ WsBwd ws_bwd(long long bh, int nb, int d, mra_dtype_t dtype) {
   L.g_row = off; off += packed;
   L.g_t = off; off += packed;
   L.ld = off; off += align256((size_t)bh * nb * 64 * sizeof(float));
+  L.bias = off; off += raw ? align256((size_t)bh * nb * kBlockSize * 16) : 0;
   L.bits = off; off += align256((size_t)bh * nb * ((nb + 31) / 32) * sizeof(uint32_t));
   L.gh = off; off += pooled;
   L.W = off; off += grid;
@@ -557,6 +558,7 @@ mra_status_t mra_attention_backward(const void* q, const void* k, const void* v,
   A.q_row = ws + L.q_row; A.q_t = ws + L.q_t; A.k_row = ws + L.k_row; A.k_t = ws + L.k_t;
   A.v_row = ws + L.v_row; A.g_row = ws + L.g_row; A.g_t = ws + L.g_t;
   A.ld = f32(L.ld);
+  A.bias = dtype == MRA_BF16 && d <= 64 ? reinterpret_cast<uint32_t*>(ws + L.bias) : nullptr;
   A.bits = reinterpret_cast<uint32_t*>(ws + L.bits);
   A.gh = f32(L.gh); A.W = f32(L.W); A.dS = f32(L.dS);
   A.dqp = f32(L.dqp); A.dkp = f32(L.dkp); A.dvp = f32(L.dvp);

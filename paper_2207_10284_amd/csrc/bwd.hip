@@ -31,7 +31,10 @@
 //    products K_y Q_x^T and V_y G_x^T on the matrix cores, then
 //    dQ^T += K_y^T dP^T.
 //  * bwd_dkdv_(stream_)kernel: per column block (a wave), over the block-rows that
-//    refined it (ascending): dV^T += G_x^T A, dK^T += c Q_x^T dP.
+//    refined it (ascending): dV^T += G_x^T A, dK^T += c Q_x^T dP. For raw
+//    tiles the row pass also writes, per query, the bfloat16 triples of
+//    -L_i/c and -delta_i, which enter the products as one more contraction
+//    step, so a lane holding 16 queries needs no per-query registers.
 // Tile operands: for bfloat16 with d <= 64 raw 32-row tiles of the inputs
 // (copied into LDS under a swizzle that serves row and transposed reads);
 // otherwise packed copies in the layouts of tile_ops.h.
@@ -44,6 +47,10 @@ namespace mra {
 constexpr int kBwdRows = 16;              // waves (block-rows) per workgroup of the row pass
 constexpr int kBwdTileWaves = 4;          // waves per workgroup of the tile passes
 constexpr int kBwdCols = 16;              // column blocks per workgroup of the column pass
+// Raw-tile slots per wave of the bfloat16 gradient passes: one (the next tile
+// is copied once the current one is in registers) measured faster than two.
+constexpr int kDqSlots = 1;
+constexpr int kDkdvSlots = 1;
 
 template <int DT>
 __device__ __forceinline__ float elem_lo(uint32_t w) {
@@ -52,6 +59,25 @@ __device__ __forceinline__ float elem_lo(uint32_t w) {
 
 __device__ __forceinline__ f32x4 mfma16x4(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// x as hi + mid + lo, each rounded to bfloat16 in turn (the two differences
+// are exact in float32, so the sum is x to about 2^-24 |x|).
+__device__ __forceinline__ uint32_t split3_bf16(float x, uint32_t& mid_lo) {
+  const __bf16 hi = (__bf16)x;
+  const float r1 = x - (float)hi;
+  const __bf16 mid = (__bf16)r1;
+  const __bf16 lo = (__bf16)(r1 - (float)mid);
+  mid_lo = (uint32_t)__builtin_bit_cast(uint16_t, mid) | ((uint32_t)__builtin_bit_cast(uint16_t, lo) << 16);
+  return __builtin_bit_cast(uint16_t, hi);
+}
+
+// One query's bias operand for the column pass: the bfloat16 elements
+// [hi(x), mid(x), lo(x), hi(y), mid(y), lo(y), 0, 0].
+__device__ __forceinline__ u32x4 bias_operand(float x, float y) {
+  uint32_t xm, ym;
+  const uint32_t xh = split3_bf16(x, xm), yh = split3_bf16(y, ym);
+  return u32x4{xh | (xm << 16), (xm >> 16) | (yh << 16), ym, 0u};
 }
 
 // ---------------------------------------------------------------------------
@@ -69,7 +95,8 @@ template <int DT, int D, bool COARSE>
 __global__ __launch_bounds__(kBwdRows * kWave) __attribute__((amdgpu_waves_per_eu(D <= 64 ? 8 : 1, 8))) void bwd_rows_kernel(
     const void* __restrict__ gin, const void* __restrict__ zin, const float* __restrict__ lse,
     const int32_t* __restrict__ idx, const float* __restrict__ qp, const float* __restrict__ kp,
-    const float* __restrict__ vp, float* __restrict__ ld, uint32_t* __restrict__ bits, float* __restrict__ gh, float* __restrict__ Wout,
+    const float* __restrict__ vp, float* __restrict__ ld, uint32_t* __restrict__ bias,
+    uint32_t* __restrict__ bits, float* __restrict__ gh, float* __restrict__ Wout,
     float* __restrict__ dSout, float* __restrict__ dqp, int nb, int m, float scale) {
   using Cfg = TileCfg<DT, D>;
   using elem = typename Cfg::elem;
@@ -122,6 +149,8 @@ __global__ __launch_bounds__(kBwdRows * kWave) __attribute__((amdgpu_waves_per_e
     if (h == 0) {                                           // the block-row's record
       ld[g * 64 + j] = L * kLog2e;
       ld[g * 64 + 32 + j] = dl;
+      if (bias != nullptr)
+        *reinterpret_cast<u32x4*>(bias + (g * 32 + j) * 4) = bias_operand(-L / scale, -dl);
     }
     // the selection as a bitmap (entries outside [0, nb) ignored)
     for (int i = lane; i < nbw; i += kWave) bm[i] = 0u;
@@ -320,6 +349,21 @@ __device__ __forceinline__ void pack16(const float (&v)[16], uint32_t (&pk)[8]) 
     pb[1] = (__bf16)v[2 * rr + 1];
     pk[rr] = __builtin_bit_cast(uint32_t, pb);
   }
+}
+
+// C = X0 Y0^T + A B^T (bfloat16, row layout): the product of one more
+// contraction step x0, y0 (16 elements of each row) followed by the KC chunks
+// of a and b.
+template <int KC>
+__device__ __forceinline__ f32x16 mfma_abt_from(const u32x4 (&a)[KC], const u32x4 (&b)[KC], u32x4 x0, u32x4 y0) {
+  f32x16 c;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) c[r] = 0.0f;
+  c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, x0), __builtin_bit_cast(bf16x8, y0), c, 0, 0, 0);
+#pragma unroll
+  for (int k = 0; k < KC; ++k)
+    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[k]), __builtin_bit_cast(bf16x8, b[k]), c, 0, 0, 0);
+  return c;
 }
 
 // ---------------------------------------------------------------------------
@@ -854,15 +898,20 @@ struct RawB {
   }
 };
 
-// Two raw tiles (sources a and b, LDS destinations as and bs), C 1 KB copies each.
+// Two raw tiles, C 1 KB copies each, as buffer loads to LDS: the heads' rows
+// are the resources ra and rb, the tiles' byte offsets ta and tb go in the
+// scalar offset (outside the hardware range check: callers copy validated
+// blocks only), this lane's swizzled source offset (c0 for even copies, c1
+// for odd ones when the offsets have period 2) in the vector offset.
 template <int C, int KP>
-__device__ __forceinline__ void copy_raw_pair(gptr_t a0, gptr_t a1, gptr_t b0, gptr_t b1, lptr_t as,
-                                              lptr_t bs) {
+__device__ __forceinline__ void copy_raw_pair_buf(i32x4 ra, i32x4 rb, unsigned ta, unsigned tb,
+                                                  unsigned c0, unsigned c1, lptr_t as, lptr_t bs) {
   if constexpr (C > 0) {
-    copy_raw_pair<C - 1, KP>(a0, a1, b0, b1, as, bs);
+    copy_raw_pair_buf<C - 1, KP>(ra, rb, ta, tb, c0, c1, as, bs);
     constexpr int i = C - 1;
-    __builtin_amdgcn_global_load_lds((KP == 2 && (i & 1)) ? a1 : a0, as, 16, i * 1024, 0);
-    __builtin_amdgcn_global_load_lds((KP == 2 && (i & 1)) ? b1 : b0, bs, 16, i * 1024, 0);
+    const unsigned vo = (KP == 2 && (i & 1)) ? c1 : c0;
+    buffer_load_lds16(ra, as + i * 1024, vo, ta + i * 1024);
+    buffer_load_lds16(rb, bs + i * 1024, vo, tb + i * 1024);
   }
 }
 
@@ -890,8 +939,10 @@ struct RawTrB {
 };
 
 // dQ (bf16, d <= 64): one wave per block-row; a slot holds the raw tiles K_y
-// and V_y (K^T is read transposed from the K tile).
-template <int D, bool COARSE, int WAVES>
+// and V_y (K^T is read transposed from the K tile). SLOTS tiles in flight per
+// wave: with one slot the next tile is copied once the current one is in
+// registers.
+template <int D, bool COARSE, int WAVES, int SLOTS>
 __global__ __launch_bounds__(WAVES * kWave) void bwd_dq_tr_kernel(
     const void* __restrict__ qin, const void* __restrict__ gin, const void* __restrict__ kin,
     const void* __restrict__ vin, const int32_t* __restrict__ idx,
@@ -904,7 +955,8 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dq_tr_kernel(
   constexpr int TB = R::TB, N = 2 * KC;                     // loads per tile
   constexpr int SLOT = 2 * TB;
   static_assert(KC == R::KC && KC <= 4 && VC <= 4, "raw tiles of d <= 64");
-  __shared__ __attribute__((aligned(16))) unsigned char slots[WAVES][2][SLOT];
+  static_assert(SLOTS == 1 || SLOTS == 2, "tiles in flight per wave");
+  __shared__ __attribute__((aligned(16))) unsigned char slots[WAVES][SLOTS][SLOT];
   extern __shared__ int32_t sidx_all[];
   const int w = wave_uniform(threadIdx.x / kWave);
   const int lane = lane_id(), jq = lane & 31;
@@ -926,20 +978,20 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dq_tr_kernel(
 
   R ro;
   ro.init();
-  const char* kh = static_cast<const char*>(kin) + (size_t)bh * nb * TB;
-  const char* vh = static_cast<const char*>(vin) + (size_t)bh * nb * TB;
+  const i32x4 krs = buffer_rsrc(static_cast<const char*>(kin) + (size_t)bh * nb * TB, (unsigned)nb * TB);
+  const i32x4 vrs = buffer_rsrc(static_cast<const char*>(vin) + (size_t)bh * nb * TB, (unsigned)nb * TB);
   const uint32_t a0 = lds_addr(slots[w][0]);
   auto issue = [&](int y, int sl) {
     const lptr_t dst = (lptr_t)slots[w][sl];
-    const gptr_t kt = (gptr_t)(kh + (size_t)y * TB), vt = (gptr_t)(vh + (size_t)y * TB);
-    copy_raw_pair<KC, R::KP>(kt + ro.c0, kt + ro.c1, vt + ro.c0, vt + ro.c1, dst, dst + TB);
+    copy_raw_pair_buf<KC, R::KP>(krs, vrs, (unsigned)y * TB, (unsigned)y * TB, ro.c0, ro.c1, dst, dst + TB);
   };
-  if (cnt > 0) issue(wave_uniform(myidx[0]), 0);
-  if (cnt > 1) issue(wave_uniform(myidx[1]), 1);
+#pragma unroll
+  for (int t = 0; t < SLOTS; ++t)
+    if (cnt > t) issue(wave_uniform(myidx[t]), t);
   for (int i = 0; i < cnt; ++i) {
-    if (i + 1 < cnt) wait_loads<N>();                       // tile i landed, i+1 may not have
+    if (SLOTS == 2 && i + 1 < cnt) wait_loads<N>();         // tile i landed, i+1 may not have
     else wait_loads<0>();
-    const uint32_t base = a0 + (uint32_t)((i & 1) * SLOT);
+    const uint32_t base = a0 + (uint32_t)((i % SLOTS) * SLOT);
     u32x4 kf[KC], vf[KC], tf[VC];
     raw_rows<0>(base, ro.rr, kf);
     raw_rows<TB>(base, ro.rr, vf);
@@ -947,7 +999,7 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dq_tr_kernel(
     lds_done(kf);
     lds_done(vf);
     lds_done(tf);
-    if (i + 2 < cnt) issue(wave_uniform(myidx[i + 2]), i & 1);
+    if (i + SLOTS < cnt) issue(wave_uniform(myidx[i + SLOTS]), i % SLOTS);
     const f32x16 s = mfma_abt<BF16, KC>(kf, qf);
     const f32x16 pv = mfma_abt<BF16, KC>(vf, gf);
     float ds[16];
@@ -963,26 +1015,32 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dq_tr_kernel(
 }
 
 // dK, dV (bf16, d <= 64): one wave per column block; a slot holds the raw
-// tiles Q_x and G_x and block-row x's record (Q^T and G^T are read
-// transposed).
-template <int D, bool COARSE, int WAVES>
+// tiles Q_x and G_x and block-row x's bias operands (Q^T and G^T are read
+// transposed). The log normalisers and deltas enter the two products of a
+// tile through one more matrix-core step each (A: the queries' bias operands,
+// B: ones at the positions of the first or of the second triple), so the
+// products come out as Q_i.K_j - L_i/c and G_i.V_j - delta_i, and each lane
+// needs one 16-byte read for the 16 queries it holds.
+template <int D, bool COARSE, int WAVES, int SLOTS>
 __global__ __launch_bounds__(WAVES * kWave) void bwd_dkdv_tr_kernel(
     const void* __restrict__ kin, const void* __restrict__ vin, const void* __restrict__ qin,
     const void* __restrict__ gin, const uint32_t* __restrict__ bits,
-    const float* __restrict__ ld, const float* __restrict__ dkp, const float* __restrict__ dvp,
+    const uint32_t* __restrict__ bias, const float* __restrict__ dkp, const float* __restrict__ dvp,
     void* __restrict__ dk, void* __restrict__ dv, int nb, long long rows, float scale,
     float scale_log2) {
   using Cfg = TileCfg<BF16, D>;
   using elem = typename Cfg::elem;
   using R = RawB<D>;
   constexpr int KC = Cfg::kKChunks, VC = Cfg::kVChunks, NT = Cfg::kNT;
-  constexpr int TB = R::TB, N = 2 * KC + 1;                 // loads per tile
-  constexpr int SLOT = 2 * TB + 256;
+  constexpr int TB = R::TB, RB = 32 * 16;                   // bytes of a raw tile, of a block-row's bias operands
+  constexpr int N = 2 * KC + 2;                             // loads per tile
+  constexpr int SLOT = 2 * TB + RB;
   static_assert(KC == R::KC && KC <= 4 && VC <= 4, "raw tiles of d <= 64");
-  __shared__ __attribute__((aligned(16))) unsigned char slots[WAVES][2][SLOT];
+  static_assert(SLOTS == 1 || SLOTS == 2, "tiles in flight per wave");
+  __shared__ __attribute__((aligned(16))) unsigned char slots[WAVES][SLOTS][SLOT];
   extern __shared__ int32_t sidx_all[];
   const int w = wave_uniform(threadIdx.x / kWave);
-  const int lane = lane_id(), h = lane >> 5;
+  const int lane = lane_id();
   const long long gy = xcd_remap(blockIdx.x, gridDim.x) * (long long)WAVES + w;
   if (gy >= rows) return;                                   // no workgroup barriers below
   const long long bh = gy / nb;
@@ -1011,53 +1069,50 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dkdv_tr_kernel(
   for (int t = 0; t < NT; ++t)
 #pragma unroll
     for (int r = 0; r < 16; ++r) ak[t][r] = av[t][r] = 0.0f;
+  // B operands of the bias steps: lane l holds B[k = 8 (l/32) + e][l % 32]
+  const bool lo_half = lane < 32;
+  const u32x4 ones_l = lo_half ? u32x4{0x3F803F80u, 0x00003F80u, 0u, 0u} : u32x4{0u, 0u, 0u, 0u};
+  const u32x4 ones_d = lo_half ? u32x4{0u, 0x3F800000u, 0x3F803F80u, 0u} : u32x4{0u, 0u, 0u, 0u};
 
   R ro;
   ro.init();
-  const char* qh = static_cast<const char*>(qin) + (size_t)hb * TB;
-  const char* gh = static_cast<const char*>(gin) + (size_t)hb * TB;
-  const char* xs = reinterpret_cast<const char*>(ld + hb * 64) + lane * 4u;
+  const i32x4 qrs = buffer_rsrc(static_cast<const char*>(qin) + (size_t)hb * TB, (unsigned)nb * TB);
+  const i32x4 grs = buffer_rsrc(static_cast<const char*>(gin) + (size_t)hb * TB, (unsigned)nb * TB);
+  const i32x4 brs = buffer_rsrc(reinterpret_cast<const char*>(bias) + (size_t)hb * RB, (unsigned)nb * RB);
   const uint32_t a0 = lds_addr(slots[w][0]);
-  const uint32_t xl = (uint32_t)(2 * TB) + 16u * h;        // this half's queries in the record
+  const uint32_t boff = (uint32_t)(2 * TB) + 16u * (lane & 31);   // this lane's query's bias operand
   auto issue = [&](int x, int sl) {
     const lptr_t dst = (lptr_t)slots[w][sl];
-    const gptr_t qt = (gptr_t)(qh + (size_t)x * TB), gt = (gptr_t)(gh + (size_t)x * TB);
-    copy_raw_pair<KC, R::KP>(qt + ro.c0, qt + ro.c1, gt + ro.c0, gt + ro.c1, dst, dst + TB);
-    __builtin_amdgcn_global_load_lds((gptr_t)(xs + (size_t)x * 256), dst + 2 * TB, 4, 0, 0);
+    copy_raw_pair_buf<KC, R::KP>(qrs, grs, (unsigned)x * TB, (unsigned)x * TB, ro.c0, ro.c1, dst, dst + TB);
+    mra_raw_buffer_load_lds(brs, dst + 2 * TB, 4, lane * 4, x * RB, 0, 0);
+    mra_raw_buffer_load_lds(brs, dst + 2 * TB + 256, 4, lane * 4, x * RB + 256, 0, 0);
   };
-  if (cnt > 0) issue(wave_uniform(myx[0]), 0);
-  if (cnt > 1) issue(wave_uniform(myx[1]), 1);
+#pragma unroll
+  for (int t = 0; t < SLOTS; ++t)
+    if (cnt > t) issue(wave_uniform(myx[t]), t);
   for (int i = 0; i < cnt; ++i) {
-    if (i + 1 < cnt) wait_loads<N>();                       // tile i landed, i+1 may not have
+    if (SLOTS == 2 && i + 1 < cnt) wait_loads<N>();         // tile i landed, i+1 may not have
     else wait_loads<0>();
-    const uint32_t base = a0 + (uint32_t)((i & 1) * SLOT);
-    u32x4 qa[KC], ga[KC], qt[VC], gtc[VC], xr[8];
+    const uint32_t base = a0 + (uint32_t)((i % SLOTS) * SLOT);
+    u32x4 qa[KC], ga[KC], qt[VC], gtc[VC], ba[1];
     raw_rows<0>(base, ro.rr, qa);
     raw_rows<TB>(base, ro.rr, ga);
     RawTrB<D, 0, 0, VC>::run(base, ro.tr, qt);
     RawTrB<D, TB, 0, VC>::run(base, ro.tr, gtc);
-    xr[0] = lds_read16<0>(base + xl);
-    xr[1] = lds_read16<32>(base + xl);
-    xr[2] = lds_read16<64>(base + xl);
-    xr[3] = lds_read16<96>(base + xl);
-    xr[4] = lds_read16<128>(base + xl);
-    xr[5] = lds_read16<160>(base + xl);
-    xr[6] = lds_read16<192>(base + xl);
-    xr[7] = lds_read16<224>(base + xl);
+    ba[0] = lds_read16<0>(base + boff);
     lds_done(qa);
     lds_done(ga);
     lds_done(qt);
     lds_done(gtc);
-    lds_done(xr);
-    if (i + 2 < cnt) issue(wave_uniform(myx[i + 2]), i & 1);
-    const f32x16 s = mfma_abt<BF16, KC>(qa, kf);            // lane: key, 16 queries
-    const f32x16 pv = mfma_abt<BF16, KC>(ga, vf);
+    lds_done(ba);
+    if (i + SLOTS < cnt) issue(wave_uniform(myx[i + SLOTS]), i % SLOTS);
+    const f32x16 s = mfma_abt_from<KC>(qa, kf, ba[0], ones_l);   // lane: key, 16 queries
+    const f32x16 pv = mfma_abt_from<KC>(ga, vf, ba[0], ones_d);
     float a[16], ds[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const float lq = __uint_as_float(xr[r / 4][r % 4]), dl = __uint_as_float(xr[4 + r / 4][r % 4]);
-      a[r] = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -lq));
-      ds[r] = a[r] * (pv[r] - dl);
+      a[r] = __builtin_amdgcn_exp2f(s[r] * scale_log2);
+      ds[r] = a[r] * pv[r];
     }
     uint32_t pa8[8], pd8[8];
     pack16(a, pa8);
@@ -1084,12 +1139,12 @@ static void launch_tiles_t(const BwdArgs& A, hipStream_t stream) {
   const size_t smem_dkdv = (size_t)kBwdTileWaves * nb * sizeof(int32_t);
   constexpr int W = kBwdTileWaves;
   if constexpr (DT == BF16 && Cfg::kKChunks <= 4 && Cfg::kVChunks <= 4) {
-    bwd_dq_tr_kernel<D, COARSE, W><<<wgs, W * kWave, smem_dq, stream>>>(
+    bwd_dq_tr_kernel<D, COARSE, W, kDqSlots><<<wgs, W * kWave, smem_dq, stream>>>(
         A.q, A.dout, A.k, A.v, A.idx, A.ld, A.dqp, A.dq, nb, A.m, rows, scale, scale_log2);
     // one wave per workgroup: column lists differ in length (a workgroup
     // keeps its LDS until its longest list is done), rows all have m tiles
-    bwd_dkdv_tr_kernel<D, COARSE, 1><<<(unsigned)rows, kWave, nb * sizeof(int32_t), stream>>>(
-        A.k, A.v, A.q, A.dout, A.bits, A.ld, A.dkp, A.dvp, A.dk, A.dv, nb, rows, scale,
+    bwd_dkdv_tr_kernel<D, COARSE, 1, kDkdvSlots><<<(unsigned)rows, kWave, nb * sizeof(int32_t), stream>>>(
+        A.k, A.v, A.q, A.dout, A.bits, A.bias, A.dkp, A.dvp, A.dk, A.dv, nb, rows, scale,
         scale_log2);
   } else if constexpr (Cfg::kKChunks <= 4 && Cfg::kVChunks <= 4) {
     bwd_dq_stream_kernel<DT, D, COARSE, W><<<wgs, W * kWave, smem_dq, stream>>>(
@@ -1116,7 +1171,7 @@ static void launch_bwd_t(const BwdArgs& A, hipStream_t stream) {
   const unsigned wg_rows = (unsigned)(A.bh * groups);
   if (A.coarse) {
     bwd_rows_kernel<DT, D, true><<<wg_rows, kBwdRows * kWave, 0, stream>>>(
-        A.dout, A.out, A.lse, A.idx, A.qp, A.kp, A.vp, A.ld, A.bits, A.gh, A.W, A.dS, A.dqp, nb,
+        A.dout, A.out, A.lse, A.idx, A.qp, A.kp, A.vp, A.ld, A.bias, A.bits, A.gh, A.W, A.dS, A.dqp, nb,
         A.m, scale);
     const unsigned wg_cols = (unsigned)(A.bh * ((nb + kBwdCols - 1) / kBwdCols));
     bwd_cols_kernel<D><<<wg_cols, ColsCfg<D>::kWaves * kWave, 0, stream>>>(
@@ -1124,7 +1179,7 @@ static void launch_bwd_t(const BwdArgs& A, hipStream_t stream) {
     launch_tiles_t<DT, D, true>(A, stream);
   } else {
     bwd_rows_kernel<DT, D, false><<<wg_rows, kBwdRows * kWave, 0, stream>>>(
-        A.dout, A.out, A.lse, A.idx, A.qp, A.kp, A.vp, A.ld, A.bits, A.gh, A.W, A.dS, A.dqp, nb,
+        A.dout, A.out, A.lse, A.idx, A.qp, A.kp, A.vp, A.ld, A.bias, A.bits, A.gh, A.W, A.dS, A.dqp, nb,
         A.m, scale);
     launch_tiles_t<DT, D, false>(A, stream);
   }

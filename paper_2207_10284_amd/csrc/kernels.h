@@ -112,8 +112,11 @@ hipError_t launch_tile(const void* q, const void* k, const void* v, const void* 
 // pointers are workspace: pooled rows (coarse only) [bh, nb, d] f32; packed
 // operand copies (row / transposed layout above) of bh*n*d elements of
 // dtype (not used for bfloat16 with d <= 64, whose passes read raw tiles); ld [bh*nb, 64] f32 (per block-row: 32 log normalisers in log2 units,
-// then 32 deltas); bits [bh*nb, ceil(nb/32)] u32; gh, dqp, dkp, dvp
-// [bh, nb, d] f32 and W, dS [bh, nb, nb] f32 (coarse only).
+// then 32 deltas); bias [bh*n] x 16 bytes (bfloat16 with d <= 64 only, else
+// NULL: per query the bfloat16 triples hi + mid + lo of -L_i/c and of
+// -delta_i, the A operand that adds both to the column pass's products);
+// bits [bh*nb, ceil(nb/32)] u32; gh, dqp, dkp, dvp [bh, nb, d] f32 and W, dS
+// [bh, nb, nb] f32 (coarse only).
 struct BwdArgs {
   const void *q, *k, *v, *out, *dout;
   const float* lse;
@@ -125,6 +128,7 @@ struct BwdArgs {
   float *qp, *kp, *vp;
   void *q_row, *q_t, *k_row, *k_t, *v_row, *g_row, *g_t;
   float* ld;
+  uint32_t* bias;
   uint32_t* bits;
   float *gh, *W, *dS, *dqp, *dkp, *dvp;
 };

@@ -289,8 +289,10 @@ def test_backward_workspace_bytes(lib):
     B, H, n, d = 8, 12, 4096, 64
     bh, nb = B * H, n // 32
     for dt, e in ((0, 4), (1, 2)):
-        copies = 0 if (dt == 1 and d <= 64) else 7    # bf16 with d <= 64 reads raw tiles
-        want = 7 * al(bh * nb * d * 4) + copies * al(bh * n * d * e) + al(bh * nb * 64 * 4) \
+        raw = dt == 1 and d <= 64                     # bf16 with d <= 64 reads raw tiles
+        copies = 0 if raw else 7
+        bias = al(bh * n * 16) if raw else 0          # per query, the column pass's bias operand
+        want = 7 * al(bh * nb * d * 4) + copies * al(bh * n * d * e) + al(bh * nb * 64 * 4) + bias \
             + al(bh * nb * (nb // 32) * 4) + 2 * al(bh * nb * nb * 4)
         assert f(B, H, n, d, 32, dt) == want
     # bf16 with d = 128 keeps its rearranged copies
