@@ -30,7 +30,10 @@ selected blocks, normalised by their own row sums) is ``mra2s_rows``.
 
 Three resolutions R = {s0, b, 1} (Alg. 1 with two refinement levels, budgets
 per block-row at each level) are ``select_multilevel``,
-``mra_multilevel_dense`` and ``mra_multilevel_factored``.
+``mra_multilevel_dense`` and ``mra_multilevel_factored``; any number of
+resolutions R = {s_0 > s_1 > ... > s_{L-1}, 1} (Alg. 1 refining level by
+level) are ``select_levels``, ``mra_levels_dense`` and
+``mra_levels_factored``.
 
 Gradients with the selection held fixed (``mra_grads``) differentiate the
 factored form written with torch float64 CPU operations (``mra_torch``, which
@@ -438,6 +441,159 @@ def mra_multilevel_factored(q, k, v, s0, b, m1, m2, idx1=None, idx2=None, rows=N
         wc = np.exp(M - top) if np.isfinite(M) else np.zeros_like(top)
         out[i * b:(i + 1) * b] = (wf @ v[cols] + wc * L[None, :]) / (wf.sum(axis=1, keepdims=True) + wc * c)
     return out, idx1, idx2
+
+
+# --------------------------------------------------------------------------
+# Sec. 4.2 Alg. 1 and Sec. 4.3 Alg. 2 with any number of resolutions
+# R = {s_0 > s_1 > ... > s_{L-1}, 1}: the blocks popped at scale s_l are
+# replaced by their s_{l+1}-blocks, whose block-rows then pop their own budget
+# among those; the blocks popped at the last coarse scale become exact
+# --------------------------------------------------------------------------
+def _check_levels(n, scales, budgets):
+    scales = [int(s) for s in scales]
+    budgets = [int(m) for m in budgets]
+    if not scales or len(scales) != len(budgets):
+        raise ValueError("one budget per coarse scale")
+    for l, s in enumerate(scales):
+        if s < 1 or n % s:
+            raise ValueError("every scale must divide the sequence length")
+        if l > 0 and (s >= scales[l - 1] or scales[l - 1] % s):
+            raise ValueError("scales must decrease, each dividing the one before")
+    return scales, budgets
+
+
+def select_levels(q, k, scales, budgets):
+    """Alg. 1 refined level by level, per block-row: every s_0-block-row keeps
+    the budgets[0] s_0-blocks with the largest S~_0; at level l every
+    s_l-block-row keeps, among the s_l-blocks inside its parent row's (scale
+    s_{l-1}) kept blocks, the budgets[l] with the largest S~_l. Ties: lower
+    index first. Returns [idx_0, ..., idx_{L-1}], idx_l [n/s_l, budgets[l]]
+    with rows ascending."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    n = q.shape[0]
+    scales, budgets = _check_levels(n, scales, budgets)
+    idx = []
+    for l, (s, m) in enumerate(zip(scales, budgets)):
+        S = coarse_logits(block_mean(q, s), block_mean(k, s))
+        if l == 0:
+            idx.append(select_blocks(S, m))
+            continue
+        p = scales[l - 1] // s
+        if not 0 <= m <= budgets[l - 1] * p:
+            raise ValueError("budget out of range")
+        out = np.empty((n // s, m), dtype=np.int64)
+        for x in range(n // s):
+            cand = [int(Y) * p + t for Y in idx[l - 1][x // p] for t in range(p)]
+            out[x] = sorted(sorted(cand, key=lambda y: (-S[x, y], y))[:m])
+        idx.append(out)
+    return idx
+
+
+def levels_logits_slab(q, k, scales, idx, x):
+    """The s_{L-1} x n logits of finest block-row x under eq.
+    actual_approx_mat_form: column j takes the coarse logit S~_l of the first
+    level l whose block around j the row's ancestor at that level did not
+    keep, and the exact P_ij if every level kept it."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    n, d = q.shape
+    b = scales[-1]
+    S = [coarse_logits(block_mean(q, s), block_mean(k, s)) for s in scales]
+    kept = [set(int(Y) for Y in idx[l][x * b // s]) for l, s in enumerate(scales)]
+    P = q[x * b:(x + 1) * b] @ k.T / math.sqrt(d)
+    slab = np.empty((b, n))
+    for j in range(n):
+        for l, s in enumerate(scales):
+            if j // s not in kept[l]:
+                slab[:, j] = S[l][x * b // s, j // s]
+                break
+        else:
+            slab[:, j] = P[:, j]
+    return slab
+
+
+def mra_levels_dense(q, k, v, scales, budgets, idx=None):
+    """Z = D^ A^ V for one head with R = {scales..., 1} (dense slab per finest
+    block-row). Returns (Z, idx list)."""
+    if idx is None:
+        idx = select_levels(q, k, scales, budgets)
+    v = np.asarray(v, dtype=np.float64)
+    nb = q.shape[0] // scales[-1]
+    Z = np.vstack([_normalised_rows(levels_logits_slab(q, k, scales, idx, x), v) for x in range(nb)])
+    return Z, idx
+
+
+def levels_coarse_term(q, k, v, scales, idx, x):
+    """Alg. 2's low-resolution part of finest block-row x, shifted by its
+    largest coarse logit M: (M, c, L), c summing s_l e^{S~_l - M} and L
+    s_l e^{S~_l - M} V~_l over, at every level l, the s_l-blocks inside the
+    ancestor's kept blocks of level l - 1 (all blocks at level 0) that the
+    ancestor at level l did not keep."""
+    return _levels_term(_levels_means(q, k, v, scales), scales, idx, x)
+
+
+def _levels_means(q, k, v, scales):
+    """[(S~_l, V~_l)] of one head: coarse logits and pooled values per scale."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    return [(coarse_logits(block_mean(q, s), block_mean(k, s)), block_mean(v, s)) for s in scales]
+
+
+def _levels_term(means, scales, idx, x):
+    """levels_coarse_term from the head's precomputed means."""
+    b = scales[-1]
+    terms = []
+    for l, s in enumerate(scales):
+        S, vp = means[l]
+        X = x * b // s
+        if l == 0:
+            cand = range(S.shape[1])
+        else:
+            p = scales[l - 1] // s
+            cand = [int(Y) * p + t for Y in idx[l - 1][x * b // scales[l - 1]] for t in range(p)]
+        kept = set(int(Y) for Y in idx[l][X])
+        terms += [(S[X, Y], s, vp[Y]) for Y in cand if Y not in kept]
+    if not terms:
+        return -np.inf, 0.0, np.zeros(means[0][1].shape[1])
+    M = max(t[0] for t in terms)
+    c = sum(w * math.exp(lg - M) for lg, w, _ in terms)
+    L = sum(w * math.exp(lg - M) * vv for lg, w, vv in terms)
+    return M, c, L
+
+
+def mra_levels_factored(q, k, v, scales, budgets, idx=None, rows=None):
+    """The same Z computed as in Alg. 2: exact tiles exp(P) V over the blocks
+    kept at the finest level merged with levels_coarse_term. With `rows`, only
+    those finest block-rows (stacked). Returns (Z, idx list)."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    n, d = q.shape
+    if idx is None:
+        idx = select_levels(q, k, scales, budgets)
+    b = scales[-1]
+    rows = list(range(n // b)) if rows is None else list(rows)
+    out = np.empty((len(rows) * b, v.shape[1]))
+    means = _levels_means(q, k, v, scales)
+    for i, x in enumerate(rows):
+        M, c, L = _levels_term(means, scales, idx, x)
+        sel = [int(y) for y in idx[-1][x]]
+        qx = q[x * b:(x + 1) * b]
+        if sel:
+            cols = np.concatenate([np.arange(y * b, (y + 1) * b) for y in sel])
+            P = qx @ k[cols].T / math.sqrt(d)
+            mf = P.max(axis=1, keepdims=True)
+        else:
+            cols = np.zeros(0, dtype=np.int64)
+            P = np.zeros((b, 0))
+            mf = np.full((b, 1), -np.inf)
+        top = np.maximum(mf, M)
+        wf = np.exp(P - top)
+        wc = np.exp(M - top) if np.isfinite(M) else np.zeros_like(top)
+        out[i * b:(i + 1) * b] = (wf @ v[cols] + wc * L[None, :]) / (wf.sum(axis=1, keepdims=True) + wc * c)
+    return out, idx
 
 
 # --------------------------------------------------------------------------

@@ -721,6 +721,129 @@ def test_multilevel_selection_nested_and_tied():
     assert (i1 == [0, 1]).all() and (i2 == [0, 1, 2]).all()
 
 
+# ---------------------------------------------------------------- any number of resolutions
+def _brute_levels(q, k, v, scales, budgets):
+    """Pure-Python loops over the definitions for R = {scales..., 1}: block
+    means by summation, logits by explicit dot products, each level's
+    selection by full sorting of its candidates (the children of the parent
+    row's picks), A^ entry by entry (the coarsest level whose block around j
+    the row's ancestor did not pick, else exact), then row normalisation."""
+    n, d = len(q), len(q[0])
+    c = 1.0 / math.sqrt(d)
+    def mean_rows(x, s):
+        return [[sum(x[i][t] for i in range(B * s, B * s + s)) / s for t in range(len(x[0]))] for B in range(n // s)]
+    def dot(a, bb):
+        return sum(a[t] * bb[t] for t in range(len(a)))
+    S = []
+    for s in scales:
+        qs, ks = mean_rows(q, s), mean_rows(k, s)
+        S.append([[c * dot(qs[X], ks[Y]) for Y in range(n // s)] for X in range(n // s)])
+    picks = []
+    for l, (s, m) in enumerate(zip(scales, budgets)):
+        rows = []
+        for X in range(n // s):
+            if l == 0:
+                cand = list(range(n // s))
+            else:
+                p = scales[l - 1] // s
+                cand = [Y * p + t for Y in picks[l - 1][X // p] for t in range(p)]
+            rows.append(set(sorted(cand, key=lambda Y: (-S[l][X][Y], Y))[:m]))
+        picks.append(rows)
+    Z = []
+    for i in range(n):
+        row = []
+        for j in range(n):
+            val = None
+            for l, s in enumerate(scales):
+                if j // s not in picks[l][i // s]:
+                    val = math.exp(S[l][i // s][j // s])
+                    break
+            row.append(math.exp(c * dot(q[i], k[j])) if val is None else val)
+        tot = sum(row)
+        Z.append([sum(row[j] * v[j][t] for j in range(n)) / tot for t in range(len(v[0]))])
+    return np.array(Z)
+
+
+@pytest.mark.parametrize("scales,budgets", [([16, 8, 4], [1, 2, 2]), ([16, 8, 4], [2, 3, 5]),
+                                            ([16, 8, 4], [0, 0, 0]), ([16, 8, 4, 2], [1, 2, 3, 4]),
+                                            ([16, 4, 2], [2, 5, 6]), ([8, 4, 2], [4, 8, 16])])
+def test_levels_brute_force(scales, budgets):
+    r = _rng(240 + sum(budgets) + len(scales))
+    n, d = 32, 3
+    q, k, v = (r.standard_normal((n, d)) for _ in range(3))
+    want = _brute_levels(q.tolist(), k.tolist(), v.tolist(), scales, budgets)
+    Zd, idx = O.mra_levels_dense(q, k, v, scales, budgets)
+    Zf, idx2 = O.mra_levels_factored(q, k, v, scales, budgets)
+    np.testing.assert_allclose(Zd, want, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(Zf, want, rtol=1e-12, atol=1e-13)
+    for a, b in zip(idx, idx2):
+        np.testing.assert_array_equal(a, b)
+
+
+def test_levels_reduce_to_fewer_levels():
+    """One coarse scale is MRA-2; two are the three-resolution scheme; budgets
+    that keep every candidate at a level make it transparent (the next level
+    then chooses among all blocks of its parent row); full budgets everywhere
+    give softmax attention."""
+    r = _rng(250)
+    n, d = 256, 8
+    q, k, v = (r.standard_normal((n, d)) for _ in range(3))
+    Z, idx = O.mra_levels_factored(q, k, v, [16], [5])
+    Z2, i2 = O.mra_factored(q, k, v, 16, 5)
+    np.testing.assert_array_equal(idx[0], i2)
+    np.testing.assert_allclose(Z, Z2, rtol=1e-12, atol=1e-13)
+    Z, idx = O.mra_levels_factored(q, k, v, [64, 16], [2, 5])
+    Z3, i1, i2 = O.mra_multilevel_factored(q, k, v, 64, 16, 2, 5)
+    np.testing.assert_array_equal(idx[0], i1)
+    np.testing.assert_array_equal(idx[1], i2)
+    np.testing.assert_allclose(Z, Z3, rtol=1e-12, atol=1e-13)
+    # level 1 keeps all 4 children of its parent's 2 picks: the finest level
+    # chooses among the same 8 candidates as with the middle level left out
+    Z, idx = O.mra_levels_factored(q, k, v, [128, 32, 16], [1, 4, 3])
+    Z4, i1, i2 = O.mra_multilevel_factored(q, k, v, 128, 16, 1, 3)
+    np.testing.assert_array_equal(idx[2], i2)
+    np.testing.assert_allclose(Z, Z4, rtol=1e-12, atol=1e-13)
+    Z, _ = O.mra_levels_factored(q, k, v, [64, 32, 16], [4, 8, 16])
+    np.testing.assert_allclose(Z, O.exact_attention(q, k, v), rtol=1e-12, atol=1e-13)
+    Z, _ = O.mra_levels_factored(q, k, v, [64, 32, 16], [0, 0, 0])
+    np.testing.assert_allclose(Z, O.mra_factored(q, k, v, 64, 0)[0], rtol=1e-12, atol=1e-13)
+
+
+def test_levels_constant_blocks_exact():
+    """Q and K constant on every coarsest block: every mu is exact at every
+    scale, so any budgets give softmax attention."""
+    r = _rng(260)
+    n, d = 128, 4
+    q = np.repeat(r.standard_normal((n // 32, d)), 32, axis=0)
+    k = np.repeat(r.standard_normal((n // 32, d)), 32, axis=0)
+    v = r.standard_normal((n, d))
+    exact = O.exact_attention(q, k, v)
+    for budgets in ([0, 0, 0], [1, 1, 1], [2, 3, 4], [4, 8, 16]):
+        np.testing.assert_allclose(O.mra_levels_factored(q, k, v, [32, 16, 8], budgets)[0], exact,
+                                   rtol=1e-12, atol=1e-13)
+
+
+def test_levels_selection_nested_and_tied():
+    r = _rng(270)
+    n, d = 256, 4
+    q, k = r.standard_normal((n, d)), r.standard_normal((n, d))
+    scales = [64, 32, 16, 8]
+    idx = O.select_levels(q, k, scales, [2, 3, 4, 5])
+    for l in range(1, len(scales)):
+        p = scales[l - 1] // scales[l]
+        for x in range(n // scales[l]):
+            assert set(int(y) // p for y in idx[l][x]) <= set(int(Y) for Y in idx[l - 1][x // p])
+            assert (np.diff(idx[l][x]) > 0).all()
+    z = np.zeros((n, d))
+    idx = O.select_levels(z, z, scales, [2, 3, 4, 5])
+    assert (idx[0] == [0, 1]).all() and (idx[1] == [0, 1, 2]).all()
+    assert (idx[2] == [0, 1, 2, 3]).all() and (idx[3] == [0, 1, 2, 3, 4]).all()
+    with pytest.raises(ValueError):
+        O.select_levels(q, k, [64, 48], [1, 1])                # 48 does not divide 64
+    with pytest.raises(ValueError):
+        O.select_levels(q, k, [64, 32], [1, 3])                # only 2 candidates
+
+
 @pytest.mark.parametrize("case", ["mra2", "mra2_budget0", "mra2_full", "mra2s", "global"])
 def test_grad_terms_signed_equal_autograd(case):
     """The chain rule written out (mra_grad_terms) equals torch's autograd of
