@@ -409,6 +409,16 @@ def main():
         variants["mra_multilevel"] = {"ms_per_step": ml_ms, "tokens_per_s": w.B * w.n / (ml_ms * 1e-3),
                                       "coarse_block": s0, "budget1": m1, "budget2": w.budget}
 
+    # Four resolutions R = {s_0, s_1, 32, 1} (Alg. 1 refined level by level).
+    if not args.no_variants:
+        scales, budgets = inputs.LEVELS[w.name]
+        lws = torch.empty(ops.forward_levels_workspace_bytes(w.B, w.H, w.n, w.d, scales, budgets, tdt),
+                          dtype=torch.uint8, device=dev)
+        lv_ms = time_launches(lambda: ops.attention_forward_levels(tq, tk, tv, scales, budgets, out=out,
+                                                                   workspace=lws), max(args.steps, 20))
+        variants["mra_levels"] = {"ms_per_step": lv_ms, "tokens_per_s": w.B * w.n / (lv_ms * 1e-3),
+                                  "scales": list(scales), "budgets": list(budgets)}
+
     if not args.no_variants:
         variants["backward"] = backward_leg(w, ops, tq, tk, tv, out, idx, ws, max(args.steps, 20))
 

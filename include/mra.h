@@ -315,10 +315,12 @@ size_t mra_forward_multilevel_workspace_bytes(int B, int H, int n, int d, int bl
  *   A^_ij = exp(c Q_i.K_j) in the refined 32-blocks, exp(S~[x,y]) in the other
  *           candidates, exp(S~0[X,Y]) in the unrefined s0-blocks
  *           (eq. actual_approx_mat_form), Z = D^ A^ V.
- * Ties go to the lower index at both levels. Launches: pooling (with K/V
- * packing), scale-s0 means, coarse logits at both scales, the two per-row
- * selections (the second over the candidates only), the low-resolution term
- * (s0 e^{S~0} V~0 and 32 e^{S~} V~ over the unrefined blocks), the tile pass.
+ * Ties go to the lower index at both levels. This is
+ * mra_attention_forward_levels with scales {s0, 32} and budgets {budget1,
+ * budget2}. Launches: pooling, scale-s0 means, coarse logits at both scales,
+ * the two per-row selections (the second over the candidates only), the
+ * low-resolution term (s0 e^{S~0} V~0 and 32 e^{S~} V~ over the unrefined
+ * blocks), the tile pass.
  *   coarse_block : s0 = 32 r with r >= 2, dividing n (MRA_ERR_UNSUPPORTED if
  *                  not a multiple of 32 above 32, MRA_ERR_INVALID_ARG if it
  *                  does not divide n).
@@ -335,6 +337,56 @@ mra_status_t mra_attention_forward_multilevel(const void* q, const void* k, cons
                                               size_t workspace_bytes, int B, int H, int n, int d,
                                               int block, int coarse_block, int budget1,
                                               int budget2, mra_dtype_t dtype, void* stream);
+
+/*
+ * mra_forward_levels_workspace_bytes — workspace of
+ * mra_attention_forward_levels: that of mra_attention_forward with the finest
+ * budget, plus for every coarser level its means, its coarse logits and its
+ * selection, and the finest level's coarse-logit grid (levels = 1: exactly
+ * mra_attention_forward's). 0 for invalid or unsupported arguments.
+ */
+size_t mra_forward_levels_workspace_bytes(int B, int H, int n, int d, int block, int levels,
+                                          const int* scales, const int* budgets,
+                                          mra_dtype_t dtype);
+
+/*
+ * mra_attention_forward_levels — any number of resolutions
+ * R = {s_0 > s_1 > ... > s_{L-1} = 32, 1} (Sec. 4.2 Alg. 1 refined level by
+ * level, Sec. 4.3 Alg. 2 over the resulting J), with a budget per block-row at
+ * each level:
+ *   level 0: every s_0-block-row keeps the budgets[0] s_0-blocks with the
+ *            largest S~_0 = c Q~_0 . K~_0 (means of s_0-row blocks, taken as
+ *            means of the consecutive 32-row means);
+ *   level l: every s_l-block-row keeps, among the s_l-blocks inside its parent
+ *            row's (scale s_{l-1}) kept blocks, the budgets[l] with the
+ *            largest S~_l;
+ *   A^_ij = exp(c Q_i.K_j) in the 32-blocks kept at the last level, else
+ *           exp(S~_l) of the first level l whose block around j the row's
+ *           ancestor at that level did not keep (eq. actual_approx_mat_form),
+ *           Z = D^ A^ V.
+ * Ties go to the lower index at every level. levels = 1 is MRA-2
+ * (mra_attention_forward, bit-identical); levels = 2 is
+ * mra_attention_forward_multilevel.
+ *   levels   : 1 <= levels <= 8 (MRA_ERR_UNSUPPORTED above 8).
+ *   scales   : host array of `levels` ints: scales[levels - 1] = 32 = block and
+ *              every other a larger multiple of the next (MRA_ERR_UNSUPPORTED
+ *              otherwise), each dividing n (MRA_ERR_INVALID_ARG otherwise).
+ *   budgets  : host array of `levels` ints: 0 <= budgets[0] <= n / scales[0],
+ *              0 <= budgets[l] <= budgets[l - 1] * scales[l - 1] / scales[l]
+ *              (MRA_ERR_INVALID_ARG otherwise).
+ *   idx_outs : NULL, or a host array of `levels` device pointers, each NULL or
+ *              [B,H,n/scales[l],budgets[l]] int32 receiving level l's
+ *              selection, rows ascending; 16-byte aligned.
+ *   lse_out  : optional [B,H,n] float32 log normalisers.
+ *   Other arguments and errors as for mra_attention_forward; workspace of at
+ *   least mra_forward_levels_workspace_bytes(...) bytes. The arrays are read
+ *   before the call returns; the caller keeps ownership.
+ */
+mra_status_t mra_attention_forward_levels(const void* q, const void* k, const void* v, void* out,
+                                          int32_t* const* idx_outs, float* lse_out,
+                                          void* workspace, size_t workspace_bytes, int B, int H,
+                                          int n, int d, int block, int levels, const int* scales,
+                                          const int* budgets, mra_dtype_t dtype, void* stream);
 
 /*
  * mra_backward_workspace_bytes — device workspace of mra_attention_backward:

@@ -186,40 +186,145 @@ WsBwd ws_bwd(long long bh, int nb, int d, mra_dtype_t dtype) {
   return L;
 }
 
-// The three-resolution forward: the forward's layout with the second-level
-// selection as its rows, plus the scale-s0 means, both coarse-logit grids and
-// the first-level selection.
-struct WsMulti {
+// The forward over levels R = {s_0 > ... > s_{L-1} = 32, 1}: the forward's
+// layout with the finest selection as its rows, plus for every coarser level
+// l < L - 1 its means, its coarse logits and its selection, and the finest
+// level's coarse-logit grid.
+struct WsLevels {
   WsLayout base;
-  size_t qp0, kp0, vp0, S0, idx1, S, total;
+  size_t qp[mra::kMaxLevels], kp[mra::kMaxLevels], vp[mra::kMaxLevels], S[mra::kMaxLevels],
+      idx[mra::kMaxLevels];
+  size_t S_fine, total;
 };
 
-WsMulti ws_multi(long long bh, int nb, int nb0, int d, int m1, int m2, mra_dtype_t dtype) {
-  WsMulti W{};
-  W.base = ws_layout(bh, nb, d, m2, dtype);
+WsLevels ws_levels(long long bh, int n, int d, int levels, const int* scales, const int* budgets,
+                   mra_dtype_t dtype) {
+  WsLevels W{};
+  const int nb = n / kBlockSize;
+  W.base = ws_layout(bh, nb, d, budgets[levels - 1], dtype);
   size_t off = W.base.total;
-  const size_t pooled0 = align256((size_t)bh * nb0 * d * sizeof(float));
-  W.qp0 = off; off += pooled0;
-  W.kp0 = off; off += pooled0;
-  W.vp0 = off; off += pooled0;
-  W.S0 = off; off += align256((size_t)bh * nb0 * nb0 * sizeof(float));
-  W.idx1 = off; off += align256((size_t)bh * nb0 * m1 * sizeof(int32_t));
-  W.S = off; off += align256((size_t)bh * nb * nb * sizeof(float));
+  for (int l = 0; l + 1 < levels; ++l) {
+    const long long nbl = n / scales[l];
+    const size_t pooled = align256((size_t)bh * nbl * d * sizeof(float));
+    W.qp[l] = off; off += pooled;
+    W.kp[l] = off; off += pooled;
+    W.vp[l] = off; off += pooled;
+    W.S[l] = off; off += align256((size_t)bh * nbl * nbl * sizeof(float));
+    W.idx[l] = off; off += align256((size_t)bh * nbl * budgets[l] * sizeof(int32_t));
+  }
+  W.S_fine = off; off += align256((size_t)bh * nb * nb * sizeof(float));
   W.total = off;
   return W;
 }
 
-// coarse_block = 32 r with r >= 2 dividing n / 32; 0 <= m1 <= n / coarse_block;
-// 0 <= m2 <= m1 r.
-mra_status_t check_multi(const Shape& s, int n, int coarse_block, int m1, int m2, int* r, int* nb0) {
-  if (coarse_block <= kBlockSize || coarse_block % kBlockSize != 0) return MRA_ERR_UNSUPPORTED;
-  if (n % coarse_block != 0) return MRA_ERR_INVALID_ARG;
-  *r = coarse_block / kBlockSize;
-  *nb0 = n / coarse_block;
-  if (m1 < 0 || m1 > *nb0) return MRA_ERR_INVALID_ARG;
-  if (m2 < 0 || (long long)m2 > (long long)m1 * *r) return MRA_ERR_INVALID_ARG;
-  (void)s;
+// 1 <= levels <= kMaxLevels; scales[levels - 1] = 32 and every coarser scale a
+// larger multiple of the next one (else unsupported) dividing n (else
+// invalid); 0 <= budgets[0] <= n / scales[0] and
+// 0 <= budgets[l] <= budgets[l - 1] * scales[l - 1] / scales[l].
+mra_status_t check_levels(int n, int levels, const int* scales, const int* budgets) {
+  if (levels < 1 || scales == nullptr || budgets == nullptr) return MRA_ERR_INVALID_ARG;
+  if (levels > mra::kMaxLevels) return MRA_ERR_UNSUPPORTED;
+  if (scales[levels - 1] != kBlockSize) return MRA_ERR_UNSUPPORTED;
+  for (int l = 0; l + 1 < levels; ++l)
+    if (scales[l] <= scales[l + 1] || scales[l] % scales[l + 1] != 0) return MRA_ERR_UNSUPPORTED;
+  for (int l = 0; l + 1 < levels; ++l)
+    if (n % scales[l] != 0) return MRA_ERR_INVALID_ARG;
+  if (budgets[0] < 0 || budgets[0] > n / scales[0]) return MRA_ERR_INVALID_ARG;
+  for (int l = 1; l < levels; ++l)
+    if (budgets[l] < 0 || (long long)budgets[l] > (long long)budgets[l - 1] * (scales[l - 1] / scales[l]))
+      return MRA_ERR_INVALID_ARG;
   return MRA_OK;
+}
+
+size_t levels_workspace_bytes(int B, int H, int n, int d, int block, int levels, const int* scales,
+                              const int* budgets, mra_dtype_t dtype) {
+  Shape s;
+  if (check_shape(B, H, n, d, block, true, &s) != MRA_OK) return 0;
+  if (check_dtype(dtype) != MRA_OK) return 0;
+  if (check_levels(n, levels, scales, budgets) != MRA_OK) return 0;
+  if (levels == 1) return ws_layout(s.bh, s.nb, d, budgets[0], dtype).total;
+  return ws_levels(s.bh, n, d, levels, scales, budgets, dtype).total;
+}
+
+// idx_outs: NULL, or `levels` optional device pointers (level l's selection
+// [B, H, n / scales[l], budgets[l]]).
+mra_status_t levels_forward(const void* q, const void* k, const void* v, void* out,
+                            int32_t* const* idx_outs, float* lse_out, void* workspace,
+                            size_t workspace_bytes, int B, int H, int n, int d, int block,
+                            int levels, const int* scales, const int* budgets, mra_dtype_t dtype,
+                            void* stream) {
+  Shape s;
+  MRA_TRY(check_shape(B, H, n, d, block, true, &s));
+  MRA_TRY(check_dtype(dtype));
+  MRA_TRY(check_levels(n, levels, scales, budgets));
+  if (s.empty) return MRA_OK;
+  MRA_TRY(check_ptr(q));
+  MRA_TRY(check_ptr(k));
+  MRA_TRY(check_ptr(v));
+  MRA_TRY(check_ptr(out));
+  int32_t* outs[mra::kMaxLevels] = {};
+  for (int l = 0; l < levels && idx_outs != nullptr; ++l) outs[l] = idx_outs[l];
+  for (int l = 0; l < levels; ++l)
+    if (outs[l] != nullptr && !aligned16(outs[l])) return MRA_ERR_MISALIGNED;
+  if (lse_out != nullptr && !aligned16(lse_out)) return MRA_ERR_MISALIGNED;
+  MRA_TRY(check_ptr(workspace));
+  if (workspace_bytes < levels_workspace_bytes(B, H, n, d, block, levels, scales, budgets, dtype))
+    return MRA_ERR_WORKSPACE;
+  if (levels == 1)                                          // R = {32, 1}: the two-level forward
+    return mra::forward_enqueue(q, k, v, out, outs[0], lse_out, workspace, B, H, n, d, budgets[0],
+                                dtype, stream);
+
+  const WsLevels W = ws_levels(s.bh, n, d, levels, scales, budgets, dtype);
+  char* ws = static_cast<char*>(workspace);
+  const WsLayout& L = W.base;
+  auto f32 = [&](size_t off) { return reinterpret_cast<float*>(ws + off); };
+  const int nb = s.nb, fin = levels - 1;
+  float *qp = f32(L.qp), *kp = f32(L.kp), *vp = f32(L.vp), *S = f32(W.S_fine);
+  void* kvpacked = raw_tiles(d, dtype) ? nullptr : ws + L.kvpacked;
+  float *cmax = f32(L.cmax), *csum = f32(L.csum), *cvec = f32(L.cvec);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  mra::LevelTerm T{};
+  T.levels = levels;
+  for (int l = 0; l < levels; ++l) {
+    T.nb[l] = n / scales[l];
+    T.m[l] = budgets[l];
+    T.r[l] = scales[l] / kBlockSize;
+  }
+  int32_t* idx[mra::kMaxLevels];
+  for (int l = 0; l < fin; ++l) {
+    idx[l] = outs[l] ? outs[l] : reinterpret_cast<int32_t*>(ws + W.idx[l]);
+    T.S[l] = f32(W.S[l]);
+    T.vp[l] = f32(W.vp[l]);
+  }
+  idx[fin] = outs[fin] ? outs[fin] : reinterpret_cast<int32_t*>(ws + L.idx);
+  T.S[fin] = S;
+  T.vp[fin] = vp;
+  for (int l = 0; l < levels; ++l) T.idx[l] = idx[l];
+
+  Fill fills[mra::kMaxLevels + 3] = {{out, (size_t)s.bh * n * d * (dtype == MRA_BF16 ? 2 : 4), nan_pattern(dtype)},
+                                     {lse_out, (size_t)s.bh * n * 4, kNanF32},
+                                     {workspace, W.total, kNanF32}};
+  for (int l = 0; l < levels; ++l) fills[3 + l] = {outs[l], (size_t)s.bh * T.nb[l] * budgets[l] * 4, kNanF32};
+  MRA_TRY(debug_fill(fills, stream));
+
+  MRA_TRY(hip_status(mra::launch_pool(q, k, v, qp, kp, vp, kvpacked, s.bh, n, d, (int)dtype, st)));
+  for (int l = 0; l <= fin; ++l) {
+    float* Sl = const_cast<float*>(T.S[l]);
+    if (l < fin) {
+      float *ql = f32(W.qp[l]), *kl = f32(W.kp[l]);
+      MRA_TRY(hip_status(mra::launch_pool_up(qp, kp, vp, ql, kl, f32(W.vp[l]), s.bh * T.nb[l], d, T.r[l], st)));
+      MRA_TRY(hip_status(mra::launch_coarse(ql, kl, Sl, s.bh, T.nb[l], d, st)));
+    } else {
+      MRA_TRY(hip_status(mra::launch_coarse(qp, kp, Sl, s.bh, nb, d, st)));
+    }
+    if (l > 0)
+      MRA_TRY(hip_status(mra::launch_mask_candidates(Sl, idx[l - 1], s.bh, T.nb[l], T.nb[l - 1],
+                                                     T.r[l - 1] / T.r[l], budgets[l - 1], st)));
+    if (budgets[l] > 0) MRA_TRY(hip_status(mra::launch_select(Sl, idx[l], s.bh, T.nb[l], budgets[l], st)));
+  }
+  MRA_TRY(hip_status(mra::launch_coarse_term_levels(T, cmax, csum, cvec, s.bh, d, st)));
+  return hip_status(mra::launch_tile(q, k, v, kvpacked, idx[fin], cmax, csum, cvec, out, lse_out, s.bh,
+                                     n, d, budgets[fin], (int)dtype, st));
 }
 
 }  // namespace
@@ -572,12 +677,8 @@ mra_status_t mra_attention_backward(const void* q, const void* k, const void* v,
 size_t mra_forward_multilevel_workspace_bytes(int B, int H, int n, int d, int block,
                                               int coarse_block, int budget1, int budget2,
                                               mra_dtype_t dtype) {
-  Shape s;
-  if (check_shape(B, H, n, d, block, true, &s) != MRA_OK) return 0;
-  if (check_dtype(dtype) != MRA_OK) return 0;
-  int r = 0, nb0 = 0;
-  if (check_multi(s, n, coarse_block, budget1, budget2, &r, &nb0) != MRA_OK) return 0;
-  return ws_multi(s.bh, s.nb, nb0, d, budget1, budget2, dtype).total;
+  const int scales[2] = {coarse_block, kBlockSize}, budgets[2] = {budget1, budget2};
+  return levels_workspace_bytes(B, H, n, d, block, 2, scales, budgets, dtype);
 }
 
 mra_status_t mra_attention_forward_multilevel(const void* q, const void* k, const void* v,
@@ -586,53 +687,25 @@ mra_status_t mra_attention_forward_multilevel(const void* q, const void* k, cons
                                               size_t workspace_bytes, int B, int H, int n, int d,
                                               int block, int coarse_block, int budget1,
                                               int budget2, mra_dtype_t dtype, void* stream) {
-  Shape s;
-  MRA_TRY(check_shape(B, H, n, d, block, true, &s));
-  MRA_TRY(check_dtype(dtype));
-  int r = 0, nb0 = 0;
-  MRA_TRY(check_multi(s, n, coarse_block, budget1, budget2, &r, &nb0));
-  if (s.empty) return MRA_OK;
-  MRA_TRY(check_ptr(q));
-  MRA_TRY(check_ptr(k));
-  MRA_TRY(check_ptr(v));
-  MRA_TRY(check_ptr(out));
-  const void* opt[3] = {idx1_out, idx2_out, lse_out};
-  for (const void* p : opt)
-    if (p != nullptr && !aligned16(p)) return MRA_ERR_MISALIGNED;
-  MRA_TRY(check_ptr(workspace));
-  const WsMulti W = ws_multi(s.bh, s.nb, nb0, d, budget1, budget2, dtype);
-  if (workspace_bytes < W.total) return MRA_ERR_WORKSPACE;
+  const int scales[2] = {coarse_block, kBlockSize}, budgets[2] = {budget1, budget2};
+  int32_t* const outs[2] = {idx1_out, idx2_out};
+  return levels_forward(q, k, v, out, outs, lse_out, workspace, workspace_bytes, B, H, n, d, block,
+                        2, scales, budgets, dtype, stream);
+}
 
-  char* ws = static_cast<char*>(workspace);
-  const WsLayout& L = W.base;
-  auto f32 = [&](size_t off) { return reinterpret_cast<float*>(ws + off); };
-  float *qp = f32(L.qp), *kp = f32(L.kp), *vp = f32(L.vp);
-  float *qp0 = f32(W.qp0), *kp0 = f32(W.kp0), *vp0 = f32(W.vp0);
-  float *S0 = f32(W.S0), *S = f32(W.S);
-  void* kvpacked = raw_tiles(d, dtype) ? nullptr : ws + L.kvpacked;
-  int32_t* idx1 = idx1_out ? idx1_out : reinterpret_cast<int32_t*>(ws + W.idx1);
-  int32_t* idx2 = idx2_out ? idx2_out : reinterpret_cast<int32_t*>(ws + L.idx);
-  float *cmax = f32(L.cmax), *csum = f32(L.csum), *cvec = f32(L.cvec);
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  const int nb = s.nb;
-  const Fill fills[5] = {{out, (size_t)s.bh * n * d * (dtype == MRA_BF16 ? 2 : 4), nan_pattern(dtype)},
-                         {idx1_out, (size_t)s.bh * nb0 * budget1 * 4, kNanF32},
-                         {idx2_out, (size_t)s.bh * nb * budget2 * 4, kNanF32},
-                         {lse_out, (size_t)s.bh * n * 4, kNanF32},
-                         {workspace, W.total, kNanF32}};
-  MRA_TRY(debug_fill(fills, stream));
+size_t mra_forward_levels_workspace_bytes(int B, int H, int n, int d, int block, int levels,
+                                          const int* scales, const int* budgets,
+                                          mra_dtype_t dtype) {
+  return levels_workspace_bytes(B, H, n, d, block, levels, scales, budgets, dtype);
+}
 
-  MRA_TRY(hip_status(mra::launch_pool(q, k, v, qp, kp, vp, kvpacked, s.bh, n, d, (int)dtype, st)));
-  MRA_TRY(hip_status(mra::launch_pool_up(qp, kp, vp, qp0, kp0, vp0, s.bh * nb0, d, r, st)));
-  MRA_TRY(hip_status(mra::launch_coarse(qp0, kp0, S0, s.bh, nb0, d, st)));
-  if (budget1 > 0) MRA_TRY(hip_status(mra::launch_select(S0, idx1, s.bh, nb0, budget1, st)));
-  MRA_TRY(hip_status(mra::launch_coarse(qp, kp, S, s.bh, nb, d, st)));
-  MRA_TRY(hip_status(mra::launch_mask_candidates(S, idx1, s.bh, nb, nb0, r, budget1, st)));
-  if (budget2 > 0) MRA_TRY(hip_status(mra::launch_select(S, idx2, s.bh, nb, budget2, st)));
-  MRA_TRY(hip_status(mra::launch_coarse_term_ml(S0, idx1, S, idx2, vp0, vp, cmax, csum, cvec, s.bh,
-                                                nb, nb0, r, budget1, budget2, d, st)));
-  return hip_status(mra::launch_tile(q, k, v, kvpacked, idx2, cmax, csum, cvec, out, lse_out, s.bh,
-                                     n, d, budget2, (int)dtype, st));
+mra_status_t mra_attention_forward_levels(const void* q, const void* k, const void* v, void* out,
+                                          int32_t* const* idx_outs, float* lse_out,
+                                          void* workspace, size_t workspace_bytes, int B, int H,
+                                          int n, int d, int block, int levels, const int* scales,
+                                          const int* budgets, mra_dtype_t dtype, void* stream) {
+  return levels_forward(q, k, v, out, idx_outs, lse_out, workspace, workspace_bytes, B, H, n, d,
+                        block, levels, scales, budgets, dtype, stream);
 }
 
 const char* mra_status_str(mra_status_t status) {

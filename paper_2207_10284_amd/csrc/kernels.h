@@ -134,22 +134,32 @@ struct BwdArgs {
 };
 hipError_t launch_bwd(const BwdArgs& args, hipStream_t stream);
 
-// Three resolutions R = {s0, 32, 1}, s0 = 32 r (multilevel.hip).
-// Scale-s0 means [bh, nb/r, d] of the scale-32 means [bh, nb, d] (f32; a NULL
+// More resolutions R = {s_0 > ... > s_{L-1} = 32, 1} (multilevel.hip).
+// Scale-32r means [bh, nb/r, d] of the scale-32 means [bh, nb, d] (f32; a NULL
 // pair is skipped); rows_out = bh * nb / r.
 hipError_t launch_pool_up(const float* qp, const float* kp, const float* vp, float* qp0,
                           float* kp0, float* vp0, long long rows_out, int d, int r,
                           hipStream_t stream);
-// S [bh, nb, nb] in place: -inf outside the s0-blocks idx1 [bh, nb/r, m1]
-// lists for each row's parent s0-block-row.
+// S [bh, nb, nb] of one level in place: -inf outside the children of the
+// parent level's kept blocks idx1 [bh, nb0, m1] (nb0 = nb / r <= 1024) of each
+// row's parent row.
 hipError_t launch_mask_candidates(float* S, const int32_t* idx1, long long bh, int nb, int nb0,
                                   int r, int m1, hipStream_t stream);
-// Low-resolution term (cmax, csum, cvec) of every 32-block-row: unrefined
-// s0-blocks of its parent row (S0 [bh, nb0, nb0], vp0 [bh, nb0, d]) and
-// unrefined candidate 32-blocks (S, vp; idx2 [bh, nb, m2] the refined ones).
-hipError_t launch_coarse_term_ml(const float* S0, const int32_t* idx1, const float* S,
-                                 const int32_t* idx2, const float* vp0, const float* vp,
-                                 float* cmax, float* csum, float* cvec, long long bh, int nb,
-                                 int nb0, int r, int m1, int m2, int d, hipStream_t stream);
+// The levels of R = {s_0 > ... > s_{L-1} = 32, 1}: per level l the coarse
+// logits S [bh, nb_l, nb_l], the kept blocks idx [bh, nb_l, m_l] (entries
+// outside [0, nb_l) ignored), the pooled values vp [bh, nb_l, d] and
+// r_l = s_l / 32.
+constexpr int kMaxLevels = 8;
+struct LevelTerm {
+  const float* S[kMaxLevels];
+  const int32_t* idx[kMaxLevels];
+  const float* vp[kMaxLevels];
+  int nb[kMaxLevels], m[kMaxLevels], r[kMaxLevels];
+  int levels;
+};
+// Low-resolution term (cmax, csum, cvec) of every 32-block-row: at every
+// level, the candidate blocks its ancestor did not keep.
+hipError_t launch_coarse_term_levels(const LevelTerm& T, float* cmax, float* csum, float* cvec,
+                                     long long bh, int d, hipStream_t stream);
 
 }  // namespace mra

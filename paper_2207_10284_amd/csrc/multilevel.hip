@@ -1,22 +1,25 @@
-// Three resolutions R = {s0, b, 1} (b = 32, s0 = r*b): Sec. 4.2 Alg. 1 with
-// two refinement levels and Sec. 4.3 Alg. 2 over the resulting set J, with a
-// budget per block-row at each level. The pieces specific to three levels:
+// Any number of resolutions R = {s_0 > s_1 > ... > s_{L-1} = b, 1} (b = 32,
+// each scale a multiple of the next): Sec. 4.2 Alg. 1 refined level by level
+// and Sec. 4.3 Alg. 2 over the resulting set J, with a budget per block-row at
+// each level. The pieces beyond the two-level path:
 //
-//  * pool_up_kernel: the scale-s0 means Q~0, K~0, V~0 as means of r
-//    consecutive scale-b means (eq. recursive_pooling applied further up);
-//  * mask_kernel: after the s0-level selection T0_X (per s0-block-row X),
-//    b-block-row x may only refine b-blocks inside its parent row's refined
-//    s0-blocks: every other entry of its row of S~ is set to -inf, so the
+//  * pool_up_kernel: the scale-s_l means Q~_l, K~_l, V~_l as means of
+//    s_l / b consecutive scale-b means (eq. recursive_pooling applied further
+//    up);
+//  * mask_kernel: after level l - 1's selection (per s_{l-1}-block-row), an
+//    s_l-block-row may only keep s_l-blocks inside its parent row's kept
+//    blocks: every other entry of its row of S~_l is set to -inf, so the
 //    per-row top-m selection of select.hip picks among the candidates only
-//    (the budget m2 never exceeds their number m1*r);
-//  * coarse_term_ml_kernel: the low-resolution part of block-row x, relative
-//    to its largest coarse logit M: s0 e^{S~0[X,Y] - M} V~0_Y over the s0-blocks
-//    X did not refine plus b e^{S~[x,y] - M} V~_y over the candidate b-blocks x
-//    did not refine (each coarse block counts the columns it spans), in the
+//    (the budget m_l never exceeds their number m_{l-1} s_{l-1} / s_l);
+//  * coarse_term_levels_kernel: the low-resolution part of b-block-row x,
+//    relative to its largest coarse logit M: s_l e^{S~_l[X_l,Y] - M} V~_l,Y
+//    over, at every level l, the candidate blocks Y (all s_0-blocks at level
+//    0, the children of the ancestor's kept blocks below) that its ancestor
+//    X_l did not keep (each coarse block counts the columns it spans), in the
 //    (M, c, L) form the tile pass merges.
 //
-// The coarse logits at both scales, the two selections and the tile pass are
-// the kernels of the two-level path.
+// The coarse logits at every scale, the selections and the tile pass are the
+// kernels of the two-level path.
 #include "common.h"
 #include "kernels.h"
 
@@ -43,7 +46,8 @@ __global__ __launch_bounds__(256) void pool_up_kernel(const float* __restrict__ 
   dst[t] = acc / (float)r;
 }
 
-// One wave per b-block-row: S[x, y] = -inf unless y / r is in idx1[x / r].
+// One wave per block-row x of a level: S[x, y] = -inf unless y / r is in
+// idx1[x / r], the parent level's kept blocks (nb0 <= 1024 parent blocks).
 __global__ __launch_bounds__(64) void mask_kernel(float* __restrict__ S,
                                                   const int32_t* __restrict__ idx1, int nb,
                                                   int nb0, int r, int m1) {
@@ -70,70 +74,82 @@ __global__ __launch_bounds__(64) void mask_kernel(float* __restrict__ S,
 constexpr int kMlWaves = 4;
 
 // One wave per b-block-row (`waves` per workgroup, no workgroup barriers).
-// Per-wave LDS: refined bitmaps (s0 level, b level), the s0-level weights,
-// the candidate list and its weights.
-__global__ __launch_bounds__(kMlWaves * kWave) void coarse_term_ml_kernel(
-    const float* __restrict__ S0, const int32_t* __restrict__ idx1, const float* __restrict__ S,
-    const int32_t* __restrict__ idx2, const float* __restrict__ vp0,
-    const float* __restrict__ vp, float* __restrict__ cmax, float* __restrict__ csum,
-    float* __restrict__ cvec, int nb, int nb0, int r, int m1, int m2, long long rows, int d,
-    int waves) {
+// Per-wave LDS: the kept-block bitmaps of the row's ancestors at every level,
+// then every level's candidate list (level 0: all its blocks; level l: the
+// children of the level l - 1 ancestor's kept blocks, in that list's order)
+// and the candidates' weights, zero for the kept ones.
+__global__ __launch_bounds__(kMlWaves * kWave) void coarse_term_levels_kernel(
+    LevelTerm T, float* __restrict__ cmax, float* __restrict__ csum, float* __restrict__ cvec,
+    long long rows, int d, int waves) {
   extern __shared__ __attribute__((aligned(16))) uint32_t ml_smem[];
-  const int nw0 = (nb0 + 31) / 32, nw1 = (nb + 31) / 32, nc = m1 * r;
-  const int per_wave = nw0 + nw1 + nb0 + 2 * nc;
+  const int L = T.levels, nbf = T.nb[L - 1];
+  int words = 0, ents = 0;
+  int woff[kMaxLevels], eoff[kMaxLevels + 1];
+  for (int l = 0; l < L; ++l) {
+    woff[l] = words;
+    words += (T.nb[l] + 31) / 32;
+    eoff[l] = ents;
+    ents += l == 0 ? T.nb[0] : T.m[l - 1] * (T.r[l - 1] / T.r[l]);
+  }
+  eoff[L] = ents;
   const int w = wave_uniform(threadIdx.x / kWave);
   const int lane = lane_id();
   const long long g = (long long)blockIdx.x * waves + w;
   if (g >= rows) return;
-  uint32_t* bm0 = ml_smem + w * per_wave;
-  uint32_t* bm1 = bm0 + nw0;
-  float* w0 = reinterpret_cast<float*>(bm1 + nw1);
-  int32_t* cy = reinterpret_cast<int32_t*>(w0 + nb0);
-  float* w1 = reinterpret_cast<float*>(cy + nc);
-  const long long bh = g / nb;
-  const int x = (int)(g - bh * nb);
-  const long long G0 = bh * nb0 + x / r;
+  uint32_t* bm = ml_smem + (size_t)w * (words + 2 * ents);
+  int32_t* cy = reinterpret_cast<int32_t*>(bm + words);
+  float* wt = reinterpret_cast<float*>(cy + ents);
+  const long long bh = g / nbf;
+  const int x = (int)(g - bh * nbf);
 
-  for (int i = lane; i < nw0 + nw1; i += kWave) bm0[i] = 0u;
+  for (int i = lane; i < words; i += kWave) bm[i] = 0u;
   wave_lds_sync();
-  for (int i = lane; i < m1; i += kWave) {
-    const int Y = idx1[G0 * m1 + i];
-    if (Y >= 0 && Y < nb0) atomicOr(&bm0[Y >> 5], 1u << (Y & 31));
+  for (int l = 0; l < L; ++l) {
+    const long long G = bh * T.nb[l] + x / T.r[l];          // the row's ancestor at level l
+    for (int i = lane; i < T.m[l]; i += kWave) {
+      const int Y = T.idx[l][G * T.m[l] + i];
+      if (Y >= 0 && Y < T.nb[l]) atomicOr(&bm[woff[l] + (Y >> 5)], 1u << (Y & 31));
+    }
   }
-  for (int i = lane; i < m2; i += kWave) {
-    const int y = idx2[g * m2 + i];
-    if (y >= 0 && y < nb) atomicOr(&bm1[y >> 5], 1u << (y & 31));
+  // candidates; -1 marks a child of an invalid parent entry (never used)
+  for (int l = 0; l < L; ++l) {
+    if (l == 0) {
+      for (int c = lane; c < T.nb[0]; c += kWave) cy[c] = c;
+    } else {
+      const int p = T.r[l - 1] / T.r[l];
+      const long long Gp = bh * T.nb[l - 1] + x / T.r[l - 1];
+      for (int c = lane; c < eoff[l + 1] - eoff[l]; c += kWave) {
+        const int Y = T.idx[l - 1][Gp * T.m[l - 1] + c / p];
+        cy[eoff[l] + c] = Y >= 0 && Y < T.nb[l - 1] ? Y * p + c % p : -1;
+      }
+    }
   }
-  wave_lds_sync();
-  // candidate b-blocks in idx1 order (ascending Y, then t)
-  for (int c = lane; c < nc; c += kWave) cy[c] = idx1[G0 * m1 + c / r] * r + c % r;
   wave_lds_sync();
 
-  const float* s0row = S0 + G0 * nb0;
-  const float* srow = S + g * nb;
+  auto unkept = [&](int l, int y) {
+    return y >= 0 && !((bm[woff[l] + (y >> 5)] >> (y & 31)) & 1u);
+  };
   float M = -INFINITY;
-  for (int Y = lane; Y < nb0; Y += kWave)
-    if (!((bm0[Y >> 5] >> (Y & 31)) & 1u)) M = fmaxf(M, s0row[Y]);
-  for (int c = lane; c < nc; c += kWave) {
-    const int y = cy[c];
-    if (!((bm1[y >> 5] >> (y & 31)) & 1u)) M = fmaxf(M, srow[y]);
+  for (int l = 0; l < L; ++l) {
+    const float* srow = T.S[l] + (bh * T.nb[l] + x / T.r[l]) * T.nb[l];
+    for (int c = eoff[l] + lane; c < eoff[l + 1]; c += kWave) {
+      const int y = cy[c];
+      if (unkept(l, y)) M = fmaxf(M, srow[y]);
+    }
   }
   M = wave_max(M);
   const bool any = M != -INFINITY;
-  const float wide = (float)(r * kBlock);
   float sum = 0.0f;
-  for (int Y = lane; Y < nb0; Y += kWave) {
-    const bool use = any && !((bm0[Y >> 5] >> (Y & 31)) & 1u);
-    const float wt = use ? wide * expf(s0row[Y] - M) : 0.0f;
-    w0[Y] = wt;
-    sum += wt;
-  }
-  for (int c = lane; c < nc; c += kWave) {
-    const int y = cy[c];
-    const bool use = any && !((bm1[y >> 5] >> (y & 31)) & 1u);
-    const float wt = use ? (float)kBlock * expf(srow[y] - M) : 0.0f;
-    w1[c] = wt;
-    sum += wt;
+  for (int l = 0; l < L; ++l) {
+    const float* srow = T.S[l] + (bh * T.nb[l] + x / T.r[l]) * T.nb[l];
+    const float wide = (float)(T.r[l] * kBlock);
+    for (int c = eoff[l] + lane; c < eoff[l + 1]; c += kWave) {
+      const int y = cy[c];
+      const bool use = any && unkept(l, y);
+      const float v = use ? wide * expf(srow[y] - M) : 0.0f;
+      wt[c] = v;
+      sum += v;
+    }
   }
   sum = wave_sum(sum);
   wave_lds_sync();
@@ -141,12 +157,15 @@ __global__ __launch_bounds__(kMlWaves * kWave) void coarse_term_ml_kernel(
     cmax[g] = M;
     csum[g] = sum;
   }
-  const float* v0 = vp0 + bh * (long long)nb0 * d;
-  const float* v1 = vp + bh * (long long)nb * d;
   for (int dd = lane; dd < d; dd += kWave) {
     float acc = 0.0f;
-    for (int Y = 0; Y < nb0; ++Y) acc = fmaf(w0[Y], v0[(long long)Y * d + dd], acc);
-    for (int c = 0; c < nc; ++c) acc = fmaf(w1[c], v1[(long long)cy[c] * d + dd], acc);
+    for (int l = 0; l < L; ++l) {
+      const float* vl = T.vp[l] + bh * (long long)T.nb[l] * d + dd;
+      for (int c = eoff[l]; c < eoff[l + 1]; ++c) {
+        const int y = cy[c];
+        acc = fmaf(wt[c], vl[(long long)(y < 0 ? 0 : y) * d], acc);
+      }
+    }
     cvec[g * d + dd] = acc;
   }
 }
@@ -166,22 +185,26 @@ hipError_t launch_mask_candidates(float* S, const int32_t* idx1, long long bh, i
   return hipGetLastError();
 }
 
-static size_t coarse_term_ml_wave_bytes(int nb, int nb0, int r, int m1) {
-  return ((size_t)(nb0 + 31) / 32 + (nb + 31) / 32 + nb0 + 2 * (size_t)m1 * r) * sizeof(uint32_t);
+static size_t coarse_term_levels_wave_bytes(const LevelTerm& T) {
+  size_t words = 0, ents = 0;
+  for (int l = 0; l < T.levels; ++l) {
+    words += (T.nb[l] + 31) / 32;
+    ents += l == 0 ? T.nb[0] : (size_t)T.m[l - 1] * (T.r[l - 1] / T.r[l]);
+  }
+  return (words + 2 * ents) * sizeof(uint32_t);
 }
 
-hipError_t launch_coarse_term_ml(const float* S0, const int32_t* idx1, const float* S,
-                                 const int32_t* idx2, const float* vp0, const float* vp,
-                                 float* cmax, float* csum, float* cvec, long long bh, int nb,
-                                 int nb0, int r, int m1, int m2, int d, hipStream_t stream) {
-  const long long rows = bh * nb;
+hipError_t launch_coarse_term_levels(const LevelTerm& T, float* cmax, float* csum, float* cvec,
+                                     long long bh, int d, hipStream_t stream) {
+  const long long rows = bh * T.nb[T.levels - 1];
   // four waves per workgroup while their lists fit 64 KB of LDS, else one
-  // (at most 21 KB: nb <= 2048, nb0 <= 1024)
-  const size_t per_wave = coarse_term_ml_wave_bytes(nb, nb0, r, m1);
+  // (under 34 KB: every level's candidates number at most its blocks, and the
+  // block counts of the levels sum to less than 2 nb <= 4096)
+  const size_t per_wave = coarse_term_levels_wave_bytes(T);
   const int waves = per_wave * kMlWaves <= 65536 ? kMlWaves : 1;
   const unsigned blocks = (unsigned)((rows + waves - 1) / waves);
-  coarse_term_ml_kernel<<<blocks, waves * kWave, per_wave * waves, stream>>>(
-      S0, idx1, S, idx2, vp0, vp, cmax, csum, cvec, nb, nb0, r, m1, m2, rows, d, waves);
+  coarse_term_levels_kernel<<<blocks, waves * kWave, per_wave * waves, stream>>>(T, cmax, csum, cvec,
+                                                                               rows, d, waves);
   return hipGetLastError();
 }
 

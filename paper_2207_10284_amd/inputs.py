@@ -161,3 +161,12 @@ MULTILEVEL = {
     "base-4096": (128, 8),
     "long-32768": (256, 8),
 }
+
+# Four resolutions R = {s_0, s_1, 32, 1} per workload: (scales, budgets per level).
+LEVELS = {
+    "tiny-512": ((256, 64, 32), (1, 3, 4)),
+    "base-512": ((256, 64, 32), (2, 6, 8)),
+    "small-4096": ((1024, 128, 32), (2, 6, 8)),
+    "base-4096": ((512, 128, 32), (3, 8, 16)),
+    "long-32768": ((2048, 256, 32), (4, 12, 32)),
+}

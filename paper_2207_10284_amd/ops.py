@@ -40,6 +40,9 @@ SIGNATURES = {
     "mra_forward_multilevel_workspace_bytes": (_Z, [_I, _I, _I, _I, _I, _I, _I, _I, _I]),
     "mra_attention_forward_multilevel": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _Z, _I, _I, _I, _I, _I, _I,
                                               _I, _I, _I, _P]),
+    "mra_forward_levels_workspace_bytes": (_Z, [_I, _I, _I, _I, _I, _I, _P, _P, _I]),
+    "mra_attention_forward_levels": (_I, [_P, _P, _P, _P, _P, _P, _P, _Z, _I, _I, _I, _I, _I, _I,
+                                          _P, _P, _I, _P]),
     "mra_backward_workspace_bytes": (_Z, [_I, _I, _I, _I, _I, _I]),
     "mra_attention_backward": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _Z,
                                     _I, _I, _I, _I, _I, _I, _I, _I, _P]),
@@ -316,6 +319,50 @@ def attention_forward_multilevel(q, k, v, coarse_block: int, budget1: int, budge
     _call("mra_attention_forward_multilevel", _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(idx1_out),
           _ptr(idx2_out), _ptr(lse_out), _ptr(workspace), workspace.numel() * workspace.element_size(),
           B, H, n, d, BLOCK, coarse_block, budget1, budget2, _dtype_code(ref), _stream(ref.device))
+    return out
+
+
+def _int_array(vals):
+    vals = [int(x) for x in vals]
+    return (ctypes.c_int * max(len(vals), 1))(*vals)
+
+
+def forward_levels_workspace_bytes(B: int, H: int, n: int, d: int, scales, budgets, dtype=torch.bfloat16) -> int:
+    code = MRA_BF16 if dtype == torch.bfloat16 else MRA_F32
+    sc, bu = _int_array(scales), _int_array(budgets)
+    return int(load().mra_forward_levels_workspace_bytes(B, H, n, d, BLOCK, len(scales),
+                                                         ctypes.cast(sc, _P), ctypes.cast(bu, _P), code))
+
+
+def attention_forward_levels(q, k, v, scales, budgets, out=None, idx_outs=None, lse_out=None,
+                             workspace=None):
+    """Any number of resolutions R = {scales[0] > ... > scales[-1] = 32, 1}
+    (Alg. 1 refined level by level, a per-row budget at every level). Returns
+    Z; level l's selection goes to ``idx_outs[l]`` (int32
+    [B, H, n/scales[l], budgets[l]]) when that entry is given."""
+    ref = _check_qkv(q, k, v)
+    B, H, n, d = ref.shape
+    L = len(scales)
+    if len(budgets) != L or L < 1:
+        raise ValueError("one budget per scale")
+    if out is None:
+        out = torch.empty_like(ref)
+    outs = list(idx_outs) if idx_outs is not None else [None] * L
+    if len(outs) != L:
+        raise ValueError("one selection output (or None) per scale")
+    for l, t in enumerate(outs):
+        if t is not None:
+            _check_idx(t, B, H, n // int(scales[l]) if int(scales[l]) > 0 else 0, int(budgets[l]), ref.device)
+    if lse_out is not None:
+        _check_f32(lse_out, (B, H, n), "lse_out")
+    need = forward_levels_workspace_bytes(B, H, n, d, scales, budgets, ref.dtype)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), device=ref.device, dtype=torch.uint8)
+    sc, bu = _int_array(scales), _int_array(budgets)
+    ptrs = (ctypes.c_void_p * L)(*[_ptr(t) for t in outs])
+    _call("mra_attention_forward_levels", _ptr(q), _ptr(k), _ptr(v), _ptr(out), ctypes.cast(ptrs, _P),
+          _ptr(lse_out), _ptr(workspace), workspace.numel() * workspace.element_size(), B, H, n, d, BLOCK,
+          L, ctypes.cast(sc, _P), ctypes.cast(bu, _P), _dtype_code(ref), _stream(ref.device))
     return out
 
 

@@ -31,7 +31,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 18, names
+    assert len(names) == 20, names
     for name in names:
         assert hasattr(lib, name), name
     assert set(names) == set(ops.SIGNATURES)
@@ -277,6 +277,63 @@ def test_multilevel_validation(lib):
     want = lib.mra_forward_workspace_bytes(B, H, n, d, 32, m2, 1) + 3 * al(bh * nb0 * d * 4) \
         + al(bh * nb0 * nb0 * 4) + al(bh * nb0 * m1 * 4) + al(bh * nb * nb * 4)
     assert lib.mra_forward_multilevel_workspace_bytes(B, H, n, d, 32, s0, m1, m2, 1) == want
+    assert lib.mra_last_hip_error() == 0
+
+
+def lfwd(lib, scales=(256, 64, 32), budgets=(2, 3, 4), levels=None, q=A, out=A, ws=A, wsb=1 << 40, n=1024,
+         d=64, dtype=1, outs=None, lse=None):
+    L = len(scales) if levels is None else levels
+    sc = (ctypes.c_int * max(len(scales), 1))(*scales)
+    bu = (ctypes.c_int * max(len(budgets), 1))(*budgets)
+    po = None if outs is None else ctypes.cast((ctypes.c_void_p * len(outs))(*outs), ctypes.c_void_p)
+    return lib.mra_attention_forward_levels(q, A, A, out, po, lse, ws, wsb, 1, 1, n, d, 32, L,
+                                            ctypes.cast(sc, ctypes.c_void_p), ctypes.cast(bu, ctypes.c_void_p),
+                                            dtype, None)
+
+
+def lws(lib, scales, budgets, n=1024, d=64, B=1, H=1):
+    sc = (ctypes.c_int * len(scales))(*scales)
+    bu = (ctypes.c_int * len(budgets))(*budgets)
+    return lib.mra_forward_levels_workspace_bytes(B, H, n, d, 32, len(scales), ctypes.cast(sc, ctypes.c_void_p),
+                                                  ctypes.cast(bu, ctypes.c_void_p), 1)
+
+
+def test_levels_validation(lib):
+    """R = {s_0 > ... > s_{L-1} = 32, 1}: each scale a larger multiple of the
+    next dividing n, the last 32, at most 8 levels; budgets within the
+    candidates of the parent level."""
+    assert lfwd(lib, scales=(256, 64, 48)) == UNSUPPORTED       # last scale not 32
+    assert lfwd(lib, scales=(64, 256, 32)) == UNSUPPORTED       # not decreasing
+    assert lfwd(lib, scales=(256, 96, 32)) == UNSUPPORTED       # 96 does not divide 256
+    assert lfwd(lib, scales=(192, 96, 32), n=1024) == INVALID   # 1024 % 192
+    assert lfwd(lib, levels=0) == INVALID
+    assert lfwd(lib, scales=(8192, 4096, 2048, 1024, 512, 256, 128, 64, 32), budgets=(1,) * 9,
+                n=8192) == UNSUPPORTED                           # nine levels
+    assert lfwd(lib, budgets=(5, 3, 4)) == INVALID              # n/s0 = 4
+    assert lfwd(lib, budgets=(2, 9, 4)) == INVALID              # 2 * 256/64 = 8 candidates
+    assert lfwd(lib, budgets=(2, 3, 7)) == INVALID              # 3 * 64/32 = 6 candidates
+    assert lfwd(lib, budgets=(2, -1, 0)) == INVALID
+    assert lfwd(lib, d=48) == UNSUPPORTED
+    assert lfwd(lib, q=None) == INVALID
+    assert lfwd(lib, outs=[None, MIS, None]) == MISALIGNED
+    assert lfwd(lib, lse=MIS) == MISALIGNED
+    need = lws(lib, (256, 64, 32), (2, 3, 4))
+    assert need > 0
+    assert lfwd(lib, wsb=need - 1) == WORKSPACE
+    assert lfwd(lib, n=0, budgets=(0, 0, 0), q=None, out=None, ws=None) == OK
+    assert lws(lib, (256, 96, 32), (2, 3, 4)) == 0
+    # one level is the two-level forward, two levels the three-resolution one
+    assert lws(lib, (32,), (16,), n=4096, B=8, H=12) == lib.mra_forward_workspace_bytes(8, 12, 4096, 64, 32, 16, 1)
+    assert lws(lib, (128, 32), (8, 16), n=4096, B=8, H=12) == \
+        lib.mra_forward_multilevel_workspace_bytes(8, 12, 4096, 64, 32, 128, 8, 16, 1)
+    al = lambda x: (x + 255) // 256 * 256
+    B, H, n, d = 8, 12, 4096, 64
+    bh, nb = B * H, n // 32
+    want = lib.mra_forward_workspace_bytes(B, H, n, d, 32, 16, 1) + al(bh * nb * nb * 4)
+    for s, m in ((512, 2), (128, 5)):
+        nbl = n // s
+        want += 3 * al(bh * nbl * d * 4) + al(bh * nbl * nbl * 4) + al(bh * nbl * m * 4)
+    assert lws(lib, (512, 128, 32), (2, 5, 16), n=n, B=B, H=H) == want
     assert lib.mra_last_hip_error() == 0
 
 

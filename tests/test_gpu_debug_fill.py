@@ -54,7 +54,11 @@ def test_forwards_write_every_output(gpu, monkeypatch, dtype, d):
         i1 = torch.empty(B, H, n // 64, 2, dtype=torch.int32, device="cuda")
         i2 = torch.empty(B, H, nb, m, dtype=torch.int32, device="cuda")
         mout = gpu.attention_forward_multilevel(q, k, v, 64, 2, m, idx1_out=i1, idx2_out=i2)
-        return out, idx, lse, sout, sidx, slse, nout, nidx, gout, gidx, mout, i1, i2
+        l0 = torch.empty(B, H, 1, 1, dtype=torch.int32, device="cuda")
+        l1 = torch.empty(B, H, 2, 1, dtype=torch.int32, device="cuda")
+        l2 = torch.empty(B, H, nb, m, dtype=torch.int32, device="cuda")
+        lout = gpu.attention_forward_levels(q, k, v, (320, 160, 32), (1, 1, m), idx_outs=[l0, l1, l2])
+        return out, idx, lse, sout, sidx, slse, nout, nidx, gout, gidx, mout, i1, i2, lout, l0, l1, l2
 
     a, b = _both(monkeypatch, run)
     _same(a, b)
