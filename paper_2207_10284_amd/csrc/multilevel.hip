@@ -76,15 +76,17 @@ constexpr int kMlWaves = 4;
 // One wave per b-block-row (`waves` per workgroup, no workgroup barriers).
 // Per-wave LDS: the kept-block bitmaps of the row's ancestors at every level,
 // then every level's candidate list (level 0: all its blocks; level l: the
-// children of the level l - 1 ancestor's kept blocks, in that list's order)
-// and the candidates' weights, zero for the kept ones.
+// children of the level l - 1 ancestor's kept blocks, in that list's order),
+// compacted to the unkept candidates with their weights.
+template <int L>
 __global__ __launch_bounds__(kMlWaves * kWave) void coarse_term_levels_kernel(
     LevelTerm T, float* __restrict__ cmax, float* __restrict__ csum, float* __restrict__ cvec,
     long long rows, int d, int waves) {
   extern __shared__ __attribute__((aligned(16))) uint32_t ml_smem[];
-  const int L = T.levels, nbf = T.nb[L - 1];
+  const int nbf = T.nb[L - 1];
   int words = 0, ents = 0;
   int woff[kMaxLevels], eoff[kMaxLevels + 1];
+#pragma unroll
   for (int l = 0; l < L; ++l) {
     woff[l] = words;
     words += (T.nb[l] + 31) / 32;
@@ -102,68 +104,119 @@ __global__ __launch_bounds__(kMlWaves * kWave) void coarse_term_levels_kernel(
   const long long bh = g / nbf;
   const int x = (int)(g - bh * nbf);
 
+  // the row's ancestor at every level; every level's candidate count
+  long long G[L];
+  int ncand[L], mmax = 0, cmaxn = 0;
+#pragma unroll
+  for (int l = 0; l < L; ++l) {
+    G[l] = bh * T.nb[l] + x / T.r[l];
+    ncand[l] = eoff[l + 1] - eoff[l];
+    mmax = max(mmax, T.m[l]);
+    cmaxn = max(cmaxn, ncand[l]);
+  }
+  // Global loads are issued for all levels before their results are used, so
+  // their latencies overlap.
   for (int i = lane; i < words; i += kWave) bm[i] = 0u;
   wave_lds_sync();
-  for (int l = 0; l < L; ++l) {
-    const long long G = bh * T.nb[l] + x / T.r[l];          // the row's ancestor at level l
-    for (int i = lane; i < T.m[l]; i += kWave) {
-      const int Y = T.idx[l][G * T.m[l] + i];
-      if (Y >= 0 && Y < T.nb[l]) atomicOr(&bm[woff[l] + (Y >> 5)], 1u << (Y & 31));
-    }
-  }
-  // candidates; -1 marks a child of an invalid parent entry (never used)
-  for (int l = 0; l < L; ++l) {
-    if (l == 0) {
-      for (int c = lane; c < T.nb[0]; c += kWave) cy[c] = c;
-    } else {
-      const int p = T.r[l - 1] / T.r[l];
-      const long long Gp = bh * T.nb[l - 1] + x / T.r[l - 1];
-      for (int c = lane; c < eoff[l + 1] - eoff[l]; c += kWave) {
-        const int Y = T.idx[l - 1][Gp * T.m[l - 1] + c / p];
-        cy[eoff[l] + c] = Y >= 0 && Y < T.nb[l - 1] ? Y * p + c % p : -1;
-      }
-    }
+  for (int i0 = 0; i0 < mmax; i0 += kWave) {
+    int Yv[L];
+#pragma unroll
+    for (int l = 0; l < L; ++l) Yv[l] = i0 + lane < T.m[l] ? T.idx[l][G[l] * T.m[l] + i0 + lane] : -1;
+#pragma unroll
+    for (int l = 0; l < L; ++l)
+      if (Yv[l] >= 0 && Yv[l] < T.nb[l]) atomicOr(&bm[woff[l] + (Yv[l] >> 5)], 1u << (Yv[l] & 31));
   }
   wave_lds_sync();
 
   auto unkept = [&](int l, int y) {
     return y >= 0 && !((bm[woff[l] + (y >> 5)] >> (y & 31)) & 1u);
   };
+  // candidates (level 0: all blocks; level l: the children of the parent's
+  // kept blocks, -1 for an invalid parent entry) and the unkept ones' logits,
+  // held in wt until the weights replace them
   float M = -INFINITY;
-  for (int l = 0; l < L; ++l) {
-    const float* srow = T.S[l] + (bh * T.nb[l] + x / T.r[l]) * T.nb[l];
-    for (int c = eoff[l] + lane; c < eoff[l + 1]; c += kWave) {
-      const int y = cy[c];
-      if (unkept(l, y)) M = fmaxf(M, srow[y]);
+  for (int c0 = 0; c0 < cmaxn; c0 += kWave) {
+    const int c = c0 + lane;
+    int yv[L];
+    float sv[L];
+#pragma unroll
+    for (int l = 0; l < L; ++l) {
+      if (l == 0) {
+        yv[l] = c < ncand[0] ? c : -1;
+      } else {
+        const int p = T.r[l - 1] / T.r[l];
+        const int Y = c < ncand[l] ? T.idx[l - 1][G[l - 1] * T.m[l - 1] + c / p] : -1;
+        yv[l] = Y >= 0 && Y < T.nb[l - 1] ? Y * p + c % p : -1;
+      }
     }
+#pragma unroll
+    for (int l = 0; l < L; ++l) {
+      const float s = T.S[l][G[l] * T.nb[l] + (yv[l] < 0 ? 0 : yv[l])];
+      sv[l] = unkept(l, yv[l]) ? s : -INFINITY;
+    }
+#pragma unroll
+    for (int l = 0; l < L; ++l)
+      if (c < ncand[l]) {
+        cy[eoff[l] + c] = yv[l];
+        wt[eoff[l] + c] = sv[l];
+        M = fmaxf(M, sv[l]);
+      }
   }
+  wave_lds_sync();
   M = wave_max(M);
   const bool any = M != -INFINITY;
+  // weights; the list keeps only the entries that carry one, in order
+  // (kept blocks would add zero: dropping them changes no bit)
   float sum = 0.0f;
+  int kept_to[kMaxLevels + 1];
+  int cnt = 0;
+#pragma unroll
   for (int l = 0; l < L; ++l) {
-    const float* srow = T.S[l] + (bh * T.nb[l] + x / T.r[l]) * T.nb[l];
+    kept_to[l] = cnt;
     const float wide = (float)(T.r[l] * kBlock);
-    for (int c = eoff[l] + lane; c < eoff[l + 1]; c += kWave) {
-      const int y = cy[c];
+    for (int c0 = eoff[l]; c0 < eoff[l + 1]; c0 += kWave) {
+      const int c = c0 + lane;
+      const int y = c < eoff[l + 1] ? cy[c] : -1;
+      const float sv = c < eoff[l + 1] ? wt[c] : -INFINITY;
       const bool use = any && unkept(l, y);
-      const float v = use ? wide * expf(srow[y] - M) : 0.0f;
-      wt[c] = v;
+      const float v = use ? wide * expf(sv - M) : 0.0f;
       sum += v;
+      const uint64_t mk = __ballot(use);
+      if (use) {
+        const int pos = cnt + __popcll(mk & lanemask_lt());
+        cy[pos] = y;                                        // pos <= c: that entry was read above
+        wt[pos] = v;
+      }
+      cnt += __popcll(mk);
     }
   }
+  kept_to[L] = cnt;
   sum = wave_sum(sum);
   wave_lds_sync();
   if (lane == 0) {
     cmax[g] = M;
     csum[g] = sum;
   }
+  // weight x pooled V row, entries in list order; the rows' loads are issued
+  // kBatch at a time so that their latencies overlap
+  constexpr int kBatch = 32;
   for (int dd = lane; dd < d; dd += kWave) {
     float acc = 0.0f;
+#pragma unroll
     for (int l = 0; l < L; ++l) {
       const float* vl = T.vp[l] + bh * (long long)T.nb[l] * d + dd;
-      for (int c = eoff[l]; c < eoff[l + 1]; ++c) {
-        const int y = cy[c];
-        acc = fmaf(wt[c], vl[(long long)(y < 0 ? 0 : y) * d], acc);
+      for (int c0 = kept_to[l]; c0 < kept_to[l + 1]; c0 += kBatch) {
+        const int nc = min(kBatch, kept_to[l + 1] - c0);  // wave-uniform
+        float vv[kBatch], ww[kBatch];
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+          const int y = j < nc ? cy[c0 + j] : 0;
+          ww[j] = j < nc ? wt[c0 + j] : 0.0f;
+          vv[j] = vl[(long long)y * d];
+        }
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j)
+          if (j < nc) acc = fmaf(ww[j], vv[j], acc);
       }
     }
     cvec[g * d + dd] = acc;
@@ -203,8 +256,24 @@ hipError_t launch_coarse_term_levels(const LevelTerm& T, float* cmax, float* csu
   const size_t per_wave = coarse_term_levels_wave_bytes(T);
   const int waves = per_wave * kMlWaves <= 65536 ? kMlWaves : 1;
   const unsigned blocks = (unsigned)((rows + waves - 1) / waves);
-  coarse_term_levels_kernel<<<blocks, waves * kWave, per_wave * waves, stream>>>(T, cmax, csum, cvec,
-                                                                               rows, d, waves);
+  const size_t smem = per_wave * waves;
+  switch (T.levels) {
+#define MRA_LEVELS_CASE(NL)                                                                          \
+  case NL:                                                                                           \
+    coarse_term_levels_kernel<NL><<<blocks, waves * kWave, smem, stream>>>(T, cmax, csum, cvec, rows, \
+                                                                           d, waves);               \
+    break;
+    MRA_LEVELS_CASE(1)
+    MRA_LEVELS_CASE(2)
+    MRA_LEVELS_CASE(3)
+    MRA_LEVELS_CASE(4)
+    MRA_LEVELS_CASE(5)
+    MRA_LEVELS_CASE(6)
+    MRA_LEVELS_CASE(7)
+    MRA_LEVELS_CASE(8)
+#undef MRA_LEVELS_CASE
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
