@@ -548,7 +548,7 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
     const void* __restrict__ qv, const void* __restrict__ kv, const void* __restrict__ vv,
     const int32_t* __restrict__ idx, const float* __restrict__ cmax,
     const float* __restrict__ csum, const float* __restrict__ cvec, void* __restrict__ outv,
-    float* __restrict__ lse, int n, int nb, int m, long long rows, float scale_log2) {
+    float* __restrict__ lse, int n, int nb, int m, long long row0, long long rows, float scale_log2) {
   using Cfg = TileCfg<DT, D>;
   using elem = typename Cfg::elem;
   constexpr int KC = Cfg::kKChunks, VC = Cfg::kVChunks, CH = Cfg::kChunks;
@@ -565,7 +565,7 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
   const int w = wave_uniform(threadIdx.x / kWave);
   const int lane = lane_id();
   const long long wg = xcd_remap(blockIdx.x, gridDim.x);
-  const long long g = wg * WAVES + w;                // global block-row
+  const long long g = row0 + wg * WAVES + w;         // global block-row (rows row0 .. rows - 1)
   if (g >= rows) return;                             // no workgroup barriers below
   const long long bh = g / nb;
   const int x = (int)(g - bh * nb);
@@ -681,20 +681,53 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
 // ---------------------------------------------------------------------------
 // Raw K/V tiles of up to 8 KB (bfloat16; float32 with d <= 64) stream through
 // LDS.
+//
+// Where a head's K and V exceed an XCD's L2 (4 MB), the pass is launched one
+// occupancy round of block-rows at a time: every block-row of a launch starts
+// together and walks its (ascending) selection in step with its neighbours,
+// so the blocks the XCD's resident rows touch at any moment stay close
+// together and more of them hit L2. Within one launch, later rows start as
+// earlier ones finish and the rows drift apart over the head. Heads that fit
+// L2 are launched whole (a launch per round costs more than it saves there).
+constexpr size_t kL2PerXcd = (size_t)4 << 20;
+
+template <class Kernel>
+static long long rows_per_round(Kernel kernel, size_t smem) {
+  int dev = 0, cus = 0, wgs = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&wgs, kernel, kStreamWaves * kWave, smem) != hipSuccess)
+    return 0;
+  return (long long)cus * wgs * kStreamWaves;
+}
+
+template <int DT, int D, bool COARSE>
+static void launch_stream_c(const void* q, const void* k, const void* v, const int32_t* idx,
+                            const float* cmax, const float* csum, const float* cvec, void* out,
+                            float* lse, long long bh, int n, int m, float scale_log2, hipStream_t stream) {
+  const int nb = n / kBlock;
+  const long long rows = bh * nb;
+  const size_t smem = (size_t)kStreamWaves * m * sizeof(int32_t);  // per-wave selection lists
+  auto kernel = tile_stream_kernel<DT, D, COARSE, kStreamWaves, kStreamSlots>;
+  const size_t head_kv = (size_t)2 * n * D * (DT == BF16 ? 2 : 4);
+  long long chunk = head_kv > kL2PerXcd ? rows_per_round(kernel, smem) : 0;
+  if (chunk <= 0) chunk = rows;
+  for (long long r0 = 0; r0 < rows; r0 += chunk) {
+    const long long r1 = r0 + chunk < rows ? r0 + chunk : rows;
+    const unsigned blocks = (unsigned)((r1 - r0 + kStreamWaves - 1) / kStreamWaves);
+    kernel<<<blocks, kStreamWaves * kWave, smem, stream>>>(q, k, v, idx, cmax, csum, cvec, out, lse, n, nb,
+                                                           m, r0, r1, scale_log2);
+  }
+}
+
 template <int DT, int D>
 static void launch_stream(const void* q, const void* k, const void* v, const int32_t* idx,
                           const float* cmax, const float* csum, const float* cvec, void* out,
                           float* lse, long long bh, int n, int m, float scale_log2, hipStream_t stream) {
-  const int nb = n / kBlock;
-  const long long rows = bh * nb;
-  const unsigned blocks = (unsigned)((rows + kStreamWaves - 1) / kStreamWaves);
-  const size_t smem = (size_t)kStreamWaves * m * sizeof(int32_t);  // per-wave selection lists
   if (cmax)
-    tile_stream_kernel<DT, D, true, kStreamWaves, kStreamSlots><<<blocks, kStreamWaves * kWave, smem, stream>>>(
-        q, k, v, idx, cmax, csum, cvec, out, lse, n, nb, m, rows, scale_log2);
+    launch_stream_c<DT, D, true>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, m, scale_log2, stream);
   else
-    tile_stream_kernel<DT, D, false, kStreamWaves, kStreamSlots><<<blocks, kStreamWaves * kWave, smem, stream>>>(
-        q, k, v, idx, cmax, csum, cvec, out, lse, n, nb, m, rows, scale_log2);
+    launch_stream_c<DT, D, false>(q, k, v, idx, cmax, csum, cvec, out, lse, bh, n, m, scale_log2, stream);
 }
 
 // float32 tiles of d = 128 (16 KB): the packed copy, or the raw rows
