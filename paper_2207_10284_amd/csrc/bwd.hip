@@ -443,8 +443,8 @@ __global__ __launch_bounds__(kBwdTileWaves * kWave) void bwd_dq_kernel(
 // A = e^{S c - L}, dP = A o (G V^T - delta), dV^T += G_x^T A,
 // dK^T += Q_x^T dP. The epilogue scales dK by c and adds dK~_y / 32 and
 // dV~_y / 32.
-template <int DT, int D, bool COARSE>
-__global__ __launch_bounds__(kBwdTileWaves * kWave) void bwd_dkdv_kernel(
+template <int DT, int D, bool COARSE, int WAVES>
+__global__ __launch_bounds__(WAVES * kWave) void bwd_dkdv_kernel(
     const void* __restrict__ kin, const void* __restrict__ vin, const void* __restrict__ qrow,
     const void* __restrict__ grow, const void* __restrict__ qt, const void* __restrict__ gt,
     const uint32_t* __restrict__ bits, const float* __restrict__ ld,
@@ -456,7 +456,7 @@ __global__ __launch_bounds__(kBwdTileWaves * kWave) void bwd_dkdv_kernel(
   extern __shared__ int32_t sidx_all[];
   const int w = wave_uniform(threadIdx.x / kWave);
   const int lane = lane_id(), h = lane >> 5;
-  const long long gy = xcd_remap(blockIdx.x, gridDim.x) * (long long)kBwdTileWaves + w;
+  const long long gy = xcd_remap(blockIdx.x, gridDim.x) * (long long)WAVES + w;
   if (gy >= rows) return;                                   // no workgroup barriers below
   const long long bh = gy / nb;
   const int y = (int)(gy - bh * nb);
@@ -1136,13 +1136,13 @@ static void launch_tiles_t(const BwdArgs& A, hipStream_t stream) {
   const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
   const unsigned wgs = (unsigned)((rows + kBwdTileWaves - 1) / kBwdTileWaves);
   const size_t smem_dq = (size_t)kBwdTileWaves * A.m * sizeof(int32_t);
-  const size_t smem_dkdv = (size_t)kBwdTileWaves * nb * sizeof(int32_t);
   constexpr int W = kBwdTileWaves;
   if constexpr (DT == BF16 && Cfg::kKChunks <= 4 && Cfg::kVChunks <= 4) {
     bwd_dq_tr_kernel<D, COARSE, W, kDqSlots><<<wgs, W * kWave, smem_dq, stream>>>(
         A.q, A.dout, A.k, A.v, A.idx, A.ld, A.dqp, A.dq, nb, A.m, rows, scale, scale_log2);
-    // one wave per workgroup: column lists differ in length (a workgroup
-    // keeps its LDS until its longest list is done), rows all have m tiles
+    // one wave per workgroup in every column pass: column lists differ in
+    // length (a workgroup keeps its resources until its longest list is
+    // done), rows all have m tiles
     bwd_dkdv_tr_kernel<D, COARSE, 1, kDkdvSlots><<<(unsigned)rows, kWave, nb * sizeof(int32_t), stream>>>(
         A.k, A.v, A.q, A.dout, A.bits, A.bias, A.dkp, A.dvp, A.dk, A.dv, nb, rows, scale,
         scale_log2);
@@ -1150,14 +1150,14 @@ static void launch_tiles_t(const BwdArgs& A, hipStream_t stream) {
     bwd_dq_stream_kernel<DT, D, COARSE, W><<<wgs, W * kWave, smem_dq, stream>>>(
         A.q, A.dout, A.k_row, A.v_row, A.k_t, A.idx, A.ld, A.dqp, A.dq, nb, A.m, rows, scale,
         scale_log2);
-    bwd_dkdv_stream_kernel<DT, D, COARSE, W><<<wgs, W * kWave, smem_dkdv, stream>>>(
+    bwd_dkdv_stream_kernel<DT, D, COARSE, 1><<<(unsigned)rows, kWave, nb * sizeof(int32_t), stream>>>(
         A.k, A.v, A.q_row, A.g_row, A.q_t, A.g_t, A.bits, A.ld, A.dkp, A.dvp, A.dk, A.dv, nb, rows,
         scale, scale_log2);
   } else {
     bwd_dq_kernel<DT, D, COARSE><<<wgs, W * kWave, smem_dq, stream>>>(
         A.q, A.dout, A.k_row, A.v_row, A.k_t, A.idx, A.ld, A.dqp, A.dq, nb, A.m, rows, scale,
         scale_log2);
-    bwd_dkdv_kernel<DT, D, COARSE><<<wgs, W * kWave, smem_dkdv, stream>>>(
+    bwd_dkdv_kernel<DT, D, COARSE, 1><<<(unsigned)rows, kWave, nb * sizeof(int32_t), stream>>>(
         A.k, A.v, A.q_row, A.g_row, A.q_t, A.g_t, A.bits, A.ld, A.dkp, A.dvp, A.dk, A.dv, nb, rows,
         scale, scale_log2);
   }
