@@ -443,8 +443,10 @@ __global__ __launch_bounds__(kBwdTileWaves * kWave) void bwd_dq_kernel(
 // A = e^{S c - L}, dP = A o (G V^T - delta), dV^T += G_x^T A,
 // dK^T += Q_x^T dP. The epilogue scales dK by c and adds dK~_y / 32 and
 // dV~_y / 32.
+// bfloat16 d = 128: two waves per SIMD at the cost of a few registers spilled
+// (measured faster than one wave with no spill); float32 would spill ~70.
 template <int DT, int D, bool COARSE, int WAVES>
-__global__ __launch_bounds__(WAVES * kWave) void bwd_dkdv_kernel(
+__global__ __launch_bounds__(WAVES * kWave) __attribute__((amdgpu_waves_per_eu(DT == BF16 && D == 128 ? 2 : 1))) void bwd_dkdv_kernel(
     const void* __restrict__ kin, const void* __restrict__ vin, const void* __restrict__ qrow,
     const void* __restrict__ grow, const void* __restrict__ qt, const void* __restrict__ gt,
     const uint32_t* __restrict__ bits, const float* __restrict__ ld,
