@@ -105,6 +105,26 @@ __device__ __forceinline__ int xcd_remap(int p, int total) {
   return (xcd < r) ? xcd * (q + 1) + slot : r * (q + 1) + (xcd - r) * q + slot;
 }
 
+// One XCD's L2. Passes whose per-head working set exceeds it are launched one
+// occupancy round at a time (see resident_items).
+constexpr size_t kL2PerXcd = (size_t)4 << 20;
+
+// Work items (waves) a launch of `kernel` keeps resident on the current
+// device: CUs x workgroups per CU x items per workgroup; 0 if unknown. A
+// pass launched this many items at a time starts all of them together, so
+// rows that walk their ascending block lists stay in loose step and share the
+// XCD's L2; launched whole, later items start as earlier ones finish and
+// drift apart.
+template <class Kernel>
+inline long long resident_items(Kernel kernel, int threads, size_t smem, int items_per_wg) {
+  int dev = 0, cus = 0, wgs = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&wgs, kernel, threads, smem) != hipSuccess)
+    return 0;
+  return (long long)cus * wgs * items_per_wg;
+}
+
 // Make LDS writes of this wave visible to the wave's other lanes.
 __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");

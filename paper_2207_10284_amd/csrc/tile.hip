@@ -689,18 +689,6 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
 // together and more of them hit L2. Within one launch, later rows start as
 // earlier ones finish and the rows drift apart over the head. Heads that fit
 // L2 are launched whole (a launch per round costs more than it saves there).
-constexpr size_t kL2PerXcd = (size_t)4 << 20;
-
-template <class Kernel>
-static long long rows_per_round(Kernel kernel, size_t smem) {
-  int dev = 0, cus = 0, wgs = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      hipOccupancyMaxActiveBlocksPerMultiprocessor(&wgs, kernel, kStreamWaves * kWave, smem) != hipSuccess)
-    return 0;
-  return (long long)cus * wgs * kStreamWaves;
-}
-
 template <int DT, int D, bool COARSE>
 static void launch_stream_c(const void* q, const void* k, const void* v, const int32_t* idx,
                             const float* cmax, const float* csum, const float* cvec, void* out,
@@ -710,7 +698,7 @@ static void launch_stream_c(const void* q, const void* k, const void* v, const i
   const size_t smem = (size_t)kStreamWaves * m * sizeof(int32_t);  // per-wave selection lists
   auto kernel = tile_stream_kernel<DT, D, COARSE, kStreamWaves, kStreamSlots>;
   const size_t head_kv = (size_t)2 * n * D * (DT == BF16 ? 2 : 4);
-  long long chunk = head_kv > kL2PerXcd ? rows_per_round(kernel, smem) : 0;
+  long long chunk = head_kv > kL2PerXcd ? resident_items(kernel, kStreamWaves * kWave, smem, kStreamWaves) : 0;
   if (chunk <= 0) chunk = rows;
   for (long long r0 = 0; r0 < rows; r0 += chunk) {
     const long long r1 = r0 + chunk < rows ? r0 + chunk : rows;
