@@ -390,10 +390,11 @@ mra_status_t mra_attention_forward_levels(const void* q, const void* k, const vo
 
 /*
  * mra_backward_workspace_bytes — device workspace of mra_attention_backward:
- * seven rearranged copies of Q, K, V and dZ (7*B*H*n*d*elem bytes; none for
- * bfloat16 with d <= 64, whose gradient passes read the inputs' rows), pooled
- * rows and their gradients, two float32 values per query, the selection as a
- * bitmap and two float32 nb x nb grids per head (W and dS~ below). 0 for
+ * for float32 seven rearranged copies of Q, K, V and dZ (7*B*H*n*d*4 bytes;
+ * the bfloat16 gradient passes read the inputs' rows and instead take 16
+ * bytes per query of bias operands), pooled rows and their gradients, two
+ * float32 values per query, the selection as a bitmap and two float32
+ * nb x nb grids per head (W and dS~ below). 0 for
  * invalid or unsupported arguments.
  */
 size_t mra_backward_workspace_bytes(int B, int H, int n, int d, int block, mra_dtype_t dtype);

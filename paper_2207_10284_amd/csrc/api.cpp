@@ -159,8 +159,8 @@ WsBwd ws_bwd(long long bh, int nb, int d, mra_dtype_t dtype) {
   WsBwd L{};
   size_t off = 0;
   const size_t pooled = align256((size_t)bh * nb * d * sizeof(float));
-  // packed operand copies: not for bfloat16 with d <= 64 (raw tiles)
-  const bool raw = dtype == MRA_BF16 && d <= 64;
+  // packed operand copies: float32 only (bfloat16 passes read raw tiles)
+  const bool raw = dtype == MRA_BF16;
   const size_t packed = raw ? 0 : align256((size_t)bh * nb * kBlockSize * d * (dtype == MRA_BF16 ? 2 : 4));
   const size_t grid = align256((size_t)bh * nb * nb * sizeof(float));
   L.qp = off; off += pooled;
@@ -663,7 +663,7 @@ mra_status_t mra_attention_backward(const void* q, const void* k, const void* v,
   A.q_row = ws + L.q_row; A.q_t = ws + L.q_t; A.k_row = ws + L.k_row; A.k_t = ws + L.k_t;
   A.v_row = ws + L.v_row; A.g_row = ws + L.g_row; A.g_t = ws + L.g_t;
   A.ld = f32(L.ld);
-  A.bias = dtype == MRA_BF16 && d <= 64 ? reinterpret_cast<uint32_t*>(ws + L.bias) : nullptr;
+  A.bias = dtype == MRA_BF16 ? reinterpret_cast<uint32_t*>(ws + L.bias) : nullptr;
   A.bits = reinterpret_cast<uint32_t*>(ws + L.bits);
   A.gh = f32(L.gh); A.W = f32(L.W); A.dS = f32(L.dS);
   A.dqp = f32(L.dqp); A.dkp = f32(L.dkp); A.dvp = f32(L.dvp);

@@ -35,9 +35,9 @@
 //    tiles the row pass also writes, per query, the bfloat16 triples of
 //    -L_i/c and -delta_i, which enter the products as one more contraction
 //    step, so a lane holding 16 queries needs no per-query registers.
-// Tile operands: for bfloat16 with d <= 64 raw 32-row tiles of the inputs
-// (copied into LDS under a swizzle that serves row and transposed reads);
-// otherwise packed copies in the layouts of tile_ops.h.
+// Tile operands: for bfloat16 raw 32-row tiles of the inputs (copied into LDS
+// under a swizzle that serves row and transposed reads); for float32 packed
+// copies in the layouts of tile_ops.h.
 #include "common.h"
 #include "kernels.h"
 #include "tile_ops.h"
@@ -443,10 +443,8 @@ __global__ __launch_bounds__(kBwdTileWaves * kWave) void bwd_dq_kernel(
 // A = e^{S c - L}, dP = A o (G V^T - delta), dV^T += G_x^T A,
 // dK^T += Q_x^T dP. The epilogue scales dK by c and adds dK~_y / 32 and
 // dV~_y / 32.
-// bfloat16 d = 128: two waves per SIMD at the cost of a few registers spilled
-// (measured faster than one wave with no spill); float32 would spill ~70.
 template <int DT, int D, bool COARSE, int WAVES>
-__global__ __launch_bounds__(WAVES * kWave) __attribute__((amdgpu_waves_per_eu(DT == BF16 && D == 128 ? 2 : 1))) void bwd_dkdv_kernel(
+__global__ __launch_bounds__(WAVES * kWave) void bwd_dkdv_kernel(
     const void* __restrict__ kin, const void* __restrict__ vin, const void* __restrict__ qrow,
     const void* __restrict__ grow, const void* __restrict__ qt, const void* __restrict__ gt,
     const uint32_t* __restrict__ bits, const float* __restrict__ ld,
@@ -856,8 +854,8 @@ struct TrChunks {
   }
 };
 
-// bfloat16, d <= 64: the passes read raw 32-row tiles of the inputs
-// themselves, no packed copies. A tile (32 consecutive rows, 2d bytes each) is
+// bfloat16: the passes read raw 32-row tiles of the inputs themselves, no
+// packed copies. A tile (32 consecutive rows, 2d bytes each) is
 // copied with direct-to-LDS loads of whole rows, every lane fetching the
 // 16-byte block that belongs at its LDS position under an XOR swizzle of the
 // blocks within a row (raw_offset / raw_copy_offset), and read both in the row
@@ -867,13 +865,14 @@ struct TrChunks {
 // different block positions, and so do the odd ones (row reads), and rows r
 // and r + 2 of a group of four take positions in opposite halves of the row
 // (transposed reads); for d = 32 rows r, r + 4, r + 8, r + 12 take 4
-// different positions. The swizzle has period 16 in the row, so the
-// transposed reads 16 rows further use the same lane address plus an
-// immediate offset; reads 8 rows further need a second address. The copy
-// offsets repeat with period 2 (d = 64) or 1 (d = 32) in the copy index.
+// different positions; for d = 128 see the d = 128 kernels below. The
+// swizzle has period 16 in the row, so the transposed reads 16 rows further
+// use the same lane address plus an immediate offset; reads 8 rows further
+// need a second address. The copy offsets repeat with period 4 (d = 128),
+// 2 (d = 64) or 1 (d = 32) in the copy index.
 template <int D>
 __host__ __device__ constexpr int raw_swz_b(int r) {
-  return D == 64 ? 4 * ((r >> 1) & 1) + ((r >> 2) & 3) : (r >> 2) & 3;
+  return D == 128 ? 4 * (r & 3) + ((r >> 2) & 3) : (D == 64 ? 4 * ((r >> 1) & 1) + ((r >> 2) & 3) : (r >> 2) & 3);
 }
 
 // This lane's offsets for the raw tiles of the gradient passes.
@@ -881,14 +880,14 @@ template <int D>
 struct RawB {
   static constexpr int KC = D / 16, NT = D / 32;
   static constexpr int TB = 64 * D;                           // bytes of a 32-row tile
-  static constexpr int KP = D == 64 ? 2 : 1;                  // period of the copy offsets
-  int c0, c1;                                                 // copy sources: even, odd copies (less 1 KB)
+  static constexpr int KP = D == 128 ? 4 : (D == 64 ? 2 : 1); // period of the copy offsets
+  unsigned cp[KP];                                            // copy sources of copies i mod KP (less their KB)
   uint32_t rr[KC];                                            // row-layout chunk c
   uint32_t tr[NT][2];                                         // transposed column tile t, half e
   __device__ __forceinline__ void init() {
     const int lane = lane_id(), h = lane >> 5, j = lane & 31, i16 = lane & 15;
-    c0 = raw_copy_offset<D, raw_swz_b<D>>(0, lane);
-    c1 = KP == 2 ? raw_copy_offset<D, raw_swz_b<D>>(1, lane) - 1024 : c0;
+#pragma unroll
+    for (int q = 0; q < KP; ++q) cp[q] = (unsigned)(raw_copy_offset<D, raw_swz_b<D>>(q, lane) - q * 1024);
 #pragma unroll
     for (int c = 0; c < KC; ++c) rr[c] = (uint32_t)raw_offset<D, raw_swz_b<D>>(j, (D / 2) * h + 8 * c);
 #pragma unroll
@@ -903,17 +902,16 @@ struct RawB {
 // Two raw tiles, C 1 KB copies each, as buffer loads to LDS: the heads' rows
 // are the resources ra and rb, the tiles' byte offsets ta and tb go in the
 // scalar offset (outside the hardware range check: callers copy validated
-// blocks only), this lane's swizzled source offset (c0 for even copies, c1
-// for odd ones when the offsets have period 2) in the vector offset.
+// blocks only), this lane's swizzled source offset of copy i (cp[i mod KP],
+// the offsets repeat with period KP) in the vector offset.
 template <int C, int KP>
 __device__ __forceinline__ void copy_raw_pair_buf(i32x4 ra, i32x4 rb, unsigned ta, unsigned tb,
-                                                  unsigned c0, unsigned c1, lptr_t as, lptr_t bs) {
+                                                  const unsigned (&cp)[KP], lptr_t as, lptr_t bs) {
   if constexpr (C > 0) {
-    copy_raw_pair_buf<C - 1, KP>(ra, rb, ta, tb, c0, c1, as, bs);
+    copy_raw_pair_buf<C - 1, KP>(ra, rb, ta, tb, cp, as, bs);
     constexpr int i = C - 1;
-    const unsigned vo = (KP == 2 && (i & 1)) ? c1 : c0;
-    buffer_load_lds16(ra, as + i * 1024, vo, ta + i * 1024);
-    buffer_load_lds16(rb, bs + i * 1024, vo, tb + i * 1024);
+    buffer_load_lds16(ra, as + i * 1024, cp[i % KP], ta + i * 1024);
+    buffer_load_lds16(rb, bs + i * 1024, cp[i % KP], tb + i * 1024);
   }
 }
 
@@ -985,7 +983,7 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dq_tr_kernel(
   const uint32_t a0 = lds_addr(slots[w][0]);
   auto issue = [&](int y, int sl) {
     const lptr_t dst = (lptr_t)slots[w][sl];
-    copy_raw_pair_buf<KC, R::KP>(krs, vrs, (unsigned)y * TB, (unsigned)y * TB, ro.c0, ro.c1, dst, dst + TB);
+    copy_raw_pair_buf<KC, R::KP>(krs, vrs, (unsigned)y * TB, (unsigned)y * TB, ro.cp, dst, dst + TB);
   };
 #pragma unroll
   for (int t = 0; t < SLOTS; ++t)
@@ -1085,7 +1083,7 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dkdv_tr_kernel(
   const uint32_t boff = (uint32_t)(2 * TB) + 16u * (lane & 31);   // this lane's query's bias operand
   auto issue = [&](int x, int sl) {
     const lptr_t dst = (lptr_t)slots[w][sl];
-    copy_raw_pair_buf<KC, R::KP>(qrs, grs, (unsigned)x * TB, (unsigned)x * TB, ro.c0, ro.c1, dst, dst + TB);
+    copy_raw_pair_buf<KC, R::KP>(qrs, grs, (unsigned)x * TB, (unsigned)x * TB, ro.cp, dst, dst + TB);
     mra_raw_buffer_load_lds(brs, dst + 2 * TB, 4, lane * 4, x * RB, 0, 0);
     mra_raw_buffer_load_lds(brs, dst + 2 * TB + 256, 4, lane * 4, x * RB + 256, 0, 0);
   };
@@ -1128,6 +1126,188 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dkdv_tr_kernel(
                        COARSE ? dvp + gy * D : nullptr);
 }
 
+// bfloat16, d = 128: raw 8 KB tiles of 32 rows x 256 bytes under the same
+// kind of swizzle (block b of row r at b ^ (4 (r mod 4) + (r / 4 mod 4)):
+// sixteen consecutive rows take sixteen positions for the row reads, four
+// consecutive rows four groups of four for the transposed reads; copy offsets
+// of period 4). A tile's operands are too many registers at this width to be
+// read at once, so each is read just before its products: the row chunks of
+// one tile, then of the other, then the transposed chunks.
+
+// dQ (bf16, d = 128): one wave per block-row, one slot per wave (K_y and V_y);
+// the next tile is copied once the current one has been read.
+template <bool COARSE, int WAVES>
+__global__ __launch_bounds__(WAVES * kWave) void bwd_dq_tr128_kernel(
+    const void* __restrict__ qin, const void* __restrict__ gin, const void* __restrict__ kin,
+    const void* __restrict__ vin, const int32_t* __restrict__ idx,
+    const float* __restrict__ ld, const float* __restrict__ dqp, void* __restrict__ dq, int nb,
+    int m, long long rows, float scale, float scale_log2) {
+  constexpr int D = 128;
+  using Cfg = TileCfg<BF16, D>;
+  using elem = typename Cfg::elem;
+  using R = RawB<D>;
+  constexpr int KC = Cfg::kKChunks, VC = Cfg::kVChunks, NT = Cfg::kNT;
+  constexpr int TB = R::TB;
+  static_assert(KC == R::KC && VC == KC, "row and transposed chunks of a tile");
+  __shared__ __attribute__((aligned(16))) unsigned char slots[WAVES][2 * TB];
+  extern __shared__ int32_t sidx_all[];
+  const int w = wave_uniform(threadIdx.x / kWave);
+  const int lane = lane_id(), jq = lane & 31;
+  const long long g = xcd_remap(blockIdx.x, gridDim.x) * (long long)WAVES + w;
+  if (g >= rows) return;                                    // no workgroup barriers below
+  const long long bh = g / nb;
+  int32_t* myidx = sidx_all + w * m;
+  const int cnt = stage_selection(idx + g * m, m, nb, myidx);
+
+  u32x4 qf[KC], gf[KC];
+  load_rows<BF16, D>(reinterpret_cast<const elem*>(qin) + g * 32 * D, qf);
+  load_rows<BF16, D>(reinterpret_cast<const elem*>(gin) + g * 32 * D, gf);
+  const float lq = ld[g * 64 + jq], dl = ld[g * 64 + 32 + jq];
+  f32x16 acc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[t][r] = 0.0f;
+
+  R ro;
+  ro.init();
+  const i32x4 krs = buffer_rsrc(static_cast<const char*>(kin) + (size_t)bh * nb * TB, (unsigned)nb * TB);
+  const i32x4 vrs = buffer_rsrc(static_cast<const char*>(vin) + (size_t)bh * nb * TB, (unsigned)nb * TB);
+  const uint32_t base = lds_addr(slots[w]);
+  auto issue = [&](int y) {
+    const lptr_t dst = (lptr_t)slots[w];
+    copy_raw_pair_buf<KC, R::KP>(krs, vrs, (unsigned)y * TB, (unsigned)y * TB, ro.cp, dst, dst + TB);
+  };
+  if (cnt > 0) issue(wave_uniform(myidx[0]));
+  for (int i = 0; i < cnt; ++i) {
+    wait_loads<0>();
+    u32x4 op[KC];
+    raw_rows<0>(base, ro.rr, op);                           // K_y rows
+    lds_done(op);
+    const f32x16 s = mfma_abt<BF16, KC>(op, qf);
+    raw_rows<TB>(base, ro.rr, op);                          // V_y rows
+    lds_done(op);
+    const f32x16 pv = mfma_abt<BF16, KC>(op, gf);
+    RawTrB<D, 0, 0, VC>::run(base, ro.tr, op);             // K_y^T
+    lds_done(op);
+    if (i + 1 < cnt) issue(wave_uniform(myidx[i + 1]));
+    float ds[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      ds[r] = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -lq)) * (pv[r] - dl);
+    uint32_t pk[8];
+    pack16(ds, pk);
+    mfma_acc_bf16<NT>(acc, pk, [&](int c) { return op[c]; });
+  }
+  store_block<BF16, D>(reinterpret_cast<elem*>(dq) + g * 32 * D, acc, scale,
+                       COARSE ? dqp + g * D : nullptr);
+}
+
+// dK, dV (bf16, d = 128): one wave per column block, two slots (raw Q_x, G_x
+// and the block-row's bias operands), the per-query terms entering the
+// products as in bwd_dkdv_tr_kernel.
+template <bool COARSE>
+__global__ __launch_bounds__(kWave) void bwd_dkdv_tr128_kernel(
+    const void* __restrict__ kin, const void* __restrict__ vin, const void* __restrict__ qin,
+    const void* __restrict__ gin, const uint32_t* __restrict__ bits,
+    const uint32_t* __restrict__ bias, const float* __restrict__ dkp, const float* __restrict__ dvp,
+    void* __restrict__ dk, void* __restrict__ dv, int nb, long long rows, float scale,
+    float scale_log2) {
+  constexpr int D = 128;
+  using Cfg = TileCfg<BF16, D>;
+  using elem = typename Cfg::elem;
+  using R = RawB<D>;
+  constexpr int KC = Cfg::kKChunks, VC = Cfg::kVChunks, NT = Cfg::kNT;
+  constexpr int TB = R::TB, RB = 32 * 16;
+  constexpr int N = 2 * KC + 2;                             // loads per tile
+  constexpr int SLOT = 2 * TB + RB;
+  static_assert(KC == R::KC && VC == KC, "row and transposed chunks of a tile");
+  __shared__ __attribute__((aligned(16))) unsigned char slots[2][SLOT];
+  extern __shared__ int32_t sidx_all[];
+  const int lane = lane_id();
+  const long long gy = xcd_remap(blockIdx.x, gridDim.x);
+  if (gy >= rows) return;
+  const long long bh = gy / nb;
+  const int y = (int)(gy - bh * nb);
+  const long long hb = bh * nb;
+  const int nbw = (nb + 31) / 32;
+
+  // block-rows whose selection holds y, ascending
+  int32_t* myx = sidx_all;
+  int cnt = 0;
+  for (int x0 = 0; x0 < nb; x0 += kWave) {
+    const int x = x0 + lane;
+    const bool ok = x < nb && ((bits[(hb + x) * nbw + (y >> 5)] >> (y & 31)) & 1u);
+    const uint64_t mk = __ballot(ok);
+    if (ok) myx[cnt + __popcll(mk & lanemask_lt())] = x;
+    cnt += __popcll(mk);
+  }
+  wave_lds_sync();
+  cnt = wave_uniform(cnt);
+
+  u32x4 kf[KC], vf[KC];
+  load_rows<BF16, D>(reinterpret_cast<const elem*>(kin) + gy * 32 * D, kf);
+  load_rows<BF16, D>(reinterpret_cast<const elem*>(vin) + gy * 32 * D, vf);
+  f32x16 ak[NT], av[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) ak[t][r] = av[t][r] = 0.0f;
+  const bool lo_half = lane < 32;
+  const u32x4 ones_l = lo_half ? u32x4{0x3F803F80u, 0x00003F80u, 0u, 0u} : u32x4{0u, 0u, 0u, 0u};
+  const u32x4 ones_d = lo_half ? u32x4{0u, 0x3F800000u, 0x3F803F80u, 0u} : u32x4{0u, 0u, 0u, 0u};
+
+  R ro;
+  ro.init();
+  const i32x4 qrs = buffer_rsrc(static_cast<const char*>(qin) + (size_t)hb * TB, (unsigned)nb * TB);
+  const i32x4 grs = buffer_rsrc(static_cast<const char*>(gin) + (size_t)hb * TB, (unsigned)nb * TB);
+  const i32x4 brs = buffer_rsrc(reinterpret_cast<const char*>(bias) + (size_t)hb * RB, (unsigned)nb * RB);
+  const uint32_t a0 = lds_addr(slots[0]);
+  const uint32_t boff = (uint32_t)(2 * TB) + 16u * (lane & 31);
+  auto issue = [&](int x, int sl) {
+    const lptr_t dst = (lptr_t)slots[sl];
+    copy_raw_pair_buf<KC, R::KP>(qrs, grs, (unsigned)x * TB, (unsigned)x * TB, ro.cp, dst, dst + TB);
+    mra_raw_buffer_load_lds(brs, dst + 2 * TB, 4, lane * 4, x * RB, 0, 0);
+    mra_raw_buffer_load_lds(brs, dst + 2 * TB + 256, 4, lane * 4, x * RB + 256, 0, 0);
+  };
+  if (cnt > 0) issue(wave_uniform(myx[0]), 0);
+  if (cnt > 1) issue(wave_uniform(myx[1]), 1);
+  for (int i = 0; i < cnt; ++i) {
+    if (i + 1 < cnt) wait_loads<N>();                       // tile i landed, i+1 may not have
+    else wait_loads<0>();
+    const uint32_t base = a0 + (uint32_t)((i & 1) * SLOT);
+    u32x4 op[KC], ba[1];
+    ba[0] = lds_read16<0>(base + boff);
+    raw_rows<0>(base, ro.rr, op);                           // Q_x rows
+    lds_done(ba);
+    lds_done(op);
+    const f32x16 s = mfma_abt_from<KC>(op, kf, ba[0], ones_l);   // lane: key, 16 queries
+    raw_rows<TB>(base, ro.rr, op);                          // G_x rows
+    lds_done(op);
+    const f32x16 pv = mfma_abt_from<KC>(op, vf, ba[0], ones_d);
+    float a[16], ds[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      a[r] = __builtin_amdgcn_exp2f(s[r] * scale_log2);
+      ds[r] = a[r] * pv[r];
+    }
+    uint32_t pa8[8], pd8[8];
+    pack16(a, pa8);
+    pack16(ds, pd8);
+    RawTrB<D, 0, 0, VC>::run(base, ro.tr, op);             // Q_x^T
+    lds_done(op);
+    mfma_acc_bf16<NT>(ak, pd8, [&](int c) { return op[c]; });
+    RawTrB<D, TB, 0, VC>::run(base, ro.tr, op);            // G_x^T
+    lds_done(op);
+    if (i + 2 < cnt) issue(wave_uniform(myx[i + 2]), i & 1);   // the slot has been read
+    mfma_acc_bf16<NT>(av, pa8, [&](int c) { return op[c]; });
+  }
+  store_block<BF16, D>(reinterpret_cast<elem*>(dk) + gy * 32 * D, ak, scale,
+                       COARSE ? dkp + gy * D : nullptr);
+  store_block<BF16, D>(reinterpret_cast<elem*>(dv) + gy * 32 * D, av, 1.0f,
+                       COARSE ? dvp + gy * D : nullptr);
+}
+
 // ---------------------------------------------------------------------------
 template <int DT, int D, bool COARSE>
 static void launch_tiles_t(const BwdArgs& A, hipStream_t stream) {
@@ -1148,6 +1328,11 @@ static void launch_tiles_t(const BwdArgs& A, hipStream_t stream) {
     bwd_dkdv_tr_kernel<D, COARSE, 1, kDkdvSlots><<<(unsigned)rows, kWave, nb * sizeof(int32_t), stream>>>(
         A.k, A.v, A.q, A.dout, A.bits, A.bias, A.dkp, A.dvp, A.dk, A.dv, nb, rows, scale,
         scale_log2);
+  } else if constexpr (DT == BF16 && D == 128) {
+    bwd_dq_tr128_kernel<COARSE, W><<<wgs, W * kWave, smem_dq, stream>>>(
+        A.q, A.dout, A.k, A.v, A.idx, A.ld, A.dqp, A.dq, nb, A.m, rows, scale, scale_log2);
+    bwd_dkdv_tr128_kernel<COARSE><<<(unsigned)rows, kWave, nb * sizeof(int32_t), stream>>>(
+        A.k, A.v, A.q, A.dout, A.bits, A.bias, A.dkp, A.dvp, A.dk, A.dv, nb, rows, scale, scale_log2);
   } else if constexpr (Cfg::kKChunks <= 4 && Cfg::kVChunks <= 4) {
     bwd_dq_stream_kernel<DT, D, COARSE, W><<<wgs, W * kWave, smem_dq, stream>>>(
         A.q, A.dout, A.k_row, A.v_row, A.k_t, A.idx, A.ld, A.dqp, A.dq, nb, A.m, rows, scale,
@@ -1189,7 +1374,7 @@ static void launch_bwd_t(const BwdArgs& A, hipStream_t stream) {
 
 hipError_t launch_bwd(const BwdArgs& A, hipStream_t stream) {
   hipError_t e = hipSuccess;
-  if (A.dtype == BF16 && A.d <= 64) {
+  if (A.dtype == BF16) {
     // the tile passes read raw tiles of Q, K, V and G = dZ: only the pooled
     // rows of the coarse term
     if (A.coarse) e = launch_pool(A.q, A.k, A.v, A.qp, A.kp, A.vp, nullptr, A.bh, A.n, A.d, A.dtype, stream);

@@ -111,8 +111,8 @@ hipError_t launch_tile(const void* q, const void* k, const void* v, const void* 
 // sparse-only variant. Outputs dq, dk, dv [bh, n, d] of dtype. The remaining
 // pointers are workspace: pooled rows (coarse only) [bh, nb, d] f32; packed
 // operand copies (row / transposed layout above) of bh*n*d elements of
-// dtype (not used for bfloat16 with d <= 64, whose passes read raw tiles); ld [bh*nb, 64] f32 (per block-row: 32 log normalisers in log2 units,
-// then 32 deltas); bias [bh*n] x 16 bytes (bfloat16 with d <= 64 only, else
+// dtype (float32 only: the bfloat16 passes read raw tiles); ld [bh*nb, 64] f32 (per block-row: 32 log normalisers in log2 units,
+// then 32 deltas); bias [bh*n] x 16 bytes (bfloat16 only, else
 // NULL: per query the bfloat16 triples hi + mid + lo of -L_i/c and of
 // -delta_i, the A operand that adds both to the column pass's products);
 // bits [bh*nb, ceil(nb/32)] u32; gh, dqp, dkp, dvp [bh, nb, d] f32 and W, dS

@@ -346,16 +346,19 @@ def test_backward_workspace_bytes(lib):
     B, H, n, d = 8, 12, 4096, 64
     bh, nb = B * H, n // 32
     for dt, e in ((0, 4), (1, 2)):
-        raw = dt == 1 and d <= 64                     # bf16 with d <= 64 reads raw tiles
+        raw = dt == 1                                 # bf16 reads raw tiles
         copies = 0 if raw else 7
         bias = al(bh * n * 16) if raw else 0          # per query, the column pass's bias operand
         want = 7 * al(bh * nb * d * 4) + copies * al(bh * n * d * e) + al(bh * nb * 64 * 4) + bias \
             + al(bh * nb * (nb // 32) * 4) + 2 * al(bh * nb * nb * 4)
         assert f(B, H, n, d, 32, dt) == want
-    # bf16 with d = 128 keeps its rearranged copies
-    want = 7 * al(bh * nb * 128 * 4) + 7 * al(bh * n * 128 * 2) + al(bh * nb * 64 * 4) \
+    # bf16 with d = 128 reads raw tiles too; float32 keeps its rearranged copies
+    want = 7 * al(bh * nb * 128 * 4) + al(bh * nb * 64 * 4) + al(bh * n * 16) \
         + al(bh * nb * (nb // 32) * 4) + 2 * al(bh * nb * nb * 4)
     assert f(B, H, n, 128, 32, 1) == want
+    want = 7 * al(bh * nb * 128 * 4) + 7 * al(bh * n * 128 * 4) + al(bh * nb * 64 * 4) \
+        + al(bh * nb * (nb // 32) * 4) + 2 * al(bh * nb * nb * 4)
+    assert f(B, H, n, 128, 32, 0) == want
 
 
 def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):

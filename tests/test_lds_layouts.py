@@ -138,15 +138,17 @@ def test_unswizzled_rows_would_conflict():
 # ---------------------------------------------------------------------------
 # The gradient passes read each raw tile twice: in the row layout
 # (ds_read_b128, as K above) and transposed (ds_read_b64_tr_b16, as V above).
-# One swizzle serves both (csrc/bwd.hip, raw_swz_b): for d = 64 block b of row
-# r sits at b ^ (4 ((r >> 1) & 1) + ((r >> 2) & 3)), for d = 32 at
-# b ^ ((r >> 2) & 3).
+# One swizzle serves both (csrc/bwd.hip, raw_swz_b): for d = 128 block b of
+# row r sits at b ^ (4 (r & 3) + ((r >> 2) & 3)), for d = 64 at
+# b ^ (4 ((r >> 1) & 1) + ((r >> 2) & 3)), for d = 32 at b ^ ((r >> 2) & 3).
 
 def swz_b(d, r):
+    if d == 128:
+        return 4 * (r & 3) + ((r >> 2) & 3)
     return 4 * ((r >> 1) & 1) + ((r >> 2) & 3) if d == 64 else (r >> 2) & 3
 
 
-@pytest.mark.parametrize("d", [32, 64])
+@pytest.mark.parametrize("d", [32, 64, 128])
 def test_b_copies_cover_whole_rows_once(d):
     rb = 2 * d
     sources = set()
@@ -162,9 +164,9 @@ def test_b_copies_cover_whole_rows_once(d):
             assert offset(d, r, 8 * blk, swz_b) == q
         assert len(rows) * rb == 1024
     assert len(sources) == 32 * rb // 16
-    # the per-lane source offsets repeat with period 2 (d = 64) or 1 (d = 32)
-    # in the copy index, up to the 1 KB step of the load's immediate offset
-    period = 2 if d == 64 else 1
+    # the per-lane source offsets repeat with period 4 (d = 128), 2 (d = 64) or
+    # 1 (d = 32) in the copy index, up to the 1 KB step of the copy
+    period = {128: 4, 64: 2, 32: 1}[d]
     for i in range(period, 32 * rb // 1024):
         for p in range(64):
             def src(ii):
@@ -174,7 +176,7 @@ def test_b_copies_cover_whole_rows_once(d):
             assert src(i) - src(i - period) == period * 1024
 
 
-@pytest.mark.parametrize("d", [32, 64])
+@pytest.mark.parametrize("d", [32, 64, 128])
 def test_b_row_reads(d):
     """Chunk s of lane (h, j) = X[j][(d/2)h + 8s .. +7], conflict-free."""
     for s in range(d // 16):
@@ -189,7 +191,7 @@ def test_b_row_reads(d):
             assert conflict_ways(addrs[p0:p0 + 16], 16) == 1
 
 
-@pytest.mark.parametrize("d", [32, 64])
+@pytest.mark.parametrize("d", [32, 64, 128])
 def test_b_transposed_reads(d):
     """Transposed chunk (u, t) of lane l = 32h + j: X[16u + 8(s/4) + 4h + s%4]
     [32t + j], s = 0..7, from two transposing reads (half e = s/4). Each lane
