@@ -9,11 +9,11 @@
 // segments, so every HBM line fetched is fully used; two threads per chunk
 // keep enough waves in flight to fill the GPU. No LDS, no barriers.
 //
-// Optionally K and V are also written in the tile kernel's matrix-core operand
-// order ("packed K/V", layout in kernels.h), so every operand load of the tile
-// pass is one contiguous 1 KB wave access; that configuration pools Q, K and V
-// in one launch that stages blocks through LDS so the packed writes stay
-// contiguous.
+// For float32 passes that read packed operands (the forward at d = 128, the
+// gradient passes) K and V (and Q, dZ) are also written in the tile kernels'
+// matrix-core operand order ("packed", layout in kernels.h), so every operand
+// load is one contiguous 1 KB wave access; that configuration pools in one
+// launch that stages blocks through LDS so the packed writes stay contiguous.
 #include "common.h"
 #include "kernels.h"
 
@@ -192,12 +192,10 @@ hipError_t launch_pack(const PackJob* jobs, int njobs, long long bh, int n, int 
   const long long nblk = cpb >= 1024 ? 1 : 1024 / cpb;
   const long long wgs = (nblocks + nblk - 1) / nblk;
   const dim3 g((unsigned)(wgs < 65536 ? wgs : 65536), (unsigned)njobs);
-#define MRA_PACK(DT_, D_) pool_pack_kernel<DT_, D_><<<g, 256, 0, stream>>>(J, nblocks)
-  if (dtype == BF16) {
-    if (d == 32) MRA_PACK(BF16, 32); else if (d == 64) MRA_PACK(BF16, 64); else MRA_PACK(BF16, 128);
-  } else {
-    if (d == 32) MRA_PACK(F32, 32); else if (d == 64) MRA_PACK(F32, 64); else MRA_PACK(F32, 128);
-  }
+  // only float32 passes read packed copies (bfloat16 tiles are read raw)
+  if (dtype != F32) return hipErrorInvalidValue;
+#define MRA_PACK(D_) pool_pack_kernel<F32, D_><<<g, 256, 0, stream>>>(J, nblocks)
+  if (d == 32) MRA_PACK(32); else if (d == 64) MRA_PACK(64); else MRA_PACK(128);
 #undef MRA_PACK
   return hipGetLastError();
 }
