@@ -86,6 +86,11 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
   return (uint64_t(1) << lane_id()) - 1;
 }
 
+// Number of set bits of m below this lane (two mbcnt instructions).
+__device__ __forceinline__ int bits_below(uint64_t m) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
 // Order-preserving map of a float's bits to uint32 (larger float -> larger
 // key). -0.0 is mapped like +0.0 so the two rank equal.
 __device__ __forceinline__ uint32_t ordered_key(float s) {
