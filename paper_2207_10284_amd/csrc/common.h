@@ -20,6 +20,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
   return __uint_as_float(bits16 << 16);
@@ -85,6 +86,23 @@ __device__ __forceinline__ float wave_sum(float v) {
 __device__ __forceinline__ uint64_t lanemask_lt() {
   return (uint64_t(1) << lane_id()) - 1;
 }
+
+// A raw buffer resource for `bytes` bytes from `base` (stride 0, 32-bit
+// data format). A buffer load returns zero where its vector plus immediate
+// offset is at or past `bytes`; the scalar offset is not range-checked.
+__device__ __forceinline__ i32x4 buffer_rsrc(const void* base, unsigned bytes) {
+  const unsigned long long a = (unsigned long long)base;
+  i32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane((int)(unsigned)a);
+  r[1] = __builtin_amdgcn_readfirstlane((int)((a >> 32) & 0xffffu));   // stride 0
+  r[2] = __builtin_amdgcn_readfirstlane((int)bytes);                    // byte range
+  r[3] = 0x00020000;                                                    // 32-bit data format (gfx9)
+  return r;
+}
+
+// One float at byte voffset + soffset of the buffer (zero past its range).
+__device__ float mra_raw_buffer_load_f32(i32x4 rsrc, int voffset, int soffset,
+                                         int aux) __asm("llvm.amdgcn.raw.buffer.load.f32");
 
 // Number of set bits of m below this lane (two mbcnt instructions).
 __device__ __forceinline__ int bits_below(uint64_t m) {

@@ -98,14 +98,21 @@ __global__ __launch_bounds__(kRows / RPW * kWave) void rows_kernel(
   const int ar = lane & 15, ak = lane >> 4;
   constexpr int ldc = rows_ldc(JMAX), BPW = 2 * JMAX / KQ;            // batches per wave
   static_assert(BPW * KQ == 2 * JMAX, "whole batches");
-  const float* vcol = vp + bh * (long long)nb * D + 16 * nt + ar;
   float ba[kU];
-  // V~ rows of this wave's batch u: blocks 32 (kq + KQ u) + 8 ak + e, e < kU
-  // (rows past nb are read at nb - 1; their weights are zero)
+  // V~ rows of this wave's batch u: blocks 32 (kq + KQ u) + 8 ak + e, e < kU,
+  // as buffer loads from the head's V~ (one lane offset per batch, the steps
+  // in the immediate offset; rows past nb read as zero, and their weights are
+  // zero too)
+  i32x4 vrs = {0, 0, 0, 0};
+  int vlane = 0;
+  if constexpr (MODE == kFused || MODE == kTermOnly) {
+    vrs = buffer_rsrc(vp + bh * (long long)nb * D, (unsigned)nb * D * (unsigned)sizeof(float));
+    vlane = ((4 * kU * kq + kU * ak) * D + 16 * nt + ar) * (int)sizeof(float);
+  }
   auto load_b = [&](int u, float (&b)[kU]) {
-    const int y0 = 4 * kU * (kq + KQ * u) + kU * ak;
+    const int vo = vlane + u * (4 * kU * KQ * D * (int)sizeof(float));
 #pragma unroll
-    for (int e = 0; e < kU; ++e) b[e] = vcol[min(y0 + e, nb - 1) * D];
+    for (int e = 0; e < kU; ++e) b[e] = mra_raw_buffer_load_f32(vrs, vo + e * D * (int)sizeof(float), 0, 0);
   };
   if constexpr ((MODE == kFused || MODE == kTermOnly) && kEarlyB) load_b(0, ba);
 

@@ -201,20 +201,9 @@ __device__ __forceinline__ int raw_copy_offset(int i, int lane) {
 // bounds only because every caller validates the block it copies first (the
 // tile passes take only block ids in [0, nb), filtered when the selection is
 // staged); the resource's size is not a safety net for the scalar offset.
-typedef int i32x4 __attribute__((ext_vector_type(4)));
 __device__ void mra_raw_buffer_load_lds(i32x4 rsrc, __attribute__((address_space(3))) void* lds, int size,
                                         int voffset, int soffset, int offset,
                                         int aux) __asm("llvm.amdgcn.raw.buffer.load.lds");
-
-__device__ __forceinline__ i32x4 buffer_rsrc(const void* base, unsigned bytes) {
-  const unsigned long long a = (unsigned long long)base;
-  i32x4 r;
-  r[0] = __builtin_amdgcn_readfirstlane((int)(unsigned)a);
-  r[1] = __builtin_amdgcn_readfirstlane((int)((a >> 32) & 0xffffu));   // stride 0
-  r[2] = __builtin_amdgcn_readfirstlane((int)bytes);                    // byte range
-  r[3] = 0x00020000;                                                    // 32-bit data format (gfx9)
-  return r;
-}
 
 __device__ __forceinline__ void buffer_load_lds16(i32x4 rsrc, __attribute__((address_space(3))) char* dst,
                                                   unsigned voff, unsigned soff) {
