@@ -193,16 +193,20 @@ __global__ __launch_bounds__(kBwdRows * kWave) __attribute__((amdgpu_waves_per_e
   if constexpr (!COARSE) return;
   __syncthreads();                                          // Q~, G^, rowm, rowd, bitmaps
 
-  const float* kh = kp + bh * (long long)nb * D;
-  const float* vh = vp + bh * (long long)nb * D;
+  // K~, V~ of the head as buffers: loads past row nb read as zero
+  const unsigned hbytes = (unsigned)nb * D * (unsigned)sizeof(float);
+  const i32x4 krs = buffer_rsrc(kp + bh * (long long)nb * D, hbytes);
+  const i32x4 vrs = buffer_rsrc(vp + bh * (long long)nb * D, hbytes);
   const int lr = lane & 15, lg = lane >> 4;
   const int kind = w >> 3, t = w & 7;                       // step 1: S~ (0) or G^V~^T (1), columns 16t..
   const float* arow = (kind ? Gx : Qx) + lr * PQ + 4 * lg;
-  const float* bsrc = kind ? vh : kh;
+  const i32x4 brs = kind ? vrs : krs;
   const int nt = w % NTD, kq = w / NTD;                     // step 3: dims 16nt.., columns kq*YK..
+  const int b1lane = ((16 * t + lr) * D + 4 * lg) * (int)sizeof(float);
+  const int b3lane = ((kq * YK + lg) * D + 16 * nt + lr) * (int)sizeof(float);
   f32x4 accq = {0.0f, 0.0f, 0.0f, 0.0f};
   for (int y0 = 0; y0 < nb; y0 += YC) {
-    const int yb = y0 + 16 * t + lr;
+    const int ystep = y0 * D * (int)sizeof(float);
     f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
     constexpr int UG = D / 16 < 4 ? D / 16 : 4;             // 16-byte loads in flight per group
 #pragma unroll
@@ -210,8 +214,7 @@ __global__ __launch_bounds__(kBwdRows * kWave) __attribute__((amdgpu_waves_per_e
       f32x4 bq[UG];
 #pragma unroll
       for (int u = 0; u < UG; ++u)
-        bq[u] = yb < nb ? *reinterpret_cast<const f32x4*>(bsrc + (long long)yb * D + 16 * (u0 + u) + 4 * lg)
-                        : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        bq[u] = mra_raw_buffer_load_f32x4(brs, b1lane + ystep + 16 * (u0 + u) * (int)sizeof(float), 0, 0);
 #pragma unroll
       for (int u = 0; u < UG; ++u) {
         const f32x4 a = *reinterpret_cast<const f32x4*>(arow + 16 * (u0 + u));
@@ -241,8 +244,8 @@ __global__ __launch_bounds__(kBwdRows * kWave) __attribute__((amdgpu_waves_per_e
     __syncthreads();
 #pragma unroll
     for (int s = 0; s < YK / 4; ++s) {
-      const int yl = kq * YK + 4 * s + lg, y = y0 + yl;
-      const float b = y < nb ? kh[(long long)y * D + 16 * nt + lr] : 0.0f;
+      const int yl = kq * YK + 4 * s + lg;
+      const float b = mra_raw_buffer_load_f32(krs, b3lane + ystep + 4 * s * D * (int)sizeof(float), 0, 0);
       accq = mfma16x4(Ds[lr * PD + yl], b, accq);
     }
   }
@@ -265,6 +268,8 @@ __global__ __launch_bounds__(kBwdRows * kWave) __attribute__((amdgpu_waves_per_e
 // 16 column blocks per workgroup on the float32 matrix cores; one output tile
 // (quantity, 16 dims) per wave and step, the contraction over the block-rows
 // x in ascending order, four per matrix-core step.
+constexpr int kColsBatch = 8;
+
 template <int D>
 struct ColsCfg {
   static constexpr int kTiles = 2 * (D / 16);
@@ -289,15 +294,26 @@ __global__ __launch_bounds__(ColsCfg<D>::kWaves * kWave) void bwd_cols_kernel(
 #pragma unroll
   for (int tp = 0; tp < TPW; ++tp) {
     const int tile = w * TPW + tp, kind = tile / NTD, nt = tile % NTD;
-    const float* A = kind ? W : dS;                         // A[y][x] = A[x * nb + y] (column y)
-    const float* B = (kind ? gh : qp) + 16 * nt + lr;
+    // A[y][x] = A[x * nb + y] (column y) and B[x][16 nt + lr] of the head as
+    // buffers: reads past the head's last row or column come back as zero
+    // (those columns' outputs are not stored)
+    const i32x4 ars = buffer_rsrc((kind ? W : dS) + hb * nb, (unsigned)nb * nb * (unsigned)sizeof(float));
+    const i32x4 brs = buffer_rsrc((kind ? gh : qp) + hb * D, (unsigned)nb * D * (unsigned)sizeof(float));
+    int ao = (lg * nb + y) * (int)sizeof(float), bo = (lg * D + 16 * nt + lr) * (int)sizeof(float);
     f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll 8
-    for (int xs = 0; xs < nb; xs += 4) {
-      const int x = xs + lg;
-      const float a = (x < nb && y < nb) ? A[(hb + x) * nb + y] : 0.0f;
-      const float b = x < nb ? B[(hb + x) * D] : 0.0f;
-      acc = mfma16x4(a, b, acc);
+    // kColsBatch steps of four block-rows per batch, every load of a batch in
+    // flight before its products (rows past nb read as zero)
+    for (int xs = 0; xs < nb; xs += 4 * kColsBatch) {
+      float a[kColsBatch], b[kColsBatch];
+#pragma unroll
+      for (int u = 0; u < kColsBatch; ++u) {
+        a[u] = mra_raw_buffer_load_f32(ars, ao + u * 4 * nb * (int)sizeof(float), 0, 0);
+        b[u] = mra_raw_buffer_load_f32(brs, bo + u * 4 * D * (int)sizeof(float), 0, 0);
+      }
+#pragma unroll
+      for (int u = 0; u < kColsBatch; ++u) acc = mfma16x4(a[u], b[u], acc);
+      ao += 4 * kColsBatch * nb * (int)sizeof(float);
+      bo += 4 * kColsBatch * D * (int)sizeof(float);
     }
     float* out = kind ? dvp : dkp;
     const float f = kind ? 1.0f : scale;

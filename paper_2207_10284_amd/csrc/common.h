@@ -100,9 +100,12 @@ __device__ __forceinline__ i32x4 buffer_rsrc(const void* base, unsigned bytes) {
   return r;
 }
 
-// One float at byte voffset + soffset of the buffer (zero past its range).
+// One float (four floats) at byte voffset + soffset of the buffer (zero past
+// its range).
 __device__ float mra_raw_buffer_load_f32(i32x4 rsrc, int voffset, int soffset,
                                          int aux) __asm("llvm.amdgcn.raw.buffer.load.f32");
+__device__ f32x4 mra_raw_buffer_load_f32x4(i32x4 rsrc, int voffset, int soffset,
+                                           int aux) __asm("llvm.amdgcn.raw.buffer.load.v4f32");
 
 // Number of set bits of m below this lane (two mbcnt instructions).
 __device__ __forceinline__ int bits_below(uint64_t m) {
