@@ -327,6 +327,9 @@ __global__ __launch_bounds__(ColsCfg<D>::kWaves * kWave) void bwd_cols_kernel(
 
 // Stores a 32 x D block from d-major tiles acc (lane: row j; register r of
 // tile t: dim 32t + 8(r/4) + 4h + r%4) as acc * a + (add ? add[dim] / 32 : 0).
+// The add terms are loaded first, all at once. bfloat16: lanes l and l^32
+// hold dims 4h..4h+3 of the groups rg (even, odd); they exchange one group so
+// that each stores 8 contiguous dims (16 bytes).
 template <int DT, int D>
 __device__ __forceinline__ void store_block(typename TileCfg<DT, D>::elem* dst,
                                             const f32x16 (&acc)[D / 32], float a,
@@ -335,24 +338,40 @@ __device__ __forceinline__ void store_block(typename TileCfg<DT, D>::elem* dst,
   const int lane = lane_id(), j = lane & 31, h = lane >> 5;
   auto* row = dst + (long long)j * D;
   constexpr float inv = 1.0f / kBlock;
+  f32x4 c4[NT][4];
 #pragma unroll
   for (int t = 0; t < NT; ++t)
 #pragma unroll
+    for (int rg = 0; rg < 4; ++rg)
+      c4[t][rg] = add != nullptr ? *reinterpret_cast<const f32x4*>(add + 32 * t + 8 * rg + 4 * h)
+                                 : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    u32x2 pend = {0u, 0u};
+#pragma unroll
     for (int rg = 0; rg < 4; ++rg) {
       const int d0 = 32 * t + 8 * rg + 4 * h;
-      f32x4 c4 = {0.0f, 0.0f, 0.0f, 0.0f};
-      if (add != nullptr) c4 = *reinterpret_cast<const f32x4*>(add + d0);
       float z[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) z[e] = fmaf(acc[t][4 * rg + e], a, c4[e] * inv);
+      for (int e = 0; e < 4; ++e) z[e] = fmaf(acc[t][4 * rg + e], a, c4[t][rg][e] * inv);
       if constexpr (DT == BF16) {
         const u32x2 pr = {pack_bf16x2(z[0], z[1]), pack_bf16x2(z[2], z[3])};
-        *reinterpret_cast<u32x2*>(row + d0) = pr;
+        if ((rg & 1) == 0) {
+          pend = pr;
+        } else {
+          const u32x2 send = h ? pend : pr;                 // h = 0 sends its odd group, h = 1 its even one
+          u32x2 recv;
+          recv[0] = (uint32_t)__shfl_xor((int)send[0], 32);
+          recv[1] = (uint32_t)__shfl_xor((int)send[1], 32);
+          const u32x4 st = h ? u32x4{recv[0], recv[1], pr[0], pr[1]} : u32x4{pend[0], pend[1], recv[0], recv[1]};
+          *reinterpret_cast<u32x4*>(row + 32 * t + 8 * (rg - 1) + 8 * h) = st;
+        }
       } else {
         const f32x4 st = {z[0], z[1], z[2], z[3]};
         *reinterpret_cast<f32x4*>(row + d0) = st;
       }
     }
+  }
 }
 
 // bfloat16 pairs of 16 float32 values in register order (the B operand of
@@ -954,6 +973,20 @@ struct RawTrB {
   }
 };
 
+// The D floats at src (a block's coarse-term gradient, added by the
+// epilogue) into LDS at dst with direct-to-LDS dword loads, 256 bytes per
+// load (lanes past D read zero), so their latency passes during the tiles;
+// the callers' waits for their tile copies (or the one before the epilogue)
+// complete them.
+template <int D>
+__device__ __forceinline__ void prefetch_vec_lds(const float* src, lptr_t dst) {
+  const i32x4 rs = buffer_rsrc(src, (unsigned)D * (unsigned)sizeof(float));
+  const int lane = lane_id();
+#pragma unroll
+  for (int p = 0; p < (D + 63) / 64; ++p) mra_raw_buffer_load_lds(rs, dst + 256 * p, 4, (lane + 64 * p) * 4, 0, 0, 0);
+}
+constexpr int add_lds_floats(int d) { return d < 64 ? 64 : d; }
+
 // dQ (bf16, d <= 64): one wave per block-row; a slot holds the raw tiles K_y
 // and V_y (K^T is read transposed from the K tile). SLOTS tiles in flight per
 // wave: with one slot the next tile is copied once the current one is in
@@ -973,12 +1006,14 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dq_tr_kernel(
   static_assert(KC == R::KC && KC <= 4 && VC <= 4, "raw tiles of d <= 64");
   static_assert(SLOTS == 1 || SLOTS == 2, "tiles in flight per wave");
   __shared__ __attribute__((aligned(16))) unsigned char slots[WAVES][SLOTS][SLOT];
+  __shared__ __attribute__((aligned(16))) float addl[WAVES][COARSE ? add_lds_floats(D) : 1];
   extern __shared__ int32_t sidx_all[];
   const int w = wave_uniform(threadIdx.x / kWave);
   const int lane = lane_id(), jq = lane & 31;
   const long long g = xcd_remap(blockIdx.x, gridDim.x) * (long long)WAVES + w;
   if (g >= rows) return;                                    // no workgroup barriers below
   const long long bh = g / nb;
+  if constexpr (COARSE) prefetch_vec_lds<D>(dqp + g * D, (lptr_t)addl[w]);
   int32_t* myidx = sidx_all + w * m;
   const int cnt = stage_selection(idx + g * m, m, nb, myidx);
 
@@ -1026,8 +1061,8 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dq_tr_kernel(
     pack16(ds, pk);
     mfma_acc_bf16<NT>(acc, pk, [&](int c) { return tf[c]; });
   }
-  store_block<BF16, D>(reinterpret_cast<elem*>(dq) + g * 32 * D, acc, scale,
-                       COARSE ? dqp + g * D : nullptr);
+  wait_loads<0>();
+  store_block<BF16, D>(reinterpret_cast<elem*>(dq) + g * 32 * D, acc, scale, COARSE ? addl[w] : nullptr);
 }
 
 // dK, dV (bf16, d <= 64): one wave per column block; a slot holds the raw
@@ -1054,12 +1089,17 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dkdv_tr_kernel(
   static_assert(KC == R::KC && KC <= 4 && VC <= 4, "raw tiles of d <= 64");
   static_assert(SLOTS == 1 || SLOTS == 2, "tiles in flight per wave");
   __shared__ __attribute__((aligned(16))) unsigned char slots[WAVES][SLOTS][SLOT];
+  __shared__ __attribute__((aligned(16))) float addl[WAVES][2][COARSE ? add_lds_floats(D) : 1];
   extern __shared__ int32_t sidx_all[];
   const int w = wave_uniform(threadIdx.x / kWave);
   const int lane = lane_id();
   const long long gy = xcd_remap(blockIdx.x, gridDim.x) * (long long)WAVES + w;
   if (gy >= rows) return;                                   // no workgroup barriers below
   const long long bh = gy / nb;
+  if constexpr (COARSE) {
+    prefetch_vec_lds<D>(dkp + gy * D, (lptr_t)addl[w][0]);
+    prefetch_vec_lds<D>(dvp + gy * D, (lptr_t)addl[w][1]);
+  }
   const int y = (int)(gy - bh * nb);
   const long long hb = bh * nb;
   const int nbw = (nb + 31) / 32;
@@ -1136,10 +1176,9 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dkdv_tr_kernel(
     mfma_acc_bf16<NT>(av, pa8, [&](int c) { return gtc[c]; });
     mfma_acc_bf16<NT>(ak, pd8, [&](int c) { return qt[c]; });
   }
-  store_block<BF16, D>(reinterpret_cast<elem*>(dk) + gy * 32 * D, ak, scale,
-                       COARSE ? dkp + gy * D : nullptr);
-  store_block<BF16, D>(reinterpret_cast<elem*>(dv) + gy * 32 * D, av, 1.0f,
-                       COARSE ? dvp + gy * D : nullptr);
+  wait_loads<0>();
+  store_block<BF16, D>(reinterpret_cast<elem*>(dk) + gy * 32 * D, ak, scale, COARSE ? addl[w][0] : nullptr);
+  store_block<BF16, D>(reinterpret_cast<elem*>(dv) + gy * 32 * D, av, 1.0f, COARSE ? addl[w][1] : nullptr);
 }
 
 // bfloat16, d = 128: raw 8 KB tiles of 32 rows x 256 bytes under the same
@@ -1166,12 +1205,14 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dq_tr128_kernel(
   constexpr int TB = R::TB;
   static_assert(KC == R::KC && VC == KC, "row and transposed chunks of a tile");
   __shared__ __attribute__((aligned(16))) unsigned char slots[WAVES][2 * TB];
+  __shared__ __attribute__((aligned(16))) float addl[WAVES][COARSE ? D : 1];
   extern __shared__ int32_t sidx_all[];
   const int w = wave_uniform(threadIdx.x / kWave);
   const int lane = lane_id(), jq = lane & 31;
   const long long g = xcd_remap(blockIdx.x, gridDim.x) * (long long)WAVES + w;
   if (g >= rows) return;                                    // no workgroup barriers below
   const long long bh = g / nb;
+  if constexpr (COARSE) prefetch_vec_lds<D>(dqp + g * D, (lptr_t)addl[w]);
   int32_t* myidx = sidx_all + w * m;
   const int cnt = stage_selection(idx + g * m, m, nb, myidx);
 
@@ -1215,8 +1256,8 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dq_tr128_kernel(
     pack16(ds, pk);
     mfma_acc_bf16<NT>(acc, pk, [&](int c) { return op[c]; });
   }
-  store_block<BF16, D>(reinterpret_cast<elem*>(dq) + g * 32 * D, acc, scale,
-                       COARSE ? dqp + g * D : nullptr);
+  wait_loads<0>();
+  store_block<BF16, D>(reinterpret_cast<elem*>(dq) + g * 32 * D, acc, scale, COARSE ? addl[w] : nullptr);
 }
 
 // dK, dV (bf16, d = 128): one wave per column block, two slots (raw Q_x, G_x
@@ -1239,11 +1280,16 @@ __global__ __launch_bounds__(kWave) void bwd_dkdv_tr128_kernel(
   constexpr int SLOT = 2 * TB + RB;
   static_assert(KC == R::KC && VC == KC, "row and transposed chunks of a tile");
   __shared__ __attribute__((aligned(16))) unsigned char slots[2][SLOT];
+  __shared__ __attribute__((aligned(16))) float addl[2][COARSE ? D : 1];
   extern __shared__ int32_t sidx_all[];
   const int lane = lane_id();
   const long long gy = xcd_remap(blockIdx.x, gridDim.x);
   if (gy >= rows) return;
   const long long bh = gy / nb;
+  if constexpr (COARSE) {
+    prefetch_vec_lds<D>(dkp + gy * D, (lptr_t)addl[0]);
+    prefetch_vec_lds<D>(dvp + gy * D, (lptr_t)addl[1]);
+  }
   const int y = (int)(gy - bh * nb);
   const long long hb = bh * nb;
   const int nbw = (nb + 31) / 32;
@@ -1318,10 +1364,9 @@ __global__ __launch_bounds__(kWave) void bwd_dkdv_tr128_kernel(
     if (i + 2 < cnt) issue(wave_uniform(myx[i + 2]), i & 1);   // the slot has been read
     mfma_acc_bf16<NT>(av, pa8, [&](int c) { return op[c]; });
   }
-  store_block<BF16, D>(reinterpret_cast<elem*>(dk) + gy * 32 * D, ak, scale,
-                       COARSE ? dkp + gy * D : nullptr);
-  store_block<BF16, D>(reinterpret_cast<elem*>(dv) + gy * 32 * D, av, 1.0f,
-                       COARSE ? dvp + gy * D : nullptr);
+  wait_loads<0>();
+  store_block<BF16, D>(reinterpret_cast<elem*>(dk) + gy * 32 * D, ak, scale, COARSE ? addl[0] : nullptr);
+  store_block<BF16, D>(reinterpret_cast<elem*>(dv) + gy * 32 * D, av, 1.0f, COARSE ? addl[1] : nullptr);
 }
 
 // ---------------------------------------------------------------------------
