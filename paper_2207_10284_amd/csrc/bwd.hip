@@ -265,24 +265,43 @@ __global__ __launch_bounds__(kBwdRows * kWave) __attribute__((amdgpu_waves_per_e
 
 // ---------------------------------------------------------------------------
 // Column pass: dK~_y = c sum_x dS~[x,y] Q~_x and dV~_y = sum_x W[x,y] G^_x for
-// 16 column blocks per workgroup on the float32 matrix cores; one output tile
-// (quantity, 16 dims) per wave and step, the contraction over the block-rows
-// x in ascending order, four per matrix-core step.
-constexpr int kColsBatch = 8;
+// 16 column blocks per workgroup on the float32 matrix cores, the contraction
+// over the block-rows x in ascending order, four per matrix-core step. A wave
+// takes one quantity and TW = min(4, D/16) dim tiles at once, with the dims
+// permuted inside its group of 16 TW: tile t, column n is dim 16 TW g +
+// TW n + t, so each lane reads its TW consecutive dims of a row of Q~ or G^
+// with one load (and stores its TW dims of an output row with one store),
+// and the column of W or dS serves all TW products.
+constexpr int kColsBatch = 8;                             // matrix-core steps per batch of loads
 
 template <int D>
 struct ColsCfg {
-  static constexpr int kTiles = 2 * (D / 16);
-  static constexpr int kWaves = kTiles < 8 ? kTiles : 8;
-  static constexpr int kTilesPerWave = kTiles / kWaves;
+  static constexpr int kTW = D / 16 < 4 ? D / 16 : 4;      // dim tiles per wave
+  static constexpr int kGroups = D / (16 * kTW);            // dim groups
+  static constexpr int kWaves = 2 * kGroups;                // (quantity, group) per wave
 };
+
+template <int TW>
+__device__ __forceinline__ void load_tw(i32x4 rs, int off, float (&b)[TW]) {
+  if constexpr (TW == 4) {
+    const f32x4 v = mra_raw_buffer_load_f32x4(rs, off, 0, 0);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) b[t] = v[t];
+  } else if constexpr (TW == 2) {
+    const f32x2 v = mra_raw_buffer_load_f32x2(rs, off, 0, 0);
+    b[0] = v[0];
+    b[1] = v[1];
+  } else {
+    b[0] = mra_raw_buffer_load_f32(rs, off, 0, 0);
+  }
+}
 
 template <int D>
 __global__ __launch_bounds__(ColsCfg<D>::kWaves * kWave) void bwd_cols_kernel(
     const float* __restrict__ qp, const float* __restrict__ gh, const float* __restrict__ W,
     const float* __restrict__ dS, float* __restrict__ dkp, float* __restrict__ dvp, int nb,
     float scale) {
-  constexpr int NTD = D / 16, TPW = ColsCfg<D>::kTilesPerWave;
+  constexpr int TW = ColsCfg<D>::kTW;
   const int w = wave_uniform(threadIdx.x / kWave);
   const int lane = lane_id(), lr = lane & 15, lg = lane >> 4;
   const int groups = (nb + kBwdCols - 1) / kBwdCols;
@@ -291,36 +310,46 @@ __global__ __launch_bounds__(ColsCfg<D>::kWaves * kWave) void bwd_cols_kernel(
   const int y0 = (int)(lwg - bh * groups) * kBwdCols;
   const long long hb = bh * nb;                             // first block of the head
   const int y = y0 + lr;
+  const int kind = w / ColsCfg<D>::kGroups, dg = w % ColsCfg<D>::kGroups;
+  const int d0 = 16 * TW * dg + TW * lr;                    // this lane's first dim
+  // A[y][x] = A[x * nb + y] (column y) and B[x][d0 ..] of the head as
+  // buffers: reads past the head's last row or column come back as zero
+  // (those columns' outputs are not stored)
+  const i32x4 ars = buffer_rsrc((kind ? W : dS) + hb * nb, (unsigned)nb * nb * (unsigned)sizeof(float));
+  const i32x4 brs = buffer_rsrc((kind ? gh : qp) + hb * D, (unsigned)nb * D * (unsigned)sizeof(float));
+  int ao = (lg * nb + y) * (int)sizeof(float), bo = (lg * D + d0) * (int)sizeof(float);
+  f32x4 acc[TW];
 #pragma unroll
-  for (int tp = 0; tp < TPW; ++tp) {
-    const int tile = w * TPW + tp, kind = tile / NTD, nt = tile % NTD;
-    // A[y][x] = A[x * nb + y] (column y) and B[x][16 nt + lr] of the head as
-    // buffers: reads past the head's last row or column come back as zero
-    // (those columns' outputs are not stored)
-    const i32x4 ars = buffer_rsrc((kind ? W : dS) + hb * nb, (unsigned)nb * nb * (unsigned)sizeof(float));
-    const i32x4 brs = buffer_rsrc((kind ? gh : qp) + hb * D, (unsigned)nb * D * (unsigned)sizeof(float));
-    int ao = (lg * nb + y) * (int)sizeof(float), bo = (lg * D + 16 * nt + lr) * (int)sizeof(float);
-    f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-    // kColsBatch steps of four block-rows per batch, every load of a batch in
-    // flight before its products (rows past nb read as zero)
-    for (int xs = 0; xs < nb; xs += 4 * kColsBatch) {
-      float a[kColsBatch], b[kColsBatch];
+  for (int t = 0; t < TW; ++t) acc[t] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  // kColsBatch steps of four block-rows per batch, every load of a batch in
+  // flight before its products (rows past nb read as zero)
+  for (int xs = 0; xs < nb; xs += 4 * kColsBatch) {
+    float a[kColsBatch], b[kColsBatch][TW];
 #pragma unroll
-      for (int u = 0; u < kColsBatch; ++u) {
-        a[u] = mra_raw_buffer_load_f32(ars, ao + u * 4 * nb * (int)sizeof(float), 0, 0);
-        b[u] = mra_raw_buffer_load_f32(brs, bo + u * 4 * D * (int)sizeof(float), 0, 0);
-      }
-#pragma unroll
-      for (int u = 0; u < kColsBatch; ++u) acc = mfma16x4(a[u], b[u], acc);
-      ao += 4 * kColsBatch * nb * (int)sizeof(float);
-      bo += 4 * kColsBatch * D * (int)sizeof(float);
+    for (int u = 0; u < kColsBatch; ++u) {
+      a[u] = mra_raw_buffer_load_f32(ars, ao + u * 4 * nb * (int)sizeof(float), 0, 0);
+      load_tw<TW>(brs, bo + u * 4 * D * (int)sizeof(float), b[u]);
     }
-    float* out = kind ? dvp : dkp;
-    const float f = kind ? 1.0f : scale;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int yy = y0 + 4 * lg + r;
-      if (yy < nb) out[(hb + yy) * D + 16 * nt + lr] = acc[r] * f;
+    for (int u = 0; u < kColsBatch; ++u)
+#pragma unroll
+      for (int t = 0; t < TW; ++t) acc[t] = mfma16x4(a[u], b[u][t], acc[t]);
+    ao += 4 * kColsBatch * nb * (int)sizeof(float);
+    bo += 4 * kColsBatch * D * (int)sizeof(float);
+  }
+  // lane: rows y0 + 4 lg + r, dims d0 + t
+  float* out = kind ? dvp : dkp;
+  const float f = kind ? 1.0f : scale;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int yy = y0 + 4 * lg + r;
+    if (yy >= nb) continue;
+    float* o = out + (hb + yy) * D + d0;
+    if constexpr (TW == 4) {
+      *reinterpret_cast<f32x4*>(o) = f32x4{acc[0][r] * f, acc[1][r] * f, acc[2][r] * f, acc[3][r] * f};
+    } else {
+#pragma unroll
+      for (int t = 0; t < TW; ++t) o[t] = acc[t][r] * f;
     }
   }
 }

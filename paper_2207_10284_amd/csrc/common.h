@@ -106,6 +106,9 @@ __device__ float mra_raw_buffer_load_f32(i32x4 rsrc, int voffset, int soffset,
                                          int aux) __asm("llvm.amdgcn.raw.buffer.load.f32");
 __device__ f32x4 mra_raw_buffer_load_f32x4(i32x4 rsrc, int voffset, int soffset,
                                            int aux) __asm("llvm.amdgcn.raw.buffer.load.v4f32");
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+__device__ f32x2 mra_raw_buffer_load_f32x2(i32x4 rsrc, int voffset, int soffset,
+                                           int aux) __asm("llvm.amdgcn.raw.buffer.load.v2f32");
 
 // Number of set bits of m below this lane (two mbcnt instructions).
 __device__ __forceinline__ int bits_below(uint64_t m) {
