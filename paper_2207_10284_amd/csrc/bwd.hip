@@ -92,7 +92,7 @@ __device__ __forceinline__ u32x4 bias_operand(float x, float y) {
 //  3. dQ~_x += dS~ K~_y: wave (dim tile, part of the step's columns), the
 //     partial sums added in part order at the end.
 template <int DT, int D, bool COARSE>
-__global__ __launch_bounds__(kBwdRows * kWave) __attribute__((amdgpu_waves_per_eu(D <= 64 ? 8 : 1, 8))) void bwd_rows_kernel(
+__global__ __launch_bounds__(kBwdRows * kWave) __attribute__((amdgpu_waves_per_eu(8, 8))) void bwd_rows_kernel(
     const void* __restrict__ gin, const void* __restrict__ zin, const float* __restrict__ lse,
     const int32_t* __restrict__ idx, const float* __restrict__ qp, const float* __restrict__ kp,
     const float* __restrict__ vp, float* __restrict__ ld, uint32_t* __restrict__ bias,
