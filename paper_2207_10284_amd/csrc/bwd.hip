@@ -979,6 +979,13 @@ __device__ __forceinline__ void copy_raw_pair_buf(i32x4 ra, i32x4 rb, unsigned t
   }
 }
 
+// One raw tile, C 1 KB copies, as buffer loads to LDS (as copy_raw_pair_buf).
+template <int C, int KP>
+__device__ __forceinline__ void copy_raw_buf(i32x4 rs, unsigned t, const unsigned (&cp)[KP], lptr_t dst) {
+#pragma unroll
+  for (int i = 0; i < C; ++i) buffer_load_lds16(rs, dst + i * 1024, cp[i % KP], t + i * 1024);
+}
+
 // Row-layout chunks of the raw tile at base + OFF.
 template <int OFF, int KC>
 __device__ __forceinline__ void raw_rows(uint32_t base, const uint32_t (&rr)[KC], u32x4 (&v)[KC]) {
@@ -1260,23 +1267,33 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dq_tr128_kernel(
   const i32x4 krs = buffer_rsrc(static_cast<const char*>(kin) + (size_t)bh * nb * TB, (unsigned)nb * TB);
   const i32x4 vrs = buffer_rsrc(static_cast<const char*>(vin) + (size_t)bh * nb * TB, (unsigned)nb * TB);
   const uint32_t base = lds_addr(slots[w]);
-  auto issue = [&](int y) {
-    const lptr_t dst = (lptr_t)slots[w];
-    copy_raw_pair_buf<KC, R::KP>(krs, vrs, (unsigned)y * TB, (unsigned)y * TB, ro.cp, dst, dst + TB);
-  };
-  if (cnt > 0) issue(wave_uniform(myidx[0]));
+  const lptr_t kdst = (lptr_t)slots[w], vdst = kdst + TB;
+  // the slot's halves are refilled separately: V_y's as soon as its rows are
+  // read (they are read first), K_y's once its rows and K_y^T are read
+  if (cnt > 0) {
+    const int y = wave_uniform(myidx[0]);
+    copy_raw_buf<KC, R::KP>(vrs, (unsigned)y * TB, ro.cp, vdst);
+    copy_raw_buf<KC, R::KP>(krs, (unsigned)y * TB, ro.cp, kdst);
+  }
   for (int i = 0; i < cnt; ++i) {
-    wait_loads<0>();
+    wait_loads<KC>();                                       // V_y landed (K_y may be in flight)
+    const int yn = i + 1 < cnt ? wave_uniform(myidx[i + 1]) : 0;
     u32x4 op[KC];
+    raw_rows<TB>(base, ro.rr, op);                          // V_y rows
+    lds_done(op);
+    if (i + 1 < cnt) {
+      copy_raw_buf<KC, R::KP>(vrs, (unsigned)yn * TB, ro.cp, vdst);
+      wait_loads<KC>();                                     // K_y landed
+    } else {
+      wait_loads<0>();
+    }
+    const f32x16 pv = mfma_abt<BF16, KC>(op, gf);
     raw_rows<0>(base, ro.rr, op);                           // K_y rows
     lds_done(op);
     const f32x16 s = mfma_abt<BF16, KC>(op, qf);
-    raw_rows<TB>(base, ro.rr, op);                          // V_y rows
-    lds_done(op);
-    const f32x16 pv = mfma_abt<BF16, KC>(op, gf);
     RawTrB<D, 0, 0, VC>::run(base, ro.tr, op);             // K_y^T
     lds_done(op);
-    if (i + 1 < cnt) issue(wave_uniform(myidx[i + 1]));
+    if (i + 1 < cnt) copy_raw_buf<KC, R::KP>(krs, (unsigned)yn * TB, ro.cp, kdst);
     float ds[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r)
