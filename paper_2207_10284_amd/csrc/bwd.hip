@@ -1009,20 +1009,6 @@ struct RawTrB {
   }
 };
 
-// The D floats at src (a block's coarse-term gradient, added by the
-// epilogue) into LDS at dst with direct-to-LDS dword loads, 256 bytes per
-// load (lanes past D read zero), so their latency passes during the tiles;
-// the callers' waits for their tile copies (or the one before the epilogue)
-// complete them.
-template <int D>
-__device__ __forceinline__ void prefetch_vec_lds(const float* src, lptr_t dst) {
-  const i32x4 rs = buffer_rsrc(src, (unsigned)D * (unsigned)sizeof(float));
-  const int lane = lane_id();
-#pragma unroll
-  for (int p = 0; p < (D + 63) / 64; ++p) mra_raw_buffer_load_lds(rs, dst + 256 * p, 4, (lane + 64 * p) * 4, 0, 0, 0);
-}
-constexpr int add_lds_floats(int d) { return d < 64 ? 64 : d; }
-
 // dQ (bf16, d <= 64): one wave per block-row; a slot holds the raw tiles K_y
 // and V_y (K^T is read transposed from the K tile). SLOTS tiles in flight per
 // wave: with one slot the next tile is copied once the current one is in

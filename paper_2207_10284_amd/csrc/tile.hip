@@ -182,24 +182,24 @@ struct TileRow {
   // Merge with the low-resolution term, normalise and store the 32 x d block;
   // if lse is not NULL also each query's log normaliser, ln of the row sum of
   // A^ (natural units).
-  __device__ __forceinline__ void finish(elem* Out, float* lse, int x, long long g,
-                                         const float* cmax, const float* csum,
-                                         const float* cvec) {
+  // cmaxg, csumg, cv: the block-row's coarse-term maximum, sum and vector
+  // (its D floats, in LDS or global memory)
+  __device__ __forceinline__ void finish(elem* Out, float* lse, int x, long long g, float cmaxg,
+                                         float csumg, const float* cv) {
     const int lane = lane_id(), jq = lane & 31, h = lane >> 5;
     const float ltot = halves_sum(lrun);
     float af = 1.0f, bc = 0.0f, den = ltot, Mt = mrun;
     if constexpr (COARSE) {
-      const float Mx = cmax[g] * kLog2e;
+      const float Mx = cmaxg * kLog2e;
       Mt = fmaxf(mrun, Mx);
       af = exp2f(mrun - Mt);
       bc = exp2f(Mx - Mt);
-      den = ltot * af + csum[g] * bc;
+      den = ltot * af + csumg * bc;
     }
     if (lse != nullptr && h == 0) lse[g * 32 + jq] = (log2f(den) + Mt) * kLn2;
     const float inv = 1.0f / den;
     const float ao = af * inv, bv = bc * inv;       // z = o * ao + cvec * bv
     elem* orow = Out + (long long)(x * 32 + jq) * D;
-    const float* cv = COARSE ? cvec + g * D : nullptr;
     u32x2 pend = {0u, 0u};                          // bf16: the even group's 4 values
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
@@ -405,7 +405,8 @@ __global__ __launch_bounds__((TileCfg<DT, D>::kWaves * kWave)) void tile_kernel(
       pass(false);
     }
   }
-  row.finish(reinterpret_cast<elem*>(outv) + hoff, lse, x, g, cmax, csum, cvec);
+  row.finish(reinterpret_cast<elem*>(outv) + hoff, lse, x, g, COARSE ? cmax[g] : 0.0f, COARSE ? csum[g] : 0.0f,
+             COARSE ? cvec + g * D : nullptr);
 }
 
 // ---------------------------------------------------------------------------
@@ -560,6 +561,13 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
   // the slots are their own LDS object, apart from the selection lists, so
   // reading a list does not wait for loads in flight into a slot
   __shared__ __attribute__((aligned(16))) u32x4 slot_all[WAVES][SLOTS][CH * 64];
+  // Tiles of 8 KB per part (two waves per SIMD) fetch the coarse term's
+  // vector into LDS while the tiles run (its maximum and sum are loaded then
+  // too): with two waves per SIMD, reading it after the last tile exposed its
+  // latency at every row's end; at four waves per SIMD the other waves hide
+  // it, and the extra load at the row's start cost more than it saved.
+  constexpr bool kTermAhead = COARSE && D2 >= 128;
+  __shared__ __attribute__((aligned(16))) float cvl[WAVES][kTermAhead ? add_lds_floats(D) : 1];
   extern __shared__ int32_t sidx_all[];
 
   const int w = wave_uniform(threadIdx.x / kWave);
@@ -567,6 +575,12 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
   const long long wg = xcd_remap(blockIdx.x, gridDim.x);
   const long long g = row0 + wg * WAVES + w;         // global block-row (rows row0 .. rows - 1)
   if (g >= rows) return;                             // no workgroup barriers below
+  float cmaxg = 0.0f, csumg = 0.0f;
+  if constexpr (kTermAhead) {
+    prefetch_vec_lds<D>(cvec + g * D, (__attribute__((address_space(3))) char*)cvl[w]);
+    cmaxg = cmax[g];
+    csumg = csum[g];
+  }
   const long long bh = g / nb;
   const int x = (int)(g - bh * nb);
   const long long hoff = bh * (long long)n * D;
@@ -675,7 +689,13 @@ __global__ __launch_bounds__(WAVES * kWave) void tile_stream_kernel(
     row.restart(mx);
     pass(false);
   }
-  row.finish(reinterpret_cast<elem*>(outv) + hoff, lse, x, g, cmax, csum, cvec);
+  if constexpr (kTermAhead) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the coarse-term vector is in LDS
+    row.finish(reinterpret_cast<elem*>(outv) + hoff, lse, x, g, cmaxg, csumg, cvl[w]);
+  } else {
+    row.finish(reinterpret_cast<elem*>(outv) + hoff, lse, x, g, COARSE ? cmax[g] : 0.0f,
+               COARSE ? csum[g] : 0.0f, COARSE ? cvec + g * D : nullptr);
+  }
 }
 
 // ---------------------------------------------------------------------------

@@ -210,6 +210,19 @@ __device__ __forceinline__ void buffer_load_lds16(i32x4 rsrc, __attribute__((add
   mra_raw_buffer_load_lds(rsrc, dst, 16, (int)voff, (int)soff, 0, 0);
 }
 
+// The D floats at src (a block's coarse-term vector, used by an epilogue)
+// into LDS at dst with direct-to-LDS dword loads, 256 bytes per load (lanes
+// past D read zero), so their latency passes during the tiles; a wait for the
+// load counter (the tile copies' or one before the epilogue) completes them.
+template <int D>
+__device__ __forceinline__ void prefetch_vec_lds(const float* src, __attribute__((address_space(3))) char* dst) {
+  const i32x4 rs = buffer_rsrc(src, (unsigned)D * (unsigned)sizeof(float));
+  const int lane = lane_id();
+#pragma unroll
+  for (int p = 0; p < (D + 63) / 64; ++p) mra_raw_buffer_load_lds(rs, dst + 256 * p, 4, (lane + 64 * p) * 4, 0, 0, 0);
+}
+constexpr int add_lds_floats(int d) { return d < 64 ? 64 : d; }
+
 // Copies a list of m block ids into LDS keeping only the entries in [0, nb),
 // in their order, and returns how many there are (wave-uniform). Reading the
 // ids from LDS keeps them off the vector-memory counter, so prefetched loads
