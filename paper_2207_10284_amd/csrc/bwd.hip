@@ -263,6 +263,35 @@ __global__ __launch_bounds__(kBwdRows * kWave) __attribute__((amdgpu_waves_per_e
   }
 }
 
+// The block-rows x whose selection holds column block y (bit y of row x's
+// bitmap), ascending, into list (LDS); returns their count (wave-uniform).
+// The bitmap words of kColBatch groups of 64 rows are all requested before
+// the first is used (rows past nb read row nb - 1's word and are dropped).
+constexpr int kColBatch = 8;
+__device__ __forceinline__ int column_list(const uint32_t* __restrict__ bits, long long hb, int nbw, int y,
+                                           int nb, int32_t* list) {
+  const int lane = lane_id();
+  int cnt = 0;
+  for (int x0 = 0; x0 < nb; x0 += kColBatch * kWave) {
+    uint32_t wv[kColBatch];
+#pragma unroll
+    for (int u = 0; u < kColBatch; ++u) {
+      const int x = min(x0 + kWave * u + lane, nb - 1);
+      wv[u] = bits[(hb + x) * nbw + (y >> 5)];
+    }
+#pragma unroll
+    for (int u = 0; u < kColBatch; ++u) {
+      const int x = x0 + kWave * u + lane;
+      const bool ok = x < nb && ((wv[u] >> (y & 31)) & 1u);
+      const uint64_t mk = __ballot(ok);
+      if (ok) list[cnt + bits_below(mk)] = x;
+      cnt += __popcll(mk);
+    }
+  }
+  wave_lds_sync();
+  return wave_uniform(cnt);
+}
+
 // ---------------------------------------------------------------------------
 // Column pass: dK~_y = c sum_x dS~[x,y] Q~_x and dV~_y = sum_x W[x,y] G^_x for
 // 16 column blocks per workgroup on the float32 matrix cores, the contraction
@@ -529,16 +558,7 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dkdv_kernel(
 
   // block-rows whose selection holds y, ascending
   int32_t* myx = sidx_all + w * nb;
-  int cnt = 0;
-  for (int x0 = 0; x0 < nb; x0 += kWave) {
-    const int x = x0 + lane;
-    const bool ok = x < nb && ((bits[(hb + x) * nbw + (y >> 5)] >> (y & 31)) & 1u);
-    const uint64_t mk = __ballot(ok);
-    if (ok) myx[cnt + __popcll(mk & lanemask_lt())] = x;
-    cnt += __popcll(mk);
-  }
-  wave_lds_sync();
-  cnt = wave_uniform(cnt);
+  const int cnt = column_list(bits, hb, nbw, y, nb, myx);
 
   u32x4 kf[KC], vf[KC];
   load_rows<DT, D>(reinterpret_cast<const elem*>(kin) + gy * 32 * D, kf);
@@ -735,16 +755,7 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dkdv_stream_kernel(
 
   // block-rows whose selection holds y, ascending
   int32_t* myx = sidx_all + w * nb;
-  int cnt = 0;
-  for (int x0 = 0; x0 < nb; x0 += kWave) {
-    const int x = x0 + lane;
-    const bool ok = x < nb && ((bits[(hb + x) * nbw + (y >> 5)] >> (y & 31)) & 1u);
-    const uint64_t mk = __ballot(ok);
-    if (ok) myx[cnt + __popcll(mk & lanemask_lt())] = x;
-    cnt += __popcll(mk);
-  }
-  wave_lds_sync();
-  cnt = wave_uniform(cnt);
+  const int cnt = column_list(bits, hb, nbw, y, nb, myx);
 
   u32x4 kf[KC], vf[KC];
   load_rows<DT, D>(reinterpret_cast<const elem*>(kin) + gy * 32 * D, kf);
@@ -1128,16 +1139,7 @@ __global__ __launch_bounds__(WAVES * kWave) void bwd_dkdv_tr_kernel(
 
   // block-rows whose selection holds y, ascending
   int32_t* myx = sidx_all + w * nb;
-  int cnt = 0;
-  for (int x0 = 0; x0 < nb; x0 += kWave) {
-    const int x = x0 + lane;
-    const bool ok = x < nb && ((bits[(hb + x) * nbw + (y >> 5)] >> (y & 31)) & 1u);
-    const uint64_t mk = __ballot(ok);
-    if (ok) myx[cnt + __popcll(mk & lanemask_lt())] = x;
-    cnt += __popcll(mk);
-  }
-  wave_lds_sync();
-  cnt = wave_uniform(cnt);
+  const int cnt = column_list(bits, hb, nbw, y, nb, myx);
 
   u32x4 kf[KC], vf[KC];
   load_rows<BF16, D>(reinterpret_cast<const elem*>(kin) + gy * 32 * D, kf);
@@ -1328,16 +1330,7 @@ __global__ __launch_bounds__(kWave) void bwd_dkdv_tr128_kernel(
 
   // block-rows whose selection holds y, ascending
   int32_t* myx = sidx_all;
-  int cnt = 0;
-  for (int x0 = 0; x0 < nb; x0 += kWave) {
-    const int x = x0 + lane;
-    const bool ok = x < nb && ((bits[(hb + x) * nbw + (y >> 5)] >> (y & 31)) & 1u);
-    const uint64_t mk = __ballot(ok);
-    if (ok) myx[cnt + __popcll(mk & lanemask_lt())] = x;
-    cnt += __popcll(mk);
-  }
-  wave_lds_sync();
-  cnt = wave_uniform(cnt);
+  const int cnt = column_list(bits, hb, nbw, y, nb, myx);
 
   u32x4 kf[KC], vf[KC];
   load_rows<BF16, D>(reinterpret_cast<const elem*>(kin) + gy * 32 * D, kf);
