@@ -17,7 +17,15 @@ covered exactly once:
   its occupancy;
 * rows_kernel (select.hip): the score/weight rows, the partial sums of the
   coarse term and the float64 query rows inside the dynamic LDS it requests,
-  for every register tier, head dim and mode, within 160 KB.
+  for every register tier, head dim and mode, within 160 KB; the coarse
+  term's V~ buffer loads (vector plus immediate offsets; reads past the head's
+  rows come back as zero, so an offset at or past the buffer's size must
+  belong to a block past nb);
+* the backward's coarse passes (bwd.hip): the column pass's dim groups (every
+  output dim once, 16-byte aligned loads and stores) and its buffer-load
+  offsets, the row pass's K~/V~ buffer-load offsets;
+* the backward's column lists: the batched bitmap-word reads stay in the
+  head's bitmap.
 """
 import pytest
 
@@ -199,3 +207,142 @@ def test_rows_kernel_lds_regions(jmax, d, mode):
                     assert col + 8 <= 64 * jmax          # inside the row (zero past nb)
     if mode in (2, 3):
         assert part_off + K_ROWS * (d + 2) * 8 <= total
+
+
+# ------------------------------------------------------------------ select.hip: the coarse term's V~ loads
+@pytest.mark.parametrize("jmax", [2, 8, 16, 32])
+@pytest.mark.parametrize("d", [32, 64, 128])
+@pytest.mark.parametrize("nb", [1, 33, 100, 128])
+def test_coarse_term_v_loads(jmax, d, nb):
+    """vo = ((4 kU kq + kU ak) d + 16 nt + ar) 4 + u 4 kU KQ d 4 + e d 4: the
+    immediate part (e d 4) fits the 12-bit field, every (block, dim) of the 64
+    JMAX columns is read once per dim tile, and an offset at or past nb d 4
+    (zero from the hardware) is a block past nb."""
+    nb = min(nb, 64 * jmax)
+    rpw = 2 if jmax <= 8 else 1
+    nw = K_ROWS // rpw
+    ntd = d // 16
+    kq_n = nw // ntd
+    bpw = 2 * jmax // kq_n
+    ku = 8
+    assert 7 * d * 4 < 4096                       # immediate offset field
+    seen = set()
+    for w in range(nw):
+        nt, kq = w % ntd, w // ntd
+        for lane in range(64):
+            ar, ak = lane & 15, lane >> 4
+            vlane = ((4 * ku * kq + ku * ak) * d + 16 * nt + ar) * 4
+            for u in range(bpw):
+                vo = vlane + u * (4 * ku * kq_n * d * 4)
+                for e in range(ku):
+                    off = vo + e * d * 4
+                    block, dim = divmod(off // 4, d)
+                    assert off % 4 == 0 and dim == 16 * nt + ar
+                    assert block == 4 * ku * (kq + kq_n * u) + ku * ak + e
+                    if off >= nb * d * 4:
+                        assert block >= nb
+                    seen.add((block, dim))
+    assert seen == {(y, c) for y in range(64 * jmax) for c in range(d)}
+
+
+# ------------------------------------------------------------------ bwd.hip: the coarse passes
+def cols_cfg(d):
+    tw = min(4, d // 16)
+    groups = d // (16 * tw)
+    return tw, groups, 2 * groups
+
+
+@pytest.mark.parametrize("d", [32, 64, 128])
+@pytest.mark.parametrize("nb", [1, 5, 66, 128])
+def test_column_pass_dim_groups_and_loads(d, nb):
+    """Wave (kind, group dg), lane (lr, lg): dims d0 + t, d0 = 16 TW dg + TW lr;
+    every output (row yy of the 16, dim) of each quantity once; the 16-byte
+    loads and stores aligned; reads at or past the head's buffer (zero from the
+    hardware) are exactly those of block-rows past nb."""
+    tw, groups, waves = cols_cfg(d)
+    assert 16 * tw * groups == d
+    batch = 8
+    for y0 in range(0, nb, 16):
+        outs = set()
+        for w in range(waves):
+            kind, dg = w // groups, w % groups
+            for lane in range(64):
+                lr, lg = lane & 15, lane >> 4
+                y = y0 + lr
+                d0 = 16 * tw * dg + tw * lr
+                assert (d0 * 4) % (4 * tw) == 0
+                ao, bo = (lg * nb + y) * 4, (lg * d + d0) * 4
+                for xs in range(0, nb, 4 * batch):
+                    for u in range(batch):
+                        x = xs + 4 * u + lg
+                        a_off = ao + u * 4 * nb * 4
+                        b_off = bo + u * 4 * d * 4
+                        assert a_off == (x * nb + y) * 4 and b_off == (x * d + d0) * 4
+                        # a lane of a column y < nb (its products reach stored
+                        # rows) reads the real value for x < nb and zero past
+                        # the head's rows; columns y >= nb feed rows not stored
+                        if y < nb:
+                            assert (a_off < nb * nb * 4) == (x < nb)
+                        assert (b_off < nb * d * 4) == (x < nb)
+                    ao += 4 * batch * nb * 4
+                    bo += 4 * batch * d * 4
+                for r in range(4):
+                    yy = y0 + 4 * lg + r
+                    if yy < nb:
+                        for t in range(tw):
+                            outs.add((kind, yy, d0 + t))
+        assert outs == {(k, yy, c) for k in (0, 1) for yy in range(y0, min(y0 + 16, nb)) for c in range(d)}
+
+
+@pytest.mark.parametrize("d", [32, 64, 128])
+@pytest.mark.parametrize("nb", [1, 66, 128, 300])
+def test_row_pass_coarse_loads(d, nb):
+    """Step 1 reads K~/V~ rows y0 + 16 t + lr, dims 16 u + 4 lg (16 bytes);
+    step 3 reads K~[y0 + kq YK + 4 s + lg][16 nt + lr]; offsets at or past
+    nb d 4 (zero from the hardware) are rows past nb; immediates fit."""
+    yc, rows_wg = 128, 16
+    ntd = d // 16
+    kq_n = rows_wg // ntd
+    yk = yc // kq_n
+    assert 16 * (d // 16 - 1) * 4 < 4096
+    for w in range(rows_wg):
+        t = w & 7
+        nt, kq = w % ntd, w // ntd
+        for lane in range(64):
+            lr, lg = lane & 15, lane >> 4
+            b1 = ((16 * t + lr) * d + 4 * lg) * 4
+            b3 = ((kq * yk + lg) * d + 16 * nt + lr) * 4
+            for y0 in range(0, nb, yc):
+                ystep = y0 * d * 4
+                for u in range(d // 16):
+                    off = b1 + ystep + 16 * u * 4
+                    row = off // 4 // d
+                    assert row == y0 + 16 * t + lr and off % 16 == 0
+                    if off >= nb * d * 4:
+                        assert row >= nb
+                for s_ in range(yk // 4):
+                    off = b3 + ystep + 4 * s_ * d * 4
+                    row, dim = divmod(off // 4, d)
+                    assert row == y0 + kq * yk + 4 * s_ + lg and dim == 16 * nt + lr
+                    if off >= nb * d * 4:
+                        assert row >= nb
+
+
+@pytest.mark.parametrize("nb", [1, 63, 64, 66, 511, 512, 513, 1024, 2048])
+def test_column_list_bitmap_reads(nb):
+    """Batches of 8 x 64 rows; row x = min(x0 + 64 u + lane, nb - 1) reads word
+    x nbw + y / 32 of the head's bitmap; rows past nb are dropped."""
+    nbw = (nb + 31) // 32
+    listed = []
+    for y in {0, nb // 2, nb - 1}:
+        listed = []
+        for x0 in range(0, nb, 8 * 64):
+            for u in range(8):
+                for lane in range(64):
+                    xr = x0 + 64 * u + lane
+                    x = min(xr, nb - 1)
+                    word = x * nbw + y // 32
+                    assert 0 <= word < nb * nbw
+                    if xr < nb:
+                        listed.append(xr)
+        assert listed == list(range(nb))
