@@ -25,7 +25,10 @@ covered exactly once:
   output dim once, 16-byte aligned loads and stores) and its buffer-load
   offsets, the row pass's K~/V~ buffer-load offsets;
 * the backward's column lists: the batched bitmap-word reads stay in the
-  head's bitmap.
+  head's bitmap;
+* the head-wide selection's register tier (select_global.hip): its three
+  radix passes of 12, 10 and 10 bits with the block-wide digit pick find the
+  budget-th largest key and the number of ties to take (against sorting).
 """
 import pytest
 
@@ -346,3 +349,63 @@ def test_column_list_bitmap_reads(nb):
                     if xr < nb:
                         listed.append(xr)
         assert listed == list(range(nb))
+
+
+# ------------------------------------------------------------------ select_global.hip: register-tier radix passes
+def pick_digit_block(hist, bins, remaining, threads=1024):
+    """Thread t sums bins bins-1-t*per .. bins-(t+1)*per (descending); the thread
+    whose exclusive..inclusive prefix holds `remaining` picks the digit."""
+    per = bins // threads
+    found = []
+    incl = 0
+    for t in range(threads):
+        top = bins - 1 - t * per
+        c = [hist[top - e] for e in range(per)]
+        excl, incl = incl, incl + sum(c)
+        if excl < remaining <= incl:
+            acc = excl
+            for e in range(per):
+                if acc + c[e] >= remaining:
+                    found.append((top - e, acc))
+                    break
+                acc += c[e]
+    assert len(found) == 1                        # exactly one thread
+    return found[0]
+
+
+def radix_threshold(keys, budget):
+    """The kernel's three passes of 12, 10 and 10 bits over the non-zero keys:
+    the budget-th largest key T and how many keys equal to T to take."""
+    prefix, remaining = 0, budget
+    for shift, bits in ((20, 12), (10, 10), (0, 10)):
+        bins = 1 << bits
+        hi_mask = 0 if shift == 20 else (~((1 << (shift + bits)) - 1)) & 0xFFFFFFFF
+        hist = [0] * bins
+        for k in keys:
+            if k != 0 and (k & hi_mask) == (prefix & hi_mask):
+                hist[(k >> shift) & (bins - 1)] += 1
+        digit, before = pick_digit_block(hist, bins, remaining)
+        prefix |= digit << shift
+        remaining -= before
+    return prefix, remaining
+
+
+@pytest.mark.parametrize("case", range(8))
+def test_head_wide_radix_passes(case):
+    import random
+    rng = random.Random(case)
+    n = rng.choice([16, 100, 1000, 4096])
+    if case % 4 == 0:       # heavy ties
+        keys = [rng.choice([0x80000000, 0xC0000000, 0xBF800000, 0x3F7FFFFF]) for _ in range(n)]
+    elif case % 4 == 1:     # one exponent range (most keys share the top 12 bits)
+        keys = [0xC0000000 | rng.getrandbits(20) for _ in range(n)]
+    else:                   # anything non-zero
+        keys = [rng.getrandbits(32) | 1 for _ in range(n)]
+    keys += [0] * rng.randint(0, 5)            # blocks that do not take part
+    nz = sorted((k for k in keys if k), reverse=True)
+    for budget in sorted({1, len(nz) // 3 or 1, len(nz) - 1 or 1}):
+        if budget >= len(nz):
+            continue
+        T, need = radix_threshold(keys, budget)
+        assert T == nz[budget - 1]
+        assert need == budget - sum(1 for k in nz if k > T) and need >= 1
