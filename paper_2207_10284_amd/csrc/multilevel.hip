@@ -204,7 +204,9 @@ __global__ __launch_bounds__(kMlWaves * kWave) void coarse_term_levels_kernel(
     float acc = 0.0f;
 #pragma unroll
     for (int l = 0; l < L; ++l) {
-      const float* vl = T.vp[l] + bh * (long long)T.nb[l] * d + dd;
+      // the level's pooled V rows of the head as a buffer (a row's offset in
+      // the vector offset; every listed y is in [0, nb_l))
+      const i32x4 vrs = buffer_rsrc(T.vp[l] + bh * (long long)T.nb[l] * d, (unsigned)T.nb[l] * d * 4u);
       for (int c0 = kept_to[l]; c0 < kept_to[l + 1]; c0 += kBatch) {
         const int nc = min(kBatch, kept_to[l + 1] - c0);  // wave-uniform
         float vv[kBatch], ww[kBatch];
@@ -212,7 +214,7 @@ __global__ __launch_bounds__(kMlWaves * kWave) void coarse_term_levels_kernel(
         for (int j = 0; j < kBatch; ++j) {
           const int y = j < nc ? cy[c0 + j] : 0;
           ww[j] = j < nc ? wt[c0 + j] : 0.0f;
-          vv[j] = vl[(long long)y * d];
+          vv[j] = mra_raw_buffer_load_f32(vrs, (y * d + dd) * 4, 0, 0);
         }
 #pragma unroll
         for (int j = 0; j < kBatch; ++j)
