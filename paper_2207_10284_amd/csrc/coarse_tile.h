@@ -43,16 +43,19 @@ __device__ __forceinline__ f64x4 coarse_tile_f64(const f32x4 (&q)[D / 16], const
 }
 
 // The same products and order with the query operands already in float64:
-// qrow points at this lane's row, column 4g, of a float64 copy of the tile's
-// query rows (16-byte aligned), so the results are the same bits.
+// qrow points at this lane's row of a float64 copy of the tile's query rows
+// (16-byte aligned) whose column c is stored at c ^ x (x even and below 32),
+// c0 = 4g is the lane's first column, so the results are the same bits.
 typedef double f64x2 __attribute__((ext_vector_type(2)));
 template <int D>
-__device__ __forceinline__ f64x4 coarse_tile_f64_qd(const double* qrow, const f32x4 (&kf)[D / 16]) {
+__device__ __forceinline__ f64x4 coarse_tile_f64_qd(const double* qrow, int c0, int x,
+                                                   const f32x4 (&kf)[D / 16]) {
   f64x4 acc[2] = {{0.0, 0.0, 0.0, 0.0}, {0.0, 0.0, 0.0, 0.0}};
 #pragma unroll
   for (int s = 0; s < D / 16; ++s) {
-    const f64x2 q01 = *reinterpret_cast<const f64x2*>(qrow + 16 * s);
-    const f64x2 q23 = *reinterpret_cast<const f64x2*>(qrow + 16 * s + 2);
+    const int c = (c0 + 16 * s) ^ x;
+    const f64x2 q01 = *reinterpret_cast<const f64x2*>(qrow + c);
+    const f64x2 q23 = *reinterpret_cast<const f64x2*>(qrow + (c ^ 2));
     acc[s & 1] = __builtin_amdgcn_mfma_f64_16x16x4f64(q01[0], (double)kf[s][0], acc[s & 1], 0, 0, 0);
     acc[s & 1] = __builtin_amdgcn_mfma_f64_16x16x4f64(q01[1], (double)kf[s][1], acc[s & 1], 0, 0, 0);
     acc[s & 1] = __builtin_amdgcn_mfma_f64_16x16x4f64(q23[0], (double)kf[s][2], acc[s & 1], 0, 0, 0);

@@ -39,21 +39,27 @@ constexpr int kU = 8;                     // coarse-term steps per batch of V~ l
 typedef float f32x4v __attribute__((ext_vector_type(4)));
 
 // LDS of a workgroup: the 16 rows' scores (fused modes) and then their
-// weights, [16][ldc] floats with ldc = 64 JMAX + 4 (zero past nb; the pad of
-// 4 keeps the reads of the coarse term's operands and of the scores free of
-// bank conflicts), followed by the partial sums of L ((16 / (d/16)) x 16 x d
-// floats).
-__host__ __device__ constexpr int rows_ldc(int jmax) { return 64 * jmax + 4; }
+// weights, [16][64 JMAX] floats (zero past nb), column c of row r stored at
+// c ^ 4r: rows start on the same bank, and the swizzle (bits 2-5 of the
+// column, so groups of four stay contiguous and every column stays in its
+// group of 64) keeps the coarse term's 16-byte operand reads across the 16
+// rows free of bank conflicts without padding; followed by the partial sums
+// of L ((16 / (d/16)) x 16 x d floats).
+__host__ __device__ constexpr int rows_ldc(int jmax) { return 64 * jmax; }
+__host__ __device__ constexpr int rows_col(int r, int c) { return c ^ ((r & 15) << 2); }
 
 struct RowsSmem {
   size_t part_off, bytes;
 };
 
 // The select-only mode uses no LDS. In the fused modes the region after the
-// score rows first holds the 16 query rows in float64 ([16][d + 2]; the pad
-// of 16 bytes keeps their reads free of bank conflicts), then the partial
-// sums of L.
-__host__ __device__ constexpr int rows_ldq(int d) { return d + 2; }
+// score rows first holds the 16 query rows in float64 ([16][d], element c of
+// row r at c ^ 2r: pairs stay contiguous, and the 16-byte reads of the 16
+// rows fall on different banks), then the partial sums of L. Unpadded, the
+// two regions of a 16-block-row workgroup at nb <= 1024 and d = 128 take
+// exactly half of a CU's LDS, so two such workgroups share a CU.
+__host__ __device__ constexpr int rows_ldq(int d) { return d; }
+__host__ __device__ constexpr int rows_qcol(int r, int c) { return c ^ ((r & 15) << 1); }
 
 static RowsSmem rows_smem(int jmax, int nw, int mode, int d) {
   RowsSmem L{};
@@ -135,18 +141,22 @@ __global__ __launch_bounds__(kRows / RPW * kWave) void rows_kernel(
     double* Qd = reinterpret_cast<double*>(smem + part_off);
     for (int i = tid; i < kRows * D; i += NTH) {
       const int rr = i / D, c = i % D;
-      Qd[rr * LDQ + c] = (double)qp[(g0 + min(rr, rows - 1)) * D + c];
+      Qd[rr * LDQ + rows_qcol(rr, c)] = (double)qp[(g0 + min(rr, rows - 1)) * D + c];
     }
     __syncthreads();
-    const double* qrow = Qd + r * LDQ + 4 * (lane >> 4);
+    const double* qrow = Qd + r * LDQ;
+    const int qc0 = 4 * (lane >> 4), qx = rows_qcol(r, 0);
     const int ntile = (nb + 15) / 16;
     auto load_k = [&](int t, f32x4 (&kv)[NQ]) {                   // keys past nb: ignored columns
       coarse_load<D>(kh + (long long)min(16 * min(t, ntile - 1) + r, nb - 1) * D, kv);
     };
     auto tile = [&](int t, const f32x4 (&kv)[NQ]) {
-      const f64x4 acc = coarse_tile_f64_qd<D>(qrow, kv);
+      const f64x4 acc = coarse_tile_f64_qd<D>(qrow, qc0, qx, kv);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) Cb[coarse_tile_row(lane, e) * ldc + 16 * t + r] = coarse_round(acc[e], scale);
+      for (int e = 0; e < 4; ++e) {
+        const int rr = coarse_tile_row(lane, e);
+        Cb[rr * ldc + rows_col(rr, 16 * t + r)] = coarse_round(acc[e], scale);
+      }
     };
     // K~ one tile ahead where a wave takes several tiles and the registers
     // allow it (not at d = 128 with two rows per wave)
@@ -180,7 +190,8 @@ __global__ __launch_bounds__(kRows / RPW * kWave) void rows_kernel(
       if (j >= J) break;
 #pragma unroll
       for (int i = 0; i < RPW; ++i)
-        if (row_of(i) < rows && kChunk * j + lane < nb) s[i][j] = Cb[row_of(i) * ldc + kChunk * j + lane];
+        if (row_of(i) < rows && kChunk * j + lane < nb)
+          s[i][j] = Cb[row_of(i) * ldc + rows_col(row_of(i), kChunk * j + lane)];
     }
   } else {
 #pragma unroll
@@ -324,19 +335,21 @@ __global__ __launch_bounds__(kRows / RPW * kWave) void rows_kernel(
   for (int j = 0; j < JMAX; ++j) {
     if (j >= J) break;
 #pragma unroll
-    for (int i = 0; i < RPW; ++i) Cb[row_of(i) * ldc + kChunk * j + lane] = s[i][j];   // zero: inactive rows, blocks >= nb
+    for (int i = 0; i < RPW; ++i)                                   // zero: inactive rows, blocks >= nb
+      Cb[row_of(i) * ldc + rows_col(row_of(i), kChunk * j + lane)] = s[i][j];
   }
   for (int c = kChunk * J + lane; c < kChunk * JMAX; c += kWave)   // columns past the scores
-    for (int i = 0; i < RPW; ++i) Cb[row_of(i) * ldc + c] = 0.0f;
+    for (int i = 0; i < RPW; ++i) Cb[row_of(i) * ldc + rows_col(row_of(i), c)] = 0.0f;
   __syncthreads();
   if constexpr (!kEarlyB) load_b(0, ba);
-  const float* wrow = Cb + ar * ldc + kU * ak;
+  const float* wrow = Cb + ar * ldc;
   f32x4v acc = {0.0f, 0.0f, 0.0f, 0.0f};
   // batch u: step e takes block 32 (kq + KQ u) + 8 ak + e in lane group ak,
   // so each lane reads its kU weights as two 16-byte LDS reads
   auto steps = [&](int u, const float (&b)[kU]) {
-    const f32x4v* wp = reinterpret_cast<const f32x4v*>(wrow + 4 * kU * (kq + KQ * u));
-    const f32x4v a0 = wp[0], a1 = wp[1];
+    const int c0 = rows_col(ar, kU * ak + 4 * kU * (kq + KQ * u));  // c0 + 4 lands at c0 ^ 4
+    const f32x4v a0 = *reinterpret_cast<const f32x4v*>(wrow + c0);
+    const f32x4v a1 = *reinterpret_cast<const f32x4v*>(wrow + (c0 ^ 4));
 #pragma unroll
     for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[e], b[e], acc, 0, 0, 0);
 #pragma unroll
@@ -376,10 +389,12 @@ static void launch_rows_j(const float* S, const float* qp, const float* kp, int3
                           float* cvec, long long bh, int nb, int d, int m, hipStream_t stream) {
   const long long groups = (nb + kRows - 1) / kRows;
   const unsigned blocks = (unsigned)(bh * groups);
-  constexpr int RPW = JMAX <= 8 ? 2 : 1;
+  constexpr int RPW = JMAX <= 16 ? 2 : 1;
   const RowsSmem L = rows_smem(JMAX, kRows / RPW, MODE, d);
   const double scale = 1.0 / sqrt((double)d);
-  // two rows per wave (8 waves) while the scores fit: four workgroups per CU
+  // two rows per wave (8 waves) while the scores fit in registers (nb <= 1024):
+  // workgroups of 16 block-rows small enough that two or more share a CU, so
+  // one's matrix-core phases overlap another's selection
 #define MRA_ROWS_LAUNCH(DD)                                                                     \
   rows_kernel<DD, MODE, JMAX, RPW><<<blocks, 64 * kRows / RPW, L.bytes, stream>>>(            \
       S, qp, kp, idx_out, idx_in, vp, cmax, csum, cvec, nb, m, (int)L.part_off, scale)

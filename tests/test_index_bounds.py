@@ -175,28 +175,47 @@ K_ROWS, K_CHUNK, K_U = 16, 64, 8
 def rows_smem(jmax, nw, mode, d):
     if mode == 0:
         return 0, 0
-    ldc = 64 * jmax + 4
+    ldc = 64 * jmax
     part_off = (K_ROWS * ldc * 4 + 15) & ~15
     part = nw * 16 * 16 * 4 if mode in (1, 2) else 0
-    qd = K_ROWS * (d + 2) * 8 if mode in (2, 3) else 0
+    qd = K_ROWS * d * 8 if mode in (2, 3) else 0
     return part_off, part_off + max(part, qd)
+
+
+def rows_col(r, c):
+    return c ^ ((r & 15) << 2)
+
+
+def rows_qcol(r, c):
+    return c ^ ((r & 15) << 1)
+
+
+def rows_rpw(jmax):
+    return 2 if jmax <= 16 else 1
 
 
 @pytest.mark.parametrize("jmax", [2, 8, 16, 32])
 @pytest.mark.parametrize("d", [32, 64, 128])
 @pytest.mark.parametrize("mode", [1, 2, 3])
 def test_rows_kernel_lds_regions(jmax, d, mode):
-    rpw = 2 if jmax <= 8 else 1
+    rpw = rows_rpw(jmax)
     nw = K_ROWS // rpw
     ntd = d // 16
     kq = nw // ntd
     assert kq >= 1 and nw % ntd == 0
     bpw = 2 * jmax // kq
     assert bpw * kq == 2 * jmax
-    ldc = 64 * jmax + 4
+    ldc = 64 * jmax
     part_off, total = rows_smem(jmax, nw, mode, d)
     assert total <= LDS_PER_CU
-    # score / weight rows: row r < 16, column c < 64 JMAX
+    if jmax <= 16:
+        assert 2 * total <= LDS_PER_CU                   # two workgroups per CU
+    # score / weight rows: row r < 16, column c < 64 JMAX, stored at c ^ 4r,
+    # a permutation of the row's columns inside each group of 64
+    for r in range(K_ROWS):
+        cols = [rows_col(r, c) for c in range(64 * jmax)]
+        assert sorted(cols) == list(range(64 * jmax))
+        assert all(cc // 64 == c // 64 for c, cc in enumerate(cols))
     assert (K_ROWS - 1) * ldc + 64 * jmax - 1 < part_off // 4
     if mode in (1, 2):
         # partial sums part[(kq' * 16 + 4 ak + e) * D + 16 nt + ar]
@@ -208,8 +227,25 @@ def test_rows_kernel_lds_regions(jmax, d, mode):
                 for ak in range(4):
                     col = K_U * ak + 4 * K_U * (kqi + kq * u)
                     assert col + 8 <= 64 * jmax          # inside the row (zero past nb)
+                    for ar in range(K_ROWS):
+                        c0 = rows_col(ar, col)         # the two 16-byte reads: c0, c0 ^ 4
+                        assert c0 % 4 == 0
+                        assert [c0 + i for i in range(4)] == [rows_col(ar, col + i) for i in range(4)]
+                        assert [(c0 ^ 4) + i for i in range(4)] == [rows_col(ar, col + 4 + i) for i in range(4)]
     if mode in (2, 3):
-        assert part_off + K_ROWS * (d + 2) * 8 <= total
+        assert part_off + K_ROWS * d * 8 <= total
+        # the float64 query rows: column c of row r at c ^ 2r (a permutation of
+        # the row); a lane reads pairs (c0 + 16 s) ^ x and that ^ 2 for
+        # c0 = 4g, g < 4
+        for r in range(K_ROWS):
+            assert sorted(rows_qcol(r, c) for c in range(d)) == list(range(d))
+            x = rows_qcol(r, 0)
+            for g in range(4):
+                for s16 in range(d // 16):
+                    c = (4 * g + 16 * s16) ^ x
+                    assert c % 2 == 0 and c + 1 < d
+                    assert [c, c + 1] == [rows_qcol(r, 4 * g + 16 * s16), rows_qcol(r, 4 * g + 16 * s16 + 1)]
+                    assert [c ^ 2, (c ^ 2) + 1] == [rows_qcol(r, 4 * g + 16 * s16 + 2), rows_qcol(r, 4 * g + 16 * s16 + 3)]
 
 
 # ------------------------------------------------------------------ select.hip: the coarse term's V~ loads
@@ -222,7 +258,7 @@ def test_coarse_term_v_loads(jmax, d, nb):
     JMAX columns is read once per dim tile, and an offset at or past nb d 4
     (zero from the hardware) is a block past nb."""
     nb = min(nb, 64 * jmax)
-    rpw = 2 if jmax <= 8 else 1
+    rpw = rows_rpw(jmax)
     nw = K_ROWS // rpw
     ntd = d // 16
     kq_n = nw // ntd
