@@ -10,7 +10,7 @@
 //   L = sum b e^{S~ - M} V~_y.
 //
 // One workgroup owns 16 consecutive block-rows of one head: 8 waves with two
-// rows each (one row per wave for heads of more than 512 blocks). Lane l of a
+// rows each (one row per wave for heads of more than 1024 blocks). Lane l of a
 // row's wave holds the row's scores for blocks y = 64j + l in registers:
 // loaded from S~, or (fused modes) computed as 16 x 16 tiles on the float64
 // matrix cores with the same tile routine as the coarse-logit kernel (so the
