@@ -8,7 +8,8 @@ Prints one JSON line with tokens/s, the roofline of the dominant kernel (the
 tile pass, timed with HIP events on the stream it runs on) and the float64
 oracle timed on the host as a reported CPU baseline. Beside the headline it
 reports MRA-2-s, the head-wide budget and the gradient pass (forward with log
-normalisers, then mra_attention_backward) on the same inputs.
+normalisers, then the backward given the forward's block means) on the same
+inputs.
 
 The CPU leg also compares the GPU's output with the oracle's on the heads it
 computed (max row-normwise error, rows whose selection differs by a near-tie)
@@ -178,9 +179,11 @@ def select_bytes(w) -> float:
 
 
 def backward_leg(w, ops, tq, tk, tv, out, idx, ws, iters):
-    """The gradient pass on the workload: mra_attention_backward alone, and a
-    forward that also writes the log normalisers followed by the backward
-    (one training step of the attention layer). Output gradient G ~ N(0, 1)."""
+    """The gradient pass on the workload: mra_attention_backward alone (it
+    pools q, k, v again), the backward given the forward's block means
+    (mra_attention_backward_pooled), and a forward that also writes the log
+    normalisers followed by that backward (one training step of the attention
+    layer). Output gradient G ~ N(0, 1)."""
     import torch
     from paper_2207_10284_amd import inputs
     dev = tq.device
@@ -197,11 +200,18 @@ def backward_leg(w, ops, tq, tk, tv, out, idx, ws, iters):
     def bwd():
         ops.attention_backward(tq, tk, tv, out, tg, lse, idx, dq=dq, dk=dk, dv=dv, workspace=bws)
 
+    pooled = ops.forward_pooled_rows(ws, w.B, w.H, w.n, w.d)      # views of the forward's workspace
+
+    def bwd_pooled():
+        ops.attention_backward(tq, tk, tv, out, tg, lse, idx, dq=dq, dk=dk, dv=dv, workspace=bws, pooled=pooled)
+
     fwd()
     bwd_ms = time_launches(bwd, iters)
-    fb_ms = time_launches(lambda: (fwd(), bwd()), iters)
+    bwdp_ms = time_launches(bwd_pooled, iters)
+    fb_ms = time_launches(lambda: (fwd(), bwd_pooled()), iters)
     tf = backward_flops(w) / (bwd_ms * 1e-3) / 1e12
-    return {"ms_per_step": bwd_ms, "fwd_bwd_ms": fb_ms, "fwd_bwd_tokens_per_s": w.B * w.n / (fb_ms * 1e-3),
+    return {"ms_per_step": bwd_ms, "pooled_given_ms_per_step": bwdp_ms, "fwd_bwd_ms": fb_ms,
+            "fwd_bwd_tokens_per_s": w.B * w.n / (fb_ms * 1e-3),
             "tile_tflops": tf, "tile_flops_per_step": backward_flops(w),
             "workspace_bytes": bws.numel()}
 

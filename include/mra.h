@@ -444,6 +444,47 @@ mra_status_t mra_attention_backward(const void* q, const void* k, const void* v,
                                     int B, int H, int n, int d, int block, int width,
                                     int coarse, mra_dtype_t dtype, void* stream);
 
+/*
+ * mra_attention_backward_pooled — mra_attention_backward with the block means
+ * of q, k, v supplied, so the backward does not compute them again: a
+ * training step keeps the forward's (mra_forward_pooled_rows) and hands them
+ * over. The gradients are bit-identical to mra_attention_backward's on the
+ * same arguments.
+ *   qp, kp, vp: [B,H,nb,d] float32 device arrays (16-byte aligned), the means
+ *               of Sec. 4.1 eq. recursive_pooling and Sec. 4.3
+ *               eq. recursive_pooling_V of these q, k, v exactly as mra_pool
+ *               or the forward computed them; read only. All three are
+ *               required for a non-empty problem (NULL: MRA_ERR_INVALID_ARG,
+ *               not 16-byte aligned: MRA_ERR_MISALIGNED); with coarse = 0
+ *               they are not read.
+ *   Every other argument, the workspace size included, and every error as
+ *   for mra_attention_backward.
+ */
+mra_status_t mra_attention_backward_pooled(const void* q, const void* k, const void* v,
+                                           const void* out, const void* dout, const float* lse,
+                                           const int32_t* idx, const float* qp, const float* kp,
+                                           const float* vp, void* dq, void* dk, void* dv,
+                                           void* workspace, size_t workspace_bytes,
+                                           int B, int H, int n, int d, int block, int width,
+                                           int coarse, mra_dtype_t dtype, void* stream);
+
+/*
+ * mra_forward_pooled_rows — where the block means Q~, K~, V~ ([B,H,nb,d]
+ * float32 each, mra_pool's layout) lie in a workspace that
+ * mra_attention_forward or mra_attention_forward_global filled for these
+ * sizes. Host-only arithmetic on the workspace address: nothing is read or
+ * launched, so the addresses are those of what the last forward enqueued on
+ * that workspace, valid until the workspace is used again. The block means
+ * do not depend on the budget, so none is taken.
+ *   qp, kp, vp: host pointers that receive the three device addresses (NULL
+ *               for an empty problem).
+ * Errors: MRA_ERR_INVALID_ARG (a NULL output pointer, a NULL workspace for a
+ * non-empty problem), MRA_ERR_UNSUPPORTED (sizes as for the forward),
+ * MRA_ERR_MISALIGNED (workspace not 16-byte aligned).
+ */
+mra_status_t mra_forward_pooled_rows(const void* workspace, int B, int H, int n, int d, int block,
+                                     const float** qp, const float** kp, const float** vp);
+
 /* Static description of a status code. */
 const char* mra_status_str(mra_status_t status);
 

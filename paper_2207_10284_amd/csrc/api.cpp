@@ -632,11 +632,13 @@ size_t mra_backward_workspace_bytes(int B, int H, int n, int d, int block, mra_d
   return ws_bwd(s.bh, s.nb, d, dtype).total;
 }
 
-mra_status_t mra_attention_backward(const void* q, const void* k, const void* v, const void* out,
-                                    const void* dout, const float* lse, const int32_t* idx,
-                                    void* dq, void* dk, void* dv, void* workspace,
-                                    size_t workspace_bytes, int B, int H, int n, int d, int block,
-                                    int width, int coarse, mra_dtype_t dtype, void* stream) {
+// The backward of mra_attention_backward(_pooled): with `given`, pq, pk, pv
+// are the block means of q, k, v, supplied by the caller.
+mra_status_t backward(const void* q, const void* k, const void* v, const void* out,
+                      const void* dout, const float* lse, const int32_t* idx, bool given,
+                      const float* pq, const float* pk, const float* pv, void* dq, void* dk,
+                      void* dv, void* workspace, size_t workspace_bytes, int B, int H, int n,
+                      int d, int block, int width, int coarse, mra_dtype_t dtype, void* stream) {
   Shape s;
   MRA_TRY(check_shape(B, H, n, d, block, true, &s));
   MRA_TRY(check_dtype(dtype));
@@ -649,6 +651,11 @@ mra_status_t mra_attention_backward(const void* q, const void* k, const void* v,
   MRA_TRY(check_ptr(dq));
   MRA_TRY(check_ptr(dk));
   MRA_TRY(check_ptr(dv));
+  if (given) {
+    MRA_TRY(check_ptr(pq));
+    MRA_TRY(check_ptr(pk));
+    MRA_TRY(check_ptr(pv));
+  }
   const WsBwd L = ws_bwd(s.bh, s.nb, d, dtype);
   if (workspace_bytes < L.total) return MRA_ERR_WORKSPACE;
 
@@ -660,6 +667,12 @@ mra_status_t mra_attention_backward(const void* q, const void* k, const void* v,
   A.dq = dq; A.dk = dk; A.dv = dv;
   A.bh = s.bh; A.n = n; A.d = d; A.m = width; A.dtype = (int)dtype; A.coarse = coarse != 0;
   A.qp = f32(L.qp); A.kp = f32(L.kp); A.vp = f32(L.vp);
+  A.pooled_in = given && coarse != 0;
+  if (A.pooled_in) {                                        // read only by the kernels
+    A.qp = const_cast<float*>(pq);
+    A.kp = const_cast<float*>(pk);
+    A.vp = const_cast<float*>(pv);
+  }
   A.q_row = ws + L.q_row; A.q_t = ws + L.q_t; A.k_row = ws + L.k_row; A.k_t = ws + L.k_t;
   A.v_row = ws + L.v_row; A.g_row = ws + L.g_row; A.g_t = ws + L.g_t;
   A.ld = f32(L.ld);
@@ -672,6 +685,44 @@ mra_status_t mra_attention_backward(const void* q, const void* k, const void* v,
                          {dv, gbytes, nan_pattern(dtype)}, {workspace, L.total, kNanF32}};
   MRA_TRY(debug_fill(fills, stream));
   return hip_status(mra::launch_bwd(A, static_cast<hipStream_t>(stream)));
+}
+
+mra_status_t mra_attention_backward(const void* q, const void* k, const void* v, const void* out,
+                                    const void* dout, const float* lse, const int32_t* idx,
+                                    void* dq, void* dk, void* dv, void* workspace,
+                                    size_t workspace_bytes, int B, int H, int n, int d, int block,
+                                    int width, int coarse, mra_dtype_t dtype, void* stream) {
+  return backward(q, k, v, out, dout, lse, idx, false, nullptr, nullptr, nullptr, dq, dk, dv,
+                  workspace, workspace_bytes, B, H, n, d, block, width, coarse, dtype, stream);
+}
+
+mra_status_t mra_attention_backward_pooled(const void* q, const void* k, const void* v,
+                                           const void* out, const void* dout, const float* lse,
+                                           const int32_t* idx, const float* qp, const float* kp,
+                                           const float* vp, void* dq, void* dk, void* dv,
+                                           void* workspace, size_t workspace_bytes, int B, int H,
+                                           int n, int d, int block, int width, int coarse,
+                                           mra_dtype_t dtype, void* stream) {
+  return backward(q, k, v, out, dout, lse, idx, true, qp, kp, vp, dq, dk, dv, workspace,
+                  workspace_bytes, B, H, n, d, block, width, coarse, dtype, stream);
+}
+
+mra_status_t mra_forward_pooled_rows(const void* workspace, int B, int H, int n, int d, int block,
+                                     const float** qp, const float** kp, const float** vp) {
+  if (qp == nullptr || kp == nullptr || vp == nullptr) return MRA_ERR_INVALID_ARG;
+  *qp = *kp = *vp = nullptr;
+  Shape s;
+  MRA_TRY(check_shape(B, H, n, d, block, true, &s));
+  if (s.empty) return MRA_OK;
+  MRA_TRY(check_ptr(workspace));
+  // Q~, K~, V~ lead the forward's layout (and the head-wide-budget forward's,
+  // which extends it); their offsets depend on neither budget nor dtype
+  const WsLayout L = ws_layout(s.bh, s.nb, d, 0, MRA_BF16);
+  const char* ws = static_cast<const char*>(workspace);
+  *qp = reinterpret_cast<const float*>(ws + L.qp);
+  *kp = reinterpret_cast<const float*>(ws + L.kp);
+  *vp = reinterpret_cast<const float*>(ws + L.vp);
+  return MRA_OK;
 }
 
 size_t mra_forward_multilevel_workspace_bytes(int B, int H, int n, int d, int block,

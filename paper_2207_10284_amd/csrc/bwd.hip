@@ -1463,12 +1463,14 @@ hipError_t launch_bwd(const BwdArgs& A, hipStream_t stream) {
   if (A.dtype == BF16) {
     // the tile passes read raw tiles of Q, K, V and G = dZ: only the pooled
     // rows of the coarse term
-    if (A.coarse) e = launch_pool(A.q, A.k, A.v, A.qp, A.kp, A.vp, nullptr, A.bh, A.n, A.d, A.dtype, stream);
+    if (A.coarse && !A.pooled_in)
+      e = launch_pool(A.q, A.k, A.v, A.qp, A.kp, A.vp, nullptr, A.bh, A.n, A.d, A.dtype, stream);
   } else {
-    // pooled rows and packed operands of Q, K, V and G = dZ
-    const PackJob jobs[4] = {{A.q, A.coarse ? A.qp : nullptr, A.q_row, A.q_t},
-                             {A.k, A.coarse ? A.kp : nullptr, A.k_row, A.k_t},
-                             {A.v, A.coarse ? A.vp : nullptr, A.v_row, nullptr},
+    // pooled rows (unless given) and packed operands of Q, K, V and G = dZ
+    const bool pool = A.coarse && !A.pooled_in;
+    const PackJob jobs[4] = {{A.q, pool ? A.qp : nullptr, A.q_row, A.q_t},
+                             {A.k, pool ? A.kp : nullptr, A.k_row, A.k_t},
+                             {A.v, pool ? A.vp : nullptr, A.v_row, nullptr},
                              {A.dout, nullptr, A.g_row, A.g_t}};
     e = launch_pack(jobs, 4, A.bh, A.n, A.d, A.dtype, stream);
   }

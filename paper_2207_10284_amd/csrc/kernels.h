@@ -125,6 +125,7 @@ struct BwdArgs {
   long long bh;
   int n, d, m, dtype;
   bool coarse;
+  bool pooled_in;                 // qp, kp, vp hold the block means already
   float *qp, *kp, *vp;
   void *q_row, *q_t, *k_row, *k_t, *v_row, *g_row, *g_t;
   float* ld;

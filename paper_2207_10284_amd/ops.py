@@ -46,6 +46,8 @@ SIGNATURES = {
     "mra_backward_workspace_bytes": (_Z, [_I, _I, _I, _I, _I, _I]),
     "mra_attention_backward": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _Z,
                                     _I, _I, _I, _I, _I, _I, _I, _I, _P]),
+    "mra_attention_backward_pooled": (_I, [_P] * 14 + [_Z] + [_I] * 8 + [_P]),
+    "mra_forward_pooled_rows": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P]),
     "mra_status_str": (ctypes.c_char_p, [_I]),
     "mra_last_hip_error": (_I, []),
 }
@@ -371,12 +373,37 @@ def backward_workspace_bytes(B: int, H: int, n: int, d: int, dtype=torch.bfloat1
     return int(load().mra_backward_workspace_bytes(B, H, n, d, BLOCK, code))
 
 
+def forward_pooled_rows(workspace, B: int, H: int, n: int, d: int):
+    """The block means (Q~, K~, V~: float32 [B, H, nb, d] each) that
+    ``attention_forward`` or ``attention_forward_global`` left in
+    ``workspace`` (a uint8 device tensor) for these sizes, as views of it (no
+    copy); they change when the workspace is used again."""
+    if workspace.dtype != torch.uint8 or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous uint8 tensor")
+    nb = n // BLOCK
+    if B * H * nb * d == 0:
+        return tuple(torch.empty(B, H, nb, d, dtype=torch.float32, device=workspace.device) for _ in range(3))
+    ptrs = [ctypes.c_void_p() for _ in range(3)]
+    _call("mra_forward_pooled_rows", _ptr(workspace), B, H, n, d, BLOCK, *(ctypes.byref(p) for p in ptrs))
+    size = B * H * nb * d * 4
+    views = []
+    for p in ptrs:
+        off = (p.value or 0) - workspace.data_ptr()
+        if p.value is None or off < 0 or off + size > workspace.numel():
+            raise ValueError("workspace too small for the pooled rows of these sizes")
+        views.append(workspace[off:off + size].view(torch.float32).view(B, H, nb, d))
+    return tuple(views)
+
+
 def attention_backward(q, k, v, out, dout, lse, idx, coarse: bool = True, dq=None, dk=None, dv=None,
-                       workspace=None):
+                       workspace=None, pooled=None):
     """Gradients (dq, dk, dv) through one forward (``coarse=True``: MRA-2,
     per-row or head-wide budget; ``False``: MRA-2-s) with its selection
     ``idx`` (int32 [B, H, nb, width]) held fixed; ``out`` and ``lse`` are the
-    forward's output and log normalisers, ``dout`` the gradient of the output."""
+    forward's output and log normalisers, ``dout`` the gradient of the output.
+    ``pooled``: the block means of q, k, v (float32 [B, H, nb, d] each, e.g.
+    from ``forward_pooled_rows``), so that the backward does not compute them
+    again; the gradients are the same bits either way."""
     ref = _check_qkv(q, k, v, out, dout)
     B, H, n, d = ref.shape
     nb = n // BLOCK
@@ -390,9 +417,17 @@ def attention_backward(q, k, v, out, dout, lse, idx, coarse: bool = True, dq=Non
     need = backward_workspace_bytes(B, H, n, d, ref.dtype)
     if workspace is None:
         workspace = torch.empty(max(need, 1), device=ref.device, dtype=torch.uint8)
-    _call("mra_attention_backward", _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(lse), _ptr(idx),
-          _ptr(dq), _ptr(dk), _ptr(dv), _ptr(workspace), workspace.numel() * workspace.element_size(),
-          B, H, n, d, BLOCK, width, int(bool(coarse)), _dtype_code(ref), _stream(ref.device))
+    head = (_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(lse), _ptr(idx))
+    tail = (_ptr(dq), _ptr(dk), _ptr(dv), _ptr(workspace), workspace.numel() * workspace.element_size(),
+            B, H, n, d, BLOCK, width, int(bool(coarse)), _dtype_code(ref), _stream(ref.device))
+    if pooled is None:
+        _call("mra_attention_backward", *head, *tail)
+    else:
+        for name, t in zip(("qp", "kp", "vp"), pooled):
+            _check_f32(t, (B, H, nb, d), name)
+            if t.device != ref.device:
+                raise ValueError(f"{name} must be on {ref.device}")
+        _call("mra_attention_backward_pooled", *head, *(_ptr(t) for t in pooled), *tail)
     return dq, dk, dv
 
 
@@ -409,23 +444,34 @@ class MraAttention(torch.autograd.Function):
         B, H, n, d = ref.shape
         nb = n // BLOCK
         lse = torch.empty(B, H, n, device=ref.device, dtype=torch.float32)
+        pooled = ()
         if variant == "global":
             idx = torch.empty(B, H, nb, nb, device=ref.device, dtype=torch.int32)
-            out = attention_forward_global(q, k, v, budget, prior_diagonal, idx_out=idx, lse_out=lse)
-        elif variant in ("mra2", "mra2s"):
+            ws = torch.empty(max(forward_global_workspace_bytes(B, H, n, d, ref.dtype), 1), device=ref.device,
+                             dtype=torch.uint8)
+            out = attention_forward_global(q, k, v, budget, prior_diagonal, idx_out=idx, workspace=ws, lse_out=lse)
+            pooled = forward_pooled_rows(ws, B, H, n, d)
+        elif variant == "mra2":
             idx = torch.empty(B, H, nb, budget, device=ref.device, dtype=torch.int32)
-            fwd = attention_forward if variant == "mra2" else sparse_attention_forward
-            out = fwd(q, k, v, budget, idx_out=idx, lse_out=lse)
+            ws = torch.empty(max(forward_workspace_bytes(B, H, n, d, budget, ref.dtype), 1), device=ref.device,
+                             dtype=torch.uint8)
+            out = attention_forward(q, k, v, budget, idx_out=idx, workspace=ws, lse_out=lse)
+            pooled = forward_pooled_rows(ws, B, H, n, d)
+        elif variant == "mra2s":
+            idx = torch.empty(B, H, nb, budget, device=ref.device, dtype=torch.int32)
+            out = sparse_attention_forward(q, k, v, budget, idx_out=idx, lse_out=lse)
         else:
             raise ValueError(f"unknown variant {variant!r}")
-        ctx.save_for_backward(q, k, v, out, lse, idx)
+        # the forward's block means (views of its workspace) go to the backward
+        ctx.save_for_backward(q, k, v, out, lse, idx, *pooled)
         ctx.coarse = variant != "mra2s"
         return out
 
     @staticmethod
     def backward(ctx, dout):
-        q, k, v, out, lse, idx = ctx.saved_tensors
-        dq, dk, dv = attention_backward(q, k, v, out, dout.contiguous(), lse, idx, coarse=ctx.coarse)
+        q, k, v, out, lse, idx, *pooled = ctx.saved_tensors
+        dq, dk, dv = attention_backward(q, k, v, out, dout.contiguous(), lse, idx, coarse=ctx.coarse,
+                                        pooled=tuple(pooled) if pooled else None)
         return dq, dk, dv, None, None, None
 
 

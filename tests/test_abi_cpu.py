@@ -31,7 +31,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(lib):
     names = declared_functions()
-    assert len(names) == 20, names
+    assert len(names) == 22, names
     for name in names:
         assert hasattr(lib, name), name
     assert set(names) == set(ops.SIGNATURES)
@@ -243,6 +243,51 @@ def test_backward_validation(lib):
     assert bwd(lib, B=0, q=None, k=None, v=None, out=None, dout=None, lse=None, idx=None, dq=None,
                dk=None, dv=None, ws=None) == OK
     assert lib.mra_last_hip_error() == 0
+
+
+def bwdp(lib, qp=A, kp=A, vp=A, ws=A, wsb=1 << 40, B=1, n=64, d=64, width=1, coarse=1, dtype=1, q=A):
+    return lib.mra_attention_backward_pooled(q, A, A, A, A, A, A, qp, kp, vp, A, A, A, ws, wsb, B, 1, n, d, 32,
+                                             width, coarse, dtype, None)
+
+
+def test_backward_pooled_validation(lib):
+    """The pooled-input backward takes the plain backward's checks plus its
+    three block-mean pointers, required (and 16-byte aligned) for any
+    non-empty problem, also with coarse = 0."""
+    assert bwdp(lib, q=None) == INVALID
+    assert bwdp(lib, d=48) == UNSUPPORTED
+    assert bwdp(lib, coarse=2) == INVALID
+    for name in ("qp", "kp", "vp"):
+        assert bwdp(lib, **{name: None}) == INVALID, name
+        assert bwdp(lib, **{name: MIS}) == MISALIGNED, name
+        assert bwdp(lib, coarse=0, **{name: None}) == INVALID, name
+    need = lib.mra_backward_workspace_bytes(1, 1, 64, 64, 32, 1)
+    assert bwdp(lib, wsb=need - 1) == WORKSPACE
+    assert bwdp(lib, B=0, q=None, qp=None, kp=None, vp=None, ws=None) == OK
+    assert lib.mra_last_hip_error() == 0
+
+
+def test_forward_pooled_rows(lib):
+    """Host arithmetic only: Q~, K~, V~ lead the forward's workspace, each
+    B*H*nb*d float32 rounded up to 256 bytes, whatever the budget or dtype;
+    checked against the offsets the workspace sizes imply."""
+    outs = [ctypes.c_void_p() for _ in range(3)]
+    refs = [ctypes.byref(o) for o in outs]
+    for B, H, n, d in ((1, 1, 64, 64), (2, 3, 96, 32), (1, 5, 4096, 128)):
+        assert lib.mra_forward_pooled_rows(A, B, H, n, d, 32, *refs) == OK
+        pooled = -(-B * H * (n // 32) * d * 4 // 256) * 256
+        assert [o.value - A for o in outs] == [0, pooled, 2 * pooled]
+        # the pooled rows fit every forward workspace of these sizes
+        for budget in (0, n // 32):
+            assert lib.mra_forward_workspace_bytes(B, H, n, d, 32, budget, 1) >= 3 * pooled
+        assert lib.mra_forward_global_workspace_bytes(B, H, n, d, 32, 0) >= 3 * pooled
+    assert lib.mra_forward_pooled_rows(None, 1, 1, 64, 64, 32, *refs) == INVALID
+    assert lib.mra_forward_pooled_rows(MIS, 1, 1, 64, 64, 32, *refs) == MISALIGNED
+    assert lib.mra_forward_pooled_rows(A, 1, 1, 64, 48, 32, *refs) == UNSUPPORTED
+    assert lib.mra_forward_pooled_rows(A, 1, 1, 48, 64, 32, *refs) == INVALID
+    assert lib.mra_forward_pooled_rows(A, 1, 1, 64, 64, 32, None, refs[1], refs[2]) == INVALID
+    assert lib.mra_forward_pooled_rows(None, 0, 1, 64, 64, 32, *refs) == OK
+    assert [o.value for o in outs] == [None, None, None]
 
 
 def mfwd(lib, q=A, out=A, ws=A, wsb=1 << 40, n=256, d=64, cb=64, m1=1, m2=1, dtype=1, i1=None, i2=None, lse=None):

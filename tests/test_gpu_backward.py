@@ -176,6 +176,42 @@ def test_autograd_function_matches_entry_points(gpu):
             assert torch.equal(a, b_), variant
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("d", [32, 64, 128])
+@pytest.mark.parametrize("variant", ["mra2", "global", "mra2s"])
+def test_backward_with_forward_pooled_rows(gpu, variant, d, dtype):
+    """The forward's block means, read from its workspace
+    (mra_forward_pooled_rows), are mra_pool's bits, and the backward that
+    takes them (mra_attention_backward_pooled) gives the plain backward's
+    gradients bit for bit (MRA-2-s does not read them)."""
+    q, k, v, g = _case(51, 2, 3, 320, d, dtype, 4)
+    tq, tk, tv, tg = dev(q, dtype), dev(k, dtype), dev(v, dtype), dev(g, dtype)
+    B, H, n, _ = tq.shape
+    nb = n // 32
+    lse = torch.empty(B, H, n, dtype=torch.float32, device="cuda")
+    if variant == "global":
+        idx = torch.empty(B, H, nb, nb, dtype=torch.int32, device="cuda")
+        ws = torch.empty(gpu.forward_global_workspace_bytes(B, H, n, d, tq.dtype), dtype=torch.uint8, device="cuda")
+        out = gpu.attention_forward_global(tq, tk, tv, 17, True, idx_out=idx, workspace=ws, lse_out=lse)
+        pooled = gpu.forward_pooled_rows(ws, B, H, n, d)
+    else:
+        idx = torch.empty(B, H, nb, 4, dtype=torch.int32, device="cuda")
+        ws = torch.empty(gpu.forward_workspace_bytes(B, H, n, d, 4, tq.dtype), dtype=torch.uint8, device="cuda")
+        fwd = gpu.attention_forward if variant == "mra2" else gpu.sparse_attention_forward
+        out = fwd(tq, tk, tv, 4, idx_out=idx, workspace=ws, lse_out=lse)
+        pooled = gpu.forward_pooled_rows(ws, B, H, n, d) if variant == "mra2" else gpu.pool(tq, tk, tv)
+    torch.cuda.synchronize()
+    for got, want in zip(pooled, gpu.pool(tq, tk, tv)):
+        assert torch.equal(got, want)
+    coarse = variant != "mra2s"
+    plain = gpu.attention_backward(tq, tk, tv, out, tg, lse, idx, coarse=coarse)
+    given = gpu.attention_backward(tq, tk, tv, out, tg, lse, idx, coarse=coarse, pooled=pooled)
+    torch.cuda.synchronize()
+    for a, b_ in zip(plain, given):
+        assert torch.isfinite(a.float()).all()
+        assert torch.equal(a, b_)
+
+
 def test_backward_is_deterministic(gpu):
     """Two calls give identical bits (no atomics in any sum)."""
     q, k, v, g = _case(41, 2, 2, 512, 64, "bf16", 4)

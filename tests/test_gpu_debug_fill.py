@@ -98,3 +98,13 @@ def test_backward_writes_every_gradient(gpu, monkeypatch, dtype, d):
 
     a, b = _both(monkeypatch, run)
     _same(a, b)
+    # given the block means, the backward reads them and not its workspace's
+    # (NaN-filled) copy
+    pooled = gpu.pool(q, k, v)
+
+    def run_pooled():
+        return gpu.attention_backward(q, k, v, out, g, lse, idx, pooled=pooled)
+
+    c, e = _both(monkeypatch, run_pooled)
+    _same(c, e)
+    _same(a, c)
