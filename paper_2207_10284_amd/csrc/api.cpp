@@ -633,8 +633,9 @@ size_t mra_backward_workspace_bytes(int B, int H, int n, int d, int block, mra_d
 }
 
 // The backward of mra_attention_backward(_pooled): with `given`, pq, pk, pv
-// are the block means of q, k, v, supplied by the caller.
-mra_status_t backward(const void* q, const void* k, const void* v, const void* out,
+// are the block means of q, k, v, supplied by the caller. (Internal linkage:
+// only the mra_ entry points are exported.)
+static mra_status_t backward(const void* q, const void* k, const void* v, const void* out,
                       const void* dout, const float* lse, const int32_t* idx, bool given,
                       const float* pq, const float* pk, const float* pv, void* dq, void* dk,
                       void* dv, void* workspace, size_t workspace_bytes, int B, int H, int n,

@@ -37,6 +37,20 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(ops.SIGNATURES)
 
 
+def test_exports_no_other_c_symbols():
+    """Every unmangled function the library exports is an entry point of
+    include/mra.h (helpers have internal linkage or live in a namespace)."""
+    import shutil
+    import subprocess
+    if shutil.which("nm") is None:
+        pytest.skip("nm not available")
+    out = subprocess.run(["nm", "-D", "--defined-only", ops.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    funcs = {line.split()[-1] for line in out.splitlines() if len(line.split()) == 3 and line.split()[1] == "T"}
+    plain = {f for f in funcs if not f.startswith("_Z")}
+    assert plain == set(declared_functions()), sorted(plain ^ set(declared_functions()))
+
+
 def test_status_strings(lib):
     for code, name in ops.STATUS.items():
         assert lib.mra_status_str(code).decode().startswith(name)
