@@ -116,3 +116,37 @@ def test_levels_and_backward_in_a_graph(gpu):
     with torch.cuda.graph(g):
         work()
     _replay_and_compare(g, [lout, dq, dk, dv], refs, lambda: gpu.attention_forward(k, q, v, m))
+
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 64), ("f32", 32)])
+def test_training_step_in_a_graph(gpu, dtype, d):
+    """A training step of the layer as one graph: the forward with log
+    normalisers, then the backward given the forward's block means (views of
+    the forward's workspace); every replay matches the eager step bit for
+    bit."""
+    B, H, n, m = 2, 2, 1024, 6
+    print("graph training step", dtype, d, flush=True)
+    q, k, v = (dev(a, dtype) for a in inputs.random_qkv(1730 + d, B, H, n, d, dtype, scale=1.1))
+    gz = dev(np.random.Generator(np.random.PCG64(1731)).standard_normal((B, H, n, d)), dtype)
+    ws = torch.empty(gpu.forward_workspace_bytes(B, H, n, d, m, q.dtype), dtype=torch.uint8, device="cuda")
+    bws = torch.empty(gpu.backward_workspace_bytes(B, H, n, d, q.dtype), dtype=torch.uint8, device="cuda")
+    pooled = gpu.forward_pooled_rows(ws, B, H, n, d)
+    out = torch.empty_like(q)
+    idx = torch.empty(B, H, n // 32, m, dtype=torch.int32, device="cuda")
+    lse = torch.empty(B, H, n, dtype=torch.float32, device="cuda")
+    dq, dk, dv = (torch.empty_like(q) for _ in range(3))
+
+    def work():
+        gpu.attention_forward(q, k, v, m, out=out, idx_out=idx, workspace=ws, lse_out=lse)
+        gpu.attention_backward(q, k, v, out, gz, lse, idx, dq=dq, dk=dk, dv=dv, workspace=bws, pooled=pooled)
+
+    work()
+    torch.cuda.synchronize()
+    refs = [t.clone() for t in (out, lse, dq, dk, dv)]
+    plain = gpu.attention_backward(q, k, v, out, gz, lse, idx)
+    for a, b in zip(plain, refs[2:]):
+        assert torch.equal(a, b)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        work()
+    _replay_and_compare(g, [out, lse, dq, dk, dv], refs, lambda: gpu.attention_forward(k, q, v, m))
